@@ -1,0 +1,276 @@
+"""Plain fp64 CPU oracle of the VideoMLA latent-attention hot path.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path imports this module: only the tests, the
+package's smoke check and the benchmark's CPU-baseline leg call it. It shares no code with the
+HIP kernels or their binding; its only inputs are the seeded bf16 bit patterns that both sides
+receive, widened here to fp64.
+
+What it computes, and where the paper defines it (VideoMLA, arXiv 2605.30351):
+
+* compress   c = W_down^KV x (Eq. 1), optional RMSNorm of c (Appendix "VideoMLA Block"),
+             k^R = W_R^K x (Eq. 5);
+* RoPE_3D    the decoupled (t, h, w) rotary encoding of k^R and q^R (Eqs. 5-6; Appendix
+             "NoPE/RoPE Split and 3D RoPE");
+* ring slot  where a token's latents live in the sliding-window cache (Appendix "Chunk-Causal
+             Sliding-Window Attention": FIFO eviction of whole frames);
+* attention  the training-time form: per-head keys/values reconstructed explicitly
+             (Eq. 2), score of Eq. 7, softmax over the active window, weighted sum of values.
+             Section "Inference-Time Reparameterization" states that the absorbed latent form
+             computes exactly this, so the textbook form is the definition the GPU path must
+             match. The absorbed form (Eqs. 8-11) is implemented separately as a self-check.
+
+Readings of points the paper leaves open (each is a parameter, never a hidden constant):
+RoPE pairs are interleaved channels (2k, 2k+1) of each axis slice, theta_{a,k} = base^(-2k/D_a);
+keys are rotated at their absolute (f, y, x) when written (a uniform shift of every position
+leaves scores unchanged, so this equals the paper's window-relative rotation without a sink);
+RMSNorm is applied before caching; the softmax scale is 1/sqrt(d_nope + d_rope) (Eq. 7).
+
+Parity pins: every function here is pinned by the `-m "not gpu"` tests against closed forms,
+invariants, library routines or printed values of the paper; the fidelity of the RoPE frequency
+convention and the RMSNorm epsilon to the trained model is "parity unpinned" (no weights).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+LOG2E = 1.4426950408889634
+
+
+# --------------------------------------------------------------------------------------------
+# bf16 <-> fp64
+# --------------------------------------------------------------------------------------------
+
+def bf16_bits_to_f64(bits) -> np.ndarray:
+    """Widen bf16 bit patterns (uint16) to fp64, exactly."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def round_to_bf16_bits(v) -> np.ndarray:
+    """Round fp64 values to bf16 (nearest, ties to even) in one step; returns uint16 bits.
+
+    bf16 keeps 8 significant bits, so the rounding quantum of v = m * 2^e (0.5 <= |m| < 1) is
+    2^(e-8); below the smallest normal (2^-126) the quantum stays at 2^-133.
+    """
+    v = np.asarray(v, dtype=np.float64)
+    _, e = np.frexp(v)
+    e = np.maximum(e, -125)
+    q = np.ldexp(np.rint(np.ldexp(v, 8 - e)), e - 8)
+    return (q.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+# --------------------------------------------------------------------------------------------
+# Shapes, positions and the ring slot map
+# --------------------------------------------------------------------------------------------
+
+def softmax_scale(dims) -> float:
+    """Eq. 7: the joint score is divided by sqrt(d_nope + d_rope)."""
+    if dims.softmax_scale and dims.softmax_scale > 0:
+        return float(dims.softmax_scale)
+    return 1.0 / np.sqrt(dims.d_nope + dims.d_rope)
+
+
+def cache_scalars_per_token(dims) -> int:
+    """Section "Compressed KV Cache Construction": each cached token stores (c^KV, k^R)."""
+    return dims.d_c + dims.d_rope
+
+
+def dense_scalars_per_token(dims) -> int:
+    """Dense per-head KV cache of the same backbone: 2 * n_h * d_h, with d_h = d / n_h."""
+    return 2 * dims.n_heads * (dims.d_model // dims.n_heads)
+
+
+def token_position(n, frame_end: int, dims):
+    """Token n of the chunk whose first frame is `frame_end`: frames in order, each frame's
+    tokens row-major over the (grid_h, grid_w) latent grid. Returns (f, y, x) arrays."""
+    n = np.asarray(n, dtype=np.int64)
+    f = frame_end + n // dims.hw
+    r = n % dims.hw
+    return f, r // dims.grid_w, r % dims.grid_w
+
+
+def ring_slot(f, y, x, dims):
+    """Slot of the token at absolute (f, y, x): frame f lives in frame slot f mod W_f, so the
+    ring holds the most recent W_f frames and the oldest whole frame is evicted first."""
+    f = np.asarray(f, dtype=np.int64)
+    return ((f % dims.window_frames) * dims.grid_h + np.asarray(y)) * dims.grid_w + np.asarray(x)
+
+
+def window_frame_range(frame_end: int, dims):
+    """Frames visible to the chunk starting at `frame_end`: the chunk itself plus past frames,
+    at most W_f in total (chunk-causal sliding window). Returns [first, last)."""
+    last = frame_end + dims.chunk_frames
+    return max(0, last - dims.window_frames), last
+
+
+# --------------------------------------------------------------------------------------------
+# Decoupled 3D RoPE
+# --------------------------------------------------------------------------------------------
+
+def rope_axis_layout(dims):
+    """Split of the d_rope channels over (t, h, w): axis a owns 2*pairs[a] consecutive channels,
+    t first. Returns [(channel_start, n_pairs, band_dim)] for the three axes."""
+    pairs = list(dims.rope_pairs)
+    assert sum(pairs) * 2 == dims.d_rope, "rope pairs must cover d_rope exactly"
+    out, start = [], 0
+    for a in range(3):
+        band = dims.rope_band_dim[a] if dims.rope_band_dim[a] else 2 * pairs[a]
+        out.append((start, pairs[a], band))
+        start += 2 * pairs[a]
+    return out
+
+
+def rope3d(v, f, y, x, dims) -> np.ndarray:
+    """Rotate each complex pair (2k, 2k+1) of each axis slice of v[..., d_rope] by the angle
+    pos_a * base^(-2k / D_a), pos = (f, y, x) broadcast over v's leading dimensions."""
+    v = np.asarray(v, dtype=np.float64)
+    out = v.copy()
+    pos = [np.asarray(f, dtype=np.float64), np.asarray(y, dtype=np.float64),
+           np.asarray(x, dtype=np.float64)]
+    for a, (start, npairs, band) in enumerate(rope_axis_layout(dims)):
+        for k in range(npairs):
+            theta = dims.rope_base ** (-2.0 * k / band)
+            phi = pos[a] * theta
+            while phi.ndim < v.ndim - 1:
+                phi = phi[..., None]
+            cs, sn = np.cos(phi), np.sin(phi)
+            u, w = v[..., start + 2 * k], v[..., start + 2 * k + 1]
+            out[..., start + 2 * k] = u * cs - w * sn
+            out[..., start + 2 * k + 1] = u * sn + w * cs
+    return out
+
+
+# --------------------------------------------------------------------------------------------
+# Cache write: compress, normalize, rotate, place
+# --------------------------------------------------------------------------------------------
+
+def compress(x, w_dkv, w_kr, gamma, dims):
+    """Eq. 1 and Eq. 5 for a block of tokens x[T, d_model] (fp64): returns (c [T, d_c] after
+    the optional RMSNorm with gain gamma, k^R [T, d_rope] unrotated)."""
+    c = x @ w_dkv.T
+    kr = x @ w_kr.T
+    if gamma is not None:
+        rms = np.sqrt(np.mean(c * c, axis=-1, keepdims=True) + dims.kv_norm_eps)
+        c = gamma * c / rms
+    return c, kr
+
+
+def cache_write(x_chunk_bits, w_dkv_bits, w_kr_bits, gamma_bits, frame_end: int, dims):
+    """What `cache_write` must produce for one batch element's chunk.
+
+    x_chunk_bits [chunk_tokens, d_model] bf16 bits of the chunk starting at frame `frame_end`.
+    Returns dict: c [T, d_c] fp64, k_rope [T, d_rope] fp64 (rotated at absolute (f, y, x)),
+    slots [T] int64.
+    """
+    x = bf16_bits_to_f64(x_chunk_bits)
+    gamma = None if gamma_bits is None else bf16_bits_to_f64(gamma_bits)
+    c, kr = compress(x, bf16_bits_to_f64(w_dkv_bits), bf16_bits_to_f64(w_kr_bits), gamma, dims)
+    f, y, xx = token_position(np.arange(x.shape[0]), frame_end, dims)
+    return {"c": c, "k_rope": rope3d(kr, f, y, xx, dims), "slots": ring_slot(f, y, xx, dims)}
+
+
+def window_latents(x_bits, w_dkv_bits, w_kr_bits, gamma_bits, frame_end: int, dims,
+                   rotate_origin: int = 0):
+    """Latents of every token visible to the chunk starting at `frame_end`, computed from the
+    raw inputs x_bits [n_frames * HW, d_model] (frames from 0). Returns (c, k_rope, (f, y, x)).
+
+    `rotate_origin` is subtracted from every temporal index before rotation (0 = absolute
+    positions; the first window frame = the paper's window-relative re-indexing)."""
+    lo, hi = window_frame_range(frame_end, dims)
+    x = bf16_bits_to_f64(x_bits[lo * dims.hw: hi * dims.hw])
+    gamma = None if gamma_bits is None else bf16_bits_to_f64(gamma_bits)
+    c, kr = compress(x, bf16_bits_to_f64(w_dkv_bits), bf16_bits_to_f64(w_kr_bits), gamma, dims)
+    n = np.arange(x.shape[0])
+    f = lo + n // dims.hw
+    y = (n % dims.hw) // dims.grid_w
+    xx = n % dims.grid_w
+    return c, rope3d(kr, f - rotate_origin, y, xx, dims), (f, y, xx)
+
+
+# --------------------------------------------------------------------------------------------
+# Attention
+# --------------------------------------------------------------------------------------------
+
+def _softmax_rows(s):
+    m = np.max(s, axis=-1, keepdims=True)
+    p = np.exp(s - m)
+    return p / np.sum(p, axis=-1, keepdims=True)
+
+
+def query_rope(q_r, q_pos, dims, rotate_origin: int = 0):
+    """Eq. 6: q^rope = RoPE_3D(q^R) at each query token's (f, y, x); q_r [Nq, H, d_rope]."""
+    f, y, x = q_pos
+    return rope3d(q_r, np.asarray(f) - rotate_origin, y, x, dims)
+
+
+def attend_unabsorbed(q_nope, q_rope, w_uk, w_uv, c_win, krope_win, dims, row_block=512):
+    """Training-time form (Eq. 2 and Eq. 7): per head h reconstruct
+    K_h[j] = [W_UK_h c_j ; k^rope_j] and V_h[j] = W_UV_h c_j for every window token j, score
+    s_ij = Q_h[i].K_h[j] / sqrt(d_nope + d_rope) with Q_h[i] = [q^nope ; q^rope], softmax over
+    all window tokens, o = sum_j p_ij V_h[j].
+
+    q_nope [Nq, H, d_nope], q_rope [Nq, H, d_rope] (already rotated), w_uk [H*d_nope, d_c],
+    w_uv [H*d_v, d_c], c_win [S, d_c], krope_win [S, d_rope], all fp64. Returns [Nq, H, d_v].
+    Rows are processed in blocks of `row_block` queries only to bound memory.
+    """
+    nq, H = q_nope.shape[0], dims.n_heads
+    scale = softmax_scale(dims)
+    out = np.empty((nq, H, dims.d_v))
+    for h in range(H):
+        w_uk_h = w_uk[h * dims.d_nope:(h + 1) * dims.d_nope]      # [d_nope, d_c]
+        w_uv_h = w_uv[h * dims.d_v:(h + 1) * dims.d_v]            # [d_v, d_c]
+        k_h = np.concatenate([c_win @ w_uk_h.T, krope_win], axis=1)
+        v_h = c_win @ w_uv_h.T
+        for r0 in range(0, nq, row_block):
+            q_h = np.concatenate([q_nope[r0:r0 + row_block, h], q_rope[r0:r0 + row_block, h]],
+                                 axis=1)
+            p = _softmax_rows(scale * (q_h @ k_h.T))
+            out[r0:r0 + row_block, h] = p @ v_h
+    return out
+
+
+def attend_absorbed(q_nope, q_rope, w_uk, w_uv, c_win, krope_win, dims):
+    """Inference-time form (Eqs. 8-11, in the per-head-query form): q_lat = W_UK_h^T q^nope,
+    score (q_lat.c_j + q^rope.k^rope_j) * scale, o_lat = sum_j p_ij c_j, o = W_UV_h o_lat.
+    Self-check only: it must equal `attend_unabsorbed` up to rounding."""
+    nq, H = q_nope.shape[0], dims.n_heads
+    scale = softmax_scale(dims)
+    out = np.empty((nq, H, dims.d_v))
+    for h in range(H):
+        w_uk_h = w_uk[h * dims.d_nope:(h + 1) * dims.d_nope]
+        w_uv_h = w_uv[h * dims.d_v:(h + 1) * dims.d_v]
+        q_lat = q_nope[:, h] @ w_uk_h                              # [Nq, d_c]
+        p = _softmax_rows(scale * (q_lat @ c_win.T + q_rope[:, h] @ krope_win.T))
+        out[:, h] = (p @ c_win) @ w_uv_h.T
+    return out
+
+
+def chunk_attention(inp, b: int, frame_end: int, rows=None, absorbed: bool = False,
+                    rotate_origin: int | None = None):
+    """End-to-end reference for one batch element: the chunk starting at `frame_end` attends
+    over its window, every latent computed from the raw inputs in fp64.
+
+    `inp` is a workloads.LayerInputs; `rows` optionally selects query tokens of the chunk.
+    `rotate_origin` None = absolute positions; otherwise positions are shifted by that amount
+    for both queries and keys. Returns [len(rows), H, d_v] fp64.
+    """
+    dims = inp.dims
+    origin = 0 if rotate_origin is None else rotate_origin
+    c_win, kro_win, _ = window_latents(inp.x[b], inp.w_dkv, inp.w_kr, inp.gamma, frame_end, dims,
+                                       rotate_origin=origin)
+    rows = np.arange(dims.chunk_tokens) if rows is None else np.asarray(rows)
+    q_nope = bf16_bits_to_f64(inp.q_nope[b][rows])
+    q_pos = token_position(rows, frame_end, dims)
+    q_rope = query_rope(bf16_bits_to_f64(inp.q_r[b][rows]), q_pos, dims, rotate_origin=origin)
+    w_uk, w_uv = bf16_bits_to_f64(inp.w_uk), bf16_bits_to_f64(inp.w_uv)
+    fn = attend_absorbed if absorbed else attend_unabsorbed
+    return fn(q_nope, q_rope, w_uk, w_uv, c_win, kro_win, dims)
+
+
+def ring_after_writes(n_frames_written: int, dims):
+    """Absolute frame held by each frame slot after frames 0 .. n_frames_written-1 were written
+    in order (-1 = never written). Follows the closed-form slot map."""
+    held = np.full(dims.window_frames, -1, dtype=np.int64)
+    for f in range(n_frames_written):
+        held[f % dims.window_frames] = f
+    return held
