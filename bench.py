@@ -1,0 +1,205 @@
+"""Benchmark of the VideoMLA latent-attention hot path on one MI355X.
+
+One step = one chunk-step of one Wan2.1-1.3B layer: `videomla_cache_write` of the chunk's 4,680
+tokens (3 frames of 30x52) into the 21-frame ring, then `videomla_attend` of its 4,680 x 12
+query rows over the 32,760-token window. Inputs are seeded synthetic tensors already resident
+in HBM; the chunk's x cycles through 32 distinct buffers (460 MB) so that the cache write reads
+x from HBM rather than from the 256 MB Infinity Cache.
+
+Prints one JSON line: whole-step throughput in TFLOP/s of algorithmic work (write 688,128 FLOP
+per token; attend 832 FLOP per query-head-key plus 98,304 per query-head for the two
+projections), the per-kernel averages measured with HIP events on the library's stream, the
+roofline of the dominant kernel and the CPU oracle's throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 256 * 4096 * 2.4e9 / 1e12   # 2516.6: 256 CUs x 4096 FLOP/clk x 2.4 GHz
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def work_model(d, batch=1):
+    """Algorithmic FLOPs and bytes of one chunk-step."""
+    nq = d.chunk_tokens
+    S = d.window_tokens
+    rows = batch * nq * d.n_heads
+    per_score = 2 * (d.d_c + d.d_rope) + 2 * d.d_c             # QK over 224, PV over 192
+    attend_core = rows * S * per_score
+    attend_proj = rows * 2 * (d.d_nope * d.d_c + d.d_c * d.d_v)  # absorption + W_UV
+    write_flop = batch * nq * 2 * d.d_model * (d.d_c + d.d_rope)
+    write_bytes = (batch * nq * (2 * d.d_model + 2 * (d.d_c + d.d_rope))
+                   + 2 * d.d_model * (d.d_c + d.d_rope))
+    return {"attend_core": attend_core, "attend": attend_core + attend_proj,
+            "write": write_flop, "write_bytes": write_bytes}
+
+
+def cpu_baseline(d, n_rows=2340):
+    """The fp64 oracle on the host: window latents from x, then reconstructed-K/V attention for
+    a sample of query tokens (all heads). Credited with the algorithmic FLOPs of that sample."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import videomla_oracle as O
+    from workloads import make_layer_inputs
+
+    inp = make_layer_inputs(d, seed=1, n_frames=24)
+    rows = np.linspace(0, d.chunk_tokens - 1, n_rows).astype(np.int64)
+    t0 = time.perf_counter()
+    O.chunk_attention(inp, 0, 21, rows=rows)
+    dt = time.perf_counter() - t0
+    per_score = 2 * (d.d_c + d.d_rope) + 2 * d.d_c
+    flop = (n_rows * d.n_heads * (d.window_tokens * per_score + 2 * (d.d_nope * d.d_c + d.d_c * d.d_v))
+            + d.chunk_tokens * 2 * d.d_model * (d.d_c + d.d_rope))
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "seconds": dt,
+            "sample": (f"fp64 numpy oracle: latents of the 32,760-token window from x, then "
+                       f"explicit per-head K/V attention for {n_rows} of 4,680 query tokens x 12 heads; "
+                       f"credited with the method's algorithmic FLOPs of that sample plus the chunk's "
+                       f"cache write; host has {len(os.sched_getaffinity(0))} usable cores")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--x-buffers", type=int, default=32)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2605_30351_amd as vm
+    from workloads import WAN, make_layer_inputs
+
+    d = WAN
+    dev = torch.device("cuda:0")
+    log("generating inputs")
+    inp = make_layer_inputs(d, seed=1, n_frames=24)
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    w_dkv, w_kr, w_uk, w_uv, gamma = (t(inp.w_dkv), t(inp.w_kr), t(inp.w_uk), t(inp.w_uv),
+                                      t(inp.gamma))
+    q_nope, q_r = t(inp.q_nope), t(inp.q_r)
+    x_all = t(inp.x)
+    c_kv = torch.zeros((1, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+    k_r = torch.zeros((1, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((1, d.chunk_tokens, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_workspace_bytes(d, 1), dtype=torch.uint8, device=dev)
+
+    # fill the ring with frames 0..20, then the step writes frames 21..23 (evicting 0..2)
+    for fe in range(0, 21, d.chunk_frames):
+        vm.cache_write(d, fe, 1, x_all[:, fe * d.hw:(fe + 3) * d.hw].contiguous(), w_dkv, w_kr,
+                       gamma, c_kv, k_r)
+    fe = 21
+    x_chunk = x_all[:, fe * d.hw:(fe + 3) * d.hw].contiguous()
+    xs = [x_chunk.clone() for _ in range(args.x_buffers)]
+    del x_all
+    torch.cuda.synchronize()
+
+    def step(i):
+        vm.cache_write(d, fe, 1, xs[i % len(xs)], w_dkv, w_kr, gamma, c_kv, k_r)
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+
+    log(f"warmup {args.warmup}")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    vm.timing_enable(True)
+    for k in ("cache_write", "q_absorb", "latent_attend", "out_proj"):
+        vm.timing_read(k)  # drop anything recorded before the timed region
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    for k in ("cache_write", "q_absorb", "latent_attend", "out_proj"):
+        n, tot = vm.timing_read(k)
+        kernels[k] = {"launches": n, "avg_us": 1e3 * tot / max(n, 1)}
+    vm.timing_enable(False)
+    log("timed region done")
+
+    ms = 1e3 * elapsed / args.steps
+    W = work_model(d)
+    att_ms = (kernels["q_absorb"]["avg_us"] + kernels["latent_attend"]["avg_us"]
+              + kernels["out_proj"]["avg_us"]) / 1e3
+    k3_s = kernels["latent_attend"]["avg_us"] / 1e6
+    k3_tflops = W["attend_core"] / k3_s / 1e12
+    wr_s = kernels["cache_write"]["avg_us"] / 1e6
+
+    result = {
+        "metric": "ms/chunk-step & TFLOP/s for latent-MLA attend (Wan-1.3B shape); % MFMA peak",
+        "value": round((W["attend"] + W["write"]) / (ms / 1e3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": ("Wan2.1-1.3B layer chunk-step: cache write of 4,680 tokens (3 frames of "
+                         "30x52) + latent attend of 4,680 tokens x 12 heads over a 32,760-token "
+                         "21-frame window, batch 1"),
+            "d_model": d.d_model, "heads": d.n_heads, "d_nope": d.d_nope, "d_rope": d.d_rope,
+            "d_c": d.d_c, "d_v": d.d_v, "chunk_tokens": d.chunk_tokens,
+            "window_tokens": d.window_tokens, "rope_pairs": list(d.rope_pairs), "seed": 1,
+        },
+        "attend": {
+            "ms": round(att_ms, 4),
+            "tflops": round(W["attend"] / (att_ms / 1e3) / 1e12, 2),
+            "mfma_frac": round(W["attend"] / (att_ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        },
+        "cache_write": {
+            "us": round(wr_s * 1e6, 3),
+            "gbps": round(W["write_bytes"] / wr_s / 1e9, 1),
+            "hbm_frac": round(W["write_bytes"] / wr_s / 1e9 / HBM_PEAK_GBPS, 4),
+        },
+        "kernels": {k: {"launches": v["launches"], "avg_us": round(v["avg_us"], 3)}
+                    for k, v in kernels.items()},
+        "roofline": {
+            "kernel": "latent_attend",
+            "bound": "mfma",
+            "achieved": round(k3_tflops, 2),
+            "peak": round(MFMA_BF16_PEAK_TFLOPS, 1),
+            "unit": "TFLOP/s",
+            "frac": round(k3_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        del xs
+        result["cpu_baseline"] = cpu_baseline(d)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,169 @@
+/*
+ * videomla.h -- C ABI of the VideoMLA latent-attention hot path for AMD Instinct MI355X (gfx950).
+ *
+ * VideoMLA (arXiv 2605.30351) caches, per video token and layer, one head-shared content
+ * latent c^KV (Eq. 1) and one head-shared decoupled 3D-RoPE key k^R (Eq. 5) instead of per-head
+ * keys and values. A chunk of new tokens attends over a sliding window of cached tokens with
+ * FIFO eviction of whole frames (Appendix "Chunk-Causal Sliding-Window Attention"), and at
+ * inference the per-head key/value up-projections are absorbed so that attention runs in the
+ * latent space (Section "Inference-Time Reparameterization", Eqs. 8-11).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are device pointers to row-major, contiguous arrays, 16-byte aligned.
+ *   - bf16 values are passed as their uint16_t bit patterns.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream). Calls only enqueue work on
+ *     it; none synchronizes the host, and none allocates device memory. The caller owns every
+ *     buffer: the ring, the workspace, the inputs and the outputs.
+ *   - All argument validation happens on the host before any launch. A non-zero return means
+ *     nothing was enqueued (except VIDEOMLA_EHIP, which reports a failed launch).
+ *   - Thread safety: calls are reentrant; the last error message is thread-local.
+ *
+ * Token geometry: a latent frame holds grid_h * grid_w tokens in row-major (y, x) order; token n
+ * of the chunk whose first frame is frame_end sits at (f, y, x) = (frame_end + n / HW,
+ * (n % HW) / grid_w, n % grid_w).
+ */
+#ifndef VIDEOMLA_H
+#define VIDEOMLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define VIDEOMLA_OK 0
+#define VIDEOMLA_EINVAL 1       /* NULL pointer, non-positive size, inconsistent dims       */
+#define VIDEOMLA_EUNSUPPORTED 2 /* dims the kernels do not tile (see each call)              */
+#define VIDEOMLA_EALIGN 3       /* a tensor pointer is not 16-byte aligned                    */
+#define VIDEOMLA_EWORKSPACE 4   /* workspace missing or smaller than the size query returned  */
+#define VIDEOMLA_EHIP 5         /* a HIP launch failed; the message carries hipGetErrorString */
+
+/*
+ * Layer shapes (Section "Method"; Appendix "VideoMLA Block" and "NoPE/RoPE Split and 3D RoPE").
+ *   d_model        attention input width d (1536 for Wan2.1-1.3B)
+ *   n_heads        n_h (12)
+ *   d_nope         per-head content (NoPE) query/key width (paper default 96)
+ *   d_rope         width of the head-shared RoPE key and of each head's RoPE query (32)
+ *   d_c            latent width of c^KV (192)
+ *   d_v            per-head value width, the output width per head (128)
+ *   grid_h, grid_w latent tokens per frame = grid_h * grid_w (30 x 52 = 1560)
+ *   window_frames  W_f: frames the ring holds, current chunk included (21)
+ *   chunk_frames   frames written and attended per call (3)
+ *   rope_pairs     complex pairs given to the (t, h, w) axes; 2 * sum = d_rope. Axis t owns the
+ *                  first 2 * rope_pairs[0] channels, then h, then w; pair k of an axis is the
+ *                  interleaved channel pair (2k, 2k+1) of that axis' slice
+ *   rope_band_dim  D_a in theta_{a,k} = rope_base^(-2k / D_a); 0 means 2 * rope_pairs[a]
+ *   rope_base      base of the RoPE frequencies (10000)
+ *   softmax_scale  multiplier of the scores; 0 means 1 / sqrt(d_nope + d_rope) (Eq. 7)
+ *   kv_norm_eps    epsilon of the RMSNorm applied to c^KV when a gain is given
+ */
+typedef struct videomla_dims {
+  int32_t d_model, n_heads, d_nope, d_rope, d_c, d_v;
+  int32_t grid_h, grid_w;
+  int32_t window_frames, chunk_frames;
+  int32_t rope_pairs[3];
+  int32_t rope_band_dim[3];
+  float rope_base;
+  float softmax_scale;
+  float kv_norm_eps;
+} videomla_dims;
+
+/* Host-side window state: absolute index of the first frame of the chunk being generated. */
+typedef struct videomla_window {
+  int64_t frame_end;
+} videomla_window;
+
+/*
+ * videomla_cache_write -- compress the chunk's tokens and write them into the ring
+ * (Eq. 1: c = W_down^KV x; RMSNorm of c when kv_norm_w != NULL; Eq. 5: k^R = W_R^K x rotated by
+ * RoPE_3D at the token's absolute (f, y, x); FIFO placement of whole frames).
+ *
+ *   x          [batch][chunk_frames * HW][d_model]           bf16, chunk tokens in order
+ *   w_dkv      [d_c][d_model]                                bf16, W_down^KV
+ *   w_kr       [d_rope][d_model]                             bf16, W_R^K
+ *   kv_norm_w  [d_c] bf16 RMSNorm gain, or NULL for no normalization
+ *   c_kv       [batch][window_frames * HW][d_c]              bf16 ring, written in place
+ *   k_r        [batch][window_frames * HW][d_rope]           bf16 ring of ROTATED keys
+ *   slots_out  [chunk_frames * HW] int32 slot of each chunk token, or NULL
+ * Token (f, y, x) is stored at slot ((f mod window_frames) * grid_h + y) * grid_w + x, so the
+ * chunk overwrites the oldest frames; every other slot is left untouched. Calling it again
+ * before videomla_window_advance (the next denoising step) overwrites the same slots.
+ * Requires d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0, d_c + d_rope <= 512.
+ */
+int videomla_cache_write(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                         const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
+                         const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
+                         int32_t* slots_out, void* stream);
+
+/* Bytes of device workspace videomla_attend needs for this shape and batch. */
+size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch);
+
+/*
+ * videomla_attend -- latent multi-head attention of the chunk's queries over the window.
+ * For every batch element b, chunk token n and head h (Section "Inference-Time
+ * Reparameterization"):
+ *   q_lat   = W_up,h^K^T q_nope[b,n,h]                          (query absorption, Eq. 8)
+ *   q_rope  = RoPE_3D(q_r[b,n,h]) at the token's absolute (f, y, x)        (Eq. 6)
+ *   s_j     = scale * (q_lat . c_kv[j] + q_rope . k_r[j])                   (Eq. 7)
+ *   o_lat   = sum_j softmax(s)_j c_kv[j]   over every valid slot j of the ring
+ *   out     = W_up,h^V o_lat                                    (value up-projection, Eq. 2)
+ * The valid slots are those of the last min(window_frames, frame_end + chunk_frames) frames:
+ * the current chunk (already written by videomla_cache_write) and the past frames, with no
+ * mask (tokens of a chunk see each other; later chunks are not in the ring yet).
+ *
+ *   q_nope  [batch][chunk_frames * HW][n_heads][d_nope]   bf16
+ *   q_r     [batch][chunk_frames * HW][n_heads][d_rope]   bf16, unrotated
+ *   w_uk    [n_heads * d_nope][d_c]   bf16, W_up^K (head h = rows h*d_nope ..)
+ *   w_uv    [n_heads * d_v][d_c]      bf16, W_up^V (head h = rows h*d_v ..)
+ *   c_kv, k_r   the rings as written by videomla_cache_write
+ *   out     [batch][chunk_frames * HW][n_heads][d_v]      bf16
+ *   workspace  device buffer of at least videomla_attend_workspace_bytes() bytes
+ * Arithmetic: bf16 operands, fp32 accumulation and softmax, bf16 round-to-nearest-even output.
+ * Requires d_c % 16 == 0, d_nope % 16 == 0, d_v % 32 == 0, (d_c, d_rope) in {(192, 32), (16, 8)}
+ * otherwise VIDEOMLA_EUNSUPPORTED.
+ */
+int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Slide the window after the last denoising step of a chunk: frame_end += chunk_frames.
+ * Host only; eviction is implicit (the next chunk's write overwrites the oldest frames). */
+int videomla_window_advance(const videomla_dims* dims, videomla_window* win);
+
+/* Bytes the ring holds per token and layer: 2 * (d_c + d_rope) (224 scalars = 448 B for Wan). */
+size_t videomla_cache_bytes_per_token(const videomla_dims* dims);
+
+/* Number of valid ring slots the chunk at win->frame_end attends over:
+ * min(window_frames, frame_end + chunk_frames) * HW. Negative on invalid arguments. */
+int64_t videomla_valid_tokens(const videomla_dims* dims, const videomla_window* win);
+
+/* Slot of the token at absolute position (f, y, x); negative on invalid arguments. */
+int64_t videomla_slot_of(const videomla_dims* dims, int64_t f, int32_t y, int32_t x);
+
+/* Message describing the last non-zero return on this thread ("" if none). */
+const char* videomla_last_error(void);
+
+/*
+ * Tuning knob: number of key-range splits used by the attention kernel (0 = automatic). Split
+ * partial results are merged exactly by their running maxima and sums. Process-wide.
+ */
+int videomla_set_attend_kv_splits(int32_t n_splits);
+
+/*
+ * Kernel timing with HIP events, for benchmarks. When enabled, every kernel the library
+ * launches is bracketed by two events recorded on the same stream. After the caller has
+ * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed
+ * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj") into
+ * *count and *total_ms, and forgets them. Timing state is process-wide and not thread-safe.
+ */
+int videomla_timing_enable(int32_t enable);
+int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VIDEOMLA_H */

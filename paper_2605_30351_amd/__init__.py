@@ -1,0 +1,22 @@
+"""VideoMLA latent-attention hot path for AMD Instinct MI355X (gfx950).
+
+The compute lives in libvideomla.so (hand-written HIP kernels behind a C ABI, declared in
+include/videomla.h). This package is its thin Python binding: torch supplies device memory and
+streams; importing it fails if the library has not been built.
+"""
+from ._lib import (  # noqa: F401
+    EXPORTED,
+    VideomlaError,
+    attend,
+    attend_workspace_bytes,
+    cache_bytes_per_token,
+    cache_write,
+    make_dims,
+    set_attend_kv_splits,
+    slot_of,
+    timing_enable,
+    timing_read,
+    valid_tokens,
+    window_advance,
+)
+from ._lib import LIB_PATH  # noqa: F401

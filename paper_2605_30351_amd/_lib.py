@@ -1,0 +1,215 @@
+"""ctypes binding of libvideomla.so: argument marshalling only.
+
+Every computation runs in the library's HIP kernels; this module converts torch tensors to
+device pointers, the current HIP stream to a handle, and return codes to exceptions. It raises
+at import time if the shared library has not been built, and never falls back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libvideomla.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2605_30351_amd.build`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
+
+EXPORTED = (
+    "videomla_cache_write", "videomla_attend_workspace_bytes", "videomla_attend",
+    "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
+    "videomla_slot_of", "videomla_last_error", "videomla_set_attend_kv_splits",
+    "videomla_timing_enable", "videomla_timing_read",
+)
+
+
+class VideomlaDims(ctypes.Structure):
+    _fields_ = [
+        ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("d_nope", ctypes.c_int32),
+        ("d_rope", ctypes.c_int32), ("d_c", ctypes.c_int32), ("d_v", ctypes.c_int32),
+        ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32),
+        ("window_frames", ctypes.c_int32), ("chunk_frames", ctypes.c_int32),
+        ("rope_pairs", ctypes.c_int32 * 3), ("rope_band_dim", ctypes.c_int32 * 3),
+        ("rope_base", ctypes.c_float), ("softmax_scale", ctypes.c_float),
+        ("kv_norm_eps", ctypes.c_float),
+    ]
+
+
+class VideomlaWindow(ctypes.Structure):
+    _fields_ = [("frame_end", ctypes.c_int64)]
+
+
+_P = ctypes.c_void_p
+_DP = ctypes.POINTER(VideomlaDims)
+_WP = ctypes.POINTER(VideomlaWindow)
+
+_lib.videomla_cache_write.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.videomla_cache_write.restype = ctypes.c_int
+_lib.videomla_attend_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
+_lib.videomla_attend_workspace_bytes.restype = ctypes.c_size_t
+_lib.videomla_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
+                                 ctypes.c_size_t, _P]
+_lib.videomla_attend.restype = ctypes.c_int
+_lib.videomla_window_advance.argtypes = [_DP, _WP]
+_lib.videomla_window_advance.restype = ctypes.c_int
+_lib.videomla_cache_bytes_per_token.argtypes = [_DP]
+_lib.videomla_cache_bytes_per_token.restype = ctypes.c_size_t
+_lib.videomla_valid_tokens.argtypes = [_DP, _WP]
+_lib.videomla_valid_tokens.restype = ctypes.c_int64
+_lib.videomla_slot_of.argtypes = [_DP, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32]
+_lib.videomla_slot_of.restype = ctypes.c_int64
+_lib.videomla_last_error.argtypes = []
+_lib.videomla_last_error.restype = ctypes.c_char_p
+_lib.videomla_set_attend_kv_splits.argtypes = [ctypes.c_int32]
+_lib.videomla_set_attend_kv_splits.restype = ctypes.c_int
+_lib.videomla_timing_enable.argtypes = [ctypes.c_int32]
+_lib.videomla_timing_enable.restype = ctypes.c_int
+_lib.videomla_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
+                                      ctypes.POINTER(ctypes.c_double)]
+_lib.videomla_timing_read.restype = ctypes.c_int
+
+
+class VideomlaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"videomla error {code}: {msg}")
+        self.code = code
+
+
+def _check(code: int):
+    if code != OK:
+        raise VideomlaError(code, _lib.videomla_last_error().decode())
+
+
+def make_dims(d) -> VideomlaDims:
+    """Build the C struct from any object with the Dims field names."""
+    s = VideomlaDims()
+    for name in ("d_model", "n_heads", "d_nope", "d_rope", "d_c", "d_v", "grid_h", "grid_w",
+                 "window_frames", "chunk_frames"):
+        setattr(s, name, int(getattr(d, name)))
+    for i in range(3):
+        s.rope_pairs[i] = int(d.rope_pairs[i])
+        s.rope_band_dim[i] = int(d.rope_band_dim[i])
+    s.rope_base = float(d.rope_base)
+    s.softmax_scale = float(d.softmax_scale)
+    s.kv_norm_eps = float(d.kv_norm_eps)
+    return s
+
+
+def _ptr(t: torch.Tensor | None, name: str, dtypes=(torch.bfloat16, torch.int16, torch.uint16)):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, numel: int):
+    if t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+
+
+def cache_write(dims, frame_end: int, batch: int, x, w_dkv, w_kr, gamma, c_kv, k_r, slots=None,
+                stream=None):
+    """videomla_cache_write on torch tensors (bf16 data, int32 slots)."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    _need(x, "x", batch * d.chunk_frames * hw * d.d_model)
+    _need(w_dkv, "w_dkv", d.d_c * d.d_model)
+    _need(w_kr, "w_kr", d.d_rope * d.d_model)
+    _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
+    _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
+    if gamma is not None:
+        _need(gamma, "gamma", d.d_c)
+    if slots is not None:
+        _need(slots, "slots", d.chunk_frames * hw)
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_cache_write(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(x, "x"), _ptr(w_dkv, "w_dkv"),
+        _ptr(w_kr, "w_kr"), _ptr(gamma, "gamma"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
+        _ptr(slots, "slots", (torch.int32,)), _stream(stream)))
+
+
+def attend_workspace_bytes(dims, batch: int) -> int:
+    return int(_lib.videomla_attend_workspace_bytes(ctypes.byref(make_dims(dims)), int(batch)))
+
+
+def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace,
+           stream=None):
+    """videomla_attend on torch tensors; `workspace` is a uint8 device tensor."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    nq = d.chunk_frames * hw
+    _need(q_nope, "q_nope", batch * nq * d.n_heads * d.d_nope)
+    _need(q_r, "q_r", batch * nq * d.n_heads * d.d_rope)
+    _need(w_uk, "w_uk", d.n_heads * d.d_nope * d.d_c)
+    _need(w_uv, "w_uv", d.n_heads * d.d_v * d.d_c)
+    _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
+    _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
+    _need(out, "out", batch * nq * d.n_heads * d.d_v)
+    w = VideomlaWindow(int(frame_end))
+    ws = _ptr(workspace, "workspace", (torch.uint8,))
+    _check(_lib.videomla_attend(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
+        _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
+        _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
+
+
+def window_advance(dims, frame_end: int) -> int:
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_window_advance(ctypes.byref(make_dims(dims)), ctypes.byref(w)))
+    return int(w.frame_end)
+
+
+def cache_bytes_per_token(dims) -> int:
+    return int(_lib.videomla_cache_bytes_per_token(ctypes.byref(make_dims(dims))))
+
+
+def valid_tokens(dims, frame_end: int) -> int:
+    w = VideomlaWindow(int(frame_end))
+    v = int(_lib.videomla_valid_tokens(ctypes.byref(make_dims(dims)), ctypes.byref(w)))
+    if v < 0:
+        raise VideomlaError(EINVAL, _lib.videomla_last_error().decode())
+    return v
+
+
+def slot_of(dims, f: int, y: int, x: int) -> int:
+    v = int(_lib.videomla_slot_of(ctypes.byref(make_dims(dims)), int(f), int(y), int(x)))
+    if v < 0:
+        raise VideomlaError(EINVAL, _lib.videomla_last_error().decode())
+    return v
+
+
+def set_attend_kv_splits(n: int):
+    _check(_lib.videomla_set_attend_kv_splits(int(n)))
+
+
+def timing_enable(on: bool = True):
+    _check(_lib.videomla_timing_enable(1 if on else 0))
+
+
+def timing_read(kernel: str) -> tuple[int, float]:
+    c, t = ctypes.c_int64(0), ctypes.c_double(0.0)
+    _check(_lib.videomla_timing_read(kernel.encode(), ctypes.byref(c), ctypes.byref(t)))
+    return int(c.value), float(t.value)
+
+
+def raw():
+    """The loaded ctypes library (for tests that call the C ABI directly)."""
+    return _lib

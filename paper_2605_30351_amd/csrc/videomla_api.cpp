@@ -1,0 +1,331 @@
+// C-ABI layer: argument validation, ring/window arithmetic, workspace carving, dispatch of the
+// kernels and optional per-kernel HIP-event timing. All checks run on the host before any
+// launch, so every error path is reachable without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "videomla.h"
+#include "vmla_internal.h"
+
+using namespace vmla;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return VIDEOMLA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Shape checks common to every call.
+int check_dims(const videomla_dims* d) {
+  if (!d) return fail(VIDEOMLA_EINVAL, "dims is NULL");
+  if (d->d_model <= 0 || d->n_heads <= 0 || d->d_nope <= 0 || d->d_rope <= 0 || d->d_c <= 0 ||
+      d->d_v <= 0 || d->grid_h <= 0 || d->grid_w <= 0 || d->window_frames <= 0 ||
+      d->chunk_frames <= 0)
+    return fail(VIDEOMLA_EINVAL, "all sizes in dims must be positive");
+  if (d->d_rope % 2) return fail(VIDEOMLA_EINVAL, "d_rope must be even (complex pairs), got %d", d->d_rope);
+  if (d->rope_pairs[0] < 0 || d->rope_pairs[1] < 0 || d->rope_pairs[2] < 0 ||
+      2 * (d->rope_pairs[0] + d->rope_pairs[1] + d->rope_pairs[2]) != d->d_rope)
+    return fail(VIDEOMLA_EINVAL, "rope_pairs (%d,%d,%d) must be non-negative and sum to d_rope/2 = %d",
+                d->rope_pairs[0], d->rope_pairs[1], d->rope_pairs[2], d->d_rope / 2);
+  for (int a = 0; a < 3; ++a)
+    if (d->rope_band_dim[a] < 0) return fail(VIDEOMLA_EINVAL, "rope_band_dim must be >= 0");
+  if (!(d->rope_base > 0.f)) return fail(VIDEOMLA_EINVAL, "rope_base must be positive");
+  if (!(d->softmax_scale >= 0.f)) return fail(VIDEOMLA_EINVAL, "softmax_scale must be >= 0");
+  if (!(d->kv_norm_eps >= 0.f)) return fail(VIDEOMLA_EINVAL, "kv_norm_eps must be >= 0");
+  if (d->chunk_frames > d->window_frames)
+    return fail(VIDEOMLA_EINVAL, "chunk_frames (%d) exceeds window_frames (%d)", d->chunk_frames,
+                d->window_frames);
+  const int64_t ring = (int64_t)d->window_frames * d->grid_h * d->grid_w;
+  if (ring > (int64_t)1 << 30) return fail(VIDEOMLA_EUNSUPPORTED, "ring of %lld tokens is too large", (long long)ring);
+  if (d->d_rope / 2 > kMaxRopePairs) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope > %d", 2 * kMaxRopePairs);
+  return VIDEOMLA_OK;
+}
+
+int check_window(const videomla_window* w) {
+  if (!w) return fail(VIDEOMLA_EINVAL, "window is NULL");
+  if (w->frame_end < 0) return fail(VIDEOMLA_EINVAL, "frame_end must be >= 0, got %lld", (long long)w->frame_end);
+  return VIDEOMLA_OK;
+}
+
+RopeTable make_rope(const videomla_dims* d) {
+  RopeTable t{};
+  t.n_pairs = d->d_rope / 2;
+  int p = 0;
+  for (int a = 0; a < 3; ++a) {
+    const int n = d->rope_pairs[a];
+    const double band = d->rope_band_dim[a] > 0 ? d->rope_band_dim[a] : 2.0 * n;
+    for (int k = 0; k < n; ++k, ++p) {
+      t.axis[p] = a;
+      t.theta[p] = std::pow((double)d->rope_base, -2.0 * k / band);
+    }
+  }
+  return t;
+}
+
+Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
+  Geometry g{};
+  g.grid_h = d->grid_h;
+  g.grid_w = d->grid_w;
+  g.window_frames = d->window_frames;
+  g.chunk_tokens = d->chunk_frames * d->grid_h * d->grid_w;
+  g.frame_end = w->frame_end;
+  g.ring_tokens = (int64_t)d->window_frames * d->grid_h * d->grid_w;
+  return g;
+}
+
+// ---- timing -------------------------------------------------------------------------------
+enum KernelId { K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ, K_COUNT };
+const char* kKernelNames[K_COUNT] = {"cache_write", "q_absorb", "latent_attend", "out_proj"};
+
+struct TimingRec {
+  int kernel;
+  hipEvent_t start, stop;
+};
+bool g_timing = false;
+std::vector<TimingRec> g_pending;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t take_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+hipError_t timed(int kernel, hipStream_t s, F&& launch) {
+  if (!g_timing) return launch();
+  hipEvent_t e0 = take_event(), e1 = take_event();
+  if (!e0 || !e1) return launch();
+  hipEventRecord(e0, s);
+  const hipError_t err = launch();
+  hipEventRecord(e1, s);
+  g_pending.push_back({kernel, e0, e1});
+  return err;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(VIDEOMLA_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
+}
+
+int g_kv_splits = 0;  // 0 = automatic
+
+int auto_splits(const videomla_dims*, int32_t) { return 1; }
+
+int effective_splits(const videomla_dims* d, int32_t batch) {
+  return g_kv_splits > 0 ? g_kv_splits : auto_splits(d, batch);
+}
+
+struct WorkspaceLayout {
+  size_t qcat_off, opart_off, ml_off, total;
+};
+
+WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_splits) {
+  const size_t rows = (size_t)batch * d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
+  const size_t dqkp = round_up((size_t)d->d_c + d->d_rope, 16);
+  WorkspaceLayout w{};
+  w.qcat_off = 0;
+  w.opart_off = round_up(rows * dqkp * 2, 256);
+  w.ml_off = w.opart_off + round_up((size_t)n_splits * rows * d->d_c * 4, 256);
+  w.total = w.ml_off + round_up((size_t)n_splits * rows * 2 * 4, 256);
+  return w;
+}
+
+int check_attend_shape(const videomla_dims* d) {
+  if (!latent_attend_supported(d->d_c, d->d_rope))
+    return fail(VIDEOMLA_EUNSUPPORTED,
+                "attention kernel is built for (d_c, d_rope) in {(192,32),(16,8)}, got (%d,%d)",
+                d->d_c, d->d_rope);
+  if (d->d_nope % 16) return fail(VIDEOMLA_EUNSUPPORTED, "d_nope must be a multiple of 16, got %d", d->d_nope);
+  if (d->d_v % 32 || d->d_v > 256)
+    return fail(VIDEOMLA_EUNSUPPORTED, "d_v must be a multiple of 32 and <= 256, got %d", d->d_v);
+  const size_t lds = (size_t)d->d_nope * (round_up(d->d_c, 32) + 8) * 2;
+  if (lds > 64 * 1024) return fail(VIDEOMLA_EUNSUPPORTED, "d_nope %d too large for the query kernel", d->d_nope);
+  return VIDEOMLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* videomla_last_error(void) { return g_err.c_str(); }
+
+size_t videomla_cache_bytes_per_token(const videomla_dims* d) {
+  if (check_dims(d)) return 0;
+  return 2 * ((size_t)d->d_c + d->d_rope);
+}
+
+int64_t videomla_valid_tokens(const videomla_dims* d, const videomla_window* w) {
+  if (check_dims(d) || check_window(w)) return -1;
+  const int64_t frames = w->frame_end + d->chunk_frames;
+  const int64_t f = frames < d->window_frames ? frames : d->window_frames;
+  return f * d->grid_h * d->grid_w;
+}
+
+int64_t videomla_slot_of(const videomla_dims* d, int64_t f, int32_t y, int32_t x) {
+  if (check_dims(d)) return -1;
+  if (f < 0 || y < 0 || y >= d->grid_h || x < 0 || x >= d->grid_w) {
+    fail(VIDEOMLA_EINVAL, "position (%lld,%d,%d) outside the grid", (long long)f, y, x);
+    return -1;
+  }
+  return ((f % d->window_frames) * d->grid_h + y) * (int64_t)d->grid_w + x;
+}
+
+int videomla_window_advance(const videomla_dims* d, videomla_window* w) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  w->frame_end += d->chunk_frames;
+  return ok();
+}
+
+int videomla_set_attend_kv_splits(int32_t n) {
+  if (n < 0 || n > 64) return fail(VIDEOMLA_EINVAL, "kv splits must be in [0, 64], got %d", n);
+  g_kv_splits = n;
+  return ok();
+}
+
+int videomla_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                         const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
+                         const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
+                         int32_t* slots_out, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!x || !w_dkv || !w_kr || !c_kv || !k_r) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
+  if (d->d_c % 16) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 16, got %d", d->d_c);
+  if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
+  if (d->d_c + d->d_rope > 288) return fail(VIDEOMLA_EUNSUPPORTED, "d_c + d_rope must be <= 288");
+  if (!aligned16(x) || !aligned16(w_dkv) || !aligned16(w_kr) || !aligned16(c_kv) || !aligned16(k_r))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  if (kv_norm_w && !aligned16(kv_norm_w)) return fail(VIDEOMLA_EALIGN, "kv_norm_w must be 16-byte aligned");
+  WriteArgs a{};
+  a.x = x; a.w_dkv = w_dkv; a.w_kr = w_kr; a.gamma = kv_norm_w;
+  a.c_kv = c_kv; a.k_r = k_r; a.slots = slots_out;
+  a.batch = batch; a.d_model = d->d_model; a.d_c = d->d_c; a.d_rope = d->d_rope;
+  a.eps = d->kv_norm_eps;
+  a.geo = make_geo(d, w);
+  a.rope = make_rope(d);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = timed(K_CACHE_WRITE, s, [&] { return launch_cache_write(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "cache_write");
+  return ok();
+}
+
+size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
+  if (check_dims(d) || batch <= 0) return 0;
+  return workspace_layout(d, batch, effective_splits(d, batch)).total;
+}
+
+int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
+    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (int e = check_attend_shape(d)) return e;
+  if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
+      !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const int n_splits = effective_splits(d, batch);
+  const WorkspaceLayout L = workspace_layout(d, batch, n_splits);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+
+  AttendArgs a{};
+  a.q_nope = q_nope; a.q_r = q_r; a.w_uk = w_uk; a.w_uv = w_uv;
+  a.c_kv = c_kv; a.k_r = k_r; a.out = out;
+  char* ws = static_cast<char*>(workspace);
+  a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
+  a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
+  a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
+  a.batch = batch; a.n_heads = d->n_heads; a.d_nope = d->d_nope; a.d_rope = d->d_rope;
+  a.d_c = d->d_c; a.d_v = d->d_v;
+  a.dqk_pad = (int32_t)round_up((size_t)d->d_c + d->d_rope, 16);
+  a.geo = make_geo(d, w);
+  a.rope = make_rope(d);
+  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
+  a.n_splits = n_splits;
+  const int bn = latent_attend_keys_per_tile(d->d_c, d->d_rope);
+  const int per = (a.n_valid + n_splits - 1) / n_splits;
+  a.keys_per_split = (int32_t)round_up((size_t)per, (size_t)bn);
+  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
+                                              : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
+  a.qscale = (float)(scale * 1.4426950408889634);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = timed(K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "q_absorb");
+  e = timed(K_LATENT_ATTEND, s, [&] { return launch_latent_attend(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "latent_attend");
+  e = timed(K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "out_proj");
+  return ok();
+}
+
+int videomla_timing_enable(int32_t enable) {
+  g_timing = enable != 0;
+  return ok();
+}
+
+int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms) {
+  if (!kernel || !count || !total_ms) return fail(VIDEOMLA_EINVAL, "NULL argument");
+  int id = -1;
+  for (int k = 0; k < K_COUNT; ++k)
+    if (std::strcmp(kernel, kKernelNames[k]) == 0) id = k;
+  if (id < 0) return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
+  *count = 0;
+  *total_ms = 0.0;
+  std::vector<TimingRec> keep;
+  for (const TimingRec& r : g_pending) {
+    if (r.kernel != id) {
+      keep.push_back(r);
+      continue;
+    }
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+      keep.push_back(r);
+      continue;
+    }
+    *count += 1;
+    *total_ms += ms;
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_pending.swap(keep);
+  return ok();
+}
+
+}  // extern "C"

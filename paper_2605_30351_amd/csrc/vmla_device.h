@@ -1,0 +1,108 @@
+// Device-side helpers for gfx950 (CDNA4): vector types, MFMA wrappers, bf16 conversion,
+// LDS transpose reads, cross-half-wave exchange and the 3D-RoPE angle.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "vmla_internal.h"
+
+namespace vmla {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// D(32x32) += A(32x16) B(16x32). Lane l holds A[l%32][8(l/32) .. +8], B[8(l/32) .. +8][l%32];
+// accumulator element 4i+j of lane l is D[8i + 4(l/32) + j][l%32].
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ u32x4 as_u32x4(bf16x8 v) { return __builtin_bit_cast(u32x4, v); }
+
+__device__ __forceinline__ u32x4 ldg16(const uint16_t* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ void stg16(uint16_t* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+// Round-to-nearest-even fp32 -> bf16 (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ bf16x8 to_bf16x8(f32x8 v) { return __builtin_convertvector(v, bf16x8); }
+__device__ __forceinline__ bf16x4 to_bf16x4(f32x4 v) { return __builtin_convertvector(v, bf16x4); }
+__device__ __forceinline__ uint16_t to_bf16_bits(float v) {
+  return __builtin_bit_cast(uint16_t, (__bf16)v);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// LDS transpose read (ds_read_b64_tr_b16). Within each group of 16 lanes, source lane s points
+// at 4 consecutive 16-bit elements M[s][0..3]; result lane i receives M[4e + i/4][i%4],
+// e = 0..3. If source lane s addresses row (R0 + s/4), columns C0 + 4(s%4) .. +4 of a row-major
+// matrix, lane i receives column C0 + i of rows R0 .. R0+3.
+__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* lds_ptr) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4*)(reinterpret_cast<__attribute__((address_space(3))) uint16_t*>(
+          (__attribute__((address_space(3))) void*)(lds_ptr))));
+}
+
+__device__ __forceinline__ bf16x8 join_bf16x8(i16x4 lo, i16x4 hi) {
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Value of lane l ^ 32 (v_permlane32_swap): the swap returns {own-or-partner} pairs whose two
+// entries are, on every lane, this lane's value and its partner's.
+__device__ __forceinline__ float half_swap_max(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_swap_sum(float v) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Absolute position of chunk token n: (f, y, x).
+struct TokenPos {
+  int64_t f;
+  int32_t y, x;
+};
+__device__ __forceinline__ TokenPos token_pos(const Geometry& g, int n) {
+  const int hw = g.grid_h * g.grid_w;
+  TokenPos p;
+  p.f = g.frame_end + n / hw;
+  const int r = n % hw;
+  p.y = r / g.grid_w;
+  p.x = r % g.grid_w;
+  return p;
+}
+__device__ __forceinline__ int64_t ring_slot(const Geometry& g, const TokenPos& p) {
+  return ((p.f % g.window_frames) * g.grid_h + p.y) * (int64_t)g.grid_w + p.x;
+}
+
+// Rotate the pair (u, v) of RoPE pair `pair` at position p: angle = pos_axis * theta, taken in
+// double precision, then (u cos - v sin, u sin + v cos) in fp32.
+__device__ __forceinline__ void rope_rotate(const RopeTable& t, int pair, const TokenPos& p,
+                                            float& u, float& v) {
+  const int ax = t.axis[pair];
+  const double pos = ax == 0 ? (double)p.f : (ax == 1 ? (double)p.y : (double)p.x);
+  double s, c;
+  sincos(pos * t.theta[pair], &s, &c);
+  const float cs = (float)c, sn = (float)s;
+  const float ru = u * cs - v * sn;
+  const float rv = u * sn + v * cs;
+  u = ru;
+  v = rv;
+}
+
+}  // namespace vmla

@@ -1,0 +1,70 @@
+// Launch arguments shared by the C-ABI layer (videomla_api.cpp) and the kernel files.
+// Host-visible plain structs only; no device code here.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vmla {
+
+constexpr int kMaxRopePairs = 32;
+
+// Per RoPE pair p (interleaved channels 2p, 2p+1 of the d_rope vector): the axis whose
+// coordinate drives it (0 = t, 1 = h, 2 = w) and theta = base^(-2k / D_axis), in double.
+struct RopeTable {
+  int32_t n_pairs;
+  int32_t axis[kMaxRopePairs];
+  double theta[kMaxRopePairs];
+};
+
+struct Geometry {
+  int32_t grid_h, grid_w, window_frames;
+  int32_t chunk_tokens;   // chunk_frames * HW
+  int64_t frame_end;      // absolute first frame of the chunk
+  int64_t ring_tokens;    // window_frames * HW (ring rows per batch element)
+};
+
+struct WriteArgs {
+  const uint16_t* x;      // [B][chunk_tokens][d_model]
+  const uint16_t* w_dkv;  // [d_c][d_model]
+  const uint16_t* w_kr;   // [d_rope][d_model]
+  const uint16_t* gamma;  // [d_c] or nullptr
+  uint16_t* c_kv;         // [B][ring_tokens][d_c]
+  uint16_t* k_r;          // [B][ring_tokens][d_rope]
+  int32_t* slots;         // [chunk_tokens] or nullptr
+  int32_t batch, d_model, d_c, d_rope;
+  float eps;
+  Geometry geo;
+  RopeTable rope;
+};
+
+struct AttendArgs {
+  const uint16_t* q_nope;  // [B][Nq][H][d_nope]
+  const uint16_t* q_r;     // [B][Nq][H][d_rope]
+  const uint16_t* w_uk;    // [H*d_nope][d_c]
+  const uint16_t* w_uv;    // [H*d_v][d_c]
+  const uint16_t* c_kv;    // ring
+  const uint16_t* k_r;     // ring
+  uint16_t* out;           // [B][Nq][H][d_v]
+  uint16_t* qcat;          // workspace: [B*Nq*H][dqk_pad] bf16
+  float* o_part;           // workspace: [n_splits][B*Nq*H][d_c] fp32
+  float* ml_part;          // workspace: [n_splits][B*Nq*H][2] fp32 (running max, sum)
+  int32_t batch, n_heads, d_nope, d_rope, d_c, d_v, dqk_pad;
+  int32_t n_valid;         // valid ring slots (prefix of the ring)
+  int32_t n_splits, keys_per_split;
+  float qscale;            // softmax scale * log2(e), folded into the absorbed query
+  Geometry geo;
+  RopeTable rope;
+};
+
+// Launchers (one per kernel). Return the launch status.
+hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);
+hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
+hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);
+hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
+
+// Shapes the attention kernel is instantiated for.
+bool latent_attend_supported(int d_c, int d_rope);
+int latent_attend_rows_per_block(int d_c, int d_rope);
+int latent_attend_keys_per_tile(int d_c, int d_rope);
+
+}  // namespace vmla

@@ -1,0 +1,144 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared symbol, and its
+host-side validation, window and slot arithmetic behave as documented. No call here reaches a
+kernel launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from tests._build_once import ensure_built
+
+ensure_built()
+
+import paper_2605_30351_amd as vm  # noqa: E402
+from paper_2605_30351_amd import _lib as L  # noqa: E402
+from oracle import videomla_oracle as O  # noqa: E402
+from workloads import TINY, WAN, WAN_PAPER  # noqa: E402
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "videomla.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(videomla_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 11
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_struct_layout_matches_header():
+    # 10 int32 + 2*3 int32 + 3 float = 19 * 4 bytes, no padding
+    assert ctypes.sizeof(L.VideomlaDims) == 76
+    assert ctypes.sizeof(L.VideomlaWindow) == 8
+
+
+def test_cache_bytes_per_token():
+    assert vm.cache_bytes_per_token(WAN) == 448
+    assert vm.cache_bytes_per_token(WAN_PAPER) == 448
+    assert vm.cache_bytes_per_token(TINY) == 48
+
+
+@pytest.mark.parametrize("dims", [TINY, WAN])
+def test_slot_of_matches_oracle(dims):
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        f = int(rng.integers(0, 500))
+        y = int(rng.integers(0, dims.grid_h))
+        x = int(rng.integers(0, dims.grid_w))
+        assert vm.slot_of(dims, f, y, x) == int(O.ring_slot(f, y, x, dims))
+
+
+def test_valid_tokens_and_advance():
+    fe = 0
+    for step in range(10):
+        lo, hi = O.window_frame_range(fe, WAN)
+        assert vm.valid_tokens(WAN, fe) == (hi - lo) * WAN.hw
+        fe = vm.window_advance(WAN, fe)
+        assert fe == (step + 1) * WAN.chunk_frames
+    assert vm.valid_tokens(TINY, 5) == 48
+    assert vm.valid_tokens(TINY, 0) == 16
+
+
+def _dims_struct(dims, **kw):
+    d = L.make_dims(dims)
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+FAKE = ctypes.c_void_p(0x1000)       # never dereferenced: validation fails first
+MISALIGNED = ctypes.c_void_p(0x1008)
+
+
+def _write(d, fe=0, batch=1, x=FAKE, gamma=None):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_cache_write(ctypes.byref(d), ctypes.byref(w), batch, x, FAKE, FAKE,
+                                        gamma, FAKE, FAKE, None, None)
+
+
+def _attend(d, fe=0, batch=1, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_attend(ctypes.byref(d), ctypes.byref(w), batch, q, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("d_rope", 7, L.EINVAL), ("d_model", 0, L.EINVAL), ("n_heads", -1, L.EINVAL),
+    ("chunk_frames", 30, L.EINVAL), ("d_model", 1000, L.EUNSUPPORTED), ("d_c", 100, L.EUNSUPPORTED),
+])
+def test_cache_write_rejects_bad_dims(field, value, code):
+    assert _write(_dims_struct(WAN, **{field: value})) == code
+    assert L.raw().videomla_last_error().decode() != ""
+
+
+def test_cache_write_rejects_bad_args():
+    d = L.make_dims(WAN)
+    assert _write(d, fe=-1) == L.EINVAL
+    assert _write(d, batch=0) == L.EINVAL
+    assert _write(d, x=None) == L.EINVAL
+    assert _write(d, x=MISALIGNED) == L.EALIGN
+    d.rope_pairs[0] = 7
+    assert _write(d) == L.EINVAL
+
+
+def test_attend_rejects_bad_args():
+    d = L.make_dims(WAN)
+    assert _attend(d, q=None) == L.EINVAL
+    assert _attend(d, q=MISALIGNED) == L.EALIGN
+    need = vm.attend_workspace_bytes(WAN, 1)
+    assert need > 0
+    assert _attend(d, ws=None) == L.EWORKSPACE
+    assert _attend(d, ws_bytes=need - 1) == L.EWORKSPACE
+    assert _attend(_dims_struct(WAN, d_c=128)) == L.EUNSUPPORTED
+    assert _attend(_dims_struct(WAN, d_v=100)) == L.EUNSUPPORTED
+    assert _attend(_dims_struct(WAN, d_nope=100)) == L.EUNSUPPORTED
+
+
+def test_workspace_grows_with_splits():
+    base = vm.attend_workspace_bytes(WAN, 1)
+    rows = WAN.chunk_tokens * WAN.n_heads
+    assert base >= rows * 224 * 2 + rows * 192 * 4 + rows * 8
+    vm.set_attend_kv_splits(3)
+    try:
+        assert vm.attend_workspace_bytes(WAN, 1) > base
+        assert vm.attend_workspace_bytes(WAN, 2) > vm.attend_workspace_bytes(WAN, 1)
+    finally:
+        vm.set_attend_kv_splits(0)
+    with pytest.raises(vm.VideomlaError):
+        vm.set_attend_kv_splits(-1)
+
+
+def test_timing_read_validates_names():
+    n, t = vm.timing_read("latent_attend")
+    assert (n, t) == (0, 0.0)
+    with pytest.raises(vm.VideomlaError):
+        vm.timing_read("nope")
