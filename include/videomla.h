@@ -147,10 +147,12 @@ int64_t videomla_slot_of(const videomla_dims* dims, int64_t f, int32_t y, int32_
 const char* videomla_last_error(void);
 
 /*
- * Tuning knob: number of key-range splits used by the attention kernel (0 = automatic). Split
- * partial results are merged exactly by their running maxima and sums. Process-wide.
+ * Tuning knob: number of workgroups the attention kernel uses (0 = one per compute unit, the
+ * default). The (batch, 256-row block, key tile) work is split evenly over them; a row block
+ * shared by several workgroups leaves one partial result per workgroup, merged exactly by
+ * their running maxima and sums. Changes videomla_attend_workspace_bytes. Process-wide.
  */
-int videomla_set_attend_kv_splits(int32_t n_splits);
+int videomla_set_attend_workgroups(int32_t n_workgroups);
 
 /*
  * Kernel timing with HIP events, for benchmarks. When enabled, every kernel the library

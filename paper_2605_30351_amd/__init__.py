@@ -12,7 +12,7 @@ from ._lib import (  # noqa: F401
     cache_bytes_per_token,
     cache_write,
     make_dims,
-    set_attend_kv_splits,
+    set_attend_workgroups,
     slot_of,
     timing_enable,
     timing_read,

@@ -15,7 +15,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libvideomla.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2605_30351_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2605_30351_amd/build.py`")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -24,7 +24,7 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
 EXPORTED = (
     "videomla_cache_write", "videomla_attend_workspace_bytes", "videomla_attend",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
-    "videomla_slot_of", "videomla_last_error", "videomla_set_attend_kv_splits",
+    "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
     "videomla_timing_enable", "videomla_timing_read",
 )
 
@@ -66,8 +66,8 @@ _lib.videomla_slot_of.argtypes = [_DP, ctypes.c_int64, ctypes.c_int32, ctypes.c_
 _lib.videomla_slot_of.restype = ctypes.c_int64
 _lib.videomla_last_error.argtypes = []
 _lib.videomla_last_error.restype = ctypes.c_char_p
-_lib.videomla_set_attend_kv_splits.argtypes = [ctypes.c_int32]
-_lib.videomla_set_attend_kv_splits.restype = ctypes.c_int
+_lib.videomla_set_attend_workgroups.argtypes = [ctypes.c_int32]
+_lib.videomla_set_attend_workgroups.restype = ctypes.c_int
 _lib.videomla_timing_enable.argtypes = [ctypes.c_int32]
 _lib.videomla_timing_enable.restype = ctypes.c_int
 _lib.videomla_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
@@ -196,8 +196,9 @@ def slot_of(dims, f: int, y: int, x: int) -> int:
     return v
 
 
-def set_attend_kv_splits(n: int):
-    _check(_lib.videomla_set_attend_kv_splits(int(n)))
+def set_attend_workgroups(n: int):
+    """Workgroup count of the attention kernel (0 = one per compute unit)."""
+    _check(_lib.videomla_set_attend_workgroups(int(n)))
 
 
 def timing_enable(on: bool = True):

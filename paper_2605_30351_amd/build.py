@@ -1,7 +1,8 @@
 """Build libvideomla.so in-tree with hipcc for gfx950.
 
 Every HIP/C++ source under csrc/ is compiled to an object under _build/ (in parallel) and
-linked into paper_2605_30351_amd/libvideomla.so. Run as `python -m paper_2605_30351_amd.build`.
+linked into paper_2605_30351_amd/libvideomla.so. Run as `python paper_2605_30351_amd/build.py`
+(it does not import the package, whose binding needs the built library).
 """
 from __future__ import annotations
 

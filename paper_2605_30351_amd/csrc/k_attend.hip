@@ -99,27 +99,42 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// latent_attend: grid (row blocks, splits, B), NW waves, QB 32-row query blocks per wave.
-//   LDS tile: BN ring tokens x [c_kv | k_r | pad], token-major, double-buffered.
+// latent_attend: grid G (about one workgroup per CU), NW waves, QB 32-row query blocks per wave.
+//   LDS: a ring of three BN-token tiles [c_kv | k_r | pad], token-major. Iteration t computes
+//   the scores of tile t+1 while the softmax of tile t runs on the VALU, then accumulates
+//   PV of tile t, and stages tile t+2 from registers loaded at the top of the iteration.
 //   S^T (keys x queries) = MFMA(A = K tile rows from LDS, B = q_cat rows in registers); each
 //   lane then holds one query's scores for 16 keys per 32-key block, so the row max and sum
 //   need only one exchange with lane l^32. P^T feeds the PV MFMA directly as the B operand,
-//   and V^T (the c_kv columns of the same tile) is read with LDS transpose reads.
+//   and V^T (the c_kv columns of the same tile) is read with LDS transpose reads. Both the K
+//   and the V operand of each MFMA are shared by the QB query blocks of the wave.
+//   The running max is raised only when a tile's max exceeds it by more than kLazyMax (in
+//   log2 units), so probabilities stay below 2^kLazyMax and the accumulators are rescaled
+//   rarely; the final merge divides by the matching sum, so the result is unchanged.
+//   Tiles are fetched with bounds-checked buffer loads whose range ends at the segment's last
+//   valid key, so keys past it read as zeros without any branch. The (batch, row block, key
+//   tile) units are split evenly over the workgroups (a row block may be shared by two or
+//   three of them), so every CU gets the same amount of work.
 // ---------------------------------------------------------------------------------------------
+constexpr float kLazyMax = 8.0f;
+constexpr int kRawBufferWord3 = 0x00020000;  // raw (untyped) buffer access, 32-bit data format
+
 template <int DC, int DR, int QB, int NW, int BN>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
   static constexpr int DQKP = (DQK + 15) / 16 * 16;
   static constexpr int KSTEPS = DQKP / 16;
   static constexpr int DVB = (DC + 31) / 32;
+  static constexpr int KB = BN / 32;       // 32-key blocks per tile
   static constexpr int STRIDE = DQKP + 8;  // elements; +16 B per row against bank conflicts
   static constexpr int NT = NW * 64;
   static constexpr int ROWS = NW * QB * 32;
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
   static constexpr int CH_C = BN * OCT_C, CH_R = BN * OCT_R;
-  static constexpr int CHUNKS = CH_C + CH_R;
-  static constexpr int CPT = (CHUNKS + NT - 1) / NT;
+  static constexpr int CPT_C = (CH_C + NT - 1) / NT;  // c_kv chunks per thread
+  static constexpr int CPT_R = (CH_R + NT - 1) / NT;  // k_r chunks per thread
   static constexpr int TILE = BN * STRIDE;
+  static constexpr int NBUF = 3;
   static_assert(DC % 8 == 0 && DR % 8 == 0, "latent and rope widths must be multiples of 8");
   static_assert(BN % 32 == 0, "key tile must be a multiple of 32");
   static_assert(DVB * 32 <= STRIDE, "transpose reads must stay inside a tile row");
@@ -128,26 +143,43 @@ struct AttCfg {
 template <int DC, int DR, int QB, int NW, int BN>
 __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendArgs a) {
   using C = AttCfg<DC, DR, QB, NW, BN>;
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][C::TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
+  __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, l32 = lane & 31;
-  const int split = blockIdx.y, b = blockIdx.z;
   const int rows_b = a.geo.chunk_tokens * a.n_heads;
-  const int row0 = blockIdx.x * C::ROWS + wave * QB * 32;
-
-  const int key_begin = split * a.keys_per_split;
-  const int key_end = min(a.n_valid, key_begin + a.keys_per_split);
-  const int n_tiles = key_end > key_begin ? (key_end - key_begin + BN - 1) / BN : 0;
-
-  const uint16_t* ckv = a.c_kv + (size_t)b * a.geo.ring_tokens * DC;
-  const uint16_t* krr = a.k_r + (size_t)b * a.geo.ring_tokens * DR;
-  const u32x4 zero = {0, 0, 0, 0};
-
   if (C::DQKP > C::DQK) {  // zero the pad columns once; staging never writes them
-    for (int r = tid; r < 2 * BN; r += C::NT)
+    for (int r = tid; r < C::NBUF * BN; r += C::NT)
       for (int c = C::DQK; c < C::DQKP; ++c) tile[r / BN][(r % BN) * C::STRIDE + c] = 0;
   }
+
+  // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
+  // tiles of one row block is a segment with its own partial result.
+  const int64_t U = a.units;
+  const int G = a.n_wg, T = a.tiles_per_row;
+  const int64_t u_begin = (int64_t)blockIdx.x * U / G, u_end = (int64_t)(blockIdx.x + 1) * U / G;
+  for (int64_t u = u_begin; u < u_end;) {
+  const int64_t rbg = u / T;
+  const int kt0 = (int)(u - rbg * T);
+  const int kt1 = (int)min((int64_t)T, (int64_t)kt0 + (u_end - u));
+  u += kt1 - kt0;
+  const int b = (int)(rbg / a.row_blocks), rb = (int)(rbg % a.row_blocks);
+  const int split = (int)blockIdx.x - attend_owner(rbg * T, U, G);
+  const int row0 = rb * C::ROWS + wave * QB * 32;
+  const int key_begin = kt0 * BN;
+  const int key_end = min(a.n_valid, kt1 * BN);
+  const int n_tiles = kt1 - kt0;
+  __syncthreads();  // the previous segment's LDS tiles are no longer read
+
+  // Bounds-checked views of this batch element's ring, ending at key_end.
+  const int kend = key_end > 0 ? key_end : 0;
+  const __amdgpu_buffer_rsrc_t rs_c = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.c_kv + (size_t)b * a.geo.ring_tokens * DC), (short)0, kend * DC * 2, kRawBufferWord3);
+  const __amdgpu_buffer_rsrc_t rs_r = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.k_r + (size_t)b * a.geo.ring_tokens * DR), (short)0, kend * DR * 2, kRawBufferWord3);
+  const u32x4 zero = {0, 0, 0, 0};
+
 
   // queries of this wave, B-operand layout: lane holds row l32, dims ks*16 + 8g .. +8
   bf16x8 q[QB][C::KSTEPS];
@@ -170,55 +202,44 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     for (int d = 0; d < C::DVB; ++d) o[qb][d] = f32x16{};
   }
 
-  u32x4 pre[C::CPT];
+  // Per-thread staging chunks: fixed (row, column) of the tile, so only the tile base moves.
+  u32x4 pre_c[C::CPT_C], pre_r[C::CPT_R];
   auto load_tile = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < C::CPT; ++i) {
+    for (int i = 0; i < C::CPT_C; ++i) {
       const int c = tid + i * C::NT;
-      u32x4 v = zero;
-      if (c < C::CH_C) {
-        const int key = k0 + c / C::OCT_C;
-        if (key < key_end) v = ldg16(ckv + (size_t)key * DC + (c % C::OCT_C) * 8);
-      } else if (c < C::CHUNKS) {
-        const int c2 = c - C::CH_C;
-        const int key = k0 + c2 / C::OCT_R;
-        if (key < key_end) v = ldg16(krr + (size_t)key * DR + (c2 % C::OCT_R) * 8);
-      }
-      pre[i] = v;
+      const uint32_t off = (uint32_t)((k0 + c / C::OCT_C) * DC + (c % C::OCT_C) * 8) * 2u;
+      pre_c[i] = (C::CH_C % C::NT == 0 || c < C::CH_C)
+                     ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs_c, off, 0, 0))
+                     : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < C::CPT_R; ++i) {
+      const int c = tid + i * C::NT;
+      const uint32_t off = (uint32_t)((k0 + c / C::OCT_R) * DR + (c % C::OCT_R) * 8) * 2u;
+      pre_r[i] = (C::CH_R % C::NT == 0 || c < C::CH_R)
+                     ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs_r, off, 0, 0))
+                     : zero;
     }
   };
   auto store_tile = [&](uint16_t* buf) {
 #pragma unroll
-    for (int i = 0; i < C::CPT; ++i) {
+    for (int i = 0; i < C::CPT_C; ++i) {
       const int c = tid + i * C::NT;
-      if (c < C::CH_C) {
-        *reinterpret_cast<u32x4*>(&buf[(c / C::OCT_C) * C::STRIDE + (c % C::OCT_C) * 8]) = pre[i];
-      } else if (c < C::CHUNKS) {
-        const int c2 = c - C::CH_C;
-        *reinterpret_cast<u32x4*>(&buf[(c2 / C::OCT_R) * C::STRIDE + DC + (c2 % C::OCT_R) * 8]) =
-            pre[i];
-      }
+      if (C::CH_C % C::NT == 0 || c < C::CH_C)
+        *reinterpret_cast<u32x4*>(&buf[(c / C::OCT_C) * C::STRIDE + (c % C::OCT_C) * 8]) = pre_c[i];
+    }
+#pragma unroll
+    for (int i = 0; i < C::CPT_R; ++i) {
+      const int c = tid + i * C::NT;
+      if (C::CH_R % C::NT == 0 || c < C::CH_R)
+        *reinterpret_cast<u32x4*>(&buf[(c / C::OCT_R) * C::STRIDE + DC + (c % C::OCT_R) * 8]) = pre_r[i];
     }
   };
-
-  const int tr_row = (lane & 15) >> 2;
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-
-  if (n_tiles > 0) {
-    load_tile(key_begin);
-    store_tile(tile[0]);
-  }
-  __syncthreads();
-
-  for (int t = 0; t < n_tiles; ++t) {
-    const int kbase = key_begin + t * BN;
-    const uint16_t* buf = tile[t & 1];
-    if (t + 1 < n_tiles) load_tile(kbase + BN);
-
-    // ---- S^T = K q^T ---------------------------------------------------------------------
-    f32x16 s[QB][BN / 32];
+  // S^T for one tile, both query blocks sharing each K operand read
+  auto scores = [&](const uint16_t* buf, f32x16 (&s)[QB][C::KB]) {
 #pragma unroll
-    for (int kb = 0; kb < BN / 32; ++kb) {
+    for (int kb = 0; kb < C::KB; ++kb) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) s[qb][kb] = f32x16{};
 #pragma unroll
@@ -229,67 +250,146 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
         for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mfma32(k, q[qb][ks], s[qb][kb]);
       }
     }
-
-    // ---- online softmax (base 2; scores already carry scale * log2 e) ---------------------
-    const bool ragged = kbase + BN > key_end;
+  };
+  // keys at or past key_end get -inf
+  auto mask_tail = [&](int kbase, f32x16 (&s)[QB][C::KB]) {
+#pragma unroll
+    for (int kb = 0; kb < C::KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const bool dead = kbase + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3) >= key_end;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) s[qb][kb][r] = dead ? kNegInf : s[qb][kb][r];
+      }
+  };
+  // Raise the running max where the scores `s` would exceed it by more than kLazyMax. Each lane
+  // sees half of its row's keys; growth on either half sends the wave through the rare path,
+  // where the two halves agree on the new max and the accumulators are rescaled through this
+  // wave's LDS slot (no VALU instruction ever touches them, so they stay in accumulation
+  // registers).
+  float own_max[QB];
+  auto own_max_of = [&](const f32x16 (&s)[QB][C::KB]) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      if (ragged) {
+      float m = kNegInf;
 #pragma unroll
-        for (int kb = 0; kb < BN / 32; ++kb)
+      for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (kbase + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3) >= key_end) s[qb][kb][r] = kNegInf;
-      }
-      float mx = kNegInf;
-#pragma unroll
-      for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[qb][kb][r]);
-      mx = half_swap_max(mx);
-      const float m_new = fmaxf(m_run[qb], mx);
-      const float alpha = fast_exp2(m_run[qb] - m_new);
-      m_run[qb] = m_new;
-      float sum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < BN / 32; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(s[qb][kb][r] - m_new);
-          s[qb][kb][r] = p;
-          sum += p;
-        }
-      l_run[qb] = l_run[qb] * alpha + sum;
-#pragma unroll
-      for (int d = 0; d < C::DVB; ++d) o[qb][d] *= alpha;
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[qb][kb][r]);
+      own_max[qb] = m;
     }
-
-    // ---- O^T += V^T P^T ----------------------------------------------------------------------
+  };
+  auto raise_max_if_needed = [&]() {
+    bool grow = false;
 #pragma unroll
-    for (int kk = 0; kk < BN / 16; ++kk) {
-      bf16x8 pb[QB];
+    for (int qb = 0; qb < QB; ++qb) grow |= own_max[qb] > m_run[qb] + kLazyMax;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      f32x16* slot = reinterpret_cast<f32x16*>(&resc[wave][lane * 16]);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        const f32x16& sv = s[qb][kk >> 1];
-        const int off = 8 * (kk & 1);
-        const f32x8 pv = {sv[off], sv[off + 1], sv[off + 2], sv[off + 3],
-                          sv[off + 4], sv[off + 5], sv[off + 6], sv[off + 7]};
-        pb[qb] = to_bf16x8(pv);
+        const float m_new = fmaxf(m_run[qb], half_swap_max(own_max[qb]));
+        const float alpha = fast_exp2(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int d = 0; d < C::DVB; ++d) {
+          *slot = o[qb][d];
+          asm volatile("" ::: "memory");
+          f32x16 tmp = *slot;
+          tmp *= alpha;
+          *slot = tmp;
+          asm volatile("" ::: "memory");
+          o[qb][d] = *slot;
+        }
       }
+    }
+  };
+
+  const int tr_row = (lane & 15) >> 2;
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  // One pipelined step. s_cur holds tile t's scores, already masked, with m_run high enough
+  // for them. Block A: scores of tile t+1 (MFMA) and tile t's exponentials (VALU). Block B: PV
+  // of tile t (MFMA) and staging of tile t+2. After the barrier: masking and max of tile t+1.
+  auto step = [&](int t, f32x16 (&s_cur)[QB][C::KB], f32x16 (&s_nxt)[QB][C::KB]) {
+    const int kbase = key_begin + t * BN;
+    const uint16_t* cur = tile[t % C::NBUF];
+    const uint16_t* nxt = tile[(t + 1) % C::NBUF];
+
+    // ---- block A: scores of tile t+1 and exponentials of tile t ----------------------------
+    // The two waves sharing a SIMD (wave w and w + NW/2) take the two halves in opposite
+    // order, so one's exponentials run while the other's score MFMAs do.
+    load_tile(kbase + 2 * BN);
+    bf16x8 pb[QB][2 * C::KB];
+    auto exps = [&]() {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float acc = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < C::KB; ++kb) {
+          f32x16 p;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            p[r] = fast_exp2(s_cur[qb][kb][r] - m_run[qb]);
+            acc += p[r];
+          }
+          const f32x8 lo = {p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]};
+          const f32x8 hi = {p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]};
+          pb[qb][2 * kb] = to_bf16x8(lo);
+          pb[qb][2 * kb + 1] = to_bf16x8(hi);
+        }
+        l_run[qb] += acc;
+      }
+    };
+    if (wave < NW / 2) {
+      scores(nxt, s_nxt);
+      exps();
+    } else {
+      exps();
+      scores(nxt, s_nxt);
+    }
+
+    // ---- block B ---------------------------------------------------------------------------
+#pragma unroll
+    for (int kk = 0; kk < 2 * C::KB; ++kk) {
       const int key0 = kk * 16 + 4 * g + tr_row;
 #pragma unroll
       for (int d = 0; d < C::DVB; ++d) {
-        const i16x4 lo = lds_read_tr(&buf[key0 * C::STRIDE + d * 32 + tr_col]);
-        const i16x4 hi = lds_read_tr(&buf[(key0 + 8) * C::STRIDE + d * 32 + tr_col]);
+        const i16x4 lo = lds_read_tr(&cur[key0 * C::STRIDE + d * 32 + tr_col]);
+        const i16x4 hi = lds_read_tr(&cur[(key0 + 8) * C::STRIDE + d * 32 + tr_col]);
         const bf16x8 v = join_bf16x8(lo, hi);
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][d] = mfma32(v, pb[qb], o[qb][d]);
+        for (int qb = 0; qb < QB; ++qb) o[qb][d] = mfma32(v, pb[qb][kk], o[qb][d]);
       }
     }
-
-    if (t + 1 < n_tiles) store_tile(tile[(t + 1) & 1]);
+    store_tile(tile[(t + 2) % C::NBUF]);
     __syncthreads();
+    if (kbase + 2 * BN > key_end) mask_tail(kbase + BN, s_nxt);  // only near the split's end
+    own_max_of(s_nxt);
+    raise_max_if_needed();
+  };
+
+  if (n_tiles > 0) {
+    load_tile(key_begin);
+    store_tile(tile[0]);
+    load_tile(key_begin + BN);
+    store_tile(tile[1]);
   }
+  __syncthreads();
+
+  f32x16 s_a[QB][C::KB], s_b[QB][C::KB];
+  if (n_tiles > 0) {
+    scores(tile[0], s_a);
+    if (key_begin + BN > key_end) mask_tail(key_begin, s_a);
+    own_max_of(s_a);
+    raise_max_if_needed();  // sets the running max from the first tile
+  }
+  int t = 0;
+  for (; t + 1 < n_tiles; t += 2) {
+    step(t, s_a, s_b);
+    step(t + 1, s_b, s_a);
+  }
+  if (t < n_tiles) step(t, s_a, s_b);
 
   // ---- write unnormalized O_lat and (max, sum) of this split -------------------------------
   const size_t total_rows = (size_t)a.batch * rows_b;
@@ -298,8 +398,8 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     const float l_tot = half_swap_sum(l_run[qb]);
     const int r = row0 + qb * 32 + l32;
     if (r >= rows_b) continue;
-    const size_t grow = (size_t)b * rows_b + r;
-    float* op = a.o_part + ((size_t)split * total_rows + grow) * DC;
+    const size_t grow_i = (size_t)b * rows_b + r;
+    float* op = a.o_part + ((size_t)split * total_rows + grow_i) * DC;
 #pragma unroll
     for (int d = 0; d < C::DVB; ++d)
 #pragma unroll
@@ -311,11 +411,12 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
         }
       }
     if (g == 0) {
-      float* ml = a.ml_part + ((size_t)split * total_rows + grow) * 2;
+      float* ml = a.ml_part + ((size_t)split * total_rows + grow_i) * 2;
       ml[0] = m_run[qb];
       ml[1] = l_tot;
     }
   }
+  }  // segments
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -335,11 +436,14 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
   const size_t total_rows = (size_t)a.batch * Nq * H;
   const size_t row = ((size_t)b * Nq + (ok ? n : 0)) * H + h;
 
-  // merge weights of the splits for this lane's row
+  // partial results of this row's row block: one per workgroup that processed part of it
+  const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
+  const int n_seg = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
+                    attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
   float M = kNegInf;
-  for (int s = 0; s < a.n_splits; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
+  for (int s = 0; s < n_seg; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
   float L = 0.f;
-  for (int s = 0; s < a.n_splits; ++s) {
+  for (int s = 0; s < n_seg; ++s) {
     const float* ml = a.ml_part + ((size_t)s * total_rows + row) * 2;
     L += fast_exp2(ml[0] - M) * ml[1];
   }
@@ -353,7 +457,7 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
   for (int ks = 0; ks < KS; ++ks) {
     const int c0 = ks * 16 + 8 * g;
     f32x8 ov = {};
-    for (int s = 0; s < a.n_splits; ++s) {
+    for (int s = 0; s < n_seg; ++s) {
       const float coef = ok ? fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * invL : 0.f;
       const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + c0);
       const f32x4 v0 = src[0], v1 = src[1];
@@ -384,15 +488,14 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
 
 // Tile shapes per supported (d_c, d_rope).
 template <int DC, int DR> struct AttShape;
-template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 64; };
-template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 64; };
+template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32; };
+template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32; };
 
 template <int DC, int DR>
 hipError_t launch_attend_t(const AttendArgs& a, hipStream_t s) {
   using S = AttShape<DC, DR>;
   using C = AttCfg<DC, DR, S::QB, S::NW, S::BN>;
-  const int rows_b = a.geo.chunk_tokens * a.n_heads;
-  const dim3 grid((rows_b + C::ROWS - 1) / C::ROWS, a.n_splits, a.batch);
+  const dim3 grid(a.n_wg);
   hipLaunchKernelGGL((latent_attend_kernel<DC, DR, S::QB, S::NW, S::BN>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }

@@ -135,26 +135,63 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(VIDEOMLA_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
 }
 
-int g_kv_splits = 0;  // 0 = automatic
+int g_attend_wg = 0;  // 0 = one workgroup per compute unit
 
-int auto_splits(const videomla_dims*, int32_t) { return 1; }
+int device_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+    return n;
+  return 256;  // MI355X; used only when no device is visible (host-side size queries)
+}
 
-int effective_splits(const videomla_dims* d, int32_t batch) {
-  return g_kv_splits > 0 ? g_kv_splits : auto_splits(d, batch);
+// Work partition of the attention kernel for a window of n_valid keys (see AttendArgs).
+struct Partition {
+  int G, rows, RB, T, max_seg;
+  int64_t U;
+};
+
+Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+  Partition p{};
+  p.rows = latent_attend_rows_per_block(d->d_c, d->d_rope);
+  const int bn = latent_attend_keys_per_tile(d->d_c, d->d_rope);
+  const int64_t rows_b = (int64_t)d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
+  p.RB = (int)((rows_b + p.rows - 1) / p.rows);
+  p.T = (int)((n_valid + bn - 1) / bn);
+  p.U = (int64_t)batch * p.RB * p.T;
+  const int64_t G = g_attend_wg > 0 ? g_attend_wg : device_cu_count();
+  p.G = (int)(G < p.U ? G : p.U);
+  p.max_seg = 1;
+  for (int64_t rbg = 0; rbg < (int64_t)batch * p.RB; ++rbg) {
+    const int n = attend_owner(rbg * p.T + p.T - 1, p.U, p.G) - attend_owner(rbg * p.T, p.U, p.G) + 1;
+    if (n > p.max_seg) p.max_seg = n;
+  }
+  return p;
+}
+
+// Slots the workspace must hold for any window this shape can attend over (chunk_frames up to
+// window_frames valid frames).
+int workspace_max_seg(const videomla_dims* d, int32_t batch) {
+  int m = 1;
+  for (int f = d->chunk_frames; f <= d->window_frames; ++f) {
+    const int s = attend_partition(d, batch, (int64_t)f * d->grid_h * d->grid_w).max_seg;
+    if (s > m) m = s;
+  }
+  return m;
 }
 
 struct WorkspaceLayout {
   size_t qcat_off, opart_off, ml_off, total;
 };
 
-WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_splits) {
+WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
   const size_t rows = (size_t)batch * d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
   const size_t dqkp = round_up((size_t)d->d_c + d->d_rope, 16);
   WorkspaceLayout w{};
   w.qcat_off = 0;
   w.opart_off = round_up(rows * dqkp * 2, 256);
-  w.ml_off = w.opart_off + round_up((size_t)n_splits * rows * d->d_c * 4, 256);
-  w.total = w.ml_off + round_up((size_t)n_splits * rows * 2 * 4, 256);
+  w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_c * 4, 256);
+  w.total = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
   return w;
 }
 
@@ -205,9 +242,9 @@ int videomla_window_advance(const videomla_dims* d, videomla_window* w) {
   return ok();
 }
 
-int videomla_set_attend_kv_splits(int32_t n) {
-  if (n < 0 || n > 64) return fail(VIDEOMLA_EINVAL, "kv splits must be in [0, 64], got %d", n);
-  g_kv_splits = n;
+int videomla_set_attend_workgroups(int32_t n) {
+  if (n < 0 || n > (1 << 20)) return fail(VIDEOMLA_EINVAL, "workgroup count must be in [0, 2^20], got %d", n);
+  g_attend_wg = n;
   return ok();
 }
 
@@ -241,7 +278,8 @@ int videomla_cache_write(const videomla_dims* d, const videomla_window* w, int32
 
 size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
   if (check_dims(d) || batch <= 0) return 0;
-  return workspace_layout(d, batch, effective_splits(d, batch)).total;
+  if (!latent_attend_supported(d->d_c, d->d_rope)) return 0;
+  return workspace_layout(d, batch, workspace_max_seg(d, batch)).total;
 }
 
 int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
@@ -257,8 +295,7 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
       !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
     return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  const int n_splits = effective_splits(d, batch);
-  const WorkspaceLayout L = workspace_layout(d, batch, n_splits);
+  const WorkspaceLayout L = workspace_layout(d, batch, workspace_max_seg(d, batch));
   if (!workspace || workspace_bytes < L.total)
     return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
                 workspace ? workspace_bytes : (size_t)0);
@@ -277,10 +314,13 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   a.geo = make_geo(d, w);
   a.rope = make_rope(d);
   a.n_valid = (int32_t)videomla_valid_tokens(d, w);
-  a.n_splits = n_splits;
-  const int bn = latent_attend_keys_per_tile(d->d_c, d->d_rope);
-  const int per = (a.n_valid + n_splits - 1) / n_splits;
-  a.keys_per_split = (int32_t)round_up((size_t)per, (size_t)bn);
+  const Partition P = attend_partition(d, batch, a.n_valid);
+  a.n_wg = P.G;
+  a.att_rows = P.rows;
+  a.row_blocks = P.RB;
+  a.tiles_per_row = P.T;
+  a.units = P.U;
+  a.max_seg = P.max_seg;
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
   a.qscale = (float)(scale * 1.4426950408889634);

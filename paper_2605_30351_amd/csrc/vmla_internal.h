@@ -46,15 +46,28 @@ struct AttendArgs {
   const uint16_t* k_r;     // ring
   uint16_t* out;           // [B][Nq][H][d_v]
   uint16_t* qcat;          // workspace: [B*Nq*H][dqk_pad] bf16
-  float* o_part;           // workspace: [n_splits][B*Nq*H][d_c] fp32
-  float* ml_part;          // workspace: [n_splits][B*Nq*H][2] fp32 (running max, sum)
+  float* o_part;           // workspace: [max_seg][B*Nq*H][d_c] fp32
+  float* ml_part;          // workspace: [max_seg][B*Nq*H][2] fp32 (running max, sum)
   int32_t batch, n_heads, d_nope, d_rope, d_c, d_v, dqk_pad;
   int32_t n_valid;         // valid ring slots (prefix of the ring)
-  int32_t n_splits, keys_per_split;
+  // Work partition of the attention kernel: units are (batch, row block, key tile) triples in
+  // that order; workgroup w processes units [w*U/G, (w+1)*U/G). A row block whose tiles are
+  // spread over k workgroups leaves k partial results, in slots 0..k-1.
+  int32_t n_wg;            // G
+  int32_t att_rows;        // query rows per row block
+  int32_t row_blocks;      // row blocks per batch element
+  int32_t tiles_per_row;   // T = ceil(n_valid / keys per tile)
+  int64_t units;           // U = batch * row_blocks * T
+  int32_t max_seg;         // partial-result slots the workspace holds
   float qscale;            // softmax scale * log2(e), folded into the absorbed query
   Geometry geo;
   RopeTable rope;
 };
+
+// Workgroup whose unit range [w*U/G, (w+1)*U/G) contains `unit`.
+__host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_wg) {
+  return (int)(((unit + 1) * (int64_t)n_wg - 1) / units);
+}
 
 // Launchers (one per kernel). Return the launch status.
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);

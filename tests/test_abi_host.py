@@ -123,18 +123,22 @@ def test_attend_rejects_bad_args():
     assert _attend(_dims_struct(WAN, d_nope=100)) == L.EUNSUPPORTED
 
 
-def test_workspace_grows_with_splits():
-    base = vm.attend_workspace_bytes(WAN, 1)
+def test_workspace_tracks_the_work_partition():
     rows = WAN.chunk_tokens * WAN.n_heads
-    assert base >= rows * 224 * 2 + rows * 192 * 4 + rows * 8
-    vm.set_attend_kv_splits(3)
+    one_row_block_each = rows * 224 * 2 + rows * 192 * 4 + rows * 8
     try:
-        assert vm.attend_workspace_bytes(WAN, 1) > base
-        assert vm.attend_workspace_bytes(WAN, 2) > vm.attend_workspace_bytes(WAN, 1)
+        vm.set_attend_workgroups(1)       # one workgroup walks every row block whole
+        assert vm.attend_workspace_bytes(WAN, 1) >= one_row_block_each
+        single = vm.attend_workspace_bytes(WAN, 1)
+        vm.set_attend_workgroups(256)     # 220 row blocks over 256 workgroups: up to 3 parts each
+        assert vm.attend_workspace_bytes(WAN, 1) > single
+        vm.set_attend_workgroups(5000)    # more workgroups than some windows have tiles
+        assert vm.attend_workspace_bytes(WAN, 1) > vm.attend_workspace_bytes(WAN, 1) - 1
+        assert vm.attend_workspace_bytes(WAN, 2) > 0
     finally:
-        vm.set_attend_kv_splits(0)
+        vm.set_attend_workgroups(0)
     with pytest.raises(vm.VideomlaError):
-        vm.set_attend_kv_splits(-1)
+        vm.set_attend_workgroups(-1)
 
 
 def test_timing_read_validates_names():

@@ -8,12 +8,14 @@ exceeds one ulp only for values within about 2^-16 of zero); slots are bit-exact
 outside the written frames is bitwise unchanged; attention outputs satisfy max-abs <= 2e-2,
 mean-abs <= 2e-3 and relative L2 <= 1e-2.
 
-Peaked-softmax variants (queries x4) have outputs of order one instead of order 1e-2, so their
-absolute bars are scaled by the output magnitude. The path rounds six times to bf16 (query,
-latent, RoPE key, probabilities, merged latent, output; unit roundoff u = 2^-9), and rounding
-the query and the cached key moves each score by about u|s|, which the softmax turns into
-relative weight errors of the same size; with |s| of a few units in the peaked case the bars
-are max|err| <= 8u * max|out| and mean|err| <= 4u * mean|out|, with the same relative-L2 bar.
+Where outputs are of order one (the tiny shapes, the peaked-softmax variants with queries x4)
+an absolute 2e-2 is about one bf16 ulp of the output itself, so the bars are the larger of the
+absolute ones and bars scaled by the output magnitude. The path rounds six times to bf16
+(query, latent, RoPE key, probabilities, merged latent, output; unit roundoff u = 2^-9), and
+rounding the query and the cached key moves each score by about u|s|, which the softmax turns
+into relative weight errors of the same size: max|err| <= max(2e-2, 8u max|out|) and
+mean|err| <= max(2e-3, 4u mean|out|), always with the relative-L2 bar. At the Wan shape the
+outputs stay below 0.4, so the absolute bars are the binding ones there.
 """
 import numpy as np
 import pytest
@@ -33,7 +35,7 @@ def vm():
     ensure_built()
     import paper_2605_30351_amd as m
     yield m
-    m.set_attend_kv_splits(0)
+    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -101,11 +103,11 @@ class Layer:
 U_BF16 = 2.0 ** -9
 
 
-def assert_attention_close(got, want, label="", scaled=False):
+def assert_attention_close(got, want, label=""):
     err = np.abs(got - want)
     rel = np.linalg.norm(got - want) / np.linalg.norm(want)
-    max_bar = 8 * U_BF16 * np.abs(want).max() if scaled else ATOL_MAX
-    mean_bar = 4 * U_BF16 * np.abs(want).mean() if scaled else ATOL_MEAN
+    max_bar = max(ATOL_MAX, 8 * U_BF16 * np.abs(want).max())
+    mean_bar = max(ATOL_MEAN, 4 * U_BF16 * np.abs(want).mean())
     msg = (f"{label}: max {err.max():.3e} (bar {max_bar:.2e}) mean {err.mean():.3e} "
            f"(bar {mean_bar:.2e}) relL2 {rel:.3e} |out| max {np.abs(want).max():.3e} "
            f"mean {np.abs(want).mean():.3e}")
@@ -142,7 +144,7 @@ def check_written_chunk(layer, fe, before_c, before_k):
 
 
 # -------------------------------------------------------------------------------------------
-# Tiny configuration: every write, partial and wrapped windows, batch 2, key splits
+# Tiny configuration: every write, partial and wrapped windows, batch 2, work partitions
 # -------------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("norm", [True, False])
@@ -155,13 +157,13 @@ def test_tiny_rollout_write_and_attend(vm, norm):
         layer.write(fe)
         for e, n in check_written_chunk(layer, fe, before_c, before_k):
             exact, total = exact + e, total + n
-        for splits in (1, 2, 5):
-            vm.set_attend_kv_splits(splits)
+        for wg in (1, 2, 3, 0):
+            vm.set_attend_workgroups(wg)
             got = layer.attend(fe)
             for b in range(2):
                 want = O.chunk_attention(inp, b, fe)
-                assert_attention_close(got[b], want, f"tiny fe={fe} b={b} splits={splits}")
-        vm.set_attend_kv_splits(0)
+                assert_attention_close(got[b], want, f"tiny fe={fe} b={b} workgroups={wg}")
+        vm.set_attend_workgroups(0)
     assert exact / total >= 0.999, f"{exact}/{total} exactly rounded"
 
 
@@ -171,7 +173,7 @@ def test_tiny_peaked_softmax(vm):
     for fe in range(6):
         layer.write(fe)
     got = layer.attend(5)
-    assert_attention_close(got[0], O.chunk_attention(inp, 0, 5), "tiny peaked", scaled=True)
+    assert_attention_close(got[0], O.chunk_attention(inp, 0, 5), "tiny peaked")
 
 
 # -------------------------------------------------------------------------------------------
@@ -213,10 +215,10 @@ def test_wan_attend_full_window(vm, variant):
     got = layer.attend(21)
     rows = _sample_rows(dims.chunk_tokens)
     want = O.chunk_attention(inp, 0, 21, rows=rows)
-    assert_attention_close(got[0][rows], want, f"wan attend {variant}", scaled=variant == "peaked")
+    assert_attention_close(got[0][rows], want, f"wan attend {variant}")
 
 
-def test_wan_attend_partial_windows_and_splits(vm):
+def test_wan_attend_partial_windows_and_work_partitions(vm):
     inp = make_layer_inputs(WAN, seed=6, n_frames=21)
     layer = Layer(vm, inp)
     rows = _sample_rows(WAN.chunk_tokens, k=12, seed=1)
@@ -225,12 +227,12 @@ def test_wan_attend_partial_windows_and_splits(vm):
     assert_attention_close(got[0][rows], O.chunk_attention(inp, 0, 0, rows=rows), "wan fe=0")
     for fe in range(3, 19, 3):
         layer.write(fe)
-    for splits in (1, 3):
-        vm.set_attend_kv_splits(splits)
-        got = layer.attend(18)  # exactly 21 frames, no wrap yet
-        assert_attention_close(got[0][rows], O.chunk_attention(inp, 0, 18, rows=rows),
-                               f"wan fe=18 splits={splits}")
-    vm.set_attend_kv_splits(0)
+    want = O.chunk_attention(inp, 0, 18, rows=rows)  # exactly 21 frames, no wrap yet
+    for wg in (0, 1, 37, 300):
+        vm.set_attend_workgroups(wg)
+        got = layer.attend(18)
+        assert_attention_close(got[0][rows], want, f"wan fe=18 workgroups={wg}")
+    vm.set_attend_workgroups(0)
 
 
 def test_wan_attend_is_deterministic(vm):
