@@ -90,7 +90,7 @@ typedef struct videomla_window {
  * Token (f, y, x) is stored at slot ((f mod window_frames) * grid_h + y) * grid_w + x, so the
  * chunk overwrites the oldest frames; every other slot is left untouched. Calling it again
  * before videomla_window_advance (the next denoising step) overwrites the same slots.
- * Requires d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0, d_c + d_rope <= 512.
+ * Requires d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0, d_c + d_rope <= 288.
  */
 int videomla_cache_write(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                          const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,

@@ -311,34 +311,34 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
   // One pipelined step. s_cur holds tile t's scores, already masked, with m_run high enough
   // for them. Block A: scores of tile t+1 (MFMA) and tile t's exponentials (VALU). Block B: PV
   // of tile t (MFMA) and staging of tile t+2. After the barrier: masking and max of tile t+1.
-  auto step = [&](int t, f32x16 (&s_cur)[QB][C::KB], f32x16 (&s_nxt)[QB][C::KB]) {
+  auto step = [&](int t, f32x16 (&s_cur)[QB][C::KB], f32x16 (&s_nxt)[QB][C::KB],
+                  const uint16_t* cur, const uint16_t* nxt, uint16_t* stg) {
     const int kbase = key_begin + t * BN;
-    const uint16_t* cur = tile[t % C::NBUF];
-    const uint16_t* nxt = tile[(t + 1) % C::NBUF];
 
     // ---- block A: scores of tile t+1 and exponentials of tile t ----------------------------
     // The two waves sharing a SIMD (wave w and w + NW/2) take the two halves in opposite
     // order, so one's exponentials run while the other's score MFMAs do.
     load_tile(kbase + 2 * BN);
     bf16x8 pb[QB][2 * C::KB];
+    // The row sum is taken over the bf16-rounded probabilities, the same values the PV MFMA
+    // multiplies, so numerator and denominator see identical weights.
     auto exps = [&]() {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
-        float acc = 0.f;
+        float acc = l_run[qb];
 #pragma unroll
         for (int kb = 0; kb < C::KB; ++kb) {
           f32x16 p;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            p[r] = fast_exp2(s_cur[qb][kb][r] - m_run[qb]);
-            acc += p[r];
-          }
+          for (int r = 0; r < 16; ++r) p[r] = fast_exp2(s_cur[qb][kb][r] - m_run[qb]);
           const f32x8 lo = {p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]};
           const f32x8 hi = {p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]};
           pb[qb][2 * kb] = to_bf16x8(lo);
           pb[qb][2 * kb + 1] = to_bf16x8(hi);
+          acc = sum_bf16x8(pb[qb][2 * kb], acc);
+          acc = sum_bf16x8(pb[qb][2 * kb + 1], acc);
         }
-        l_run[qb] += acc;
+        l_run[qb] = acc;
       }
     };
     if (wave < NW / 2) {
@@ -350,19 +350,19 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     }
 
     // ---- block B ---------------------------------------------------------------------------
+    const lds_u16* vb = as_lds(cur) + (4 * g + tr_row) * C::STRIDE + tr_col;
 #pragma unroll
     for (int kk = 0; kk < 2 * C::KB; ++kk) {
-      const int key0 = kk * 16 + 4 * g + tr_row;
 #pragma unroll
       for (int d = 0; d < C::DVB; ++d) {
-        const i16x4 lo = lds_read_tr(&cur[key0 * C::STRIDE + d * 32 + tr_col]);
-        const i16x4 hi = lds_read_tr(&cur[(key0 + 8) * C::STRIDE + d * 32 + tr_col]);
+        const i16x4 lo = lds_read_tr(vb + kk * 16 * C::STRIDE + d * 32);
+        const i16x4 hi = lds_read_tr(vb + (kk * 16 + 8) * C::STRIDE + d * 32);
         const bf16x8 v = join_bf16x8(lo, hi);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) o[qb][d] = mfma32(v, pb[qb][kk], o[qb][d]);
       }
     }
-    store_tile(tile[(t + 2) % C::NBUF]);
+    store_tile(stg);
     __syncthreads();
     if (kbase + 2 * BN > key_end) mask_tail(kbase + BN, s_nxt);  // only near the split's end
     own_max_of(s_nxt);
@@ -384,12 +384,18 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     own_max_of(s_a);
     raise_max_if_needed();  // sets the running max from the first tile
   }
+  // tile t lives in buffer t mod 3; the three buffer pointers rotate with the tiles
+  uint16_t *pc = tile[0], *pn = tile[1], *ps = tile[2];
   int t = 0;
   for (; t + 1 < n_tiles; t += 2) {
-    step(t, s_a, s_b);
-    step(t + 1, s_b, s_a);
+    step(t, s_a, s_b, pc, pn, ps);
+    step(t + 1, s_b, s_a, pn, ps, pc);
+    uint16_t* tmp = pc;
+    pc = ps;
+    ps = pn;
+    pn = tmp;
   }
-  if (t < n_tiles) step(t, s_a, s_b);
+  if (t < n_tiles) step(t, s_a, s_b, pc, pn, ps);
 
   // ---- write unnormalized O_lat and (max, sum) of this split -------------------------------
   const size_t total_rows = (size_t)a.batch * rows_b;

@@ -1,122 +1,189 @@
 // Fused cache write: compress (Eq. 1), optional RMSNorm of the latent, decoupled RoPE key
 // (Eq. 5) rotated at the token's absolute (f, y, x), and FIFO placement into the ring.
 //
-// One workgroup takes 32 chunk tokens of one batch element and all d_c + d_rope outputs. The
-// contraction over d_model is split four ways across the waves, so x is read once per
-// workgroup and the weight panel once per workgroup. Each wave computes
-// out^T[o][token] = W[o][:] . x[token][:] with MFMA 32x32x16 (A = weight rows, B = x rows), the
-// four partial products are summed in LDS, and the epilogue normalizes, rotates, rounds to bf16
-// and scatters each token's row to its ring slot with 16-byte stores.
+// One workgroup takes 32 chunk tokens of one batch element and all d_c + d_rope outputs:
+// out^T[o][token] = W[o][:] . x[token][:] with MFMA 32x32x16 (A = rows of [W_DKV; W_KR],
+// B = x rows). The contraction over d_model streams through a ring of kStages LDS stages of
+// kKC columns each, filled by direct global-to-LDS loads (no registers, several chunks in
+// flight) in an XOR-swizzled layout that makes the MFMA operand reads conflict-free. The four
+// waves share every staged chunk and split the 32-row output blocks between them. The epilogue
+// combines the RMSNorm sum of squares across waves in LDS, normalizes, rotates the RoPE block,
+// rounds to bf16 and stores each token's values to its ring slot.
 #include "vmla_device.h"
 
 namespace vmla {
 namespace {
 
-constexpr int kTok = 32;      // tokens per workgroup
-constexpr int kWaves = 4;     // waves per workgroup (split of the d_model contraction)
+constexpr int kTok = 32;     // tokens per workgroup
+constexpr int kWaves = 4;
+constexpr int kKC = 64;      // contraction columns per stage: 8 chunks of 16 B per row
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct global-to-LDS load of 16 B per lane: lane l's bytes land at LDS address lds_base + 16 l.
+// Issued as inline assembly so that the compiler does not treat it as an LDS write it must wait
+// for before every LDS read and barrier; the callers order it with explicit vmcnt waits (the
+// load counts as one outstanding vector-memory operation until its data is in LDS).
+__device__ __forceinline__ void lds_dma16(const uint16_t* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_void*)(p);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Position (16 B units) of chunk c of staged row r: row-major with 8 chunks per row, the chunk
+// index XOR-ed with (r / 2) mod 8, so 16 consecutive rows read at one chunk hit distinct banks.
+__device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
 
 template <int NB>  // 32-wide output blocks covering d_c + d_rope
 __global__ __launch_bounds__(kWaves * 64) void cache_write_kernel(const WriteArgs a) {
-  constexpr int OUT_STRIDE = NB * 32 + 4;
-  __shared__ __attribute__((aligned(16))) float red[kTok][OUT_STRIDE];
+  constexpr int ROWS = NB * 32 + kTok;        // staged rows: weight rows, then x rows
+  constexpr int INSTR = ROWS * 8 / 64;        // 1 KB load instructions per stage
+  constexpr int PER_WAVE = (INSTR + kWaves - 1) / kWaves;
+  constexpr int MAXB = (NB + kWaves - 1) / kWaves;  // output blocks per wave
+  // LDS stages (kStages - 1 chunks in flight): four while they fit in 150 KB, else three
+  constexpr int kStages = ROWS * kKC * 2 * 4 <= 150 * 1024 ? 4 : 3;
+  static_assert(ROWS % 8 == 0, "stage is a whole number of 1 KB loads");
+  static_assert(INSTR % kWaves == 0, "every wave issues the same number of loads per stage");
+  __shared__ __attribute__((aligned(16))) uint16_t stage[kStages][ROWS * kKC];
+  __shared__ float ssq_part[kWaves][kTok];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches, SGPR m0
   const int g = lane >> 5, l32 = lane & 31;
   const int b = blockIdx.y;
   const int n0 = blockIdx.x * kTok;
   const int dm = a.d_model, DC = a.d_c, DR = a.d_rope;
   const int n_tok = a.geo.chunk_tokens;
 
-  // A operand rows: output o = ob*32 + l32 reads row o of [W_DKV; W_KR] (zero past the end).
-  const uint16_t* wrow[NB];
+  // Global source of each of this wave's load instructions (instruction j = wave + kWaves*i):
+  // its lane covers LDS position p = j*64 + lane = (row r, swizzled chunk); rows past the
+  // weights or the chunk read a valid row whose results are discarded.
+  const uint16_t* src[PER_WAVE];
 #pragma unroll
-  for (int ob = 0; ob < NB; ++ob) {
-    const int o = ob * 32 + l32;
-    wrow[ob] = o < DC ? a.w_dkv + (size_t)o * dm
-                      : (o < DC + DR ? a.w_kr + (size_t)(o - DC) * dm : nullptr);
-  }
-  const int n_mine = n0 + l32;
-  const bool tok_ok = n_mine < n_tok;
-  const uint16_t* xrow = a.x + ((size_t)b * n_tok + (tok_ok ? n_mine : 0)) * dm;
-
-  f32x16 acc[NB];
-#pragma unroll
-  for (int ob = 0; ob < NB; ++ob) acc[ob] = f32x16{};
-
-  const int kq = dm / kWaves;
-  const int kb = wave * kq;
-  const u32x4 zero = {0, 0, 0, 0};
-#pragma unroll 2
-  for (int k = kb; k < kb + kq; k += 16) {
-    const bf16x8 bx = as_bf16x8(tok_ok ? ldg16(xrow + k + g * 8) : zero);
-#pragma unroll
-    for (int ob = 0; ob < NB; ++ob) {
-      const bf16x8 aw = as_bf16x8(wrow[ob] ? ldg16(wrow[ob] + k + g * 8) : zero);
-      acc[ob] = mfma32(aw, bx, acc[ob]);
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int j = wave + kWaves * i;
+    const int p = (j < INSTR ? j : 0) * 64 + lane;
+    const int r = p >> 3, cs = p & 7;
+    const int c = cs ^ ((r >> 1) & 7);  // logical chunk stored at this position
+    const uint16_t* row;
+    if (r < NB * 32) {
+      row = r < DC ? a.w_dkv + (size_t)r * dm
+                   : (r < DC + DR ? a.w_kr + (size_t)(r - DC) * dm : a.w_dkv);
+    } else {
+      const int n = n0 + (r - NB * 32);
+      row = a.x + ((size_t)b * n_tok + (n < n_tok ? n : 0)) * dm;
     }
+    src[i] = row + c * 8;
   }
+  auto issue = [&](int chunk) {
+    uint16_t* st = stage[chunk % kStages];
+#pragma unroll
+    for (int i = 0; i < PER_WAVE; ++i) {
+      const int j = wave + kWaves * i;
+      if (INSTR % kWaves == 0 || j < INSTR)
+        lds_dma16(src[i] + chunk * kKC, __builtin_amdgcn_readfirstlane(lds_addr(st + j * 512)));
+    }
+  };
 
-  // Sum the four partial products in LDS, one wave at a time.
-#pragma unroll 1
-  for (int w = 0; w < kWaves; ++w) {
-    if (wave == w) {
+  f32x16 acc[MAXB];
 #pragma unroll
-      for (int ob = 0; ob < NB; ++ob) {
+  for (int m = 0; m < MAXB; ++m) acc[m] = f32x16{};
+
+  const int nchunks = dm / kKC;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          f32x4* dst = reinterpret_cast<f32x4*>(&red[l32][ob * 32 + 8 * i + 4 * g]);
-          const f32x4 v = {acc[ob][4 * i], acc[ob][4 * i + 1], acc[ob][4 * i + 2], acc[ob][4 * i + 3]};
-          *dst = w == 0 ? v : *dst + v;
-        }
+  for (int c = 0; c < kStages - 1; ++c)
+    if (c < nchunks) issue(c);
+  for (int i = 0; i < nchunks; ++i) {
+    // chunk i has landed once at most (kStages - 2) later chunks are still outstanding
+    if (i + kStages - 2 < nchunks) wait_vmcnt<(kStages - 2) * PER_WAVE>();
+    else wait_vmcnt<0>();
+    __syncthreads();  // all waves' parts of chunk i are in LDS; chunk i-1 is no longer read
+    if (i + kStages - 1 < nchunks) issue(i + kStages - 1);
+    const uint16_t* st = stage[i % kStages];
+#pragma unroll
+    for (int ks = 0; ks < kKC / 16; ++ks) {
+      const int c = ks * 2 + g;
+      const bf16x8 bx = as_bf16x8(*reinterpret_cast<const u32x4*>(&st[swz(NB * 32 + l32, c) * 8]));
+#pragma unroll
+      for (int m = 0; m < MAXB; ++m) {
+        // a wave with fewer blocks repeats the last one (discarded) instead of branching
+        const int ob = wave + kWaves * m < NB ? wave + kWaves * m : NB - 1;
+        const bf16x8 aw =
+            as_bf16x8(*reinterpret_cast<const u32x4*>(&st[swz(ob * 32 + l32, c) * 8]));
+        acc[m] = mfma32(aw, bx, acc[m]);
       }
     }
-    __syncthreads();
   }
 
-  // Epilogue: 8 threads per token.
-  const int tok = tid >> 3, sub = tid & 7;
-  const int n = n0 + tok;
-  const int oct_c = DC / 8;
+  // ---- epilogue: lane holds token l32, outputs ob*32 + 8i + 4g + j of its blocks ----------
   float ss = 0.f;
-  for (int ch = sub; ch < oct_c; ch += 8) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float v = red[tok][ch * 8 + e];
-      ss += v * v;
+  for (int m = 0; m < MAXB; ++m) {
+    const int ob = wave + kWaves * m;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int o = ob * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+      if (ob < NB && o < DC) ss += acc[m][r] * acc[m][r];
     }
   }
-  ss += __shfl_xor(ss, 1, 8);
-  ss += __shfl_xor(ss, 2, 8);
-  ss += __shfl_xor(ss, 4, 8);
-  const float rstd = a.gamma ? rsqrtf(ss / (float)DC + a.eps) : 1.f;
-  if (n >= n_tok) return;
+  ss = half_swap_sum(ss);
+  if (g == 0) ssq_part[wave][l32] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) tot += ssq_part[w][l32];
+  const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
 
+  const int n = n0 + l32;
+  if (n >= n_tok) return;
   const TokenPos pos = token_pos(a.geo, n);
   const int64_t slot = ring_slot(a.geo, pos);
   uint16_t* cdst = a.c_kv + ((size_t)b * a.geo.ring_tokens + slot) * DC;
-  for (int ch = sub; ch < oct_c; ch += 8) {
-    f32x8 v;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float c = red[tok][ch * 8 + e] * rstd;
-      if (a.gamma) c *= bf16_bits_to_f32(a.gamma[ch * 8 + e]);
-      v[e] = c;
-    }
-    stg16(cdst + ch * 8, as_u32x4(to_bf16x8(v)));
-  }
   uint16_t* kdst = a.k_r + ((size_t)b * a.geo.ring_tokens + slot) * DR;
-  for (int p = sub; p < DR / 2; p += 8) {
-    float u = red[tok][DC + 2 * p], v = red[tok][DC + 2 * p + 1];
-    rope_rotate(a.rope, p, pos, u, v);
-    const uint32_t packed = (uint32_t)to_bf16_bits(u) | ((uint32_t)to_bf16_bits(v) << 16);
-    *reinterpret_cast<uint32_t*>(kdst + 2 * p) = packed;
+#pragma unroll
+  for (int m = 0; m < MAXB; ++m) {
+    const int ob = wave + kWaves * m;
+    if (ob >= NB) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int o = ob * 32 + 8 * i + 4 * g;  // first of 4 consecutive outputs
+      float v[4] = {acc[m][4 * i], acc[m][4 * i + 1], acc[m][4 * i + 2], acc[m][4 * i + 3]};
+      if (o + 4 <= DC) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] *= rstd;
+          if (a.gamma) v[e] *= bf16_bits_to_f32(a.gamma[o + e]);
+        }
+        const f32x4 fv = {v[0], v[1], v[2], v[3]};
+        *reinterpret_cast<bf16x4*>(cdst + o) = to_bf16x4(fv);
+      } else if (o >= DC && o + 4 <= DC + DR) {
+        const int ch = o - DC;  // channels ch .. ch+3 = RoPE pairs ch/2 and ch/2 + 1
+        rope_rotate(a.rope, ch / 2, pos, v[0], v[1]);
+        rope_rotate(a.rope, ch / 2 + 1, pos, v[2], v[3]);
+        const f32x4 fv = {v[0], v[1], v[2], v[3]};
+        *reinterpret_cast<bf16x4*>(kdst + ch) = to_bf16x4(fv);
+      }
+    }
   }
-  if (a.slots && b == 0 && sub == 0) a.slots[n] = (int32_t)slot;
+  if (a.slots && b == 0 && wave == 0 && g == 0) a.slots[n] = (int32_t)slot;
 }
 
 }  // namespace
 
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s) {
+  // validated by the caller: d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0,
+  // d_c + d_rope <= 288
   const int nb = (a.d_c + a.d_rope + 31) / 32;
   const dim3 grid((a.geo.chunk_tokens + kTok - 1) / kTok, a.batch);
   const dim3 block(kWaves * 64);

@@ -43,15 +43,22 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }
 
+typedef __attribute__((address_space(3))) uint16_t lds_u16;
+
+// Pointer into LDS in the LDS address space (so that constant offsets fold into the
+// instruction's immediate offset).
+__device__ __forceinline__ const lds_u16* as_lds(const uint16_t* p) {
+  return (const lds_u16*)(p);
+}
+
 // LDS transpose read (ds_read_b64_tr_b16). Within each group of 16 lanes, source lane s points
 // at 4 consecutive 16-bit elements M[s][0..3]; result lane i receives M[4e + i/4][i%4],
 // e = 0..3. If source lane s addresses row (R0 + s/4), columns C0 + 4(s%4) .. +4 of a row-major
 // matrix, lane i receives column C0 + i of rows R0 .. R0+3.
-__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* lds_ptr) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4*)(reinterpret_cast<__attribute__((address_space(3))) uint16_t*>(
-          (__attribute__((address_space(3))) void*)(lds_ptr))));
+__device__ __forceinline__ i16x4 lds_read_tr(const lds_u16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
 }
+__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) { return lds_read_tr(as_lds(p)); }
 
 __device__ __forceinline__ bf16x8 join_bf16x8(i16x4 lo, i16x4 hi) {
   typedef short i16x8 __attribute__((ext_vector_type(8)));
@@ -71,6 +78,18 @@ __device__ __forceinline__ float half_swap_sum(float v) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// acc + sum of the 8 bf16 values of v, accumulated in fp32 (v_dot2 against (1, 1)).
+__device__ __forceinline__ float sum_bf16x8(bf16x8 v, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 pair = {v[2 * i], v[2 * i + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
+  }
+  return acc;
+}
 
 // Absolute position of chunk token n: (f, y, x).
 struct TokenPos {
