@@ -22,8 +22,16 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-MFMA_BF16_PEAK_TFLOPS = 256 * 4096 * 2.4e9 / 1e12   # 2516.6: 256 CUs x 4096 FLOP/clk x 2.4 GHz
-HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X published dense bf16 MFMA peak
+HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
+
+# HBM traffic of one latent_attend launch at this workload, from two rocprofv3 --pmc runs
+# (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only
+# for the kernel source it was measured on (sha256 of the listed files), else reported as null.
+ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
+                              "paper_2605_30351_amd/csrc/vmla_device.h"),
+                  "sha256": "967dab4dd8da36da3087a066eb63e7fb943b2fc59e0f927e8ec64153f7c5b7a9",
+                  "bytes": 959701971}
 
 
 def log(msg):
@@ -45,7 +53,7 @@ def work_model(d, batch=1):
             "write": write_flop, "write_bytes": write_bytes}
 
 
-def cpu_baseline(d, n_rows=2340):
+def cpu_baseline(d, n_rows=4680):
     """The fp64 oracle on the host: window latents from x, then reconstructed-K/V attention for
     a sample of query tokens (all heads). Credited with the algorithmic FLOPs of that sample."""
     import numpy as np
@@ -66,18 +74,49 @@ def cpu_baseline(d, n_rows=2340):
     return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "seconds": dt,
             "sample": (f"fp64 numpy oracle: latents of the 32,760-token window from x, then "
-                       f"explicit per-head K/V attention for {n_rows} of 4,680 query tokens x 12 heads; "
+                       f"explicit per-head K/V attention for {n_rows} of the 4,680 query tokens x 12 heads; "
                        f"credited with the method's algorithmic FLOPs of that sample plus the chunk's "
                        f"cache write; host has {len(os.sched_getaffinity(0))} usable cores")}
+
+
+def source_digest(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def attend_traffic():
+    """Measured HBM bytes per attend launch if the kernel is unchanged since the measurement."""
+    if ATTEND_TRAFFIC["sha256"] is None:
+        return None
+    if source_digest(ATTEND_TRAFFIC["sources"]) != ATTEND_TRAFFIC["sha256"]:
+        return None
+    return ATTEND_TRAFFIC["bytes"]
+
+
+def copy_probe(torch, dev, nbytes=1 << 28, reps=3):
+    """A plain device copy of known size, whose FETCH_SIZE / WRITE_SIZE counters calibrate the
+    counters of the library's kernels (each launch reads and writes nbytes)."""
+    a = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--x-buffers", type=int, default=32)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a 256 MiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -126,16 +165,24 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
+    if args.copy_probe:
+        log("copy probe")
+        copy_probe(torch, dev)
+
     log(f"timing {args.steps} steps")
     vm.timing_enable(True)
     for k in ("cache_write", "q_absorb", "latent_attend", "out_proj"):
         vm.timing_read(k)  # drop anything recorded before the timed region
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    marks[0].record()
     for i in range(args.steps):
         step(i)
+        marks[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
     kernels = {}
     for k in ("cache_write", "q_absorb", "latent_attend", "out_proj"):
         n, tot = vm.timing_read(k)
@@ -159,6 +206,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -191,7 +239,7 @@ def main():
             "peak": round(MFMA_BF16_PEAK_TFLOPS, 1),
             "unit": "TFLOP/s",
             "frac": round(k3_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": attend_traffic(),
         },
     }
     if not args.no_cpu_baseline:
