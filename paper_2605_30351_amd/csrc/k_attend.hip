@@ -111,13 +111,12 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 //   The running max is raised only when a tile's max exceeds it by more than kLazyMax (in
 //   log2 units), so probabilities stay below 2^kLazyMax and the accumulators are rescaled
 //   rarely; the final merge divides by the matching sum, so the result is unchanged.
-//   Tiles are fetched with bounds-checked buffer loads whose range ends at the segment's last
-//   valid key, so keys past it read as zeros without any branch. The (batch, row block, key
-//   tile) units are split evenly over the workgroups (a row block may be shared by two or
-//   three of them), so every CU gets the same amount of work.
+//   Tiles go from global memory straight into LDS (global_load_lds, no registers), two tiles
+//   ahead of their PV step. The (batch, row block, key tile) units are split evenly over the
+//   workgroups (a row block may be shared by two or three of them), so every CU gets the same
+//   amount of work.
 // ---------------------------------------------------------------------------------------------
 constexpr float kLazyMax = 8.0f;
-constexpr int kRawBufferWord3 = 0x00020000;  // raw (untyped) buffer access, 32-bit data format
 
 template <int DC, int DR, int QB, int NW, int BN>
 struct AttCfg {
@@ -126,18 +125,27 @@ struct AttCfg {
   static constexpr int KSTEPS = DQKP / 16;
   static constexpr int DVB = (DC + 31) / 32;
   static constexpr int KB = BN / 32;       // 32-key blocks per tile
-  static constexpr int STRIDE = DQKP + 8;  // elements; +16 B per row against bank conflicts
+  // Tile rows are DQKP elements with no padding; the 16-byte chunks of row r sit at chunk
+  // index XOR ((r / 4) mod 4), which makes the 16-row operand reads of the score MFMA and the
+  // 4-row transpose reads of the PV MFMA hit 16 distinct 4-bank groups each.
+  static constexpr int STRIDE = DQKP;
   static constexpr int NT = NW * 64;
   static constexpr int ROWS = NW * QB * 32;
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
-  static constexpr int CH_C = BN * OCT_C, CH_R = BN * OCT_R;
-  static constexpr int CPT_C = (CH_C + NT - 1) / NT;  // c_kv chunks per thread
-  static constexpr int CPT_R = (CH_R + NT - 1) / NT;  // k_r chunks per thread
+  static constexpr int CPR = DQKP / 8;            // 16-byte chunks per tile row
+  static constexpr int NDMA = BN * CPR / 64;      // 1 KB direct-to-LDS loads per tile
+  static constexpr int DMA_PER_WAVE = (NDMA + NW - 1) / NW;
   static constexpr int TILE = BN * STRIDE;
   static constexpr int NBUF = 3;
   static_assert(DC % 8 == 0 && DR % 8 == 0, "latent and rope widths must be multiples of 8");
   static_assert(BN % 32 == 0, "key tile must be a multiple of 32");
   static_assert(DVB * 32 <= STRIDE, "transpose reads must stay inside a tile row");
+  static_assert(DQKP % 32 == 0, "the swizzle permutes chunks within aligned groups of four");
+  static_assert(BN * CPR % 64 == 0, "a tile is a whole number of 64-lane loads");
+  // element offset of (row r, column c) inside a tile
+  __device__ static constexpr int at(int r, int c) {
+    return r * STRIDE + ((((c >> 3) ^ (r >> 2)) & 3) | ((c >> 3) & ~3)) * 8 + (c & 7);
+  }
 };
 
 template <int DC, int DR, int QB, int NW, int BN>
@@ -146,13 +154,10 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int rows_b = a.geo.chunk_tokens * a.n_heads;
-  if (C::DQKP > C::DQK) {  // zero the pad columns once; staging never writes them
-    for (int r = tid; r < C::NBUF * BN; r += C::NT)
-      for (int c = C::DQK; c < C::DQKP; ++c) tile[r / BN][(r % BN) * C::STRIDE + c] = 0;
-  }
 
   // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
   // tiles of one row block is a segment with its own partial result.
@@ -172,13 +177,31 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
   const int n_tiles = kt1 - kt0;
   __syncthreads();  // the previous segment's LDS tiles are no longer read
 
-  // Bounds-checked views of this batch element's ring, ending at key_end.
-  const int kend = key_end > 0 ? key_end : 0;
-  const __amdgpu_buffer_rsrc_t rs_c = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(a.c_kv + (size_t)b * a.geo.ring_tokens * DC), (short)0, kend * DC * 2, kRawBufferWord3);
-  const __amdgpu_buffer_rsrc_t rs_r = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(a.k_r + (size_t)b * a.geo.ring_tokens * DR), (short)0, kend * DR * 2, kRawBufferWord3);
   const u32x4 zero = {0, 0, 0, 0};
+
+  // Direct global-to-LDS staging. Load instruction j (of NDMA per tile) fills the 64 chunk
+  // slots 64 j .. 64 j + 63 of a tile; this wave issues j = wave + NW i. Each lane fetches the
+  // chunk whose swizzled slot is its own: row r = slot / CPR, logical chunk = physical chunk
+  // with the swizzle undone (c_kv chunks, then k_r chunks, then padding that reads k_r data and
+  // meets the zero padding of q_cat). Rows at or past key_end are clamped to key_end - 1, so
+  // every read stays inside the valid ring and every staged value is finite; their scores
+  // are masked below.
+  const uint16_t* c_base = a.c_kv + (size_t)b * a.geo.ring_tokens * DC;
+  const uint16_t* r_base = a.k_r + (size_t)b * a.geo.ring_tokens * DR;
+  int dma_row[C::DMA_PER_WAVE];
+  const uint16_t* dma_src[C::DMA_PER_WAVE];
+  bool dma_kr[C::DMA_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+    const int j = wave + NW * i;
+    const int slot = (j < C::NDMA ? j : 0) * 64 + lane;
+    const int r = slot / C::CPR, pcn = slot % C::CPR;
+    const int lc = (pcn & ~3) | ((pcn & 3) ^ ((r >> 2) & 3));
+    dma_row[i] = r;
+    dma_kr[i] = lc >= C::OCT_C;
+    dma_src[i] = lc < C::OCT_C ? c_base + lc * 8
+                               : r_base + (lc < C::OCT_C + C::OCT_R ? (lc - C::OCT_C) * 8 : 0);
+  }
 
 
   // queries of this wave, B-operand layout: lane holds row l32, dims ks*16 + 8g .. +8
@@ -202,41 +225,24 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     for (int d = 0; d < C::DVB; ++d) o[qb][d] = f32x16{};
   }
 
-  // Per-thread staging chunks: fixed (row, column) of the tile, so only the tile base moves.
-  u32x4 pre_c[C::CPT_C], pre_r[C::CPT_R];
-  auto load_tile = [&](int k0) {
+  auto dma_tile = [&](int k0, uint16_t* buf) {
+    const uint32_t base = lds_addr(buf);
 #pragma unroll
-    for (int i = 0; i < C::CPT_C; ++i) {
-      const int c = tid + i * C::NT;
-      const uint32_t off = (uint32_t)((k0 + c / C::OCT_C) * DC + (c % C::OCT_C) * 8) * 2u;
-      pre_c[i] = (C::CH_C % C::NT == 0 || c < C::CH_C)
-                     ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs_c, off, 0, 0))
-                     : zero;
-    }
-#pragma unroll
-    for (int i = 0; i < C::CPT_R; ++i) {
-      const int c = tid + i * C::NT;
-      const uint32_t off = (uint32_t)((k0 + c / C::OCT_R) * DR + (c % C::OCT_R) * 8) * 2u;
-      pre_r[i] = (C::CH_R % C::NT == 0 || c < C::CH_R)
-                     ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs_r, off, 0, 0))
-                     : zero;
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const int j = wave + NW * i;
+      if (C::NDMA % NW == 0 || j < C::NDMA) {
+        const int key = min(k0 + dma_row[i], key_end - 1);
+        const uint16_t* src = dma_src[i] + (size_t)key * (dma_kr[i] ? DR : DC);
+        lds_dma16(src, __builtin_amdgcn_readfirstlane(base + 1024u * j));
+      }
     }
   };
-  auto store_tile = [&](uint16_t* buf) {
-#pragma unroll
-    for (int i = 0; i < C::CPT_C; ++i) {
-      const int c = tid + i * C::NT;
-      if (C::CH_C % C::NT == 0 || c < C::CH_C)
-        *reinterpret_cast<u32x4*>(&buf[(c / C::OCT_C) * C::STRIDE + (c % C::OCT_C) * 8]) = pre_c[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::CPT_R; ++i) {
-      const int c = tid + i * C::NT;
-      if (C::CH_R % C::NT == 0 || c < C::CH_R)
-        *reinterpret_cast<u32x4*>(&buf[(c / C::OCT_R) * C::STRIDE + DC + (c % C::OCT_R) * 8]) = pre_r[i];
-    }
-  };
-  // S^T for one tile, both query blocks sharing each K operand read
+  // K operand of step ks: row l32 (+32 kb), chunk 2 ks + g, i.e. C::at() with the XOR folded
+  // into one of two per-lane bases (ks even / odd) so that ks and kb become immediate offsets
+  const int hk = (l32 >> 2) & 3;
+  const int koff_e = l32 * C::STRIDE + ((g ^ hk) << 3);
+  const int koff_o = l32 * C::STRIDE + (((2 + g) ^ hk) << 3) - 16;
+  // S^T for one tile, the query blocks sharing each K operand read
   auto scores = [&](const uint16_t* buf, f32x16 (&s)[QB][C::KB]) {
 #pragma unroll
     for (int kb = 0; kb < C::KB; ++kb) {
@@ -244,8 +250,8 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
       for (int qb = 0; qb < QB; ++qb) s[qb][kb] = f32x16{};
 #pragma unroll
       for (int ks = 0; ks < C::KSTEPS; ++ks) {
-        const bf16x8 k = as_bf16x8(
-            *reinterpret_cast<const u32x4*>(&buf[(kb * 32 + l32) * C::STRIDE + ks * 16 + 8 * g]));
+        const bf16x8 k = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            &buf[((ks & 1) ? koff_o : koff_e) + kb * 32 * C::STRIDE + ks * 16]));
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mfma32(k, q[qb][ks], s[qb][kb]);
       }
@@ -305,8 +311,12 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     }
   };
 
+  // V^T transpose reads: lane addresses row 4g + tr_row (+8 for the upper half, +16 kk) and
+  // column tr_col (+32 d); rows 4g.. have swizzle g, rows 4g+8.. have g+2, for every kk
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int vofs_lo = C::at(4 * g + tr_row, tr_col);
+  const int vofs_hi = C::at(4 * g + tr_row + 8, tr_col);
 
   // One pipelined step. s_cur holds tile t's scores, already masked, with m_run high enough
   // for them. Block A: scores of tile t+1 (MFMA) and tile t's exponentials (VALU). Block B: PV
@@ -318,7 +328,7 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     // ---- block A: scores of tile t+1 and exponentials of tile t ----------------------------
     // The two waves sharing a SIMD (wave w and w + NW/2) take the two halves in opposite
     // order, so one's exponentials run while the other's score MFMAs do.
-    load_tile(kbase + 2 * BN);
+    dma_tile(kbase + 2 * BN, stg);  // buffer of tile t-1, free since the last barrier
     bf16x8 pb[QB][2 * C::KB];
     // The row sum is taken over the bf16-rounded probabilities, the same values the PV MFMA
     // multiplies, so numerator and denominator see identical weights.
@@ -350,19 +360,20 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     }
 
     // ---- block B ---------------------------------------------------------------------------
-    const lds_u16* vb = as_lds(cur) + (4 * g + tr_row) * C::STRIDE + tr_col;
+    const lds_u16* vlo = as_lds(cur) + vofs_lo;
+    const lds_u16* vhi = as_lds(cur) + vofs_hi;
 #pragma unroll
     for (int kk = 0; kk < 2 * C::KB; ++kk) {
 #pragma unroll
       for (int d = 0; d < C::DVB; ++d) {
-        const i16x4 lo = lds_read_tr(vb + kk * 16 * C::STRIDE + d * 32);
-        const i16x4 hi = lds_read_tr(vb + (kk * 16 + 8) * C::STRIDE + d * 32);
+        const i16x4 lo = lds_read_tr(vlo + kk * 16 * C::STRIDE + d * 32);
+        const i16x4 hi = lds_read_tr(vhi + kk * 16 * C::STRIDE + d * 32);
         const bf16x8 v = join_bf16x8(lo, hi);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) o[qb][d] = mfma32(v, pb[qb][kk], o[qb][d]);
       }
     }
-    store_tile(stg);
+    wait_vmcnt<0>();  // this wave's part of tile t+2 is in LDS
     __syncthreads();
     if (kbase + 2 * BN > key_end) mask_tail(kbase + BN, s_nxt);  // only near the split's end
     own_max_of(s_nxt);
@@ -370,11 +381,10 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
   };
 
   if (n_tiles > 0) {
-    load_tile(key_begin);
-    store_tile(tile[0]);
-    load_tile(key_begin + BN);
-    store_tile(tile[1]);
+    dma_tile(key_begin, tile[0]);
+    dma_tile(key_begin + BN, tile[1]);
   }
+  wait_vmcnt<0>();
   __syncthreads();
 
   f32x16 s_a[QB][C::KB], s_b[QB][C::KB];

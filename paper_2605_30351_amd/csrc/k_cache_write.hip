@@ -18,29 +18,6 @@ constexpr int kTok = 32;     // tokens per workgroup
 constexpr int kWaves = 4;
 constexpr int kKC = 64;      // contraction columns per stage: 8 chunks of 16 B per row
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Direct global-to-LDS load of 16 B per lane: lane l's bytes land at LDS address lds_base + 16 l.
-// Issued as inline assembly so that the compiler does not treat it as an LDS write it must wait
-// for before every LDS read and barrier; the callers order it with explicit vmcnt waits (the
-// load counts as one outstanding vector-memory operation until its data is in LDS).
-__device__ __forceinline__ void lds_dma16(const uint16_t* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(gptr), "s"(lds_base)
-               : "memory", "m0");
-}
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(lds_void*)(p);
-}
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-template <int VM>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 // Position (16 B units) of chunk c of staged row r: row-major with 8 chunks per row, the chunk
 // index XOR-ed with (r / 2) mod 8, so 16 consecutive rows read at one chunk hit distinct banks.
 __device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }

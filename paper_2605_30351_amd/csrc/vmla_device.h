@@ -51,6 +51,29 @@ __device__ __forceinline__ const lds_u16* as_lds(const uint16_t* p) {
   return (const lds_u16*)(p);
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Direct global-to-LDS load of 16 B per lane: lane l's bytes land at LDS address lds_base + 16 l.
+// Issued as inline assembly so that the compiler does not treat it as an LDS write it must wait
+// for before every LDS read and barrier; the callers order it with explicit vmcnt waits (the
+// load counts as one outstanding vector-memory operation until its data is in LDS).
+__device__ __forceinline__ void lds_dma16(const uint16_t* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds_base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_void*)(p);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // LDS transpose read (ds_read_b64_tr_b16). Within each group of 16 lanes, source lane s points
 // at 4 consecutive 16-bit elements M[s][0..3]; result lane i receives M[4e + i/4][i%4],
 // e = 0..3. If source lane s addresses row (R0 + s/4), columns C0 + 4(s%4) .. +4 of a row-major
