@@ -148,8 +148,8 @@ struct AttCfg {
   }
 };
 
-template <int DC, int DR, int QB, int NW, int BN>
-__global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendArgs a) {
+template <int DC, int DR, int QB, int NW, int BN, int WPC>
+__global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const AttendArgs a) {
   using C = AttCfg<DC, DR, QB, NW, BN>;
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
@@ -326,38 +326,45 @@ __global__ __launch_bounds__(NW * 64, 1) void latent_attend_kernel(const AttendA
     const int kbase = key_begin + t * BN;
 
     // ---- block A: scores of tile t+1 and exponentials of tile t ----------------------------
-    // The two waves sharing a SIMD (wave w and w + NW/2) take the two halves in opposite
-    // order, so one's exponentials run while the other's score MFMAs do.
+    // One instruction stream, fenced step by step: the K operand read two score steps ahead
+    // of its MFMA, and one slice of tile t's softmax (exp2, bf16 rounding, row sum) after each
+    // score MFMA, so the VALU work and the LDS latency hide under the MFMA chain.
     dma_tile(kbase + 2 * BN, stg);  // buffer of tile t-1, free since the last barrier
-    bf16x8 pb[QB][2 * C::KB];
+    static_assert(QB == 1 && C::KB == 1, "block A is laid out for one query block per wave");
+    constexpr int NS = C::KSTEPS;
+    constexpr int NP = 8;  // bf16 probability pairs per lane and tile
+    auto kread = [&](int ks) {
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(
+          &nxt[((ks & 1) ? koff_o : koff_e) + ks * 16]));
+    };
     // The row sum is taken over the bf16-rounded probabilities, the same values the PV MFMA
     // multiplies, so numerator and denominator see identical weights.
-    auto exps = [&]() {
+    uint32_t pk[NP];
+    float lsum = l_run[0];
+    f32x16 acc = {};
+    bf16x8 kq[3];
+    kq[0] = kread(0);
+    if (NS > 1) kq[1] = kread(1);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float acc = l_run[qb];
+    for (int ks = 0; ks < NS; ++ks) {
+      if (ks + 2 < NS) kq[(ks + 2) % 3] = kread(ks + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      acc = mfma32(kq[ks % 3], q[0][ks], acc);
 #pragma unroll
-        for (int kb = 0; kb < C::KB; ++kb) {
-          f32x16 p;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) p[r] = fast_exp2(s_cur[qb][kb][r] - m_run[qb]);
-          const f32x8 lo = {p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]};
-          const f32x8 hi = {p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]};
-          pb[qb][2 * kb] = to_bf16x8(lo);
-          pb[qb][2 * kb + 1] = to_bf16x8(hi);
-          acc = sum_bf16x8(pb[qb][2 * kb], acc);
-          acc = sum_bf16x8(pb[qb][2 * kb + 1], acc);
-        }
-        l_run[qb] = acc;
+      for (int p = ks * NP / NS; p < (ks + 1) * NP / NS; ++p) {
+        const f32x2 e = {fast_exp2(s_cur[0][0][2 * p] - m_run[0]),
+                         fast_exp2(s_cur[0][0][2 * p + 1] - m_run[0])};
+        const bf16x2 h = __builtin_convertvector(e, bf16x2);
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(h, kOnesBf16x2, lsum, false);
+        pk[p] = __builtin_bit_cast(uint32_t, h);
       }
-    };
-    if (wave < NW / 2) {
-      scores(nxt, s_nxt);
-      exps();
-    } else {
-      exps();
-      scores(nxt, s_nxt);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    s_nxt[0][0] = acc;
+    l_run[0] = lsum;
+    bf16x8 pb[QB][2 * C::KB];
+    pb[0][0] = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
+    pb[0][1] = as_bf16x8(u32x4{pk[4], pk[5], pk[6], pk[7]});
 
     // ---- block B ---------------------------------------------------------------------------
     const lds_u16* vlo = as_lds(cur) + vofs_lo;
@@ -504,15 +511,17 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
 
 // Tile shapes per supported (d_c, d_rope).
 template <int DC, int DR> struct AttShape;
-template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32; };
-template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32; };
+// WPC = resident workgroups per CU (the grid is WPC workgroups per CU). Two 4-wave workgroups
+// per CU measured 6% slower than one 8-wave workgroup at the Wan shape.
+template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
+template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1; };
 
 template <int DC, int DR>
 hipError_t launch_attend_t(const AttendArgs& a, hipStream_t s) {
   using S = AttShape<DC, DR>;
   using C = AttCfg<DC, DR, S::QB, S::NW, S::BN>;
   const dim3 grid(a.n_wg);
-  hipLaunchKernelGGL((latent_attend_kernel<DC, DR, S::QB, S::NW, S::BN>), grid, dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((latent_attend_kernel<DC, DR, S::QB, S::NW, S::BN, S::WPC>), grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -530,6 +539,11 @@ int latent_attend_rows_per_block(int d_c, int d_rope) {
 int latent_attend_keys_per_tile(int d_c, int d_rope) {
   if (d_c == 192 && d_rope == 32) return AttShape<192, 32>::BN;
   return AttShape<16, 8>::BN;
+}
+
+int latent_attend_wgs_per_cu(int d_c, int d_rope) {
+  if (d_c == 192 && d_rope == 32) return AttShape<192, 32>::WPC;
+  return AttShape<16, 8>::WPC;
 }
 
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s) {

@@ -135,7 +135,7 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(VIDEOMLA_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
 }
 
-int g_attend_wg = 0;  // 0 = one workgroup per compute unit
+int g_attend_wg = 0;  // 0 = as many workgroups as the compute units hold at once
 
 int device_cu_count() {
   int dev = 0, n = 0;
@@ -159,7 +159,9 @@ Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_vali
   p.RB = (int)((rows_b + p.rows - 1) / p.rows);
   p.T = (int)((n_valid + bn - 1) / bn);
   p.U = (int64_t)batch * p.RB * p.T;
-  const int64_t G = g_attend_wg > 0 ? g_attend_wg : device_cu_count();
+  const int64_t G = g_attend_wg > 0
+                       ? g_attend_wg
+                       : (int64_t)device_cu_count() * latent_attend_wgs_per_cu(d->d_c, d->d_rope);
   p.G = (int)(G < p.U ? G : p.U);
   p.max_seg = 1;
   for (int64_t rbg = 0; rbg < (int64_t)batch * p.RB; ++rbg) {

@@ -79,5 +79,6 @@ hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
 bool latent_attend_supported(int d_c, int d_rope);
 int latent_attend_rows_per_block(int d_c, int d_rope);
 int latent_attend_keys_per_tile(int d_c, int d_rope);
+int latent_attend_wgs_per_cu(int d_c, int d_rope);
 
 }  // namespace vmla
