@@ -118,6 +118,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 // ---------------------------------------------------------------------------------------------
 constexpr float kLazyMax = 8.0f;
 
+
 template <int DC, int DR, int QB, int NW, int BN>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
@@ -325,60 +326,79 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
                   const uint16_t* cur, const uint16_t* nxt, uint16_t* stg) {
     const int kbase = key_begin + t * BN;
 
-    // ---- block A: scores of tile t+1 and exponentials of tile t ----------------------------
-    // One instruction stream, fenced step by step: the K operand read two score steps ahead
-    // of its MFMA, and one slice of tile t's softmax (exp2, bf16 rounding, row sum) after each
-    // score MFMA, so the VALU work and the LDS latency hide under the MFMA chain.
+    // Work of one step: QK = scores of tile t+1 (14 MFMAs, one LDS read each), SM = the
+    // softmax of tile t (exp2, bf16 rounding, row sums; VALU), PV = O += V^T P^T of tile t
+    // (12 MFMAs, two LDS transpose reads each). They run as one fenced instruction stream of
+    // slots: slot i holds QK MFMA i, then (for the first four slots) a quarter of SM, then PV
+    // MFMA i - 2, with every K read issued two slots ahead and every V^T read one slot ahead,
+    // so the wave's LDS traffic and VALU work are spread evenly under its MFMAs.
     dma_tile(kbase + 2 * BN, stg);  // buffer of tile t-1, free since the last barrier
-    static_assert(QB == 1 && C::KB == 1, "block A is laid out for one query block per wave");
+    static_assert(C::KB == 1, "the step is laid out for 32-key tiles");
     constexpr int NS = C::KSTEPS;
-    constexpr int NP = 8;  // bf16 probability pairs per lane and tile
+    constexpr int NPV = 2 * C::DVB;  // PV operand reads per tile (each feeds QB MFMAs)
+    constexpr int NSLOT = NS > NPV + 2 ? NS : NPV + 2;
+    constexpr int NSM = NS < 4 ? NS : 4;  // slots carrying the softmax; pairs 0-3 precede PV
     auto kread = [&](int ks) {
       return as_bf16x8(*reinterpret_cast<const u32x4*>(
           &nxt[((ks & 1) ? koff_o : koff_e) + ks * 16]));
     };
+    const lds_u16* vlo = as_lds(cur) + vofs_lo;
+    const lds_u16* vhi = as_lds(cur) + vofs_hi;
+    auto vread = [&](int j) {  // A operand of PV MFMA j: kk = j / DVB, d = j % DVB
+      const int kk = j / C::DVB, d = j % C::DVB;
+      return join_bf16x8(lds_read_tr(vlo + kk * 16 * C::STRIDE + d * 32),
+                         lds_read_tr(vhi + kk * 16 * C::STRIDE + d * 32));
+    };
     // The row sum is taken over the bf16-rounded probabilities, the same values the PV MFMA
     // multiplies, so numerator and denominator see identical weights.
-    uint32_t pk[NP];
-    float lsum = l_run[0];
-    f32x16 acc = {};
-    bf16x8 kq[3];
+    uint32_t pk[QB][8];
+    float lsum[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) lsum[qb] = l_run[qb];
+    auto sm_pair = [&](int qb, int p) {
+      const f32x2 e = {fast_exp2(s_cur[qb][0][2 * p] - m_run[qb]),
+                       fast_exp2(s_cur[qb][0][2 * p + 1] - m_run[qb])};
+      const bf16x2 h = __builtin_convertvector(e, bf16x2);
+      lsum[qb] = __builtin_amdgcn_fdot2_f32_bf16(h, kOnesBf16x2, lsum[qb], false);
+      pk[qb][p] = __builtin_bit_cast(uint32_t, h);
+    };
+    f32x16 acc[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) acc[qb] = f32x16{};
+    bf16x8 kq[3], vq[2];
     kq[0] = kread(0);
     if (NS > 1) kq[1] = kread(1);
 #pragma unroll
-    for (int ks = 0; ks < NS; ++ks) {
+    for (int ks = 0; ks < NSLOT; ++ks) {
       if (ks + 2 < NS) kq[(ks + 2) % 3] = kread(ks + 2);
+      const int j = ks - 2;  // PV operand of this slot
+      if (j + 1 >= 0 && j + 1 < NPV) vq[(j + 1) & 1] = vread(j + 1);
       __builtin_amdgcn_sched_barrier(0);
-      acc = mfma32(kq[ks % 3], q[0][ks], acc);
+      if (ks < NS) {
 #pragma unroll
-      for (int p = ks * NP / NS; p < (ks + 1) * NP / NS; ++p) {
-        const f32x2 e = {fast_exp2(s_cur[0][0][2 * p] - m_run[0]),
-                         fast_exp2(s_cur[0][0][2 * p + 1] - m_run[0])};
-        const bf16x2 h = __builtin_convertvector(e, bf16x2);
-        lsum = __builtin_amdgcn_fdot2_f32_bf16(h, kOnesBf16x2, lsum, false);
-        pk[p] = __builtin_bit_cast(uint32_t, h);
+        for (int qb = 0; qb < QB; ++qb) acc[qb] = mfma32(kq[ks % 3], q[qb][ks], acc[qb]);
+      }
+      if (ks < NSM) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int p = ks * 8 / NSM; p < (ks + 1) * 8 / NSM; ++p) sm_pair(qb, p);
+      }
+      if (j >= 0 && j < NPV) {
+        const int kk = j / C::DVB, d = j % C::DVB;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          const bf16x8 pb = as_bf16x8(kk == 0 ? u32x4{pk[qb][0], pk[qb][1], pk[qb][2], pk[qb][3]}
+                                              : u32x4{pk[qb][4], pk[qb][5], pk[qb][6], pk[qb][7]});
+          o[qb][d] = mfma32(vq[j & 1], pb, o[qb][d]);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    s_nxt[0][0] = acc;
-    l_run[0] = lsum;
-    bf16x8 pb[QB][2 * C::KB];
-    pb[0][0] = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
-    pb[0][1] = as_bf16x8(u32x4{pk[4], pk[5], pk[6], pk[7]});
-
-    // ---- block B ---------------------------------------------------------------------------
-    const lds_u16* vlo = as_lds(cur) + vofs_lo;
-    const lds_u16* vhi = as_lds(cur) + vofs_hi;
 #pragma unroll
-    for (int kk = 0; kk < 2 * C::KB; ++kk) {
-#pragma unroll
-      for (int d = 0; d < C::DVB; ++d) {
-        const i16x4 lo = lds_read_tr(vlo + kk * 16 * C::STRIDE + d * 32);
-        const i16x4 hi = lds_read_tr(vhi + kk * 16 * C::STRIDE + d * 32);
-        const bf16x8 v = join_bf16x8(lo, hi);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][d] = mfma32(v, pb[qb][kk], o[qb][d]);
-      }
+    for (int qb = 0; qb < QB; ++qb) {
+      s_nxt[qb][0] = acc[qb];
+      l_run[qb] = lsum[qb];
     }
     wait_vmcnt<0>();  // this wave's part of tile t+2 is in LDS
     __syncthreads();
