@@ -121,7 +121,8 @@ size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch)
  *   out     [batch][chunk_frames * HW][n_heads][d_v]      bf16
  *   workspace  device buffer of at least videomla_attend_workspace_bytes() bytes
  * Arithmetic: bf16 operands, fp32 accumulation and softmax, bf16 round-to-nearest-even output.
- * Requires d_c % 16 == 0, d_nope % 16 == 0, d_v % 32 == 0, (d_c, d_rope) in {(192, 32), (16, 8)}
+ * Requires d_nope % 16 == 0 and d_nope <= 128, d_v % 32 == 0 and d_v <= 256,
+ * (d_c, d_rope) in {(192, 32), (16, 8)},
  * otherwise VIDEOMLA_EUNSUPPORTED.
  */
 int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,

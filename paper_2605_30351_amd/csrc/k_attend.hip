@@ -23,19 +23,38 @@ constexpr float kNegInf = -__builtin_huge_valf();
 // ---------------------------------------------------------------------------------------------
 // q_absorb: grid (ceil(Nq/128), H, B), 4 waves, 32 tokens per wave, one head per workgroup.
 // out^T[c][token] = W_UK_h^T[c][k] q_nope^T[k][token]; W_UK_h ([d_nope][d_c] row-major) is
-// staged in LDS and read transposed with ds_read_b64_tr_b16.
+// staged in LDS and read transposed with ds_read_b64_tr_b16, each lane's q_nope row is loaded
+// once (all d_nope <= kMaxNope dims) and feeds every 32-wide output block.
 // ---------------------------------------------------------------------------------------------
+constexpr int kMaxNope = 128;
+
 template <int DC, int DR>
 __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   constexpr int DCP = (DC + 31) / 32 * 32;
   constexpr int WS = DCP + 8;  // LDS row stride (elements)
   constexpr int DQKP = (DC + DR + 15) / 16 * 16;
+  constexpr int NCB = DCP / 32;
+  constexpr int KN = kMaxNope / 16;
   extern __shared__ __attribute__((aligned(16))) uint16_t wuk[];  // [d_nope][WS]
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int h = blockIdx.y, b = blockIdx.z;
   const int H = a.n_heads, dn = a.d_nope, Nq = a.geo.chunk_tokens;
+  const int nks = dn / 16;
+
+  const int n = blockIdx.x * 128 + wave * 32 + l32;
+  const bool ok = n < Nq;
+  const size_t row = ((size_t)b * Nq + (ok ? n : 0)) * H + h;
+  const uint16_t* qn = a.q_nope + row * dn;
+  uint16_t* dst = a.qcat + row * DQKP;
+
+  // this lane's query row, B-operand layout (dims ks*16 + 8g .. +8), issued before the W wait
+  const u32x4 zero = {0, 0, 0, 0};
+  bf16x8 bq[KN];
+#pragma unroll
+  for (int ks = 0; ks < KN; ++ks) bq[ks] = as_bf16x8(ok && ks < nks ? ldg16(qn + ks * 16 + 8 * g) : zero);
 
   const uint16_t* wsrc = a.w_uk + (size_t)h * dn * DC;
   for (int c = tid; c < dn * (DC / 8); c += 256) {
@@ -44,37 +63,36 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   }
   __syncthreads();
 
-  const int n = blockIdx.x * 128 + wave * 32 + l32;
-  const bool ok = n < Nq;
-  const size_t row = ((size_t)b * Nq + (ok ? n : 0)) * H + h;
-  const uint16_t* qn = a.q_nope + row * dn;
-  uint16_t* dst = a.qcat + row * DQKP;
-
   // tr-read addressing inside a 16-lane group
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const u32x4 zero = {0, 0, 0, 0};
+  f32x16 acc[NCB];
 #pragma unroll
-  for (int cb = 0; cb < DCP / 32; ++cb) {
-    f32x16 acc = {};
-    for (int ks = 0; ks < dn / 16; ++ks) {
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < KN; ++ks) {
+    if (ks < nks) {
       const int k0 = ks * 16 + 8 * g;
-      const i16x4 lo = lds_read_tr(&wuk[(k0 + tr_row) * WS + cb * 32 + tr_col]);
-      const i16x4 hi = lds_read_tr(&wuk[(k0 + 4 + tr_row) * WS + cb * 32 + tr_col]);
-      const bf16x8 bq = as_bf16x8(ok ? ldg16(qn + k0) : zero);
-      acc = mfma32(join_bf16x8(lo, hi), bq, acc);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) {
+        const i16x4 lo = lds_read_tr(&wuk[(k0 + tr_row) * WS + cb * 32 + tr_col]);
+        const i16x4 hi = lds_read_tr(&wuk[(k0 + 4 + tr_row) * WS + cb * 32 + tr_col]);
+        acc[cb] = mfma32(join_bf16x8(lo, hi), bq[ks], acc[cb]);
+      }
     }
-    if (ok) {
+  }
+  if (ok) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = cb * 32 + 8 * i + 4 * g;
         if (c < DC) {
-          const f32x4 v = {acc[4 * i] * a.qscale, acc[4 * i + 1] * a.qscale,
-                           acc[4 * i + 2] * a.qscale, acc[4 * i + 3] * a.qscale};
+          const f32x4 v = {acc[cb][4 * i] * a.qscale, acc[cb][4 * i + 1] * a.qscale,
+                           acc[cb][4 * i + 2] * a.qscale, acc[cb][4 * i + 3] * a.qscale};
           *reinterpret_cast<bf16x4*>(dst + c) = to_bf16x4(v);
         }
       }
-    }
   }
 
   // RoPE part and zero padding: 32 tokens x (DR/2) pairs per wave.
@@ -463,69 +481,111 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 }
 
 // ---------------------------------------------------------------------------------------------
-// out_proj: grid (ceil(Nq/128), H, B), 4 waves x 32 tokens, one head per workgroup.
-// out^T[v][token] = W_UV_h[v][c] o_lat^T[c][token], where o_lat merges the key splits:
-// o_lat = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// out_proj: grid (ceil(Nq/128), H, B), 4 waves x 32 tokens, one head per workgroup. Each wave
+// handles the rows (token n, head h) of its 32 tokens:
+//   1. merge scale of every row over its key splits s: M = max_s m_s, 1/L with
+//      L = sum_s 2^(m_s - M) l_s
+//   2. o_lat = (1/L) sum_s 2^(m_s - M) O_s, streamed as 16-byte chunks that cover the rows'
+//      partial results contiguously, rounded to bf16 into an LDS tile [32][DC]
+//   3. out^T[v][token] = W_UV_h[v][:] . o_lat[token][:] with MFMA (A = W_UV rows from global
+//      memory, B = o_lat rows from LDS)
+//   4. the bf16 result is staged through the same LDS tile so that every output row is stored
+//      as whole 16-byte chunks.
+// Lanes of tokens past the chunk work on the chunk's last token and store nothing.
 // ---------------------------------------------------------------------------------------------
 template <int DC, int NVB>  // NVB = d_v / 32
 __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
   constexpr int KS = DC / 16;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int DV = NVB * 32;
+  constexpr int LS = (DC > DV ? DC : DV) + 8;  // LDS row stride (elements); +16 B per row
+  constexpr int CH = DC / 4;                   // fp32 chunks of 16 B per partial row
+  static_assert((32 * CH) % 64 == 0 && (32 * DV / 8) % 64 == 0, "whole 64-lane passes");
+  __shared__ __attribute__((aligned(16))) uint16_t tileo[4][32 * LS];
+  __shared__ float row_m[4][32], row_il[4][32];
+  __shared__ int row_ns[4][32];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int h = blockIdx.y, b = blockIdx.z;
-  const int H = a.n_heads, dv = a.d_v, Nq = a.geo.chunk_tokens;
-  const int n = blockIdx.x * 128 + wave * 32 + l32;
-  const bool ok = n < Nq;
+  const int H = a.n_heads, Nq = a.geo.chunk_tokens;
+  const int n0 = blockIdx.x * 128 + wave * 32;
   const size_t total_rows = (size_t)a.batch * Nq * H;
-  const size_t row = ((size_t)b * Nq + (ok ? n : 0)) * H + h;
+  auto row_of = [&](int t) {  // global row of the wave's token t
+    const int n = min(n0 + t, Nq - 1);
+    return ((size_t)b * Nq + n) * H + h;
+  };
+  uint16_t* tw = tileo[wave];
 
-  // partial results of this row's row block: one per workgroup that processed part of it
-  const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
-  const int n_seg = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
-                    attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
-  float M = kNegInf;
-  for (int s = 0; s < n_seg; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
-  float L = 0.f;
-  for (int s = 0; s < n_seg; ++s) {
-    const float* ml = a.ml_part + ((size_t)s * total_rows + row) * 2;
-    L += fast_exp2(ml[0] - M) * ml[1];
+  // 1. merge scale per row (lanes 0..31, one row each)
+  if (lane < 32) {
+    const size_t row = row_of(lane);
+    const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
+    const int ns = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
+                   attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
+    float M = kNegInf;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
+    float L = 0.f;
+    for (int s = 0; s < ns; ++s) {
+      const float* ml = a.ml_part + ((size_t)s * total_rows + row) * 2;
+      L += fast_exp2(ml[0] - M) * ml[1];
+    }
+    row_m[wave][lane] = M;
+    row_il[wave][lane] = 1.f / L;
+    row_ns[wave][lane] = ns;
   }
-  const float invL = ok ? 1.f / L : 0.f;
+  __syncthreads();
 
-  const uint16_t* w = a.w_uv + (size_t)h * dv * DC;
+  // 2. merged, normalized o_lat rows -> bf16 LDS tile
+#pragma unroll 4
+  for (int it = 0; it < 32 * CH / 64; ++it) {
+    const int q = it * 64 + lane;
+    const int t = q / CH, k = q % CH;
+    const size_t row = row_of(t);
+    const float M = row_m[wave][t], il = row_il[wave][t];
+    const int ns = row_ns[wave][t];
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < ns; ++s) {
+      const float coef = fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * il;
+      const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
+      acc += coef * v;
+    }
+    *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
+  }
+  __syncthreads();
+
+  // 3. out^T = W_UV_h o_lat^T
+  const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
   f32x16 acc[NVB];
 #pragma unroll
   for (int vb = 0; vb < NVB; ++vb) acc[vb] = f32x16{};
-
-  for (int ks = 0; ks < KS; ++ks) {
-    const int c0 = ks * 16 + 8 * g;
-    f32x8 ov = {};
-    for (int s = 0; s < n_seg; ++s) {
-      const float coef = ok ? fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * invL : 0.f;
-      const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + c0);
-      const f32x4 v0 = src[0], v1 = src[1];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        ov[e] += coef * v0[e];
-        ov[4 + e] += coef * v1[e];
-      }
-    }
-    const bf16x8 bo = to_bf16x8(ov);
+  for (int ks = 0; ks < KS; ++ks) {
+    const bf16x8 bo = as_bf16x8(*reinterpret_cast<const u32x4*>(&tw[l32 * LS + ks * 16 + 8 * g]));
 #pragma unroll
     for (int vb = 0; vb < NVB; ++vb) {
-      const bf16x8 aw = as_bf16x8(ldg16(w + (size_t)(vb * 32 + l32) * DC + c0));
+      const bf16x8 aw = as_bf16x8(ldg16(w + (size_t)(vb * 32 + l32) * DC + ks * 16 + 8 * g));
       acc[vb] = mfma32(aw, bo, acc[vb]);
     }
   }
-  if (!ok) return;
-  uint16_t* dst = a.out + row * dv;
+  __syncthreads();  // every lane is done reading the o_lat tile
+
+  // 4. stage the bf16 output rows and store them whole
 #pragma unroll
-  for (int vb = 0; vb < NVB; ++vb) {
+  for (int vb = 0; vb < NVB; ++vb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const f32x4 v = {acc[vb][4 * i], acc[vb][4 * i + 1], acc[vb][4 * i + 2], acc[vb][4 * i + 3]};
-      *reinterpret_cast<bf16x4*>(dst + vb * 32 + 8 * i + 4 * g) = to_bf16x4(v);
+      *reinterpret_cast<bf16x4*>(&tw[l32 * LS + vb * 32 + 8 * i + 4 * g]) = to_bf16x4(v);
     }
+  __syncthreads();
+#pragma unroll
+  for (int it = 0; it < 32 * DV / 8 / 64; ++it) {
+    const int q = it * 64 + lane;
+    const int t = q / (DV / 8), k = q % (DV / 8);
+    if (n0 + t < Nq)
+      *reinterpret_cast<u32x4*>(a.out + row_of(t) * DV + 8 * k) =
+          *reinterpret_cast<const u32x4*>(&tw[t * LS + 8 * k]);
   }
 }
 

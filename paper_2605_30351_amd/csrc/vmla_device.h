@@ -135,15 +135,17 @@ __device__ __forceinline__ int64_t ring_slot(const Geometry& g, const TokenPos& 
   return ((p.f % g.window_frames) * g.grid_h + p.y) * (int64_t)g.grid_w + p.x;
 }
 
-// Rotate the pair (u, v) of RoPE pair `pair` at position p: angle = pos_axis * theta, taken in
-// double precision, then (u cos - v sin, u sin + v cos) in fp32.
+// Rotate the pair (u, v) of RoPE pair `pair` at position p by the angle pos_axis * theta: the
+// angle is reduced to [-pi, pi] in double precision (pos * theta / 2pi minus its nearest
+// integer), then sin and cos are taken in fp32 and (u cos - v sin, u sin + v cos) in fp32.
 __device__ __forceinline__ void rope_rotate(const RopeTable& t, int pair, const TokenPos& p,
                                             float& u, float& v) {
   const int ax = t.axis[pair];
   const double pos = ax == 0 ? (double)p.f : (ax == 1 ? (double)p.y : (double)p.x);
-  double s, c;
-  sincos(pos * t.theta[pair], &s, &c);
-  const float cs = (float)c, sn = (float)s;
+  const double turns = pos * t.theta[pair] * 0.15915494309189533577;  // 1 / (2 pi)
+  const float r = (float)((turns - rint(turns)) * 6.283185307179586477);
+  float sn, cs;
+  sincosf(r, &sn, &cs);
   const float ru = u * cs - v * sn;
   const float rv = u * sn + v * cs;
   u = ru;
