@@ -1,0 +1,117 @@
+"""Helpers shared by the GPU parity tests: device copies of seeded inputs, a layer with its
+ring, and the comparison bars (see tests/test_gpu_parity.py for their derivation)."""
+import numpy as np
+import torch
+
+from oracle import videomla_oracle as O
+
+ATOL_MAX, ATOL_MEAN, REL_L2 = 2e-2, 2e-3, 1e-2
+
+SENTINEL = 0x4242  # bf16 bits of 48.5: never produced by the ring writes here
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def host_bits(t: torch.Tensor) -> np.ndarray:
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    return O.bf16_bits_to_f64(bits)
+
+
+def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
+    """Distance in bf16 steps between two bit patterns (ordered sign-magnitude)."""
+    def ordered(b):
+        b = b.astype(np.int32)
+        return np.where(b & 0x8000, 0x8000 - (b & 0x7FFF), 0x8000 + b)
+    return np.abs(ordered(a_bits) - ordered(b_bits))
+
+
+class Layer:
+    """Device copies of one layer's inputs plus its ring."""
+
+    def __init__(self, vm, inp, sentinel=True):
+        self.vm, self.inp, d = vm, inp, inp.dims
+        self.x = dev(inp.x)
+        self.w_dkv, self.w_kr = dev(inp.w_dkv), dev(inp.w_kr)
+        self.w_uk, self.w_uv = dev(inp.w_uk), dev(inp.w_uv)
+        self.gamma = dev(inp.gamma) if inp.gamma is not None else None
+        self.q_nope, self.q_r = dev(inp.q_nope), dev(inp.q_r)
+        B = inp.batch
+        fill = SENTINEL if sentinel else 0
+        self.c_kv = torch.full((B, d.window_tokens, d.d_c), fill, dtype=torch.int16,
+                               device="cuda").view(torch.bfloat16)
+        self.k_r = torch.full((B, d.window_tokens, d.d_rope), fill, dtype=torch.int16,
+                              device="cuda").view(torch.bfloat16)
+        self.slots = torch.full((d.chunk_tokens,), -1, dtype=torch.int32, device="cuda")
+        self.out = torch.zeros((B, d.chunk_tokens, d.n_heads, d.d_v), dtype=torch.bfloat16,
+                               device="cuda")
+
+    def write(self, fe):
+        d = self.inp.dims
+        xs = self.x[:, fe * d.hw:(fe + d.chunk_frames) * d.hw].contiguous()
+        self.vm.cache_write(d, fe, self.inp.batch, xs, self.w_dkv, self.w_kr, self.gamma,
+                            self.c_kv, self.k_r, self.slots)
+
+    def attend(self, fe):
+        d = self.inp.dims
+        ws = torch.empty(self.vm.attend_workspace_bytes(d, self.inp.batch), dtype=torch.uint8,
+                         device="cuda")
+        self.vm.attend(d, fe, self.inp.batch, self.q_nope, self.q_r, self.w_uk, self.w_uv,
+                       self.c_kv, self.k_r, self.out, ws)
+        torch.cuda.synchronize()
+        return bf16_to_f64(host_bits(self.out))
+
+
+U_BF16 = 2.0 ** -9
+
+
+def assert_attention_close(got, want, label=""):
+    err = np.abs(got - want)
+    rel = np.linalg.norm(got - want) / np.linalg.norm(want)
+    max_bar = max(ATOL_MAX, 8 * U_BF16 * np.abs(want).max())
+    mean_bar = max(ATOL_MEAN, 4 * U_BF16 * np.abs(want).mean())
+    msg = (f"{label}: max {err.max():.3e} (bar {max_bar:.2e}) mean {err.mean():.3e} "
+           f"(bar {mean_bar:.2e}) relL2 {rel:.3e} |out| max {np.abs(want).max():.3e} "
+           f"mean {np.abs(want).mean():.3e}")
+    print(msg, flush=True)
+    assert err.max() <= max_bar, msg
+    assert err.mean() <= mean_bar, msg
+    assert rel <= REL_L2, msg
+
+
+def check_written_chunk(layer, fe, before_c, before_k):
+    """Slots bit-exact, untouched slots unchanged, contents within the rounding bar."""
+    inp, d = layer.inp, layer.inp.dims
+    torch.cuda.synchronize()
+    c_bits, k_bits = host_bits(layer.c_kv), host_bits(layer.k_r)
+    slots = layer.slots.cpu().numpy()
+    stats = []
+    for b in range(inp.batch):
+        ref = O.cache_write(inp.x[b, fe * d.hw:(fe + d.chunk_frames) * d.hw], inp.w_dkv, inp.w_kr,
+                            inp.gamma, fe, d)
+        assert np.array_equal(slots, ref["slots"].astype(np.int32))
+        written = np.zeros(d.window_tokens, bool)
+        written[ref["slots"]] = True
+        assert np.array_equal(c_bits[b][~written], before_c[b][~written])
+        assert np.array_equal(k_bits[b][~written], before_k[b][~written])
+        for got, exact in ((c_bits[b][ref["slots"]], ref["c"]),
+                           (k_bits[b][ref["slots"]], ref["k_rope"])):
+            dist = ulp_distance(got, O.round_to_bf16_bits(exact))
+            floor = 2.0 ** -16 * np.sqrt(np.mean(exact * exact, axis=1, keepdims=True))
+            near = np.abs(bf16_to_f64(got) - exact) <= floor
+            bad = (dist > 1) & ~near
+            assert not bad.any(), f"{bad.sum()} elements beyond 1 ulp; max distance {dist.max()}"
+            stats.append((np.count_nonzero(dist == 0), dist.size))
+    return stats
+
+
+def sample_rows(nq, k=40, seed=0):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, 51, 52, 1559, 1560, 3119, 3120, nq - 1]
+    return np.unique(np.concatenate([fixed, rng.integers(0, nq, k)]))
+
+
