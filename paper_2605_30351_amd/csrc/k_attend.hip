@@ -183,11 +183,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   const int64_t U = a.units;
   const int G = a.n_wg, T = a.tiles_per_row;
   const int64_t u_begin = (int64_t)blockIdx.x * U / G, u_end = (int64_t)(blockIdx.x + 1) * U / G;
-  for (int64_t u = u_begin; u < u_end;) {
-  const int64_t rbg = u / T;
-  const int kt0 = (int)(u - rbg * T);
-  const int kt1 = (int)min((int64_t)T, (int64_t)kt0 + (u_end - u));
-  u += kt1 - kt0;
+  // Segments are taken last to first: a workgroup's last segment is the head of a row block
+  // (keys from 0) and its first the tail of another, so in this order every workgroup walks the
+  // keys at about the same position at the same time (all ranges have the same length), and
+  // the workgroups of one XCD find most tiles already in its L2.
+  for (int64_t u = u_end; u > u_begin;) {
+  const int64_t rbg = (u - 1) / T;
+  const int64_t seg_lo = max(u_begin, rbg * T);
+  const int kt0 = (int)(seg_lo - rbg * T);
+  const int kt1 = (int)(u - rbg * T);
+  u = seg_lo;
   const int b = (int)(rbg / a.row_blocks), rb = (int)(rbg % a.row_blocks);
   const int split = (int)blockIdx.x - attend_owner(rbg * T, U, G);
   const int row0 = rb * C::ROWS + wave * QB * 32;
