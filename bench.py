@@ -108,6 +108,87 @@ def copy_probe(torch, dev, nbytes=1 << 28, reps=3):
     del a, b
 
 
+def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
+    """One chunk through the whole network's attention layers: for each of 4 denoising steps,
+    every one of the 30 layers (own weights, own ring, filled with frames 0..20) writes the
+    chunk's latents and attends over its window; then the window advances. Activations and
+    weights are seeded synthetic bf16 drawn on the GPU (N(0,1) activations, N(0, 1/fan_in)
+    weights); `steps` counts chunks."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    hw, nq = d.hw, d.chunk_tokens
+    log(f"building {n_layers} layers")
+    layers = []
+    for _ in range(n_layers):
+        L = {
+            "w_dkv": normal((d.d_c, d.d_model), d.d_model ** -0.5),
+            "w_kr": normal((d.d_rope, d.d_model), d.d_model ** -0.5),
+            "w_uk": normal((d.n_heads * d.d_nope, d.d_c), d.d_c ** -0.5),
+            "w_uv": normal((d.n_heads * d.d_v, d.d_c), d.d_c ** -0.5),
+            "gamma": torch.ones(d.d_c, dtype=torch.bfloat16, device=dev),
+            "x": normal((1, nq, d.d_model)),
+            "q_nope": normal((1, nq, d.n_heads, d.d_nope)),
+            "q_r": normal((1, nq, d.n_heads, d.d_rope)),
+            "c_kv": torch.zeros((1, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev),
+            "k_r": torch.zeros((1, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev),
+        }
+        for fe in range(0, d.window_frames, d.chunk_frames):  # frames 0..20 in the ring
+            vm.cache_write(d, fe, 1, normal((1, nq, d.d_model)), L["w_dkv"], L["w_kr"],
+                           L["gamma"], L["c_kv"], L["k_r"])
+        layers.append(L)
+    out = torch.empty((1, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_workspace_bytes(d, 1), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    frame = [d.window_frames]  # the chunk being generated: frames 21..23, then 24..26, ...
+
+    def chunk():
+        fe = frame[0]
+        for _ in range(n_steps):
+            for L in layers:
+                vm.cache_write(d, fe, 1, L["x"], L["w_dkv"], L["w_kr"], L["gamma"], L["c_kv"],
+                               L["k_r"])
+                vm.attend(d, fe, 1, L["q_nope"], L["q_r"], L["w_uk"], L["w_uv"], L["c_kv"],
+                          L["k_r"], out, ws)
+        frame[0] = vm.window_advance(d, fe)
+
+    n_warm, n_time = max(1, min(args.warmup, 3)), max(1, min(args.steps, 10))
+    log(f"warmup {n_warm} chunks, timing {n_time}")
+    for _ in range(n_warm):
+        chunk()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_time + 1)]
+    ev[0].record()
+    for i in range(n_time):
+        chunk()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n_time)]
+    W = work_model(d)
+    flop = n_layers * n_steps * (W["attend"] + W["write"])
+    latent = n_layers * d.window_tokens * vm.cache_bytes_per_token(d)
+    # the dense per-head cache the latent one replaces: K and V of 12 heads x 128 per token
+    dense = n_layers * d.window_tokens * d.n_heads * 2 * d.d_v * 2
+    mean = sum(ms) / len(ms)
+    print(json.dumps({
+        "metric": "ms per chunk: 30 layers x 4 denoising steps of cache write + latent attend",
+        "value": round(mean, 3), "unit": "ms", "n_gpus": 1, "steps": n_time, "warmup": n_warm,
+        "higher_is_better": False, "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "ms_per_chunk_min_max": [round(min(ms), 3), round(max(ms), 3)],
+        "tflops": round(flop / (mean / 1e3) / 1e12, 2),
+        "latent_cache_bytes": latent, "dense_cache_bytes_same_window": dense,
+        "config": {"workload": ("Wan2.1-1.3B, one 3-frame chunk (4,680 tokens x 12 heads) "
+                                "through 30 attention layers x 4 denoising steps over a "
+                                "32,760-token 21-frame window each, then the window advance"),
+                   "layers": n_layers, "denoising_steps": n_steps, "seed": 3},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,6 +198,11 @@ def main():
     ap.add_argument("--x-buffers", type=int, default=32)
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a 256 MiB device copy (counter calibration)")
+    ap.add_argument("--workload", default="wan-layer-chunk-step",
+                    choices=("wan-layer-chunk-step", "wan-30-layer-chunk"),
+                    help="wan-layer-chunk-step: the headline (one layer's write + attend); "
+                         "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
+                         "plus the window advance")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -128,6 +214,10 @@ def main():
 
     import paper_2605_30351_amd as vm
     from workloads import WAN, make_layer_inputs
+
+    if args.workload == "wan-30-layer-chunk":
+        thirty_layer_chunk(args, vm, torch, WAN)
+        return
 
     d = WAN
     dev = torch.device("cuda:0")
