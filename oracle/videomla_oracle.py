@@ -13,6 +13,8 @@ What it computes, and where the paper defines it (VideoMLA, arXiv 2605.30351):
              "NoPE/RoPE Split and 3D RoPE");
 * ring slot  where a token's latents live in the sliding-window cache (Appendix "Chunk-Causal
              Sliding-Window Attention": FIFO eviction of whole frames);
+* dense      the comparator the latent cache replaces: per-head K = W_K x (rotated by 3D RoPE
+             over the whole head) and V = W_V x cached for every token, standard attention;
 * attention  the training-time form: per-head keys/values reconstructed explicitly
              (Eq. 2), score of Eq. 7, softmax over the active window, weighted sum of values.
              Section "Inference-Time Reparameterization" states that the absorbed latent form
@@ -265,6 +267,75 @@ def chunk_attention(inp, b: int, frame_end: int, rows=None, absorbed: bool = Fal
     w_uk, w_uv = bf16_bits_to_f64(inp.w_uk), bf16_bits_to_f64(inp.w_uv)
     fn = attend_absorbed if absorbed else attend_unabsorbed
     return fn(q_nope, q_rope, w_uk, w_uv, c_win, kro_win, dims)
+
+
+# --------------------------------------------------------------------------------------------
+# Dense per-head comparator: the cache VideoMLA replaces (Sec. "Introduction" and Table 3's
+# dense-KV baseline; Eq. 2 without the shared latent)
+# --------------------------------------------------------------------------------------------
+
+def dense_head_rope_dims(dims):
+    """RoPE geometry of a full dense head of width d = d_v: the Wan split of a head's channels
+    over (t, h, w), (d - 4*floor(d/6), 2*floor(d/6), 2*floor(d/6)) channels, with each axis'
+    band width equal to its channel count. At d = 128 this is (44, 42, 42) channels, the groups
+    the paper takes its RoPE key bands from (App. "NoPE/RoPE Split and 3D RoPE")."""
+    d = dims.d_v
+    k = d // 6
+    ch = (d - 4 * k, 2 * k, 2 * k)
+    return dims.replace(d_rope=d, rope_pairs=tuple(c // 2 for c in ch), rope_band_dim=ch)
+
+
+def dense_kv(x, w_k, w_v, pos, dims):
+    """Per-head keys and values of tokens x[T, d_model] (fp64): K_h = W_K,h x rotated by 3D
+    RoPE over the whole head at pos = (f, y, x), V_h = W_V,h x. w_k, w_v [H*d_v, d_model].
+    Returns (K [T, H, d_v], V [T, H, d_v])."""
+    T, H, d = x.shape[0], dims.n_heads, dims.d_v
+    k = (x @ w_k.T).reshape(T, H, d)
+    v = (x @ w_v.T).reshape(T, H, d)
+    f, y, xx = pos
+    hd = dense_head_rope_dims(dims)
+    k = rope3d(k, np.asarray(f)[:, None], np.asarray(y)[:, None], np.asarray(xx)[:, None], hd)
+    return k, v
+
+
+def dense_cache_write(x_chunk_bits, w_k_bits, w_v_bits, frame_end: int, dims):
+    """What the dense comparator's cache write must produce for one batch element's chunk:
+    rotated keys, values and the slots (the same FIFO ring placement as the latent cache)."""
+    x = bf16_bits_to_f64(x_chunk_bits)
+    pos = token_position(np.arange(x.shape[0]), frame_end, dims)
+    k, v = dense_kv(x, bf16_bits_to_f64(w_k_bits), bf16_bits_to_f64(w_v_bits), pos, dims)
+    return {"k": k, "v": v, "slots": ring_slot(*pos, dims)}
+
+
+def dense_attend(q, k_win, v_win, q_pos, dims, row_block=512):
+    """Standard per-head attention of queries q [Nq, H, d_v] (unrotated) over window keys
+    k_win [S, H, d_v] (rotated) and values v_win [S, H, d_v]: q rotated by the full-head RoPE
+    at q_pos, scores scaled by 1/sqrt(d_v) (or dims.softmax_scale when given), softmax over the
+    window. Returns [Nq, H, d_v] fp64."""
+    hd = dense_head_rope_dims(dims)
+    f, y, x = q_pos
+    qr = rope3d(q, np.asarray(f)[:, None], np.asarray(y)[:, None], np.asarray(x)[:, None], hd)
+    scale = dims.softmax_scale if dims.softmax_scale else 1.0 / np.sqrt(dims.d_v)
+    nq, H = q.shape[0], dims.n_heads
+    out = np.empty((nq, H, dims.d_v))
+    for h in range(H):
+        for r0 in range(0, nq, row_block):
+            p = _softmax_rows(scale * (qr[r0:r0 + row_block, h] @ k_win[:, h].T))
+            out[r0:r0 + row_block, h] = p @ v_win[:, h]
+    return out
+
+
+def dense_chunk_attention(inp, b: int, frame_end: int, rows=None):
+    """End-to-end dense reference for one batch element (inp: workloads.DenseInputs)."""
+    dims = inp.dims
+    lo, hi = window_frame_range(frame_end, dims)
+    x = bf16_bits_to_f64(inp.x[b][lo * dims.hw: hi * dims.hw])
+    n = np.arange(x.shape[0])
+    pos = (lo + n // dims.hw, (n % dims.hw) // dims.grid_w, n % dims.grid_w)
+    k, v = dense_kv(x, bf16_bits_to_f64(inp.w_k), bf16_bits_to_f64(inp.w_v), pos, dims)
+    rows = np.arange(dims.chunk_tokens) if rows is None else np.asarray(rows)
+    q = bf16_bits_to_f64(inp.q[b][rows])
+    return dense_attend(q, k, v, token_position(rows, frame_end, dims), dims)
 
 
 def ring_after_writes(n_frames_written: int, dims):

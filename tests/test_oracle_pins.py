@@ -369,3 +369,83 @@ def test_cache_write_positions_and_slots():
     assert y.tolist() == [0, 0, 1, 29, 0, 29]
     assert x.tolist() == [0, 51, 0, 51, 0, 51]
     assert O.ring_slot(f, y, x, WAN).tolist() == [0, 51, 52, 1559, 1560, 2 * 1560 + 1559]
+
+
+# ------------------------------------------------------------------------------------------
+# Dense per-head comparator
+# ------------------------------------------------------------------------------------------
+
+def test_dense_head_rope_split():
+    """The full-head split rule gives (44, 42, 42) channels at d = 128, Wan's own axis groups,
+    and (12, 10, 10) channels = (6, 5, 5) pairs at d = 32, the paper's RoPE-key split."""
+    hd = O.dense_head_rope_dims(WAN)
+    assert hd.d_rope == 128 and hd.rope_pairs == (22, 21, 21) and hd.rope_band_dim == (44, 42, 42)
+    hd32 = O.dense_head_rope_dims(WAN.replace(d_v=32))
+    assert hd32.rope_pairs == WAN_PAPER.rope_pairs
+
+
+def test_dense_zero_positions_equal_sdpa():
+    """At position 0 every rotation is the identity, so the comparator is plain scaled
+    dot-product attention per head (library routine, fp64)."""
+    rng = np.random.default_rng(11)
+    dims = TINY
+    nq, S, H, d = 9, 23, dims.n_heads, dims.d_v
+    q, k, v = rng.standard_normal((nq, H, d)), rng.standard_normal((S, H, d)), rng.standard_normal((S, H, d))
+    zero = (np.zeros(nq, np.int64),) * 3
+    got = O.dense_attend(q, k, v, zero, dims)
+    for h in range(H):
+        want = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(q[:, h])[None], torch.from_numpy(k[:, h])[None],
+            torch.from_numpy(v[:, h])[None]).numpy()[0]
+        np.testing.assert_allclose(got[:, h], want, rtol=0, atol=1e-12)
+
+
+def test_dense_equals_latent_with_composed_weights():
+    """With W_K,h = W_UK,h W_DKV and W_V,h = W_UV,h W_DKV (no norm, no RoPE key, no rotation),
+    dense per-head attention and the latent reconstruction of Eq. 2 compute the same thing:
+    the latent cache is a factorization of the dense one."""
+    dims = TINY.replace(softmax_scale=1.0 / math.sqrt(TINY.d_nope + TINY.d_rope))
+    assert dims.d_nope == dims.d_v
+    rng = np.random.default_rng(12)
+    H, dn, dc, dv, D = dims.n_heads, dims.d_nope, dims.d_c, dims.d_v, dims.d_model
+    x = rng.standard_normal((40, D))
+    w_dkv, w_uk, w_uv = rng.standard_normal((dc, D)), rng.standard_normal((H * dn, dc)), rng.standard_normal((H * dv, dc))
+    c = x @ w_dkv.T
+    q = rng.standard_normal((7, H, dn))
+    latent = O.attend_unabsorbed(q, np.zeros((7, H, dims.d_rope)), w_uk, w_uv, c,
+                                 np.zeros((40, dims.d_rope)), dims)
+    w_k = np.concatenate([w_uk[h * dn:(h + 1) * dn] @ w_dkv for h in range(H)])
+    w_v = np.concatenate([w_uv[h * dv:(h + 1) * dv] @ w_dkv for h in range(H)])
+    k = (x @ w_k.T).reshape(40, H, dv)
+    v = (x @ w_v.T).reshape(40, H, dv)
+    dense = O.dense_attend(q, k, v, (np.zeros(7, np.int64),) * 3, dims)
+    np.testing.assert_allclose(dense, latent, rtol=1e-11, atol=1e-11)
+
+
+def test_dense_scores_invariant_under_common_shift():
+    """Shifting every query and key position by the same (t, h, w) offset leaves the comparator's
+    output unchanged (relative-position property of the full-head RoPE)."""
+    dims = TINY
+    rng = np.random.default_rng(13)
+    x = rng.standard_normal((20, dims.d_model))
+    w_k = rng.standard_normal((dims.n_heads * dims.d_v, dims.d_model)) / 8
+    w_v = rng.standard_normal((dims.n_heads * dims.d_v, dims.d_model)) / 8
+    q = rng.standard_normal((5, dims.n_heads, dims.d_v))
+    kpos = (rng.integers(0, 9, 20), rng.integers(0, 4, 20), rng.integers(0, 4, 20))
+    qpos = (rng.integers(0, 9, 5), rng.integers(0, 4, 5), rng.integers(0, 4, 5))
+    shift = (17, 3, -5)
+    k, v = O.dense_kv(x, w_k, w_v, kpos, dims)
+    ks, _ = O.dense_kv(x, w_k, w_v, tuple(p + s for p, s in zip(kpos, shift)), dims)
+    a = O.dense_attend(q, k, v, qpos, dims)
+    b = O.dense_attend(q, ks, v, tuple(p + s for p, s in zip(qpos, shift)), dims)
+    np.testing.assert_allclose(b, a, rtol=0, atol=1e-11)
+
+
+def test_dense_cache_write_places_like_the_latent_cache():
+    from workloads import make_dense_inputs
+    inp = make_dense_inputs(TINY, seed=3, n_frames=6)
+    hw = TINY.hw
+    got = O.dense_cache_write(inp.x[0, 5 * hw:6 * hw], inp.w_k, inp.w_v, 5, TINY)
+    f, y, x = O.token_position(np.arange(hw), 5, TINY)
+    assert np.array_equal(got["slots"], O.ring_slot(f, y, x, TINY))
+    assert got["k"].shape == (hw, TINY.n_heads, TINY.d_v)

@@ -136,6 +136,36 @@ def make_layer_inputs(dims: Dims, seed: int, n_frames: int, batch: int = 1, norm
                        f32_to_bf16_bits(qn), f32_to_bf16_bits(qr))
 
 
+@dataclass
+class DenseInputs:
+    """Seeded inputs of the dense per-head comparator (bf16 bit patterns).
+
+    x      [batch, n_frames * HW, d_model]   token activations
+    w_k    [n_heads * d_v, d_model]          per-head key projection
+    w_v    [n_heads * d_v, d_model]          per-head value projection
+    q      [batch, chunk_tokens, n_heads, d_v]   unrotated queries of the chunk
+    """
+
+    dims: Dims
+    batch: int
+    n_frames: int
+    x: np.ndarray
+    w_k: np.ndarray
+    w_v: np.ndarray
+    q: np.ndarray
+
+
+def make_dense_inputs(dims: Dims, seed: int, n_frames: int, batch: int = 1) -> DenseInputs:
+    """Draw the comparator's inputs in a fixed order: x frames, W_K, W_V, q."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    d = dims
+    x = _normal_bf16(rng, (batch, n_frames * d.hw, d.d_model))
+    w_k = _normal_bf16(rng, (d.n_heads * d.d_v, d.d_model), 1.0 / np.sqrt(d.d_model))
+    w_v = _normal_bf16(rng, (d.n_heads * d.d_v, d.d_model), 1.0 / np.sqrt(d.d_model))
+    q = _normal_bf16(rng, (batch, d.chunk_tokens, d.n_heads, d.d_v))
+    return DenseInputs(d, batch, n_frames, x, w_k, w_v, q)
+
+
 def chunk_frame_ends(dims: Dims, n_frames: int) -> list[int]:
     """First frame of each chunk when frames 0 .. n_frames-1 are written chunk by chunk."""
     assert n_frames % dims.chunk_frames == 0
