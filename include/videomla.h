@@ -130,6 +130,56 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
                     const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Dense per-head comparator: the cache VideoMLA replaces, built only to measure the latent
+ * path against it on the same GPU (per-head keys and values of Eq. 2 without the shared
+ * latent; the 3,072-scalar-per-token layout of the Introduction). Head width d = d_v.
+ *
+ * Full-head 3D RoPE: the d channels of a head are split over (t, h, w) as
+ * (d - 4 floor(d/6), 2 floor(d/6), 2 floor(d/6)) channels (44, 42, 42 at d = 128), t first,
+ * interleaved pairs as for k^R, each axis with band width D_a equal to its channel count;
+ * rope_base is shared with the latent path, dims->rope_pairs and rope_band_dim are ignored.
+ */
+
+/* Bytes the dense ring holds per token and layer: 2 * n_heads * d_v * 2 (6,144 B for Wan). */
+size_t videomla_dense_cache_bytes_per_token(const videomla_dims* dims);
+
+/*
+ * videomla_dense_cache_write -- K_h = W_K,h x rotated by the full-head 3D RoPE at the token's
+ * absolute (f, y, x), V_h = W_V,h x, written at the same ring slots as videomla_cache_write.
+ *   x          [batch][chunk_frames * HW][d_model]        bf16
+ *   w_k, w_v   [n_heads * d_v][d_model]                   bf16 (head h = rows h*d_v ..)
+ *   kv         [batch][window_frames * HW][n_heads][2 * d_v]   bf16 ring, written in place:
+ *              row (slot, h) holds the rotated K_h, then V_h
+ *   slots_out  [chunk_frames * HW] int32, or NULL
+ * Arithmetic: bf16 operands, fp32 accumulation and rotation, bf16 round-to-nearest-even.
+ * Requires d_model % 64 == 0, d_v % 4 == 0, d_v <= 128, (2 n_heads d_v) % 128 == 0.
+ */
+int videomla_dense_cache_write(const videomla_dims* dims, const videomla_window* win,
+                               int32_t batch, const uint16_t* x, const uint16_t* w_k,
+                               const uint16_t* w_v, uint16_t* kv, int32_t* slots_out,
+                               void* stream);
+
+/* Bytes of device workspace videomla_dense_attend needs for this shape and batch. */
+size_t videomla_dense_attend_workspace_bytes(const videomla_dims* dims, int32_t batch);
+
+/*
+ * videomla_dense_attend -- standard per-head softmax attention of the chunk's queries over the
+ * same window as videomla_attend:
+ *   q'   = RoPE_3D,head(q[b,n,h]) at the token's absolute (f, y, x)
+ *   out  = sum_j softmax_j(scale * q' . K_h[j]) V_h[j]
+ * with scale = softmax_scale, or 1 / sqrt(d_v) when it is 0.
+ *   q     [batch][chunk_frames * HW][n_heads][d_v]   bf16, unrotated
+ *   kv    the ring as written by videomla_dense_cache_write
+ *   out   [batch][chunk_frames * HW][n_heads][d_v]   bf16
+ *   workspace  device buffer of at least videomla_dense_attend_workspace_bytes() bytes
+ * Arithmetic as videomla_attend. Requires d_v == 128. The work partition follows
+ * videomla_set_attend_workgroups.
+ */
+int videomla_dense_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                          const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 /* Slide the window after the last denoising step of a chunk: frame_end += chunk_frames.
  * Host only; eviction is implicit (the next chunk's write overwrites the oldest frames). */
 int videomla_window_advance(const videomla_dims* dims, videomla_window* win);
@@ -159,7 +209,8 @@ int videomla_set_attend_workgroups(int32_t n_workgroups);
  * Kernel timing with HIP events, for benchmarks. When enabled, every kernel the library
  * launches is bracketed by two events recorded on the same stream. After the caller has
  * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed
- * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj") into
+ * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj",
+ * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge") into
  * *count and *total_ms, and forgets them. Timing state is process-wide and not thread-safe.
  */
 int videomla_timing_enable(int32_t enable);

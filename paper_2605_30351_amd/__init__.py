@@ -11,6 +11,10 @@ from ._lib import (  # noqa: F401
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,
+    dense_attend,
+    dense_attend_workspace_bytes,
+    dense_cache_bytes_per_token,
+    dense_cache_write,
     make_dims,
     set_attend_workgroups,
     slot_of,

@@ -26,6 +26,8 @@ EXPORTED = (
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
     "videomla_timing_enable", "videomla_timing_read",
+    "videomla_dense_cache_bytes_per_token", "videomla_dense_cache_write",
+    "videomla_dense_attend_workspace_bytes", "videomla_dense_attend",
 )
 
 
@@ -73,6 +75,15 @@ _lib.videomla_timing_enable.restype = ctypes.c_int
 _lib.videomla_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
                                       ctypes.POINTER(ctypes.c_double)]
 _lib.videomla_timing_read.restype = ctypes.c_int
+_lib.videomla_dense_cache_bytes_per_token.argtypes = [_DP]
+_lib.videomla_dense_cache_bytes_per_token.restype = ctypes.c_size_t
+_lib.videomla_dense_cache_write.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P]
+_lib.videomla_dense_cache_write.restype = ctypes.c_int
+_lib.videomla_dense_attend_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
+_lib.videomla_dense_attend_workspace_bytes.restype = ctypes.c_size_t
+_lib.videomla_dense_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t,
+                                       _P]
+_lib.videomla_dense_attend.restype = ctypes.c_int
 
 
 class VideomlaError(RuntimeError):
@@ -168,6 +179,46 @@ def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r,
     _check(_lib.videomla_attend(
         ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
         _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
+        _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
+
+
+def dense_cache_bytes_per_token(dims) -> int:
+    return int(_lib.videomla_dense_cache_bytes_per_token(ctypes.byref(make_dims(dims))))
+
+
+def dense_cache_write(dims, frame_end: int, batch: int, x, w_k, w_v, kv, slots=None,
+                      stream=None):
+    """videomla_dense_cache_write on torch tensors (the dense per-head comparator)."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    _need(x, "x", batch * d.chunk_frames * hw * d.d_model)
+    _need(w_k, "w_k", d.n_heads * d.d_v * d.d_model)
+    _need(w_v, "w_v", d.n_heads * d.d_v * d.d_model)
+    _need(kv, "kv", batch * d.window_frames * hw * d.n_heads * 2 * d.d_v)
+    if slots is not None:
+        _need(slots, "slots", d.chunk_frames * hw)
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_dense_cache_write(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(x, "x"), _ptr(w_k, "w_k"),
+        _ptr(w_v, "w_v"), _ptr(kv, "kv"), _ptr(slots, "slots", (torch.int32,)), _stream(stream)))
+
+
+def dense_attend_workspace_bytes(dims, batch: int) -> int:
+    return int(_lib.videomla_dense_attend_workspace_bytes(ctypes.byref(make_dims(dims)), int(batch)))
+
+
+def dense_attend(dims, frame_end: int, batch: int, q, kv, out, workspace, stream=None):
+    """videomla_dense_attend on torch tensors; `workspace` is a uint8 device tensor."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    nq = d.chunk_frames * hw
+    _need(q, "q", batch * nq * d.n_heads * d.d_v)
+    _need(kv, "kv", batch * d.window_frames * hw * d.n_heads * 2 * d.d_v)
+    _need(out, "out", batch * nq * d.n_heads * d.d_v)
+    w = VideomlaWindow(int(frame_end))
+    ws = _ptr(workspace, "workspace", (torch.uint8,))
+    _check(_lib.videomla_dense_attend(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q, "q"), _ptr(kv, "kv"),
         _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
 
 

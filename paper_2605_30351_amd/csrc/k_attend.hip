@@ -137,46 +137,61 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 constexpr float kLazyMax = 8.0f;
 
 
-template <int DC, int DR, int QB, int NW, int BN>
+// Tile layouts. Latent (DENSE = false): a tile row is [c_kv (DC) | k_r (DR) | pad], the scores
+// contract over all of it and V is its first DC columns. Dense comparator (DENSE = true, DC =
+// head width, DR = 0): a tile row is [K_h | V_h] of one head, the scores contract over K_h and V
+// is the second half.
+template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
   static constexpr int DQKP = (DQK + 15) / 16 * 16;
   static constexpr int KSTEPS = DQKP / 16;
   static constexpr int DVB = (DC + 31) / 32;
   static constexpr int KB = BN / 32;       // 32-key blocks per tile
-  // Tile rows are DQKP elements with no padding; the 16-byte chunks of row r sit at chunk
-  // index XOR ((r / 4) mod 4), which makes the 16-row operand reads of the score MFMA and the
-  // 4-row transpose reads of the PV MFMA hit 16 distinct 4-bank groups each.
-  static constexpr int STRIDE = DQKP;
+  static constexpr int VOFF = DENSE ? DQKP : 0;  // first V column of a tile row
+  // Tile rows have no padding. Latent rows (DQKP elements): the 16-byte chunks of row r sit at
+  // chunk index XOR ((r / 4) mod 4). Dense rows (2 DQKP = 32 chunks, a multiple of 16 bank
+  // groups): chunk index XOR (4 (r mod 4) + (r / 4) mod 4) within groups of 16. Either way the
+  // 16-row operand reads of the score MFMA and the 4-row transpose reads of the PV MFMA hit 16
+  // distinct 4-bank groups each.
+  static constexpr int STRIDE = DENSE ? 2 * DQKP : DQKP;
   static constexpr int NT = NW * 64;
   static constexpr int ROWS = NW * QB * 32;
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
-  static constexpr int CPR = DQKP / 8;            // 16-byte chunks per tile row
+  static constexpr int CPR = STRIDE / 8;          // 16-byte chunks per tile row
   static constexpr int NDMA = BN * CPR / 64;      // 1 KB direct-to-LDS loads per tile
   static constexpr int DMA_PER_WAVE = (NDMA + NW - 1) / NW;
   static constexpr int TILE = BN * STRIDE;
   static constexpr int NBUF = 3;
   static_assert(DC % 8 == 0 && DR % 8 == 0, "latent and rope widths must be multiples of 8");
   static_assert(BN % 32 == 0, "key tile must be a multiple of 32");
-  static_assert(DVB * 32 <= STRIDE, "transpose reads must stay inside a tile row");
+  static_assert(VOFF + DVB * 32 <= STRIDE, "transpose reads must stay inside a tile row");
   static_assert(DQKP % 32 == 0, "the swizzle permutes chunks within aligned groups of four");
+  static_assert(!DENSE || (CPR % 16 == 0 && DR == 0 && DC % 32 == 0), "dense tile layout");
   static_assert(BN * CPR % 64 == 0, "a tile is a whole number of 64-lane loads");
+  // chunk position of logical chunk c in row r (an involution: it also maps back)
+  __device__ static constexpr int pos(int r, int c) {
+    return DENSE ? ((c & ~15) | ((c ^ (((r & 3) << 2) | ((r >> 2) & 3))) & 15))
+                 : ((c & ~3) | ((c ^ (r >> 2)) & 3));
+  }
   // element offset of (row r, column c) inside a tile
   __device__ static constexpr int at(int r, int c) {
-    return r * STRIDE + ((((c >> 3) ^ (r >> 2)) & 3) | ((c >> 3) & ~3)) * 8 + (c & 7);
+    return r * STRIDE + pos(r, c >> 3) * 8 + (c & 7);
   }
 };
 
-template <int DC, int DR, int QB, int NW, int BN, int WPC>
+template <int DC, int DR, int QB, int NW, int BN, int WPC, bool DENSE = false>
 __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const AttendArgs a) {
-  using C = AttCfg<DC, DR, QB, NW, BN>;
+  using C = AttCfg<DC, DR, QB, NW, BN, DENSE>;
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
-  const int rows_b = a.geo.chunk_tokens * a.n_heads;
+  // query rows per batch element: (token, head) pairs, head-minor (latent); (head, token)
+  // pairs with every head padded to whole row blocks (dense: a row block is one head's)
+  const int rows_b = DENSE ? a.n_heads * a.nq_pad : a.geo.chunk_tokens * a.n_heads;
 
   // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
   // tiles of one row block is a segment with its own partial result.
@@ -210,21 +225,36 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // meets the zero padding of q_cat). Rows at or past key_end are clamped to key_end - 1, so
   // every read stays inside the valid ring and every staged value is finite; their scores
   // are masked below.
-  const uint16_t* c_base = a.c_kv + (size_t)b * a.geo.ring_tokens * DC;
-  const uint16_t* r_base = a.k_r + (size_t)b * a.geo.ring_tokens * DR;
   int dma_row[C::DMA_PER_WAVE];
   const uint16_t* dma_src[C::DMA_PER_WAVE];
   bool dma_kr[C::DMA_PER_WAVE];
+  if constexpr (DENSE) {
+    // one head's [K | V] rows: ring [B][ring_tokens][H][2 * head width]
+    const int h = rb / (a.row_blocks / a.n_heads);
+    const uint16_t* kv_base = a.kv + ((size_t)b * a.geo.ring_tokens * a.n_heads + h) * C::STRIDE;
 #pragma unroll
-  for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
-    const int j = wave + NW * i;
-    const int slot = (j < C::NDMA ? j : 0) * 64 + lane;
-    const int r = slot / C::CPR, pcn = slot % C::CPR;
-    const int lc = (pcn & ~3) | ((pcn & 3) ^ ((r >> 2) & 3));
-    dma_row[i] = r;
-    dma_kr[i] = lc >= C::OCT_C;
-    dma_src[i] = lc < C::OCT_C ? c_base + lc * 8
-                               : r_base + (lc < C::OCT_C + C::OCT_R ? (lc - C::OCT_C) * 8 : 0);
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const int j = wave + NW * i;
+      const int slot = (j < C::NDMA ? j : 0) * 64 + lane;
+      const int r = slot / C::CPR;
+      dma_row[i] = r;
+      dma_kr[i] = false;
+      dma_src[i] = kv_base + C::pos(r, slot % C::CPR) * 8;
+    }
+  } else {
+    const uint16_t* c_base = a.c_kv + (size_t)b * a.geo.ring_tokens * DC;
+    const uint16_t* r_base = a.k_r + (size_t)b * a.geo.ring_tokens * DR;
+#pragma unroll
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const int j = wave + NW * i;
+      const int slot = (j < C::NDMA ? j : 0) * 64 + lane;
+      const int r = slot / C::CPR, pcn = slot % C::CPR;
+      const int lc = (pcn & ~3) | ((pcn & 3) ^ ((r >> 2) & 3));
+      dma_row[i] = r;
+      dma_kr[i] = lc >= C::OCT_C;
+      dma_src[i] = lc < C::OCT_C ? c_base + lc * 8
+                                 : r_base + (lc < C::OCT_C + C::OCT_R ? (lc - C::OCT_C) * 8 : 0);
+    }
   }
 
 
@@ -256,16 +286,27 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       const int j = wave + NW * i;
       if (C::NDMA % NW == 0 || j < C::NDMA) {
         const int key = min(k0 + dma_row[i], key_end - 1);
-        const uint16_t* src = dma_src[i] + (size_t)key * (dma_kr[i] ? DR : DC);
+        const uint16_t* src =
+            dma_src[i] + (size_t)key * (DENSE ? a.n_heads * C::STRIDE : (dma_kr[i] ? DR : DC));
         lds_dma16(src, __builtin_amdgcn_readfirstlane(base + 1024u * j));
       }
     }
   };
-  // K operand of step ks: row l32 (+32 kb), chunk 2 ks + g, i.e. C::at() with the XOR folded
-  // into one of two per-lane bases (ks even / odd) so that ks and kb become immediate offsets
+  // K operand of step ks: row l32 (+32 kb), chunk 2 ks + g, i.e. C::at(). Latent: the XOR folded
+  // into one of two per-lane bases (ks even / odd) so that ks and kb become immediate offsets;
+  // dense: one offset per step (its 4-bit XOR reaches every chunk of a group).
   const int hk = (l32 >> 2) & 3;
   const int koff_e = l32 * C::STRIDE + ((g ^ hk) << 3);
   const int koff_o = l32 * C::STRIDE + (((2 + g) ^ hk) << 3) - 16;
+  int koff_d[DENSE ? C::KSTEPS : 1];
+  if constexpr (DENSE) {
+#pragma unroll
+    for (int ks = 0; ks < C::KSTEPS; ++ks) koff_d[ks] = C::at(l32, ks * 16 + 8 * g);
+  }
+  auto koff = [&](int ks) {
+    if constexpr (DENSE) return koff_d[ks];
+    else return ((ks & 1) ? koff_o : koff_e) + ks * 16;
+  };
   // S^T for one tile, the query blocks sharing each K operand read
   auto scores = [&](const uint16_t* buf, f32x16 (&s)[QB][C::KB]) {
 #pragma unroll
@@ -275,7 +316,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 #pragma unroll
       for (int ks = 0; ks < C::KSTEPS; ++ks) {
         const bf16x8 k = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            &buf[((ks & 1) ? koff_o : koff_e) + kb * 32 * C::STRIDE + ks * 16]));
+            &buf[koff(ks) + kb * 32 * C::STRIDE]));
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mfma32(k, q[qb][ks], s[qb][kb]);
       }
@@ -339,8 +380,17 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // column tr_col (+32 d); rows 4g.. have swizzle g, rows 4g+8.. have g+2, for every kk
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int vofs_lo = C::at(4 * g + tr_row, tr_col);
-  const int vofs_hi = C::at(4 * g + tr_row + 8, tr_col);
+  const int vofs_lo = C::at(4 * g + tr_row, C::VOFF + tr_col);
+  const int vofs_hi = C::at(4 * g + tr_row + 8, C::VOFF + tr_col);
+  // dense: the 4-bit XOR also permutes the 32-column blocks d, so one offset per (half, d)
+  int vofs_d[2][DENSE ? C::DVB : 1];
+  if constexpr (DENSE) {
+#pragma unroll
+    for (int d = 0; d < C::DVB; ++d) {
+      vofs_d[0][d] = C::at(4 * g + tr_row, C::VOFF + tr_col + 32 * d);
+      vofs_d[1][d] = C::at(4 * g + tr_row + 8, C::VOFF + tr_col + 32 * d);
+    }
+  }
 
   // One pipelined step. s_cur holds tile t's scores, already masked, with m_run high enough
   // for them. Block A: scores of tile t+1 (MFMA) and tile t's exponentials (VALU). Block B: PV
@@ -362,15 +412,18 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     constexpr int NSLOT = NS > NPV + 2 ? NS : NPV + 2;
     constexpr int NSM = NS < 4 ? NS : 4;  // slots carrying the softmax; pairs 0-3 precede PV
     auto kread = [&](int ks) {
-      return as_bf16x8(*reinterpret_cast<const u32x4*>(
-          &nxt[((ks & 1) ? koff_o : koff_e) + ks * 16]));
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(&nxt[koff(ks)]));
     };
     const lds_u16* vlo = as_lds(cur) + vofs_lo;
     const lds_u16* vhi = as_lds(cur) + vofs_hi;
     auto vread = [&](int j) {  // A operand of PV MFMA j: kk = j / DVB, d = j % DVB
       const int kk = j / C::DVB, d = j % C::DVB;
-      return join_bf16x8(lds_read_tr(vlo + kk * 16 * C::STRIDE + d * 32),
-                         lds_read_tr(vhi + kk * 16 * C::STRIDE + d * 32));
+      if constexpr (DENSE)
+        return join_bf16x8(lds_read_tr(as_lds(cur) + vofs_d[0][d] + kk * 16 * C::STRIDE),
+                           lds_read_tr(as_lds(cur) + vofs_d[1][d] + kk * 16 * C::STRIDE));
+      else
+        return join_bf16x8(lds_read_tr(vlo + kk * 16 * C::STRIDE + d * 32),
+                           lds_read_tr(vhi + kk * 16 * C::STRIDE + d * 32));
     };
     // The row sum is taken over the bf16-rounded probabilities, the same values the PV MFMA
     // multiplies, so numerator and denominator see identical weights.
@@ -610,7 +663,24 @@ hipError_t launch_attend_t(const AttendArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Dense comparator: one head of 128 channels per row block, K and V rows interleaved per head.
+using DenseShape = AttShape<192, 32>;  // same wave count, tile and occupancy as the latent kernel
+constexpr int kDenseHead = 128;
+using DenseCfg = AttCfg<kDenseHead, 0, DenseShape::QB, DenseShape::NW, DenseShape::BN, true>;
+
 }  // namespace
+
+bool dense_attend_supported(int d_head) { return d_head == kDenseHead; }
+int dense_attend_rows_per_block() { return DenseCfg::ROWS; }
+int dense_attend_keys_per_tile() { return DenseShape::BN; }
+
+hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s) {
+  if (a.d_v != kDenseHead) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((latent_attend_kernel<kDenseHead, 0, DenseShape::QB, DenseShape::NW,
+                                           DenseShape::BN, DenseShape::WPC, true>),
+                     dim3(a.n_wg), dim3(DenseCfg::NT), 0, s, a);
+  return hipGetLastError();
+}
 
 bool latent_attend_supported(int d_c, int d_rope) {
   return (d_c == 192 && d_rope == 32) || (d_c == 16 && d_rope == 8);

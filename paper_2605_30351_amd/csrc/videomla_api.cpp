@@ -97,8 +97,13 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
 }
 
 // ---- timing -------------------------------------------------------------------------------
-enum KernelId { K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ, K_COUNT };
-const char* kKernelNames[K_COUNT] = {"cache_write", "q_absorb", "latent_attend", "out_proj"};
+enum KernelId {
+  K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
+  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_COUNT
+};
+const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
+                                     "out_proj",          "dense_cache_write", "dense_q_prep",
+                                     "dense_attend",      "dense_merge"};
 
 struct TimingRec {
   int kernel;
@@ -151,17 +156,15 @@ struct Partition {
   int64_t U;
 };
 
-Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+// rows: query rows per row block; RB: row blocks per batch element; bn: keys per tile;
+// wpc: resident workgroups per compute unit.
+Partition make_partition(int rows, int RB, int bn, int wpc, int32_t batch, int64_t n_valid) {
   Partition p{};
-  p.rows = latent_attend_rows_per_block(d->d_c, d->d_rope);
-  const int bn = latent_attend_keys_per_tile(d->d_c, d->d_rope);
-  const int64_t rows_b = (int64_t)d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
-  p.RB = (int)((rows_b + p.rows - 1) / p.rows);
+  p.rows = rows;
+  p.RB = RB;
   p.T = (int)((n_valid + bn - 1) / bn);
   p.U = (int64_t)batch * p.RB * p.T;
-  const int64_t G = g_attend_wg > 0
-                       ? g_attend_wg
-                       : (int64_t)device_cu_count() * latent_attend_wgs_per_cu(d->d_c, d->d_rope);
+  const int64_t G = g_attend_wg > 0 ? g_attend_wg : (int64_t)device_cu_count() * wpc;
   p.G = (int)(G < p.U ? G : p.U);
   p.max_seg = 1;
   for (int64_t rbg = 0; rbg < (int64_t)batch * p.RB; ++rbg) {
@@ -171,12 +174,34 @@ Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_vali
   return p;
 }
 
+Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+  const int rows = latent_attend_rows_per_block(d->d_c, d->d_rope);
+  const int64_t rows_b = (int64_t)d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
+  return make_partition(rows, (int)((rows_b + rows - 1) / rows),
+                        latent_attend_keys_per_tile(d->d_c, d->d_rope),
+                        latent_attend_wgs_per_cu(d->d_c, d->d_rope), batch, n_valid);
+}
+
+// Dense comparator: every head's chunk rows padded to whole row blocks.
+int dense_nq_pad(const videomla_dims* d) {
+  const int rows = dense_attend_rows_per_block();
+  const int nq = d->chunk_frames * d->grid_h * d->grid_w;
+  return (nq + rows - 1) / rows * rows;
+}
+
+Partition dense_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+  const int rows = dense_attend_rows_per_block();
+  return make_partition(rows, d->n_heads * (dense_nq_pad(d) / rows), dense_attend_keys_per_tile(),
+                        1, batch, n_valid);
+}
+
 // Slots the workspace must hold for any window this shape can attend over (chunk_frames up to
 // window_frames valid frames).
-int workspace_max_seg(const videomla_dims* d, int32_t batch) {
+int workspace_max_seg(const videomla_dims* d, int32_t batch, bool dense = false) {
   int m = 1;
   for (int f = d->chunk_frames; f <= d->window_frames; ++f) {
-    const int s = attend_partition(d, batch, (int64_t)f * d->grid_h * d->grid_w).max_seg;
+    const int64_t n_valid = (int64_t)f * d->grid_h * d->grid_w;
+    const int s = (dense ? dense_partition(d, batch, n_valid) : attend_partition(d, batch, n_valid)).max_seg;
     if (s > m) m = s;
   }
   return m;
@@ -195,6 +220,38 @@ WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_se
   w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_c * 4, 256);
   w.total = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
   return w;
+}
+
+// Dense comparator workspace: q_cat [B][H][nq_pad][d_v] bf16, then the partial results.
+WorkspaceLayout dense_workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
+  const size_t rows = (size_t)batch * d->n_heads * dense_nq_pad(d);
+  WorkspaceLayout w{};
+  w.qcat_off = 0;
+  w.opart_off = round_up(rows * d->d_v * 2, 256);
+  w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_v * 4, 256);
+  w.total = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
+  return w;
+}
+
+// Full-head RoPE of the dense comparator: channels (d - 4 floor(d/6), 2 floor(d/6),
+// 2 floor(d/6)) over (t, h, w), each axis' band width equal to its channel count.
+RopeTable make_dense_rope(const videomla_dims* d) {
+  videomla_dims hd = *d;
+  const int k = d->d_v / 6;
+  const int ch[3] = {d->d_v - 4 * k, 2 * k, 2 * k};
+  hd.d_rope = d->d_v;
+  for (int a = 0; a < 3; ++a) {
+    hd.rope_pairs[a] = ch[a] / 2;
+    hd.rope_band_dim[a] = ch[a];
+  }
+  return make_rope(&hd);
+}
+
+int check_dense_head(const videomla_dims* d) {
+  if (d->d_v % 4 || d->d_v / 2 > kMaxRopePairs)
+    return fail(VIDEOMLA_EUNSUPPORTED, "dense head width d_v must be a multiple of 4 and <= %d, got %d",
+                2 * kMaxRopePairs, d->d_v);
+  return VIDEOMLA_OK;
 }
 
 int check_attend_shape(const videomla_dims* d) {
@@ -335,6 +392,92 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   if (e != hipSuccess) return hip_fail(e, "latent_attend");
   e = timed(K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
   if (e != hipSuccess) return hip_fail(e, "out_proj");
+  return ok();
+}
+
+size_t videomla_dense_cache_bytes_per_token(const videomla_dims* d) {
+  if (check_dims(d)) return 0;
+  return 2 * (size_t)d->n_heads * d->d_v * 2;
+}
+
+int videomla_dense_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                               const uint16_t* x, const uint16_t* w_k, const uint16_t* w_v,
+                               uint16_t* kv, int32_t* slots_out, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!x || !w_k || !w_v || !kv) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
+  if (int e = check_dense_head(d)) return e;
+  if ((2 * d->n_heads * d->d_v) % 128)
+    return fail(VIDEOMLA_EUNSUPPORTED, "2 * n_heads * d_v must be a multiple of 128, got %d",
+                2 * d->n_heads * d->d_v);
+  if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) || !aligned16(kv))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  DenseWriteArgs a{};
+  a.x = x; a.w_k = w_k; a.w_v = w_v; a.kv = kv; a.slots = slots_out;
+  a.batch = batch; a.d_model = d->d_model; a.n_heads = d->n_heads; a.d_head = d->d_v;
+  a.geo = make_geo(d, w);
+  a.rope = make_dense_rope(d);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = timed(K_DENSE_CACHE_WRITE, s, [&] { return launch_dense_cache_write(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_cache_write");
+  return ok();
+}
+
+size_t videomla_dense_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
+  if (check_dims(d) || batch <= 0) return 0;
+  if (!dense_attend_supported(d->d_v)) return 0;
+  return dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true)).total;
+}
+
+int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                          const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!q || !kv || !out) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (!dense_attend_supported(d->d_v))
+    return fail(VIDEOMLA_EUNSUPPORTED, "dense attention is built for d_v = 128, got %d", d->d_v);
+  if (!aligned16(q) || !aligned16(kv) || !aligned16(out))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const WorkspaceLayout L = dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true));
+  if (!workspace || workspace_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+
+  AttendArgs a{};
+  a.q = q; a.kv = kv; a.out = out;
+  char* ws = static_cast<char*>(workspace);
+  a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
+  a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
+  a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
+  a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v;
+  a.d_c = d->d_v; a.d_rope = 0; a.d_nope = 0;
+  a.dqk_pad = d->d_v;
+  a.nq_pad = dense_nq_pad(d);
+  a.geo = make_geo(d, w);
+  a.rope = make_dense_rope(d);
+  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
+  const Partition P = dense_partition(d, batch, a.n_valid);
+  a.n_wg = P.G;
+  a.att_rows = P.rows;
+  a.row_blocks = P.RB;
+  a.tiles_per_row = P.T;
+  a.units = P.U;
+  a.max_seg = P.max_seg;
+  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale : 1.0 / std::sqrt((double)d->d_v);
+  a.qscale = (float)(scale * 1.4426950408889634);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = timed(K_DENSE_Q_PREP, s, [&] { return launch_dense_q_prep(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_q_prep");
+  e = timed(K_DENSE_ATTEND, s, [&] { return launch_dense_attend(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_attend");
+  e = timed(K_DENSE_MERGE, s, [&] { return launch_dense_merge(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_merge");
   return ok();
 }
 

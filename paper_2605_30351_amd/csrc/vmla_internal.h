@@ -6,7 +6,7 @@
 
 namespace vmla {
 
-constexpr int kMaxRopePairs = 32;
+constexpr int kMaxRopePairs = 64;  // a whole dense head of 128 channels
 
 // Per RoPE pair p (interleaved channels 2p, 2p+1 of the d_rope vector): the axis whose
 // coordinate drives it (0 = t, 1 = h, 2 = w) and theta = base^(-2k / D_axis), in double.
@@ -62,6 +62,22 @@ struct AttendArgs {
   float qscale;            // softmax scale * log2(e), folded into the absorbed query
   Geometry geo;
   RopeTable rope;
+  // dense per-head comparator only (rows are (head, token) pairs, each head padded to nq_pad)
+  const uint16_t* q;       // [B][Nq][H][d_v] unrotated queries
+  const uint16_t* kv;      // ring [B][ring_tokens][H][2 * d_v]: rotated K_h, then V_h
+  int32_t nq_pad;          // query rows per head, a whole number of row blocks
+};
+
+// Dense comparator's cache write: K = W_K x (rotated by 3D RoPE over each whole head), V = W_V x.
+struct DenseWriteArgs {
+  const uint16_t* x;       // [B][chunk_tokens][d_model]
+  const uint16_t* w_k;     // [H*d_v][d_model]
+  const uint16_t* w_v;     // [H*d_v][d_model]
+  uint16_t* kv;            // [B][ring_tokens][H][2 * d_v]
+  int32_t* slots;          // [chunk_tokens] or nullptr
+  int32_t batch, d_model, n_heads, d_head;
+  Geometry geo;
+  RopeTable rope;          // d_head / 2 pairs
 };
 
 // Workgroup whose unit range [w*U/G, (w+1)*U/G) contains `unit`.
@@ -74,11 +90,18 @@ hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
+hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);
+hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s);
+hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s);
+hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s);
 
 // Shapes the attention kernel is instantiated for.
 bool latent_attend_supported(int d_c, int d_rope);
 int latent_attend_rows_per_block(int d_c, int d_rope);
 int latent_attend_keys_per_tile(int d_c, int d_rope);
 int latent_attend_wgs_per_cu(int d_c, int d_rope);
+bool dense_attend_supported(int d_head);
+int dense_attend_rows_per_block();
+int dense_attend_keys_per_tile();
 
 }  // namespace vmla

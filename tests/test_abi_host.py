@@ -146,3 +146,48 @@ def test_timing_read_validates_names():
     assert (n, t) == (0, 0.0)
     with pytest.raises(vm.VideomlaError):
         vm.timing_read("nope")
+
+
+def test_dense_cache_bytes_per_token():
+    # 2 (K and V) * 12 heads * 128 * 2 bytes = 3,072 bf16 scalars per token and layer
+    assert vm.dense_cache_bytes_per_token(WAN) == 6144
+    assert vm.dense_cache_bytes_per_token(WAN) == 2 * O.dense_scalars_per_token(WAN)
+    # the 13.7x memory ratio of the latent cache at the Wan shape
+    assert round(vm.dense_cache_bytes_per_token(WAN) / vm.cache_bytes_per_token(WAN), 2) == 13.71
+
+
+def _dense_write(d, fe=0, batch=1, x=FAKE):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_dense_cache_write(ctypes.byref(d), ctypes.byref(w), batch, x, FAKE,
+                                              FAKE, FAKE, None, None)
+
+
+def _dense_attend(d, fe=0, batch=1, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_dense_attend(ctypes.byref(d), ctypes.byref(w), batch, q, FAKE, FAKE,
+                                         ws, ws_bytes, None)
+
+
+def test_dense_calls_reject_bad_args():
+    d = L.make_dims(WAN)
+    assert _dense_write(d, x=None) == L.EINVAL
+    assert _dense_write(d, batch=0) == L.EINVAL
+    assert _dense_write(d, x=MISALIGNED) == L.EALIGN
+    assert _dense_write(_dims_struct(WAN, d_model=1000)) == L.EUNSUPPORTED
+    assert _dense_write(_dims_struct(WAN, d_v=130)) == L.EUNSUPPORTED   # more than 64 RoPE pairs
+    assert _dense_write(_dims_struct(WAN, d_v=36)) == L.EUNSUPPORTED    # 2 * 12 * 36 % 128 != 0
+    assert _dense_attend(d, q=None) == L.EINVAL
+    assert _dense_attend(d, q=MISALIGNED) == L.EALIGN
+    need = vm.dense_attend_workspace_bytes(WAN, 1)
+    assert need > 0
+    assert _dense_attend(d, ws=None) == L.EWORKSPACE
+    assert _dense_attend(d, ws_bytes=need - 1) == L.EWORKSPACE
+    assert _dense_attend(_dims_struct(WAN, d_v=64)) == L.EUNSUPPORTED
+    assert vm.dense_attend_workspace_bytes(_dims_struct(WAN, d_v=64), 1) == 0
+
+
+def test_dense_workspace_covers_padded_rows():
+    # q_cat holds every head's rows padded to whole 256-row blocks: 4680 -> 4864 rows per head
+    rows = 12 * 4864
+    assert vm.dense_attend_workspace_bytes(WAN, 1) >= rows * 128 * 2 + rows * 128 * 4 + rows * 8
+    assert vm.dense_attend_workspace_bytes(WAN, 4) >= 4 * (rows * 128 * 2 + rows * 128 * 4 + rows * 8)
