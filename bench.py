@@ -189,6 +189,146 @@ def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
     }), flush=True)
 
 
+def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
+    """Minute-scale rollout at batch 4: `--chunks` consecutive 3-frame chunks (80 = frames
+    0..239, temporal RoPE index up to 239, the ring wrapping eleven times) through 30 attention
+    layers x 4 denoising steps, each layer with its own weights, queries and ring; the window
+    advances after every chunk. Run once with the latent path (cache write + latent attend) and
+    once with the dense per-head comparator (per-head K/V cache write + standard attention) on
+    the same schedule, shapes and activations. Seeded synthetic bf16 drawn on the GPU; chunk
+    activations cycle through 8 distinct buffers (460 MB) so that each call reads them from
+    HBM. Per-kernel averages are taken with HIP events over the last chunk (full window)."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq, B = d.chunk_tokens, batch
+    n_chunks = args.chunks
+    xs = [normal((B, nq, d.d_model)) for _ in range(8)]
+
+    def x_of(c, s, li):
+        return xs[(c * n_steps * n_layers + s * n_layers + li) % len(xs)]
+
+    def run(path):
+        log(f"{path}: building {n_layers} layers at batch {B}")
+        layers = []
+        for _ in range(n_layers):
+            if path == "latent":
+                L = {"w_dkv": normal((d.d_c, d.d_model), d.d_model ** -0.5),
+                     "w_kr": normal((d.d_rope, d.d_model), d.d_model ** -0.5),
+                     "w_uk": normal((d.n_heads * d.d_nope, d.d_c), d.d_c ** -0.5),
+                     "w_uv": normal((d.n_heads * d.d_v, d.d_c), d.d_c ** -0.5),
+                     "gamma": torch.ones(d.d_c, dtype=torch.bfloat16, device=dev),
+                     "q_nope": normal((B, nq, d.n_heads, d.d_nope)),
+                     "q_r": normal((B, nq, d.n_heads, d.d_rope)),
+                     "c_kv": torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16,
+                                         device=dev),
+                     "k_r": torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16,
+                                        device=dev)}
+            else:
+                L = {"w_k": normal((d.n_heads * d.d_v, d.d_model), d.d_model ** -0.5),
+                     "w_v": normal((d.n_heads * d.d_v, d.d_model), d.d_model ** -0.5),
+                     "q": normal((B, nq, d.n_heads, d.d_v)),
+                     "kv": torch.zeros((B, d.window_tokens, d.n_heads, 2 * d.d_v),
+                                       dtype=torch.bfloat16, device=dev)}
+            layers.append(L)
+        out = torch.empty((B, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
+        if path == "latent":
+            ws = torch.empty(vm.attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
+            names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
+        else:
+            ws = torch.empty(vm.dense_attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
+            names = ("dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge")
+
+        def call(L, fe, x):
+            if path == "latent":
+                vm.cache_write(d, fe, B, x, L["w_dkv"], L["w_kr"], L["gamma"], L["c_kv"], L["k_r"])
+                vm.attend(d, fe, B, L["q_nope"], L["q_r"], L["w_uk"], L["w_uv"], L["c_kv"],
+                          L["k_r"], out, ws)
+            else:
+                vm.dense_cache_write(d, fe, B, x, L["w_k"], L["w_v"], L["kv"])
+                vm.dense_attend(d, fe, B, L["q"], L["kv"], out, ws)
+
+        # warm-up: one chunk-step of every layer at frame 0 (rewritten by chunk 0 below)
+        for li, L in enumerate(layers):
+            call(L, 0, x_of(0, 0, li))
+        torch.cuda.synchronize()
+        log(f"{path}: timing {n_chunks} chunks")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks + 1)]
+        fe = 0
+        t0 = time.perf_counter()
+        ev[0].record()
+        for c in range(n_chunks):
+            if c == n_chunks - 1:
+                torch.cuda.synchronize()
+                vm.timing_enable(True)
+                for k in names:
+                    vm.timing_read(k)
+            for s in range(n_steps):
+                for li, L in enumerate(layers):
+                    call(L, fe, x_of(c, s, li))
+            ev[c + 1].record()
+            fe = vm.window_advance(d, fe)
+            if c % 10 == 9:
+                log(f"{path}: chunk {c + 1}/{n_chunks}")
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        kern = {}
+        for k in names:
+            n, tot = vm.timing_read(k)
+            kern[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 2)}
+        vm.timing_enable(False)
+        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n_chunks)]
+        full = ms[(d.window_frames - 1) // d.chunk_frames:] or ms
+        del layers, out, ws
+        torch.cuda.empty_cache()
+        return {"seconds": round(wall, 3), "ms_per_chunk": round(sum(ms) / len(ms), 3),
+                "ms_per_chunk_full_window": round(sum(full) / len(full), 3),
+                "ms_first_chunk": round(ms[0], 3), "kernels_last_chunk": kern}
+
+    lat = run("latent")
+    den = run("dense")
+    # algorithmic work of the whole rollout (valid window per chunk)
+    lat_flop = den_flop = 0
+    fe = 0
+    for c in range(n_chunks):
+        S = vm.valid_tokens(d, fe)
+        rows = B * nq * d.n_heads
+        lat_flop += n_layers * n_steps * (
+            rows * S * (2 * (d.d_c + d.d_rope) + 2 * d.d_c)
+            + rows * 2 * (d.d_nope * d.d_c + d.d_c * d.d_v)
+            + B * nq * 2 * d.d_model * (d.d_c + d.d_rope))
+        den_flop += n_layers * n_steps * (rows * S * 4 * d.d_v
+                                          + B * nq * 2 * d.d_model * 2 * d.n_heads * d.d_v)
+        fe = vm.window_advance(d, fe)
+    lat["tflops"] = round(lat_flop / lat["seconds"] / 1e12, 2)
+    den["tflops"] = round(den_flop / den["seconds"] / 1e12, 2)
+    lat_bytes = n_layers * B * d.window_tokens * vm.cache_bytes_per_token(d)
+    den_bytes = n_layers * B * d.window_tokens * vm.dense_cache_bytes_per_token(d)
+    la, da = lat["kernels_last_chunk"], den["kernels_last_chunk"]
+    lat_call = sum(v["avg_us"] for v in la.values())
+    den_call = sum(v["avg_us"] for v in da.values())
+    print(json.dumps({
+        "metric": "ms per chunk: 30 layers x 4 denoising steps, latent vs dense per-head cache",
+        "value": lat["ms_per_chunk"], "unit": "ms", "n_gpus": 1, "steps": n_chunks, "warmup": 1,
+        "higher_is_better": False, "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "latent": lat, "dense": den,
+        "latent_over_dense_time": round(lat["seconds"] / den["seconds"], 3),
+        "latent_over_dense_time_per_call_full_window": round(lat_call / den_call, 3),
+        "cache_bytes": {"latent": lat_bytes, "dense": den_bytes,
+                        "dense_over_latent": round(den_bytes / lat_bytes, 3)},
+        "config": {"workload": (f"Wan2.1-1.3B rollout, batch 4: {n_chunks} chunks of 3 frames "
+                                f"(frames 0..{3 * n_chunks - 1}) x 30 layers x 4 denoising "
+                                "steps, 21-frame window; latent path and dense per-head "
+                                "comparator on the same schedule"),
+                   "batch": B, "layers": n_layers, "denoising_steps": n_steps,
+                   "chunks": n_chunks, "seed": 4},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,10 +339,12 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="wan-layer-chunk-step",
-                    choices=("wan-layer-chunk-step", "wan-30-layer-chunk"),
+                    choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
-                         "plus the window advance")
+                         "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
+                         "chunks through 30 layers, latent path and dense comparator")
+    ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -217,6 +359,9 @@ def main():
 
     if args.workload == "wan-30-layer-chunk":
         thirty_layer_chunk(args, vm, torch, WAN)
+        return
+    if args.workload == "wan-rollout-b4":
+        rollout_comparison(args, vm, torch, WAN)
         return
 
     d = WAN
