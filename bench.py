@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "967dab4dd8da36da3087a066eb63e7fb943b2fc59e0f927e8ec64153f7c5b7a9",
-                  "bytes": 959701971}
+                  "sha256": "3b05faede8e9c0e78c699edbfdf4fb43da62e73409bb17cef524debd3d1168d9",
+                  "bytes": 307992794}
 
 
 def log(msg):
