@@ -23,8 +23,10 @@ What it computes, and where the paper defines it (VideoMLA, arXiv 2605.30351):
 
 Readings of points the paper leaves open (each is a parameter, never a hidden constant):
 RoPE pairs are interleaved channels (2k, 2k+1) of each axis slice, theta_{a,k} = base^(-2k/D_a);
-keys are rotated at their absolute (f, y, x) when written (a uniform shift of every position
-leaves scores unchanged, so this equals the paper's window-relative rotation without a sink);
+without a sink, keys are rotated at their absolute (f, y, x) when written (a uniform shift of
+every position leaves scores unchanged, so this equals the paper's window-relative rotation);
+with S sink frames, the cache holds unrotated keys, and the context (sink frames, then the most
+recent frames) is rotated at window-local time, the frame's index in the context;
 RMSNorm is applied before caching; the softmax scale is 1/sqrt(d_nope + d_rope) (Eq. 7).
 
 Parity pins: every function here is pinned by the `-m "not gpu"` tests against closed forms,
@@ -91,18 +93,53 @@ def token_position(n, frame_end: int, dims):
     return f, r // dims.grid_w, r % dims.grid_w
 
 
-def ring_slot(f, y, x, dims):
-    """Slot of the token at absolute (f, y, x): frame f lives in frame slot f mod W_f, so the
-    ring holds the most recent W_f frames and the oldest whole frame is evicted first."""
+def frame_slot(f, dims):
+    """Frame slot of absolute frame f. Without a sink, frame f lives in slot f mod W_f, so the
+    ring holds the most recent W_f frames and the oldest whole frame is evicted first. With S
+    sink frames (App. "Chunk-Causal Sliding-Window Attention": one sink frame plus the most
+    recent frames, FIFO eviction outside the sink), frames 0..S-1 keep slots 0..S-1 for good and
+    later frames cycle through the other W_f - S slots."""
     f = np.asarray(f, dtype=np.int64)
-    return ((f % dims.window_frames) * dims.grid_h + np.asarray(y)) * dims.grid_w + np.asarray(x)
+    S, W = dims.sink_frames, dims.window_frames
+    if S == 0:
+        return f % W
+    return np.where(f < S, f, S + (f - S) % (W - S))
+
+
+def ring_slot(f, y, x, dims):
+    """Slot of the token at absolute (f, y, x): its frame slot, then row-major (y, x)."""
+    return (frame_slot(f, dims) * dims.grid_h + np.asarray(y)) * dims.grid_w + np.asarray(x)
 
 
 def window_frame_range(frame_end: int, dims):
-    """Frames visible to the chunk starting at `frame_end`: the chunk itself plus past frames,
-    at most W_f in total (chunk-causal sliding window). Returns [first, last)."""
+    """Frames visible to the chunk starting at `frame_end` when there is no sink: the chunk
+    itself plus past frames, at most W_f in total (chunk-causal sliding window).
+    Returns [first, last)."""
+    assert dims.sink_frames == 0, "a sink context is not a contiguous range: use context_frames"
     last = frame_end + dims.chunk_frames
     return max(0, last - dims.window_frames), last
+
+
+def context_frames(frame_end: int, dims) -> list:
+    """Frames of the active context of the chunk starting at `frame_end`, in time order: the
+    sink frames generated so far, then the most recent frames (the chunk included), W_f frames
+    at most in total."""
+    hi = frame_end + dims.chunk_frames
+    S, W = dims.sink_frames, dims.window_frames
+    if S == 0:
+        return list(range(max(0, hi - W), hi))
+    return list(range(min(S, hi))) + list(range(max(S, hi - (W - S)), hi))
+
+
+def local_time(f, frame_end: int, dims):
+    """Window-relative temporal coordinate of context frame f (App. "Long-Horizon RoPE
+    Re-indexing"): its index in the context's time order, so the sink frames take 0..S-1 and the
+    recent frames follow without a gap. Queries of the chunk take the coordinates of their
+    frames. Bounded by W_f - 1 however long the rollout."""
+    frames = context_frames(frame_end, dims)
+    index = {fr: i for i, fr in enumerate(frames)}
+    f = np.asarray(f, dtype=np.int64)
+    return np.vectorize(lambda v: index[int(v)], otypes=[np.int64])(f)
 
 
 # --------------------------------------------------------------------------------------------
@@ -161,32 +198,42 @@ def cache_write(x_chunk_bits, w_dkv_bits, w_kr_bits, gamma_bits, frame_end: int,
     """What `cache_write` must produce for one batch element's chunk.
 
     x_chunk_bits [chunk_tokens, d_model] bf16 bits of the chunk starting at frame `frame_end`.
-    Returns dict: c [T, d_c] fp64, k_rope [T, d_rope] fp64 (rotated at absolute (f, y, x)),
-    slots [T] int64.
+    Returns dict: c [T, d_c] fp64; k_cached [T, d_rope] fp64, the positional key as the ring
+    holds it: without a sink rotated at the token's absolute (f, y, x) (k_rope, the same array),
+    with a sink unrotated (Sec. "Decoupled 3D-RoPE": the cache holds the position-free state,
+    rotated when the window is assembled); slots [T] int64.
     """
     x = bf16_bits_to_f64(x_chunk_bits)
     gamma = None if gamma_bits is None else bf16_bits_to_f64(gamma_bits)
     c, kr = compress(x, bf16_bits_to_f64(w_dkv_bits), bf16_bits_to_f64(w_kr_bits), gamma, dims)
     f, y, xx = token_position(np.arange(x.shape[0]), frame_end, dims)
-    return {"c": c, "k_rope": rope3d(kr, f, y, xx, dims), "slots": ring_slot(f, y, xx, dims)}
+    out = {"c": c, "k_r": kr, "slots": ring_slot(f, y, xx, dims)}
+    if dims.sink_frames == 0:
+        out["k_rope"] = out["k_cached"] = rope3d(kr, f, y, xx, dims)
+    else:
+        out["k_cached"] = kr
+    return out
 
 
 def window_latents(x_bits, w_dkv_bits, w_kr_bits, gamma_bits, frame_end: int, dims,
                    rotate_origin: int = 0):
     """Latents of every token visible to the chunk starting at `frame_end`, computed from the
-    raw inputs x_bits [n_frames * HW, d_model] (frames from 0). Returns (c, k_rope, (f, y, x)).
+    raw inputs x_bits [n_frames * HW, d_model] (frames from 0), context frames in time order.
+    Returns (c, k_rope, (f, y, x)).
 
-    `rotate_origin` is subtracted from every temporal index before rotation (0 = absolute
-    positions; the first window frame = the paper's window-relative re-indexing)."""
-    lo, hi = window_frame_range(frame_end, dims)
-    x = bf16_bits_to_f64(x_bits[lo * dims.hw: hi * dims.hw])
+    Without a sink, `rotate_origin` is subtracted from every temporal index before rotation
+    (0 = absolute positions; the first window frame = the paper's window-relative re-indexing).
+    With a sink, keys are rotated at their window-local time (`local_time`)."""
+    frames = context_frames(frame_end, dims)
+    x = bf16_bits_to_f64(np.concatenate([x_bits[fr * dims.hw:(fr + 1) * dims.hw] for fr in frames]))
     gamma = None if gamma_bits is None else bf16_bits_to_f64(gamma_bits)
     c, kr = compress(x, bf16_bits_to_f64(w_dkv_bits), bf16_bits_to_f64(w_kr_bits), gamma, dims)
     n = np.arange(x.shape[0])
-    f = lo + n // dims.hw
+    f = np.asarray(frames, dtype=np.int64)[n // dims.hw]
     y = (n % dims.hw) // dims.grid_w
     xx = n % dims.grid_w
-    return c, rope3d(kr, f - rotate_origin, y, xx, dims), (f, y, xx)
+    t = f - rotate_origin if dims.sink_frames == 0 else local_time(f, frame_end, dims)
+    return c, rope3d(kr, t, y, xx, dims), (f, y, xx)
 
 
 # --------------------------------------------------------------------------------------------
@@ -263,6 +310,9 @@ def chunk_attention(inp, b: int, frame_end: int, rows=None, absorbed: bool = Fal
     rows = np.arange(dims.chunk_tokens) if rows is None else np.asarray(rows)
     q_nope = bf16_bits_to_f64(inp.q_nope[b][rows])
     q_pos = token_position(rows, frame_end, dims)
+    if dims.sink_frames:  # the chunk's frames in the same window-local time as the keys
+        q_pos = (local_time(q_pos[0], frame_end, dims), q_pos[1], q_pos[2])
+        origin = 0
     q_rope = query_rope(bf16_bits_to_f64(inp.q_r[b][rows]), q_pos, dims, rotate_origin=origin)
     w_uk, w_uv = bf16_bits_to_f64(inp.w_uk), bf16_bits_to_f64(inp.w_uv)
     fn = attend_absorbed if absorbed else attend_unabsorbed
@@ -343,5 +393,5 @@ def ring_after_writes(n_frames_written: int, dims):
     in order (-1 = never written). Follows the closed-form slot map."""
     held = np.full(dims.window_frames, -1, dtype=np.int64)
     for f in range(n_frames_written):
-        held[f % dims.window_frames] = f
+        held[int(frame_slot(f, dims))] = f
     return held

@@ -99,7 +99,7 @@ def check_written_chunk(layer, fe, before_c, before_k):
         assert np.array_equal(c_bits[b][~written], before_c[b][~written])
         assert np.array_equal(k_bits[b][~written], before_k[b][~written])
         for got, exact in ((c_bits[b][ref["slots"]], ref["c"]),
-                           (k_bits[b][ref["slots"]], ref["k_rope"])):
+                           (k_bits[b][ref["slots"]], ref["k_cached"])):
             dist = ulp_distance(got, O.round_to_bf16_bits(exact))
             floor = 2.0 ** -16 * np.sqrt(np.mean(exact * exact, axis=1, keepdims=True))
             near = np.abs(bf16_to_f64(got) - exact) <= floor

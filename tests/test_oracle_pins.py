@@ -4,6 +4,7 @@ worked by hand, closed forms, invariants the paper relies on, library routines a
 Each test names the mistake it is there to catch.
 """
 import collections
+import dataclasses
 import json
 import math
 import os
@@ -449,3 +450,121 @@ def test_dense_cache_write_places_like_the_latent_cache():
     f, y, x = O.token_position(np.arange(hw), 5, TINY)
     assert np.array_equal(got["slots"], O.ring_slot(f, y, x, TINY))
     assert got["k"].shape == (hw, TINY.n_heads, TINY.d_v)
+
+
+# ------------------------------------------------------------------------------------------
+# Sink frame + local window with window-relative RoPE re-indexing
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("W_f,S,chunk,grid", [(4, 1, 1, (2, 2)), (7, 1, 3, (1, 3)), (9, 2, 3, (2, 1))])
+def test_sink_slot_map_matches_simulation(W_f, S, chunk, grid):
+    """Brute force: the first S frames stay in the cache for good and a FIFO (deque) of the
+    most recent W_f - S later frames holds the rest. The closed-form slot map must hold exactly
+    those frames, the context of each chunk must be them in time order, and slots are distinct."""
+    dims = Dims(d_model=8, n_heads=1, d_nope=2, d_rope=2, d_c=2, d_v=2, grid_h=grid[0],
+                grid_w=grid[1], window_frames=W_f, chunk_frames=chunk, rope_pairs=(1, 0, 0),
+                sink_frames=S)
+    sink, fifo = [], collections.deque(maxlen=W_f - S)
+    ring_frame = {}
+    for frame_end in range(0, 8 * W_f, chunk):
+        n = np.arange(dims.chunk_tokens)
+        f, y, x = O.token_position(n, frame_end, dims)
+        slots = O.ring_slot(f, y, x, dims)
+        assert len(set(slots.tolist())) == len(slots)
+        for s, ff, yy, xx in zip(slots, f, y, x):
+            ring_frame[int(s)] = (int(ff), int(yy), int(xx))
+        for ff in range(frame_end, frame_end + chunk):
+            (sink if ff < S else fifo).append(ff)
+        held = sorted({v[0] for v in ring_frame.values()})
+        assert held == sorted(sink + list(fifo))
+        assert O.context_frames(frame_end, dims) == sink + list(fifo)
+        rw = O.ring_after_writes(frame_end + chunk, dims)
+        assert sorted(rw[rw >= 0].tolist()) == held
+        assert all(0 <= s < dims.window_tokens for s in ring_frame)
+        # the sink frames never move
+        for ff in sink:
+            assert int(O.frame_slot(ff, dims)) == ff
+
+
+def test_sink_local_time_table():
+    """The paper's long-rollout context (one sink frame, six recent frames, 3-frame chunks):
+    the sink takes local time 0 and the recent frames 1..6 however far the rollout has gone;
+    before the cache is full local time is the absolute frame index."""
+    from workloads import WAN_SINK
+    assert O.context_frames(0, WAN_SINK) == [0, 1, 2]
+    assert O.context_frames(3, WAN_SINK) == [0, 1, 2, 3, 4, 5]
+    assert O.context_frames(6, WAN_SINK) == [0, 3, 4, 5, 6, 7, 8]
+    assert O.context_frames(237, WAN_SINK) == [0, 234, 235, 236, 237, 238, 239]
+    assert O.local_time([0, 1, 2], 0, WAN_SINK).tolist() == [0, 1, 2]
+    assert O.local_time([0, 3, 5], 3, WAN_SINK).tolist() == [0, 3, 5]
+    assert O.local_time([0, 3, 6, 8], 6, WAN_SINK).tolist() == [0, 1, 4, 6]
+    assert O.local_time([0, 234, 237, 239], 237, WAN_SINK).tolist() == [0, 1, 4, 6]
+    # frame slots: the sink keeps slot 0, frames 1.. cycle through slots 1..6
+    assert O.frame_slot([0, 1, 6, 7, 12, 239], WAN_SINK).tolist() == [0, 1, 6, 1, 6, 5]
+
+
+def test_sink_equals_plain_window_before_eviction():
+    """While every generated frame still fits in the cache, the sink context is the plain
+    window, local time is absolute time, and both modes give the same attention."""
+    from workloads import TINY_SINK
+    plain = TINY_SINK.replace(sink_frames=0)
+    inp_s = make_layer_inputs(TINY_SINK, seed=3, n_frames=4)
+    inp_p = make_layer_inputs(plain, seed=3, n_frames=4)
+    for frame_end in range(4):
+        a = O.chunk_attention(inp_s, 0, frame_end)
+        b = O.chunk_attention(inp_p, 0, frame_end)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def _absolute_time_attention(inp, frame_end):
+    """The same context keys and queries rotated at absolute time instead of window-local
+    time (what the cache would give if the re-indexing were skipped)."""
+    d = inp.dims
+    frames = O.context_frames(frame_end, d)
+    x = O.bf16_bits_to_f64(np.concatenate([inp.x[0][f * d.hw:(f + 1) * d.hw] for f in frames]))
+    c, kr = O.compress(x, O.bf16_bits_to_f64(inp.w_dkv), O.bf16_bits_to_f64(inp.w_kr),
+                       O.bf16_bits_to_f64(inp.gamma), d)
+    n = np.arange(x.shape[0])
+    f = np.asarray(frames)[n // d.hw]
+    k = O.rope3d(kr, f, (n % d.hw) // d.grid_w, n % d.grid_w, d)
+    rows = np.arange(d.chunk_tokens)
+    q_rope = O.query_rope(O.bf16_bits_to_f64(inp.q_r[0]), O.token_position(rows, frame_end, d), d)
+    return O.attend_unabsorbed(O.bf16_bits_to_f64(inp.q_nope[0]), q_rope,
+                               O.bf16_bits_to_f64(inp.w_uk), O.bf16_bits_to_f64(inp.w_uv), c, k, d)
+
+
+def test_sink_rollout_depends_only_on_window_content():
+    """Window-relative re-indexing: two chunks far apart in the rollout whose contexts hold the
+    same content (same sink frame, same recent frames) give the same attention, so positions
+    stay bounded. Rotating at absolute time instead gives different results (the sink's offset
+    to the queries grows), which shows this check can fail."""
+    from workloads import TINY_SINK
+    d = TINY_SINK
+    inp = make_layer_inputs(d, seed=4, n_frames=40)
+    x = inp.x.copy()
+    F1, F2 = 5, 37
+    for k in range(d.window_frames - d.sink_frames):   # recent frames of F2 := those of F1
+        a, b = F1 - k, F2 - k
+        x[:, b * d.hw:(b + 1) * d.hw] = x[:, a * d.hw:(a + 1) * d.hw]
+    inp = dataclasses.replace(inp, x=x)
+    o1 = O.chunk_attention(inp, 0, F1)
+    o2 = O.chunk_attention(inp, 0, F2)
+    np.testing.assert_allclose(o2, o1, rtol=0, atol=1e-12)
+    assert np.abs(_absolute_time_attention(inp, F2) - o2).max() > 1e-4
+
+
+def test_sink_cache_write_keeps_keys_unrotated():
+    """With a sink the cache holds the position-free key W_R^K x; without one it holds the key
+    rotated at the token's absolute position."""
+    from workloads import TINY_SINK
+    inp = make_layer_inputs(TINY_SINK, seed=5, n_frames=8)
+    fe = 6
+    xs = inp.x[0][fe * TINY_SINK.hw:(fe + 1) * TINY_SINK.hw]
+    ref = O.cache_write(xs, inp.w_dkv, inp.w_kr, inp.gamma, fe, TINY_SINK)
+    kr = O.bf16_bits_to_f64(xs) @ O.bf16_bits_to_f64(inp.w_kr).T
+    np.testing.assert_allclose(ref["k_cached"], kr, rtol=0, atol=1e-12)
+    # frame 6 lives in frame slot 1 + (6 - 1) mod 3 = 3
+    assert (ref["slots"] // TINY_SINK.hw == 3).all()
+    plain = O.cache_write(xs, inp.w_dkv, inp.w_kr, inp.gamma, fe, TINY_SINK.replace(sink_frames=0))
+    f, y, x = O.token_position(np.arange(TINY_SINK.hw), fe, TINY_SINK)
+    np.testing.assert_allclose(plain["k_cached"], O.rope3d(kr, f, y, x, TINY_SINK), rtol=0, atol=1e-12)

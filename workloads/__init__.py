@@ -36,6 +36,7 @@ class Dims:
     rope_base: float = 10000.0
     softmax_scale: float = 0.0             # 0 means 1/sqrt(d_nope + d_rope)
     kv_norm_eps: float = 1e-6
+    sink_frames: int = 0                   # leading frames kept for good (attention sink)
 
     @property
     def hw(self) -> int:
@@ -64,6 +65,13 @@ WAN = Dims(d_model=1536, n_heads=12, d_nope=128, d_rope=32, d_c=192, d_v=128, gr
 # The paper's own default split: d_nope = 96, (6, 5, 5) pairs taken from the highest-frequency
 # bands of Wan's full-head axis groups (44, 42, 42 channels).
 WAN_PAPER = WAN.replace(d_nope=96, rope_pairs=(6, 5, 5), rope_band_dim=(44, 42, 42))
+
+# The paper's long-rollout context: one sink frame and the six most recent frames (7 frame
+# slots, 10,920 cached tokens); keys are cached unrotated and rotated in window-local time.
+WAN_SINK = WAN.replace(window_frames=7, sink_frames=1)
+
+# Tiny sink case: one sink frame and three local frames, 1-frame chunks.
+TINY_SINK = TINY.replace(window_frames=4, sink_frames=1)
 
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
