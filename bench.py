@@ -206,6 +206,86 @@ def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
     }), flush=True)
 
 
+def sink_chunk_step(args, vm, torch, d, fe=237):
+    """One chunk-step with the paper's long-rollout context: one sink frame and the six most
+    recent frames (10,920 keys), late in a rollout (the chunk of frames 237..239, context frames
+    0 and 234..239), batch 1. The ring holds unrotated keys; the step is the cache write of the
+    chunk, then the attend call, which also rotates the context's keys at window-local time.
+    Seeded synthetic bf16 drawn on the GPU; the chunk's x cycles through 32 buffers (460 MB)."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(9)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq = d.chunk_tokens
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    w_uk = normal((d.n_heads * d.d_nope, d.d_c), d.d_c ** -0.5)
+    w_uv = normal((d.n_heads * d.d_v, d.d_c), d.d_c ** -0.5)
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    q_nope, q_r = normal((1, nq, d.n_heads, d.d_nope)), normal((1, nq, d.n_heads, d.d_rope))
+    c_kv = torch.zeros((1, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+    k_r = torch.zeros((1, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((1, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_workspace_bytes(d, 1), dtype=torch.uint8, device=dev)
+    for f in (0, fe - 6, fe - 3):  # the sink (first chunk) and the recent frames before fe
+        vm.cache_write(d, f, 1, normal((1, nq, d.d_model)), w_dkv, w_kr, gamma, c_kv, k_r)
+    xs = [normal((1, nq, d.d_model)) for _ in range(args.x_buffers)]
+    torch.cuda.synchronize()
+
+    def step(i):
+        vm.cache_write(d, fe, 1, xs[i % len(xs)], w_dkv, w_kr, gamma, c_kv, k_r)
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    names = ("cache_write", "q_absorb", "rope_window", "latent_attend", "out_proj")
+    vm.timing_enable(True)
+    for k in names:
+        vm.timing_read(k)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    marks[0].record()
+    for i in range(args.steps):
+        step(i)
+        marks[i + 1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
+    kernels = {}
+    for k in names:
+        n, tot = vm.timing_read(k)
+        kernels[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 3)}
+    vm.timing_enable(False)
+    S = vm.valid_tokens(d, fe)
+    rows = nq * d.n_heads
+    attend_core = rows * S * (2 * (d.d_c + d.d_rope) + 2 * d.d_c)
+    attend_flop = attend_core + rows * 2 * (d.d_nope * d.d_c + d.d_c * d.d_v)
+    write_flop = nq * 2 * d.d_model * (d.d_c + d.d_rope)
+    ms = 1e3 * elapsed / args.steps
+    k3 = kernels["latent_attend"]["avg_us"] / 1e6
+    print(json.dumps({
+        "metric": "ms/chunk-step & TFLOP/s, sink frame + 6-frame local window (window-local RoPE)",
+        "value": round((attend_flop + write_flop) / (ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
+        "higher_is_better": True, "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "kernels": kernels,
+        "latent_attend_tflops": round(attend_core / k3 / 1e12, 2),
+        "latent_attend_mfma_frac": round(attend_core / k3 / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+        "config": {"workload": (f"Wan2.1-1.3B layer chunk-step late in a rollout (frames "
+                                f"{fe}..{fe + 2}): cache write of 4,680 tokens + latent attend "
+                                f"of 4,680 x 12 query rows over {S:,} keys (1 sink frame + 6 "
+                                "recent frames), batch 1"),
+                   "sink_frames": d.sink_frames, "window_frames": d.window_frames,
+                   "window_tokens": S, "seed": 9},
+    }), flush=True)
+
+
 def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
     """Minute-scale rollout at batch 4: `--chunks` consecutive 3-frame chunks (80 = frames
     0..239, temporal RoPE index up to 239, the ring wrapping eleven times) through 30 attention
@@ -359,11 +439,14 @@ def main():
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="wan-layer-chunk-step",
-                    choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4"),
+                    choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
+                             "wan-sink-chunk-step"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
-                         "chunks through 30 layers, latent path and dense comparator")
+                         "chunks through 30 layers, latent path and dense comparator; "
+                         "wan-sink-chunk-step: one chunk-step with a sink frame + 6 recent "
+                         "frames late in a rollout")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -382,6 +465,10 @@ def main():
         return
     if args.workload == "wan-rollout-b4":
         rollout_comparison(args, vm, torch, WAN)
+        return
+    if args.workload == "wan-sink-chunk-step":
+        from workloads import WAN_SINK
+        sink_chunk_step(args, vm, torch, WAN_SINK)
         return
 
     d = WAN

@@ -58,6 +58,17 @@ extern "C" {
  *   rope_base      base of the RoPE frequencies (10000)
  *   softmax_scale  multiplier of the scores; 0 means 1 / sqrt(d_nope + d_rope) (Eq. 7)
  *   kv_norm_eps    epsilon of the RMSNorm applied to c^KV when a gain is given
+ *   sink_frames    S: leading frames the cache keeps for good (attention sink, App.
+ *                  "Chunk-Causal Sliding-Window Attention"); 0 = none. The ring has
+ *                  window_frames frame slots: frames 0..S-1 keep slots 0..S-1, later frames
+ *                  cycle FIFO through the other window_frames - S slots, which must hold a
+ *                  whole chunk (window_frames - S >= chunk_frames).
+ *                  RoPE time: with S = 0 keys are rotated at their absolute frame when written
+ *                  (a uniform shift of all positions leaves scores unchanged, so this equals a
+ *                  window-relative frame). With S > 0 the ring holds UNROTATED keys, and
+ *                  videomla_attend rotates the context's keys and the chunk's queries at
+ *                  window-local time (App. "Long-Horizon RoPE Re-indexing"): sink frame f at
+ *                  t = f, the recent frames in time order at t = S, S+1, ...
  */
 typedef struct videomla_dims {
   int32_t d_model, n_heads, d_nope, d_rope, d_c, d_v;
@@ -68,6 +79,7 @@ typedef struct videomla_dims {
   float rope_base;
   float softmax_scale;
   float kv_norm_eps;
+  int32_t sink_frames;
 } videomla_dims;
 
 /* Host-side window state: absolute index of the first frame of the chunk being generated. */
@@ -87,8 +99,10 @@ typedef struct videomla_window {
  *   c_kv       [batch][window_frames * HW][d_c]              bf16 ring, written in place
  *   k_r        [batch][window_frames * HW][d_rope]           bf16 ring of ROTATED keys
  *   slots_out  [chunk_frames * HW] int32 slot of each chunk token, or NULL
- * Token (f, y, x) is stored at slot ((f mod window_frames) * grid_h + y) * grid_w + x, so the
- * chunk overwrites the oldest frames; every other slot is left untouched. Calling it again
+ * Token (f, y, x) is stored at slot (fs * grid_h + y) * grid_w + x with frame slot
+ * fs = f mod window_frames (no sink), or fs = f for f < S and S + (f - S) mod (window_frames - S)
+ * otherwise, so the chunk overwrites the oldest non-sink frames; every other slot is left
+ * untouched. With a sink, k_r receives the unrotated W_R^K x. Calling it again
  * before videomla_window_advance (the next denoising step) overwrites the same slots.
  * Requires d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0, d_c + d_rope <= 288.
  */
@@ -109,9 +123,11 @@ size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch)
  *   s_j     = scale * (q_lat . c_kv[j] + q_rope . k_r[j])                   (Eq. 7)
  *   o_lat   = sum_j softmax(s)_j c_kv[j]   over every valid slot j of the ring
  *   out     = W_up,h^V o_lat                                    (value up-projection, Eq. 2)
- * The valid slots are those of the last min(window_frames, frame_end + chunk_frames) frames:
- * the current chunk (already written by videomla_cache_write) and the past frames, with no
- * mask (tokens of a chunk see each other; later chunks are not in the ring yet).
+ * The valid slots are the first min(window_frames, frame_end + chunk_frames) frame slots:
+ * the current chunk (already written by videomla_cache_write), the past frames still held and
+ * the sink frames, with no mask (tokens of a chunk see each other; later chunks are not in the
+ * ring yet). With a sink, q_r and the ring's keys are rotated at window-local time (see
+ * sink_frames) and the workspace also holds the rotated keys.
  *
  *   q_nope  [batch][chunk_frames * HW][n_heads][d_nope]   bf16
  *   q_r     [batch][chunk_frames * HW][n_heads][d_rope]   bf16, unrotated
@@ -153,7 +169,8 @@ size_t videomla_dense_cache_bytes_per_token(const videomla_dims* dims);
  *              row (slot, h) holds the rotated K_h, then V_h
  *   slots_out  [chunk_frames * HW] int32, or NULL
  * Arithmetic: bf16 operands, fp32 accumulation and rotation, bf16 round-to-nearest-even.
- * Requires d_model % 64 == 0, d_v % 4 == 0, d_v <= 128, (2 n_heads d_v) % 128 == 0.
+ * Requires d_model % 64 == 0, d_v % 4 == 0, d_v <= 128, (2 n_heads d_v) % 128 == 0,
+ * sink_frames == 0.
  */
 int videomla_dense_cache_write(const videomla_dims* dims, const videomla_window* win,
                                int32_t batch, const uint16_t* x, const uint16_t* w_k,
@@ -173,8 +190,8 @@ size_t videomla_dense_attend_workspace_bytes(const videomla_dims* dims, int32_t 
  *   kv    the ring as written by videomla_dense_cache_write
  *   out   [batch][chunk_frames * HW][n_heads][d_v]   bf16
  *   workspace  device buffer of at least videomla_dense_attend_workspace_bytes() bytes
- * Arithmetic as videomla_attend. Requires d_v == 128. The work partition follows
- * videomla_set_attend_workgroups.
+ * Arithmetic as videomla_attend. Requires d_v == 128 and sink_frames == 0. The work
+ * partition follows videomla_set_attend_workgroups.
  */
 int videomla_dense_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                           const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
@@ -210,7 +227,7 @@ int videomla_set_attend_workgroups(int32_t n_workgroups);
  * launches is bracketed by two events recorded on the same stream. After the caller has
  * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed
  * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj",
- * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge") into
+ * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge", "rope_window") into
  * *count and *total_ms, and forgets them. Timing state is process-wide and not thread-safe.
  */
 int videomla_timing_enable(int32_t enable);

@@ -39,7 +39,7 @@ class VideomlaDims(ctypes.Structure):
         ("window_frames", ctypes.c_int32), ("chunk_frames", ctypes.c_int32),
         ("rope_pairs", ctypes.c_int32 * 3), ("rope_band_dim", ctypes.c_int32 * 3),
         ("rope_base", ctypes.c_float), ("softmax_scale", ctypes.c_float),
-        ("kv_norm_eps", ctypes.c_float),
+        ("kv_norm_eps", ctypes.c_float), ("sink_frames", ctypes.c_int32),
     ]
 
 
@@ -109,6 +109,7 @@ def make_dims(d) -> VideomlaDims:
     s.rope_base = float(d.rope_base)
     s.softmax_scale = float(d.softmax_scale)
     s.kv_norm_eps = float(d.kv_norm_eps)
+    s.sink_frames = int(getattr(d, "sink_frames", 0))
     return s
 
 

@@ -103,7 +103,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
     const size_t r = ((size_t)b * Nq + t) * H + h;
     const uint32_t raw = *reinterpret_cast<const uint32_t*>(a.q_r + r * DR + 2 * p);
     float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff)), v = bf16_bits_to_f32((uint16_t)(raw >> 16));
-    rope_rotate(a.rope, p, token_pos(a.geo, t), u, v);
+    rope_rotate(a.rope, p, rope_pos(a.geo, token_pos(a.geo, t)), u, v);
     const uint32_t packed =
         (uint32_t)to_bf16_bits(u * a.qscale) | ((uint32_t)to_bf16_bits(v * a.qscale) << 16);
     *reinterpret_cast<uint32_t*>(a.qcat + r * DQKP + DC + 2 * p) = packed;
@@ -114,6 +114,42 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
       for (int c = DC + DR; c < DQKP; ++c) a.qcat[r * DQKP + c] = 0;
     }
   }
+}
+
+// ---------------------------------------------------------------------------------------------
+// rope_window (attention sink only): the ring holds unrotated positional keys; rotate the keys
+// of every valid slot at their window-local time (App. "Long-Horizon RoPE Re-indexing") into
+// k_rot, which the attention kernel then reads in place of the ring. One thread per (slot,
+// RoPE pair). Slot s holds frame slot fs = s / HW: a sink frame (fs < S, local time fs) or the
+// recent frame f with S + (f - S) mod L = fs (L = W - S), whose local time is
+// S + (f - local_lo) = S + ((fs - S) - (local_lo - S)) mod L.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void rope_window_kernel(const AttendArgs a) {
+  const int np = a.d_rope / 2;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int b = blockIdx.y;
+  if (e >= (int64_t)a.n_valid * np) return;
+  const int64_t slot = e / np;
+  const int p = (int)(e % np);
+  const Geometry& g = a.geo;
+  const int hw = g.grid_h * g.grid_w;
+  const int fs = (int)(slot / hw), r = (int)(slot % hw);
+  const int S = g.sink_frames, L = g.window_frames - S;
+  TokenPos pos;
+  if (fs < S) {
+    pos.f = fs;
+  } else {
+    const int64_t d = ((int64_t)(fs - S) - (g.local_lo - S)) % L;
+    pos.f = S + (d < 0 ? d + L : d);
+  }
+  pos.y = r / g.grid_w;
+  pos.x = r % g.grid_w;
+  const size_t off = ((size_t)b * g.ring_tokens + slot) * a.d_rope + 2 * p;
+  const uint32_t raw = *reinterpret_cast<const uint32_t*>(a.k_r + off);
+  float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff)), v = bf16_bits_to_f32((uint16_t)(raw >> 16));
+  rope_rotate(a.rope, p, pos, u, v);
+  *reinterpret_cast<uint32_t*>(a.k_rot + off) =
+      (uint32_t)to_bf16_bits(u) | ((uint32_t)to_bf16_bits(v) << 16);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -712,6 +748,13 @@ hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s) {
   } else {
     return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s) {
+  const int64_t threads = (int64_t)a.n_valid * (a.d_rope / 2);
+  hipLaunchKernelGGL(rope_window_kernel, dim3((unsigned)((threads + 255) / 256), a.batch),
+                     dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

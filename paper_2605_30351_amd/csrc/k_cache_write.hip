@@ -1,5 +1,6 @@
 // Fused cache write: compress (Eq. 1), optional RMSNorm of the latent, decoupled RoPE key
-// (Eq. 5) rotated at the token's absolute (f, y, x), and FIFO placement into the ring.
+// (Eq. 5) rotated at the token's absolute (f, y, x) (kept unrotated when the cache has an
+// attention sink, Sec. "Decoupled 3D-RoPE"), and FIFO placement into the ring.
 //
 // One workgroup takes 32 chunk tokens of one batch element and all d_c + d_rope outputs:
 // out^T[o][token] = W[o][:] . x[token][:] with MFMA 32x32x16 (A = rows of [W_DKV; W_KR],
@@ -146,8 +147,10 @@ __global__ __launch_bounds__(kWaves * 64) void cache_write_kernel(const WriteArg
         *reinterpret_cast<bf16x4*>(cdst + o) = to_bf16x4(fv);
       } else if (o >= DC && o + 4 <= DC + DR) {
         const int ch = o - DC;  // channels ch .. ch+3 = RoPE pairs ch/2 and ch/2 + 1
-        rope_rotate(a.rope, ch / 2, pos, v[0], v[1]);
-        rope_rotate(a.rope, ch / 2 + 1, pos, v[2], v[3]);
+        if (a.geo.sink_frames == 0) {  // with a sink the ring keeps the unrotated key
+          rope_rotate(a.rope, ch / 2, pos, v[0], v[1]);
+          rope_rotate(a.rope, ch / 2 + 1, pos, v[2], v[3]);
+        }
         const f32x4 fv = {v[0], v[1], v[2], v[3]};
         *reinterpret_cast<bf16x4*>(kdst + ch) = to_bf16x4(fv);
       }

@@ -58,6 +58,10 @@ int check_dims(const videomla_dims* d) {
   if (d->chunk_frames > d->window_frames)
     return fail(VIDEOMLA_EINVAL, "chunk_frames (%d) exceeds window_frames (%d)", d->chunk_frames,
                 d->window_frames);
+  if (d->sink_frames < 0 || d->window_frames - d->sink_frames < d->chunk_frames)
+    return fail(VIDEOMLA_EINVAL,
+                "sink_frames (%d) must be >= 0 and leave a whole chunk (%d frames) of the %d-frame window",
+                d->sink_frames, d->chunk_frames, d->window_frames);
   const int64_t ring = (int64_t)d->window_frames * d->grid_h * d->grid_w;
   if (ring > (int64_t)1 << 30) return fail(VIDEOMLA_EUNSUPPORTED, "ring of %lld tokens is too large", (long long)ring);
   if (d->d_rope / 2 > kMaxRopePairs) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope > %d", 2 * kMaxRopePairs);
@@ -93,17 +97,23 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
   g.chunk_tokens = d->chunk_frames * d->grid_h * d->grid_w;
   g.frame_end = w->frame_end;
   g.ring_tokens = (int64_t)d->window_frames * d->grid_h * d->grid_w;
+  g.sink_frames = d->sink_frames;
+  if (d->sink_frames > 0) {  // first recent frame of the context: max(S, hi - (W - S))
+    const int64_t hi = w->frame_end + d->chunk_frames;
+    const int64_t lo = hi - (d->window_frames - d->sink_frames);
+    g.local_lo = lo > d->sink_frames ? lo : d->sink_frames;
+  }
   return g;
 }
 
 // ---- timing -------------------------------------------------------------------------------
 enum KernelId {
   K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
-  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_COUNT
+  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW, K_COUNT
 };
 const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
                                      "out_proj",          "dense_cache_write", "dense_q_prep",
-                                     "dense_attend",      "dense_merge"};
+                                     "dense_attend",      "dense_merge",  "rope_window"};
 
 struct TimingRec {
   int kernel;
@@ -208,7 +218,7 @@ int workspace_max_seg(const videomla_dims* d, int32_t batch, bool dense = false)
 }
 
 struct WorkspaceLayout {
-  size_t qcat_off, opart_off, ml_off, total;
+  size_t qcat_off, opart_off, ml_off, krot_off, total;
 };
 
 WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
@@ -218,7 +228,12 @@ WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_se
   w.qcat_off = 0;
   w.opart_off = round_up(rows * dqkp * 2, 256);
   w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_c * 4, 256);
-  w.total = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
+  w.krot_off = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
+  // with a sink: the window's keys rotated at window-local time, [B][ring][d_rope]
+  const size_t krot = d->sink_frames > 0
+                          ? (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->d_rope * 2
+                          : 0;
+  w.total = w.krot_off + round_up(krot, 256);
   return w;
 }
 
@@ -292,7 +307,9 @@ int64_t videomla_slot_of(const videomla_dims* d, int64_t f, int32_t y, int32_t x
     fail(VIDEOMLA_EINVAL, "position (%lld,%d,%d) outside the grid", (long long)f, y, x);
     return -1;
   }
-  return ((f % d->window_frames) * d->grid_h + y) * (int64_t)d->grid_w + x;
+  const int64_t S = d->sink_frames;
+  const int64_t fs = f < S ? f : S + (f - S) % (d->window_frames - S);
+  return (fs * d->grid_h + y) * (int64_t)d->grid_w + x;
 }
 
 int videomla_window_advance(const videomla_dims* d, videomla_window* w) {
@@ -368,6 +385,7 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
   a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
   a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
+  a.k_rot = d->sink_frames > 0 ? reinterpret_cast<uint16_t*>(ws + L.krot_off) : nullptr;
   a.batch = batch; a.n_heads = d->n_heads; a.d_nope = d->d_nope; a.d_rope = d->d_rope;
   a.d_c = d->d_c; a.d_v = d->d_v;
   a.dqk_pad = (int32_t)round_up((size_t)d->d_c + d->d_rope, 16);
@@ -388,6 +406,11 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = timed(K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
   if (e != hipSuccess) return hip_fail(e, "q_absorb");
+  if (a.k_rot) {  // attention sink: rotate the context's keys at window-local time
+    e = timed(K_ROPE_WINDOW, s, [&] { return launch_rope_window(a, s); });
+    if (e != hipSuccess) return hip_fail(e, "rope_window");
+    a.k_r = a.k_rot;
+  }
   e = timed(K_LATENT_ATTEND, s, [&] { return launch_latent_attend(a, s); });
   if (e != hipSuccess) return hip_fail(e, "latent_attend");
   e = timed(K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
@@ -409,6 +432,7 @@ int videomla_dense_cache_write(const videomla_dims* d, const videomla_window* w,
   if (!x || !w_k || !w_v || !kv) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
   if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
   if (int e = check_dense_head(d)) return e;
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
   if ((2 * d->n_heads * d->d_v) % 128)
     return fail(VIDEOMLA_EUNSUPPORTED, "2 * n_heads * d_v must be a multiple of 128, got %d",
                 2 * d->n_heads * d->d_v);
@@ -440,6 +464,7 @@ int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int3
   if (!q || !kv || !out) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
   if (!dense_attend_supported(d->d_v))
     return fail(VIDEOMLA_EUNSUPPORTED, "dense attention is built for d_v = 128, got %d", d->d_v);
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
   if (!aligned16(q) || !aligned16(kv) || !aligned16(out))
     return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
   const WorkspaceLayout L = dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true));

@@ -131,8 +131,19 @@ __device__ __forceinline__ TokenPos token_pos(const Geometry& g, int n) {
   p.x = r % g.grid_w;
   return p;
 }
+// Frame slot of absolute frame f: f mod W without a sink; with S sink frames, f for f < S and
+// S + (f - S) mod (W - S) otherwise.
+__device__ __forceinline__ int64_t frame_slot(const Geometry& g, int64_t f) {
+  const int S = g.sink_frames;
+  return f < S ? f : S + (f - S) % (g.window_frames - S);
+}
 __device__ __forceinline__ int64_t ring_slot(const Geometry& g, const TokenPos& p) {
-  return ((p.f % g.window_frames) * g.grid_h + p.y) * (int64_t)g.grid_w + p.x;
+  return (frame_slot(g, p.f) * g.grid_h + p.y) * (int64_t)g.grid_w + p.x;
+}
+// Position a query of the chunk is rotated at: absolute without a sink, window-local with one.
+__device__ __forceinline__ TokenPos rope_pos(const Geometry& g, TokenPos p) {
+  if (g.sink_frames > 0 && p.f >= g.sink_frames) p.f = g.sink_frames + (p.f - g.local_lo);
+  return p;
 }
 
 // Rotate the pair (u, v) of RoPE pair `pair` at position p by the angle pos_axis * theta: the

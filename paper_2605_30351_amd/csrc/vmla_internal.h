@@ -21,6 +21,12 @@ struct Geometry {
   int32_t chunk_tokens;   // chunk_frames * HW
   int64_t frame_end;      // absolute first frame of the chunk
   int64_t ring_tokens;    // window_frames * HW (ring rows per batch element)
+  // Attention sink: frames 0 .. sink_frames-1 keep frame slots 0 .. sink_frames-1, later frames
+  // cycle through the other window_frames - sink_frames slots. With a sink, positional keys are
+  // cached unrotated and the context is rotated at window-local time: frame f < sink_frames at
+  // f, a recent frame f at sink_frames + (f - local_lo).
+  int32_t sink_frames;
+  int64_t local_lo;       // first recent frame of the chunk's context (sink_frames > 0 only)
 };
 
 struct WriteArgs {
@@ -48,6 +54,7 @@ struct AttendArgs {
   uint16_t* qcat;          // workspace: [B*Nq*H][dqk_pad] bf16
   float* o_part;           // workspace: [max_seg][B*Nq*H][d_c] fp32
   float* ml_part;          // workspace: [max_seg][B*Nq*H][2] fp32 (running max, sum)
+  uint16_t* k_rot;         // workspace (sink only): [B][ring_tokens][d_rope], rotated window keys
   int32_t batch, n_heads, d_nope, d_rope, d_c, d_v, dqk_pad;
   int32_t n_valid;         // valid ring slots (prefix of the ring)
   // Work partition of the attention kernel: units are (batch, row block, key tile) triples in
@@ -88,6 +95,7 @@ __host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_w
 // Launchers (one per kernel). Return the launch status.
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
+hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s);
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);

@@ -36,8 +36,8 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_struct_layout_matches_header():
-    # 10 int32 + 2*3 int32 + 3 float = 19 * 4 bytes, no padding
-    assert ctypes.sizeof(L.VideomlaDims) == 76
+    # 10 int32 + 2*3 int32 + 3 float + 1 int32 = 20 * 4 bytes, no padding
+    assert ctypes.sizeof(L.VideomlaDims) == 80
     assert ctypes.sizeof(L.VideomlaWindow) == 8
 
 
@@ -191,3 +191,25 @@ def test_dense_workspace_covers_padded_rows():
     rows = 12 * 4864
     assert vm.dense_attend_workspace_bytes(WAN, 1) >= rows * 128 * 2 + rows * 128 * 4 + rows * 8
     assert vm.dense_attend_workspace_bytes(WAN, 4) >= 4 * (rows * 128 * 2 + rows * 128 * 4 + rows * 8)
+
+
+def test_sink_slots_and_validation():
+    from workloads import TINY_SINK, WAN_SINK
+    rng = np.random.default_rng(1)
+    for dims in (TINY_SINK, WAN_SINK):
+        for _ in range(200):
+            f = int(rng.integers(0, 500))
+            y = int(rng.integers(0, dims.grid_h))
+            x = int(rng.integers(0, dims.grid_w))
+            assert vm.slot_of(dims, f, y, x) == int(O.ring_slot(f, y, x, dims))
+        for fe in range(0, 30, dims.chunk_frames):
+            assert vm.valid_tokens(dims, fe) == len(O.context_frames(fe, dims)) * dims.hw
+    # the non-sink slots must hold a whole chunk
+    assert _write(_dims_struct(WAN, window_frames=7, sink_frames=5)) == L.EINVAL
+    assert _write(_dims_struct(WAN, sink_frames=-1)) == L.EINVAL
+    # the workspace also holds the window's rotated keys
+    plain = vm.attend_workspace_bytes(WAN_SINK.replace(sink_frames=0), 1)
+    assert vm.attend_workspace_bytes(WAN_SINK, 1) >= plain + WAN_SINK.window_tokens * 32 * 2
+    # the dense comparator has no sink mode
+    assert _dense_write(_dims_struct(WAN, window_frames=7, sink_frames=1)) == L.EUNSUPPORTED
+    assert _dense_attend(_dims_struct(WAN, window_frames=7, sink_frames=1)) == L.EUNSUPPORTED
