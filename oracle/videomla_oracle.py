@@ -15,6 +15,9 @@ What it computes, and where the paper defines it (VideoMLA, arXiv 2605.30351):
              Sliding-Window Attention": FIFO eviction of whole frames);
 * dense      the comparator the latent cache replaces: per-head K = W_K x (rotated by 3D RoPE
              over the whole head) and V = W_V x cached for every token, standard attention;
+* layer      the whole attention layer: query latent c^Q = RMSNorm(W_down^Q x), per-head
+             queries from it, attention, and the output projection W_O; with the absorbed
+             A_h / B_h form of Section "Inference-Time Reparameterization" as a self-check;
 * attention  the training-time form: per-head keys/values reconstructed explicitly
              (Eq. 2), score of Eq. 7, softmax over the active window, weighted sum of values.
              Section "Inference-Time Reparameterization" states that the absorbed latent form
@@ -246,6 +249,15 @@ def _softmax_rows(s):
     return p / np.sum(p, axis=-1, keepdims=True)
 
 
+def query_positions(rows, frame_end: int, dims):
+    """Positions the chunk's query tokens `rows` are rotated at: absolute (f, y, x) without a
+    sink, the frames' window-local time with one (the same frame as the context's keys)."""
+    f, y, x = token_position(rows, frame_end, dims)
+    if dims.sink_frames:
+        f = local_time(f, frame_end, dims)
+    return f, y, x
+
+
 def query_rope(q_r, q_pos, dims, rotate_origin: int = 0):
     """Eq. 6: q^rope = RoPE_3D(q^R) at each query token's (f, y, x); q_r [Nq, H, d_rope]."""
     f, y, x = q_pos
@@ -309,14 +321,83 @@ def chunk_attention(inp, b: int, frame_end: int, rows=None, absorbed: bool = Fal
                                        rotate_origin=origin)
     rows = np.arange(dims.chunk_tokens) if rows is None else np.asarray(rows)
     q_nope = bf16_bits_to_f64(inp.q_nope[b][rows])
-    q_pos = token_position(rows, frame_end, dims)
-    if dims.sink_frames:  # the chunk's frames in the same window-local time as the keys
-        q_pos = (local_time(q_pos[0], frame_end, dims), q_pos[1], q_pos[2])
+    q_pos = query_positions(rows, frame_end, dims)
+    if dims.sink_frames:
         origin = 0
     q_rope = query_rope(bf16_bits_to_f64(inp.q_r[b][rows]), q_pos, dims, rotate_origin=origin)
     w_uk, w_uv = bf16_bits_to_f64(inp.w_uk), bf16_bits_to_f64(inp.w_uv)
     fn = attend_absorbed if absorbed else attend_unabsorbed
     return fn(q_nope, q_rope, w_uk, w_uv, c_win, kro_win, dims)
+
+
+# --------------------------------------------------------------------------------------------
+# Whole attention layer: query path and output projection
+# --------------------------------------------------------------------------------------------
+
+def rms_norm(v, gain, eps):
+    """RMSNorm over the last axis: gain * v / sqrt(mean(v^2) + eps) (App. "VideoMLA Block":
+    c^KV and c^Q are normalized before their up-projections)."""
+    return gain * v / np.sqrt(np.mean(v * v, axis=-1, keepdims=True) + eps)
+
+
+def query_latent(x, w_dq, gamma_q, dims):
+    """c^Q = RMSNorm(W_down^Q x) for tokens x[T, d_model] (Eq. 3), fp64."""
+    return rms_norm(x @ w_dq.T, gamma_q, dims.kv_norm_eps)
+
+
+def attention_layer(inp, b: int, frame_end: int, rows=None):
+    """The whole attention layer for the chunk starting at `frame_end`, training-time form:
+    c^Q (Eq. 3); per head q^nope = W_up,h^Q c^Q (Eq. 4) and q^R = W_R,h^Q c^Q rotated (Eq. 6);
+    keys and values reconstructed from the window latents (Eq. 2); scores of Eq. 7, softmax over
+    the window; the head outputs concatenated and mixed by W_O. `inp` is a
+    workloads.FullLayerInputs. Returns y [len(rows), d_model] fp64."""
+    d = inp.dims
+    rows = np.arange(d.chunk_tokens) if rows is None else np.asarray(rows)
+    x = bf16_bits_to_f64(inp.x[b][frame_end * d.hw:(frame_end + d.chunk_frames) * d.hw][rows])
+    cq = query_latent(x, bf16_bits_to_f64(inp.w_dq), bf16_bits_to_f64(inp.gamma_q), d)
+    n, H = len(rows), d.n_heads
+    q_nope = (cq @ bf16_bits_to_f64(inp.w_uq).T).reshape(n, H, d.d_nope)
+    q_r = (cq @ bf16_bits_to_f64(inp.w_qr).T).reshape(n, H, d.d_rope)
+    q_rope = query_rope(q_r, query_positions(rows, frame_end, d), d)
+    c_win, kro_win, _ = window_latents(inp.x[b], inp.w_dkv, inp.w_kr, inp.gamma, frame_end, d)
+    o = attend_unabsorbed(q_nope, q_rope, bf16_bits_to_f64(inp.w_uk), bf16_bits_to_f64(inp.w_uv),
+                          c_win, kro_win, d)
+    return o.reshape(n, H * d.d_v) @ bf16_bits_to_f64(inp.w_o).T
+
+
+def absorbed_layer_weights(inp):
+    """App. "Inference-Time Reparameterization": A_h = (W_up,h^Q)^T W_up,h^K [d_q, d_c] and
+    B_h = W_h^O W_up,h^V [d_model, d_c] for every head, fp64. Returns (A [H, d_q, d_c],
+    B [H, d_model, d_c])."""
+    d = inp.dims
+    w_uq, w_uk = bf16_bits_to_f64(inp.w_uq), bf16_bits_to_f64(inp.w_uk)
+    w_uv, w_o = bf16_bits_to_f64(inp.w_uv), bf16_bits_to_f64(inp.w_o)
+    A = np.stack([w_uq[h * d.d_nope:(h + 1) * d.d_nope].T @ w_uk[h * d.d_nope:(h + 1) * d.d_nope]
+                  for h in range(d.n_heads)])
+    B = np.stack([w_o[:, h * d.d_v:(h + 1) * d.d_v] @ w_uv[h * d.d_v:(h + 1) * d.d_v]
+                  for h in range(d.n_heads)])
+    return A, B
+
+
+def attention_layer_absorbed(inp, b: int, frame_end: int, rows=None):
+    """The same layer in latent form (Eqs. 8-11): content score (c^Q)^T A_h c_j, positional
+    score q^rope . k^rope_j, o_lat = sum_j p_j c_j, y = sum_h B_h o_lat_h. Self-check only: it
+    must equal `attention_layer` up to rounding."""
+    d = inp.dims
+    rows = np.arange(d.chunk_tokens) if rows is None else np.asarray(rows)
+    x = bf16_bits_to_f64(inp.x[b][frame_end * d.hw:(frame_end + d.chunk_frames) * d.hw][rows])
+    cq = query_latent(x, bf16_bits_to_f64(inp.w_dq), bf16_bits_to_f64(inp.gamma_q), d)
+    n, H = len(rows), d.n_heads
+    q_r = (cq @ bf16_bits_to_f64(inp.w_qr).T).reshape(n, H, d.d_rope)
+    q_rope = query_rope(q_r, query_positions(rows, frame_end, d), d)
+    c_win, kro_win, _ = window_latents(inp.x[b], inp.w_dkv, inp.w_kr, inp.gamma, frame_end, d)
+    A, B = absorbed_layer_weights(inp)
+    scale = softmax_scale(d)
+    y = np.zeros((n, d.d_model))
+    for h in range(H):
+        p = _softmax_rows(scale * ((cq @ A[h]) @ c_win.T + q_rope[:, h] @ kro_win.T))
+        y += (p @ c_win) @ B[h].T
+    return y
 
 
 # --------------------------------------------------------------------------------------------

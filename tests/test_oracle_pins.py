@@ -568,3 +568,60 @@ def test_sink_cache_write_keeps_keys_unrotated():
     plain = O.cache_write(xs, inp.w_dkv, inp.w_kr, inp.gamma, fe, TINY_SINK.replace(sink_frames=0))
     f, y, x = O.token_position(np.arange(TINY_SINK.hw), fe, TINY_SINK)
     np.testing.assert_allclose(plain["k_cached"], O.rope3d(kr, f, y, x, TINY_SINK), rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------------
+# Whole attention layer (query path + output projection)
+# ------------------------------------------------------------------------------------------
+
+def _full_tiny(sink=False, seed=10, n_frames=6, d_q=48):
+    from workloads import TINY_SINK, make_full_layer_inputs
+    return make_full_layer_inputs(TINY_SINK if sink else TINY, seed=seed, n_frames=n_frames, d_q=d_q)
+
+
+@pytest.mark.parametrize("sink", [False, True])
+@pytest.mark.parametrize("frame_end", [0, 2, 5])
+def test_layer_absorbed_equals_reconstructed(sink, frame_end):
+    """Eqs. 8-11: the latent form with A_h = (W_up,h^Q)^T W_up,h^K and B_h = W_h^O W_up,h^V
+    equals the reconstructed per-head form followed by W_O."""
+    inp = _full_tiny(sink)
+    a = O.attention_layer(inp, 0, frame_end)
+    b = O.attention_layer_absorbed(inp, 0, frame_end)
+    np.testing.assert_allclose(b, a, rtol=0, atol=1e-12 * np.abs(a).max())
+
+
+def test_layer_query_latent_is_normalized(monkeypatch):
+    """With the positional queries zeroed, the scores see only normalized latents, so scaling
+    every activation by a constant leaves the layer output unchanged (up to eps). A planted
+    mistake, c^Q without its RMSNorm, breaks the invariance."""
+    inp = _full_tiny()
+    inp = dataclasses.replace(inp, w_qr=np.zeros_like(inp.w_qr))
+    x4 = f32_to_bf16_bits(bf16_bits_to_f32(inp.x) * np.float32(4.0))  # exact in bf16
+    a = O.attention_layer(inp, 0, 3)
+    b = O.attention_layer(dataclasses.replace(inp, x=x4), 0, 3)
+    np.testing.assert_allclose(b, a, rtol=0, atol=1e-5 * np.abs(a).max())
+    monkeypatch.setattr(O, "query_latent", lambda x, w_dq, gamma_q, dims: gamma_q * (x @ w_dq.T))
+    a2 = O.attention_layer(inp, 0, 3)
+    b2 = O.attention_layer(dataclasses.replace(inp, x=x4), 0, 3)
+    assert np.abs(b2 - a2).max() > 1e-3 * np.abs(a2).max()
+
+
+def test_layer_head_permutation_invariance():
+    """Relabelling the heads in every per-head weight (W_UQ, W_QR, W_UK, W_UV row blocks and
+    W_O column blocks) leaves the layer output unchanged: catches a head mixed with another
+    head's slice of the output projection."""
+    inp = _full_tiny(seed=11)
+    d = inp.dims
+    perm = [1, 0]
+
+    def rows(w, k):
+        return np.concatenate([w[h * k:(h + 1) * k] for h in perm])
+
+    p = dataclasses.replace(
+        inp, w_uq=rows(inp.w_uq, d.d_nope), w_qr=rows(inp.w_qr, d.d_rope),
+        w_uk=rows(inp.w_uk, d.d_nope), w_uv=rows(inp.w_uv, d.d_v),
+        w_o=np.concatenate([inp.w_o[:, h * d.d_v:(h + 1) * d.d_v] for h in perm], axis=1))
+    a = O.attention_layer(inp, 0, 4)
+    b = O.attention_layer(p, 0, 4)
+    np.testing.assert_allclose(b, a, rtol=0, atol=1e-12 * np.abs(a).max())
+    assert np.abs(O.attention_layer(dataclasses.replace(p, w_o=inp.w_o), 0, 4) - a).max() > 1e-3

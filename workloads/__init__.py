@@ -145,6 +145,58 @@ def make_layer_inputs(dims: Dims, seed: int, n_frames: int, batch: int = 1, norm
 
 
 @dataclass
+class FullLayerInputs:
+    """Seeded inputs of a whole attention layer: the cache path of LayerInputs plus the query
+    path and the output projection (App. "VideoMLA Block"), bf16 bit patterns.
+
+    x, w_dkv, w_kr, w_uk, w_uv, gamma   as in LayerInputs (gamma: RMSNorm gain of c^KV)
+    w_dq     [d_q, d_model]               query down-projection W_down^Q
+    gamma_q  [d_q]                        RMSNorm gain of c^Q
+    w_uq     [n_heads * d_nope, d_q]      query up-projection W_up^Q, head h = rows h*d_nope ..
+    w_qr     [n_heads * d_rope, d_q]      RoPE query projection W_R^Q, head h = rows h*d_rope ..
+    w_o      [d_model, n_heads * d_v]     output projection W_O, head h = columns h*d_v ..
+    """
+
+    dims: Dims
+    batch: int
+    n_frames: int
+    d_q: int
+    x: np.ndarray
+    w_dkv: np.ndarray
+    w_kr: np.ndarray
+    w_uk: np.ndarray
+    w_uv: np.ndarray
+    gamma: np.ndarray | None
+    w_dq: np.ndarray
+    gamma_q: np.ndarray
+    w_uq: np.ndarray
+    w_qr: np.ndarray
+    w_o: np.ndarray
+
+
+def make_full_layer_inputs(dims: Dims, seed: int, n_frames: int, d_q: int,
+                           batch: int = 1) -> FullLayerInputs:
+    """Draw a whole layer's inputs in a fixed order: x frames, W_DKV, W_KR, W_UK, W_UV (as
+    make_layer_inputs), then W_DQ, the c^Q gain (uniform in [0.5, 1.5], so that folding it into
+    the query weights is exercised), W_UQ, W_QR, W_O."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    d = dims
+    x = _normal_bf16(rng, (batch, n_frames * d.hw, d.d_model))
+    w_dkv = _normal_bf16(rng, (d.d_c, d.d_model), 1.0 / np.sqrt(d.d_model))
+    w_kr = _normal_bf16(rng, (d.d_rope, d.d_model), 1.0 / np.sqrt(d.d_model))
+    w_uk = _normal_bf16(rng, (d.n_heads * d.d_nope, d.d_c), 1.0 / np.sqrt(d.d_c))
+    w_uv = _normal_bf16(rng, (d.n_heads * d.d_v, d.d_c), 1.0 / np.sqrt(d.d_c))
+    gamma = f32_to_bf16_bits(np.ones(d.d_c, np.float32))
+    w_dq = _normal_bf16(rng, (d_q, d.d_model), 1.0 / np.sqrt(d.d_model))
+    gamma_q = f32_to_bf16_bits(rng.uniform(0.5, 1.5, size=d_q).astype(np.float32))
+    w_uq = _normal_bf16(rng, (d.n_heads * d.d_nope, d_q), 1.0 / np.sqrt(d_q))
+    w_qr = _normal_bf16(rng, (d.n_heads * d.d_rope, d_q), 1.0 / np.sqrt(d_q))
+    w_o = _normal_bf16(rng, (d.d_model, d.n_heads * d.d_v), 1.0 / np.sqrt(d.n_heads * d.d_v))
+    return FullLayerInputs(d, batch, n_frames, d_q, x, w_dkv, w_kr, w_uk, w_uv, gamma, w_dq,
+                           gamma_q, w_uq, w_qr, w_o)
+
+
+@dataclass
 class DenseInputs:
     """Seeded inputs of the dense per-head comparator (bf16 bit patterns).
 
