@@ -286,6 +286,91 @@ def sink_chunk_step(args, vm, torch, d, fe=237):
     }), flush=True)
 
 
+def full_layer_chunk_step(args, vm, torch, d, d_q=768, fe=21):
+    """One chunk-step of the whole attention layer in latent form: the cache write of the chunk
+    (frames 21..23, evicting 0..2), then videomla_attend_layer from the chunk's attention input x
+    to the output of W_O (query latent, absorbed queries, latent attention over the 32,760-key
+    window, value/output absorption), batch 1, d_q = 768. Weights are packed once before the
+    timed region. Seeded synthetic bf16 drawn on the GPU; x cycles through 32 buffers."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(12)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq, H = d.chunk_tokens, d.n_heads
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    weights = torch.empty(vm.layer_weights_bytes(d, d_q), dtype=torch.uint8, device=dev)
+    vm.prepare_layer_weights(
+        d, d_q, normal((d_q, d.d_model), d.d_model ** -0.5),
+        torch.ones(d_q, dtype=torch.bfloat16, device=dev),
+        normal((H * d.d_nope, d_q), d_q ** -0.5), normal((H * d.d_rope, d_q), d_q ** -0.5),
+        normal((H * d.d_nope, d.d_c), d.d_c ** -0.5), normal((H * d.d_v, d.d_c), d.d_c ** -0.5),
+        normal((d.d_model, H * d.d_v), (H * d.d_v) ** -0.5), weights)
+    c_kv = torch.zeros((1, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+    k_r = torch.zeros((1, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+    y = torch.empty((1, nq, d.d_model), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_layer_workspace_bytes(d, d_q, 1), dtype=torch.uint8, device=dev)
+    for f in range(0, fe, d.chunk_frames):
+        vm.cache_write(d, f, 1, normal((1, nq, d.d_model)), w_dkv, w_kr, gamma, c_kv, k_r)
+    xs = [normal((1, nq, d.d_model)) for _ in range(args.x_buffers)]
+    torch.cuda.synchronize()
+
+    def step(i):
+        x = xs[i % len(xs)]
+        vm.cache_write(d, fe, 1, x, w_dkv, w_kr, gamma, c_kv, k_r)
+        vm.attend_layer(d, fe, 1, d_q, x, weights, c_kv, k_r, y, ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    names = ("cache_write", "q_down", "q_up", "latent_attend", "latent_merge", "out_mix")
+    vm.timing_enable(True)
+    for k in names:
+        vm.timing_read(k)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    marks[0].record()
+    for i in range(args.steps):
+        step(i)
+        marks[i + 1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
+    kernels = {}
+    for k in names:
+        n, tot = vm.timing_read(k)
+        kernels[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 3)}
+    vm.timing_enable(False)
+    S = d.window_tokens
+    rows = nq * H
+    flop = {"cache_write": nq * 2 * d.d_model * (d.d_c + d.d_rope),
+            "q_down": nq * 2 * d.d_model * d_q,
+            "q_up": nq * 2 * d_q * H * (d.d_c + d.d_rope),
+            "latent_attend": rows * S * (2 * (d.d_c + d.d_rope) + 2 * d.d_c),
+            "out_mix": nq * 2 * H * d.d_c * d.d_model}
+    for k, f in flop.items():
+        kernels[k]["tflops"] = round(f / (kernels[k]["avg_us"] / 1e6) / 1e12, 1)
+    ms = 1e3 * elapsed / args.steps
+    print(json.dumps({
+        "metric": "ms/chunk-step & TFLOP/s, whole attention layer in latent form (x -> W_O output)",
+        "value": round(sum(flop.values()) / (ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
+        "higher_is_better": True, "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "kernels": kernels,
+        "config": {"workload": ("Wan2.1-1.3B attention layer chunk-step, latent form: cache write "
+                                "of 4,680 tokens, then c^Q = RMSNorm(W_DQ x) (d_q = 768), "
+                                "absorbed queries, latent attend over 32,760 keys x 12 heads, "
+                                "y = sum_h B_h o_lat_h; batch 1"),
+                   "d_q": d_q, "seed": 12},
+    }), flush=True)
+
+
 def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
     """Minute-scale rollout at batch 4: `--chunks` consecutive 3-frame chunks (80 = frames
     0..239, temporal RoPE index up to 239, the ring wrapping eleven times) through 30 attention
@@ -440,13 +525,14 @@ def main():
                     help="also run a 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="wan-layer-chunk-step",
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
-                             "wan-sink-chunk-step"),
+                             "wan-sink-chunk-step", "wan-full-layer-chunk-step"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
                          "chunks through 30 layers, latent path and dense comparator; "
                          "wan-sink-chunk-step: one chunk-step with a sink frame + 6 recent "
-                         "frames late in a rollout")
+                         "frames late in a rollout; wan-full-layer-chunk-step: the whole "
+                         "attention layer in latent form (query path and W_O absorbed)")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -465,6 +551,9 @@ def main():
         return
     if args.workload == "wan-rollout-b4":
         rollout_comparison(args, vm, torch, WAN)
+        return
+    if args.workload == "wan-full-layer-chunk-step":
+        full_layer_chunk_step(args, vm, torch, WAN)
         return
     if args.workload == "wan-sink-chunk-step":
         from workloads import WAN_SINK

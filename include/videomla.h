@@ -147,6 +147,62 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * The whole attention layer in latent form (App. "Inference-Time Reparameterization",
+ * Eqs. 8-11, and App. "VideoMLA Block"): from the chunk's attention input x to the output of
+ * the output projection W_O, with the query path absorbed.
+ *
+ *   c^Q      = RMSNorm(W_down^Q x) with gain gamma_q and eps kv_norm_eps       (Eq. 3)
+ *   q_lat_h  = A_h^T c^Q,  A_h = (W_up,h^Q)^T W_up,h^K   [d_q x d_c]           (Eq. 8)
+ *   q^rope_h = RoPE_3D(W_R,h^Q c^Q) at the token's position                     (Eq. 6)
+ *   o_lat_h  = sum_j softmax_j(scale (q_lat_h . c_j + q^rope_h . k^rope_j)) c_j  (Eqs. 7, 10)
+ *   y        = sum_h B_h o_lat_h,  B_h = W_h^O W_up,h^V   [d_model x d_c]       (Eq. 11)
+ *
+ * A_h and B_h depend only on the weights: videomla_prepare_layer_weights computes them once
+ * (fp32 sums, rounded to bf16, the gain gamma_q folded into the query matrices) into an opaque
+ * device buffer of videomla_layer_weights_bytes() bytes, which videomla_attend_layer reads.
+ */
+
+/* Bytes of the packed layer weights for this shape and query latent width d_q (0 on error). */
+size_t videomla_layer_weights_bytes(const videomla_dims* dims, int32_t d_q);
+
+/*
+ * videomla_prepare_layer_weights -- pack one layer's weights for videomla_attend_layer.
+ *   w_dq     [d_q][d_model]          W_down^Q
+ *   gamma_q  [d_q] RMSNorm gain of c^Q, or NULL for ones
+ *   w_uq     [n_heads * d_nope][d_q] W_up^Q (head h = rows h*d_nope ..)
+ *   w_qr     [n_heads * d_rope][d_q] W_R^Q  (head h = rows h*d_rope ..)
+ *   w_uk     [n_heads * d_nope][d_c] W_up^K,  w_uv [n_heads * d_v][d_c] W_up^V
+ *   w_o      [d_model][n_heads * d_v] W_O (head h = columns h*d_v ..)
+ *   weights  device buffer of at least videomla_layer_weights_bytes() bytes, written
+ * Requires d_model % 64 == 0 and 1 <= d_q <= 65536.
+ */
+int videomla_prepare_layer_weights(const videomla_dims* dims, int32_t d_q, const uint16_t* w_dq,
+                                   const uint16_t* gamma_q, const uint16_t* w_uq,
+                                   const uint16_t* w_qr, const uint16_t* w_uk,
+                                   const uint16_t* w_uv, const uint16_t* w_o, void* weights,
+                                   size_t weights_bytes, void* stream);
+
+/* Bytes of device workspace videomla_attend_layer needs for this shape, d_q and batch. */
+size_t videomla_attend_layer_workspace_bytes(const videomla_dims* dims, int32_t d_q,
+                                             int32_t batch);
+
+/*
+ * videomla_attend_layer -- the layer above for the chunk at win->frame_end, over the same
+ * window (and sink context) as videomla_attend.
+ *   x        [batch][chunk_frames * HW][d_model]   bf16, the chunk's attention input
+ *   weights  as packed by videomla_prepare_layer_weights for the same dims and d_q
+ *   c_kv, k_r  the rings as written by videomla_cache_write
+ *   y        [batch][chunk_frames * HW][d_model]   bf16, output of the output projection
+ * Arithmetic: bf16 operands (c^Q before its normalization, q_cat, o_lat and the packed weights
+ * are rounded to bf16), fp32 accumulation, softmax and normalization factors.
+ * Requirements of videomla_attend and of videomla_prepare_layer_weights.
+ */
+int videomla_attend_layer(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                          int32_t d_q, const uint16_t* x, const void* weights,
+                          size_t weights_bytes, const uint16_t* c_kv, const uint16_t* k_r,
+                          uint16_t* y, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Dense per-head comparator: the cache VideoMLA replaces, built only to measure the latent
  * path against it on the same GPU (per-head keys and values of Eq. 2 without the shared
  * latent; the 3,072-scalar-per-token layout of the Introduction). Head width d = d_v.
@@ -227,7 +283,8 @@ int videomla_set_attend_workgroups(int32_t n_workgroups);
  * launches is bracketed by two events recorded on the same stream. After the caller has
  * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed
  * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj",
- * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge", "rope_window") into
+ * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge", "rope_window", "q_down",
+ * "q_up", "latent_merge", "out_mix", "prepare_layer_weights") into
  * *count and *total_ms, and forgets them. Timing state is process-wide and not thread-safe.
  */
 int videomla_timing_enable(int32_t enable);

@@ -8,6 +8,8 @@ from ._lib import (  # noqa: F401
     EXPORTED,
     VideomlaError,
     attend,
+    attend_layer,
+    attend_layer_workspace_bytes,
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,
@@ -15,7 +17,9 @@ from ._lib import (  # noqa: F401
     dense_attend_workspace_bytes,
     dense_cache_bytes_per_token,
     dense_cache_write,
+    layer_weights_bytes,
     make_dims,
+    prepare_layer_weights,
     set_attend_workgroups,
     slot_of,
     timing_enable,

@@ -28,6 +28,8 @@ EXPORTED = (
     "videomla_timing_enable", "videomla_timing_read",
     "videomla_dense_cache_bytes_per_token", "videomla_dense_cache_write",
     "videomla_dense_attend_workspace_bytes", "videomla_dense_attend",
+    "videomla_layer_weights_bytes", "videomla_prepare_layer_weights",
+    "videomla_attend_layer_workspace_bytes", "videomla_attend_layer",
 )
 
 
@@ -84,6 +86,16 @@ _lib.videomla_dense_attend_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_dense_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t,
                                        _P]
 _lib.videomla_dense_attend.restype = ctypes.c_int
+_lib.videomla_layer_weights_bytes.argtypes = [_DP, ctypes.c_int32]
+_lib.videomla_layer_weights_bytes.restype = ctypes.c_size_t
+_lib.videomla_prepare_layer_weights.argtypes = [_DP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P,
+                                                _P, ctypes.c_size_t, _P]
+_lib.videomla_prepare_layer_weights.restype = ctypes.c_int
+_lib.videomla_attend_layer_workspace_bytes.argtypes = [_DP, ctypes.c_int32, ctypes.c_int32]
+_lib.videomla_attend_layer_workspace_bytes.restype = ctypes.c_size_t
+_lib.videomla_attend_layer.argtypes = [_DP, _WP, ctypes.c_int32, ctypes.c_int32, _P, _P,
+                                       ctypes.c_size_t, _P, _P, _P, _P, ctypes.c_size_t, _P]
+_lib.videomla_attend_layer.restype = ctypes.c_int
 
 
 class VideomlaError(RuntimeError):
@@ -221,6 +233,53 @@ def dense_attend(dims, frame_end: int, batch: int, q, kv, out, workspace, stream
     _check(_lib.videomla_dense_attend(
         ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q, "q"), _ptr(kv, "kv"),
         _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
+
+
+def layer_weights_bytes(dims, d_q: int) -> int:
+    return int(_lib.videomla_layer_weights_bytes(ctypes.byref(make_dims(dims)), int(d_q)))
+
+
+def prepare_layer_weights(dims, d_q: int, w_dq, gamma_q, w_uq, w_qr, w_uk, w_uv, w_o, weights,
+                          stream=None):
+    """videomla_prepare_layer_weights; `weights` is a uint8 device tensor."""
+    d = make_dims(dims)
+    H = d.n_heads
+    _need(w_dq, "w_dq", d_q * d.d_model)
+    if gamma_q is not None:
+        _need(gamma_q, "gamma_q", d_q)
+    _need(w_uq, "w_uq", H * d.d_nope * d_q)
+    _need(w_qr, "w_qr", H * d.d_rope * d_q)
+    _need(w_uk, "w_uk", H * d.d_nope * d.d_c)
+    _need(w_uv, "w_uv", H * d.d_v * d.d_c)
+    _need(w_o, "w_o", d.d_model * H * d.d_v)
+    _check(_lib.videomla_prepare_layer_weights(
+        ctypes.byref(d), int(d_q), _ptr(w_dq, "w_dq"), _ptr(gamma_q, "gamma_q"),
+        _ptr(w_uq, "w_uq"), _ptr(w_qr, "w_qr"), _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"),
+        _ptr(w_o, "w_o"), _ptr(weights, "weights", (torch.uint8,)), weights.numel(),
+        _stream(stream)))
+
+
+def attend_layer_workspace_bytes(dims, d_q: int, batch: int) -> int:
+    return int(_lib.videomla_attend_layer_workspace_bytes(ctypes.byref(make_dims(dims)), int(d_q),
+                                                          int(batch)))
+
+
+def attend_layer(dims, frame_end: int, batch: int, d_q: int, x, weights, c_kv, k_r, y, workspace,
+                 stream=None):
+    """videomla_attend_layer on torch tensors; `weights` and `workspace` are uint8 device tensors."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    nq = d.chunk_frames * hw
+    _need(x, "x", batch * nq * d.d_model)
+    _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
+    _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
+    _need(y, "y", batch * nq * d.d_model)
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_attend_layer(
+        ctypes.byref(d), ctypes.byref(w), int(batch), int(d_q), _ptr(x, "x"),
+        _ptr(weights, "weights", (torch.uint8,)), weights.numel(), _ptr(c_kv, "c_kv"),
+        _ptr(k_r, "k_r"), _ptr(y, "y"), _ptr(workspace, "workspace", (torch.uint8,)),
+        workspace.numel() if workspace is not None else 0, _stream(stream)))
 
 
 def window_advance(dims, frame_end: int) -> int:

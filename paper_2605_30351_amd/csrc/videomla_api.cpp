@@ -109,11 +109,14 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
 // ---- timing -------------------------------------------------------------------------------
 enum KernelId {
   K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
-  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW, K_COUNT
+  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW,
+  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_COUNT
 };
 const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
                                      "out_proj",          "dense_cache_write", "dense_q_prep",
-                                     "dense_attend",      "dense_merge",  "rope_window"};
+                                     "dense_attend",      "dense_merge",  "rope_window",
+                                     "q_down",            "q_up",         "latent_merge",
+                                     "out_mix",           "prepare_layer_weights"};
 
 struct TimingRec {
   int kernel;
@@ -269,6 +272,31 @@ int check_dense_head(const videomla_dims* d) {
   return VIDEOMLA_OK;
 }
 
+// Packed weights of the whole layer: W_down^Q [d_q_pad][d_model], the per-head query matrix
+// [H (d_c + d_rope)][d_q_pad], B [d_model][k_out_pad]; zero padding to whole 64-column chunks.
+struct LayerWeightsLayout {
+  int d_q_pad, k_out_pad;
+  size_t wdq_off, wq_off, bo_off, total;
+};
+
+LayerWeightsLayout layer_weights_layout(const videomla_dims* d, int32_t d_q) {
+  LayerWeightsLayout L{};
+  L.d_q_pad = (int)round_up((size_t)d_q, 64);
+  L.k_out_pad = (int)round_up((size_t)d->n_heads * d->d_c, 64);
+  L.wdq_off = 0;
+  L.wq_off = round_up((size_t)L.d_q_pad * d->d_model * 2, 256);
+  L.bo_off = L.wq_off + round_up((size_t)d->n_heads * (d->d_c + d->d_rope) * L.d_q_pad * 2, 256);
+  L.total = L.bo_off + round_up((size_t)d->d_model * L.k_out_pad * 2, 256);
+  return L;
+}
+
+int check_layer_shape(const videomla_dims* d, int32_t d_q) {
+  if (d_q <= 0 || d_q > (1 << 16)) return fail(VIDEOMLA_EINVAL, "d_q must be in [1, 65536], got %d", d_q);
+  if (d->d_model % 64)
+    return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
+  return VIDEOMLA_OK;
+}
+
 int check_attend_shape(const videomla_dims* d) {
   if (!latent_attend_supported(d->d_c, d->d_rope))
     return fail(VIDEOMLA_EUNSUPPORTED,
@@ -359,29 +387,15 @@ size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
   return workspace_layout(d, batch, workspace_max_seg(d, batch)).total;
 }
 
-int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
-                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
-                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
-  if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
-    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
-  if (int e = check_attend_shape(d)) return e;
-  if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
-      !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
-    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  const WorkspaceLayout L = workspace_layout(d, batch, workspace_max_seg(d, batch));
-  if (!workspace || workspace_bytes < L.total)
-    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+namespace {
 
+// Attention arguments common to videomla_attend and videomla_attend_layer (shapes, window,
+// work partition, workspace carving); the caller sets the query and projection pointers.
+AttendArgs attend_args(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                       const WorkspaceLayout& L, char* ws, const uint16_t* c_kv,
+                       const uint16_t* k_r) {
   AttendArgs a{};
-  a.q_nope = q_nope; a.q_r = q_r; a.w_uk = w_uk; a.w_uv = w_uv;
-  a.c_kv = c_kv; a.k_r = k_r; a.out = out;
-  char* ws = static_cast<char*>(workspace);
+  a.c_kv = c_kv; a.k_r = k_r;
   a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
   a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
   a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
@@ -402,17 +416,50 @@ int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t ba
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
   a.qscale = (float)(scale * 1.4426950408889634);
+  return a;
+}
 
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = timed(K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "q_absorb");
-  if (a.k_rot) {  // attention sink: rotate the context's keys at window-local time
+// The window keys at window-local time (sink only), then the attention kernel.
+int run_attention(AttendArgs& a, hipStream_t s) {
+  hipError_t e;
+  if (a.k_rot) {
     e = timed(K_ROPE_WINDOW, s, [&] { return launch_rope_window(a, s); });
     if (e != hipSuccess) return hip_fail(e, "rope_window");
     a.k_r = a.k_rot;
   }
   e = timed(K_LATENT_ATTEND, s, [&] { return launch_latent_attend(a, s); });
   if (e != hipSuccess) return hip_fail(e, "latent_attend");
+  return VIDEOMLA_OK;
+}
+
+}  // namespace
+
+int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
+    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (int e = check_attend_shape(d)) return e;
+  if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
+      !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const WorkspaceLayout L = workspace_layout(d, batch, workspace_max_seg(d, batch));
+  if (!workspace || workspace_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+
+  AttendArgs a = attend_args(d, w, batch, L, static_cast<char*>(workspace), c_kv, k_r);
+  a.q_nope = q_nope; a.q_r = q_r; a.w_uk = w_uk; a.w_uv = w_uv; a.out = out;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = timed(K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "q_absorb");
+  if (int r = run_attention(a, s)) return r;
   e = timed(K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
   if (e != hipSuccess) return hip_fail(e, "out_proj");
   return ok();
@@ -503,6 +550,121 @@ int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int3
   if (e != hipSuccess) return hip_fail(e, "dense_attend");
   e = timed(K_DENSE_MERGE, s, [&] { return launch_dense_merge(a, s); });
   if (e != hipSuccess) return hip_fail(e, "dense_merge");
+  return ok();
+}
+
+size_t videomla_layer_weights_bytes(const videomla_dims* d, int32_t d_q) {
+  if (check_dims(d) || check_layer_shape(d, d_q)) return 0;
+  return layer_weights_layout(d, d_q).total;
+}
+
+int videomla_prepare_layer_weights(const videomla_dims* d, int32_t d_q, const uint16_t* w_dq,
+                                   const uint16_t* gamma_q, const uint16_t* w_uq,
+                                   const uint16_t* w_qr, const uint16_t* w_uk,
+                                   const uint16_t* w_uv, const uint16_t* w_o, void* weights,
+                                   size_t weights_bytes, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_layer_shape(d, d_q)) return e;
+  if (!w_dq || !w_uq || !w_qr || !w_uk || !w_uv || !w_o || !weights)
+    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  const LayerWeightsLayout L = layer_weights_layout(d, d_q);
+  if (weights_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "layer weights need %zu bytes, %zu given", L.total, weights_bytes);
+  if (!aligned16(weights)) return fail(VIDEOMLA_EALIGN, "weights must be 16-byte aligned");
+  PrepArgs a{};
+  a.w_dq = w_dq; a.gamma_q = gamma_q; a.w_uq = w_uq; a.w_qr = w_qr; a.w_uk = w_uk; a.w_uv = w_uv;
+  a.w_o = w_o;
+  char* base = static_cast<char*>(weights);
+  a.w_dq_pad = reinterpret_cast<uint16_t*>(base + L.wdq_off);
+  a.wq_cat = reinterpret_cast<uint16_t*>(base + L.wq_off);
+  a.b_o = reinterpret_cast<uint16_t*>(base + L.bo_off);
+  a.n_heads = d->n_heads; a.d_model = d->d_model; a.d_nope = d->d_nope; a.d_rope = d->d_rope;
+  a.d_c = d->d_c; a.d_v = d->d_v; a.d_q = d_q; a.d_q_pad = L.d_q_pad; a.k_out_pad = L.k_out_pad;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = timed(K_PREPARE, s, [&] { return launch_prepare_weights(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "prepare_layer_weights");
+  return ok();
+}
+
+namespace {
+// attention workspace, then u = W_down^Q x [B Nq][d_q_pad] and o_lat [B Nq][k_out_pad], bf16
+struct LayerWorkspace {
+  WorkspaceLayout att;
+  size_t u_off, olat_off, total;
+};
+
+LayerWorkspace layer_workspace(const videomla_dims* d, int32_t d_q, int32_t batch) {
+  const LayerWeightsLayout W = layer_weights_layout(d, d_q);
+  LayerWorkspace L{};
+  L.att = workspace_layout(d, batch, workspace_max_seg(d, batch));
+  const size_t tokens = (size_t)batch * d->chunk_frames * d->grid_h * d->grid_w;
+  L.u_off = L.att.total;
+  L.olat_off = L.u_off + round_up(tokens * W.d_q_pad * 2, 256);
+  L.total = L.olat_off + round_up(tokens * W.k_out_pad * 2, 256);
+  return L;
+}
+}  // namespace
+
+size_t videomla_attend_layer_workspace_bytes(const videomla_dims* d, int32_t d_q, int32_t batch) {
+  if (check_dims(d) || check_layer_shape(d, d_q) || batch <= 0) return 0;
+  if (!latent_attend_supported(d->d_c, d->d_rope)) return 0;
+  return layer_workspace(d, d_q, batch).total;
+}
+
+int videomla_attend_layer(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                          int32_t d_q, const uint16_t* x, const void* weights,
+                          size_t weights_bytes, const uint16_t* c_kv, const uint16_t* k_r,
+                          uint16_t* y, void* workspace, size_t workspace_bytes, void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (int e = check_layer_shape(d, d_q)) return e;
+  if (!x || !weights || !c_kv || !k_r || !y) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (int e = check_attend_shape(d)) return e;
+  if (!aligned16(x) || !aligned16(weights) || !aligned16(c_kv) || !aligned16(k_r) || !aligned16(y))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const LayerWeightsLayout W = layer_weights_layout(d, d_q);
+  if (weights_bytes < W.total)
+    return fail(VIDEOMLA_EWORKSPACE, "layer weights of %zu bytes expected, %zu given", W.total,
+                weights_bytes);
+  const LayerWorkspace L = layer_workspace(d, d_q, batch);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+
+  char* ws = static_cast<char*>(workspace);
+  const char* wb = static_cast<const char*>(weights);
+  AttendArgs a = attend_args(d, w, batch, L.att, ws, c_kv, k_r);
+  uint16_t* u = reinterpret_cast<uint16_t*>(ws + L.u_off);
+  uint16_t* o_lat = reinterpret_cast<uint16_t*>(ws + L.olat_off);
+  const int M = batch * a.geo.chunk_tokens;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+
+  GemmArgs g1{};  // u = W_down^Q x
+  g1.a = reinterpret_cast<const uint16_t*>(wb + W.wdq_off); g1.b = x; g1.out = u;
+  g1.M = M; g1.N = W.d_q_pad; g1.K = d->d_model; g1.ldo = W.d_q_pad; g1.epi = kEpiStore;
+  hipError_t e = timed(K_Q_DOWN, s, [&] { return launch_gemm_nt(g1, s); });
+  if (e != hipSuccess) return hip_fail(e, "q_down");
+
+  GemmArgs g2{};  // q_cat from c^Q = g_Q u / rms(u) (the gain is in the packed weights)
+  g2.a = reinterpret_cast<const uint16_t*>(wb + W.wq_off); g2.b = u; g2.out = a.qcat;
+  g2.M = M; g2.N = d->n_heads * (d->d_c + d->d_rope); g2.K = W.d_q_pad; g2.ldo = a.dqk_pad;
+  g2.epi = kEpiQcat;
+  g2.q_heads = d->n_heads; g2.q_dc = d->d_c; g2.q_dr = d->d_rope; g2.q_norm_dim = d_q;
+  g2.qscale = a.qscale; g2.eps = d->kv_norm_eps; g2.geo = a.geo; g2.rope = a.rope;
+  e = timed(K_Q_UP, s, [&] { return launch_gemm_nt(g2, s); });
+  if (e != hipSuccess) return hip_fail(e, "q_up");
+
+  if (int r = run_attention(a, s)) return r;
+  e = timed(K_LATENT_MERGE, s, [&] { return launch_latent_merge(a, o_lat, W.k_out_pad, s); });
+  if (e != hipSuccess) return hip_fail(e, "latent_merge");
+
+  GemmArgs g3{};  // y = [B_1 .. B_H] o_lat
+  g3.a = reinterpret_cast<const uint16_t*>(wb + W.bo_off); g3.b = o_lat; g3.out = y;
+  g3.M = M; g3.N = d->d_model; g3.K = W.k_out_pad; g3.ldo = d->d_model; g3.epi = kEpiStore;
+  e = timed(K_OUT_MIX, s, [&] { return launch_gemm_nt(g3, s); });
+  if (e != hipSuccess) return hip_fail(e, "out_mix");
   return ok();
 }
 

@@ -106,17 +106,6 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 constexpr bf16x2 kOnesBf16x2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-// acc + sum of the 8 bf16 values of v, accumulated in fp32 (v_dot2 against (1, 1)).
-__device__ __forceinline__ float sum_bf16x8(bf16x8 v, float acc) {
-  const bf16x2 one = kOnesBf16x2;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const bf16x2 pair = {v[2 * i], v[2 * i + 1]};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
-  }
-  return acc;
-}
-
 // Absolute position of chunk token n: (f, y, x).
 struct TokenPos {
   int64_t f;

@@ -87,6 +87,29 @@ struct DenseWriteArgs {
   RopeTable rope;          // d_head / 2 pairs
 };
 
+// Plain bf16 GEMM out^T[o][token] = a[o][:] . b[token][:] (a [N][K], b [M][K], K % 64 == 0).
+constexpr int kEpiStore = 0;  // out[token][o] (row stride ldo), bf16
+constexpr int kEpiQcat = 1;   // q_cat rows (token, head): RMSNorm factor, RoPE, scale; see k_layer.hip
+struct GemmArgs {
+  const uint16_t* a;       // [N][K] weight rows
+  const uint16_t* b;       // [M][K] token rows
+  uint16_t* out;
+  int32_t M, N, K, ldo;
+  int32_t epi;
+  // q_cat epilogue: output column o = h (q_dc + q_dr) + c; row (token, h) of width ldo
+  int32_t q_heads, q_dc, q_dr, q_norm_dim;
+  float qscale, eps;
+  Geometry geo;            // token t of the flat [B][Nq] order sits at chunk index t % Nq
+  RopeTable rope;
+};
+
+// Packing of the whole layer's weights (see k_layer.hip).
+struct PrepArgs {
+  const uint16_t *w_dq, *gamma_q, *w_uq, *w_qr, *w_uk, *w_uv, *w_o;
+  uint16_t *w_dq_pad, *wq_cat, *b_o;
+  int32_t n_heads, d_model, d_nope, d_rope, d_c, d_v, d_q, d_q_pad, k_out_pad;
+};
+
 // Workgroup whose unit range [w*U/G, (w+1)*U/G) contains `unit`.
 __host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_wg) {
   return (int)(((unit + 1) * (int64_t)n_wg - 1) / units);
@@ -102,6 +125,9 @@ hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);
 hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s);
+hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
+hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat, hipStream_t s);
+hipError_t launch_prepare_weights(const PrepArgs& a, hipStream_t s);
 
 // Shapes the attention kernel is instantiated for.
 bool latent_attend_supported(int d_c, int d_rope);

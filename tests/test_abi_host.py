@@ -213,3 +213,31 @@ def test_sink_slots_and_validation():
     # the dense comparator has no sink mode
     assert _dense_write(_dims_struct(WAN, window_frames=7, sink_frames=1)) == L.EUNSUPPORTED
     assert _dense_attend(_dims_struct(WAN, window_frames=7, sink_frames=1)) == L.EUNSUPPORTED
+
+
+def test_layer_calls_validate_and_size():
+    d = L.make_dims(WAN)
+    # W_down^Q [768][1536], query matrix [12 * 224][768], B [1536][2304], bf16, 256-aligned
+    assert vm.layer_weights_bytes(WAN, 768) == 768 * 1536 * 2 + 2688 * 768 * 2 + 1536 * 2304 * 2
+    assert vm.layer_weights_bytes(TINY, 48) >= 64 * 64 * 2 + 48 * 64 * 2 + 64 * 64 * 2  # padded
+    assert vm.layer_weights_bytes(WAN, 0) == 0
+    ws = vm.attend_layer_workspace_bytes(WAN, 768, 1)
+    assert ws >= vm.attend_workspace_bytes(WAN, 1) + 4680 * 768 * 2 + 4680 * 2304 * 2
+    w = L.VideomlaWindow(21)
+    wb = vm.layer_weights_bytes(WAN, 768)
+
+    def layer(d=d, d_q=768, x=FAKE, weights=FAKE, weights_bytes=wb, ws_ptr=FAKE, ws_bytes=1 << 40):
+        return L.raw().videomla_attend_layer(ctypes.byref(d), ctypes.byref(w), 1, d_q, x, weights,
+                                             weights_bytes, FAKE, FAKE, FAKE, ws_ptr, ws_bytes, None)
+    assert layer(x=None) == L.EINVAL
+    assert layer(d_q=0) == L.EINVAL
+    assert layer(x=MISALIGNED) == L.EALIGN
+    assert layer(weights_bytes=wb - 1) == L.EWORKSPACE
+    assert layer(ws_ptr=None) == L.EWORKSPACE
+    assert layer(ws_bytes=ws - 1) == L.EWORKSPACE
+    assert layer(d=_dims_struct(WAN, d_c=128)) == L.EUNSUPPORTED
+    assert layer(d=_dims_struct(WAN, d_model=1000)) == L.EUNSUPPORTED
+    prep = L.raw().videomla_prepare_layer_weights
+    assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, wb, None) == L.EINVAL
+    assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, wb - 1, None) == L.EWORKSPACE
+    assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, wb, None) == L.EALIGN
