@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "3b05faede8e9c0e78c699edbfdf4fb43da62e73409bb17cef524debd3d1168d9",
-                  "bytes": 307992794}
+                  "sha256": "527b467b623a1fe6e1e27d7548f6c7c452ef2e288252b113ac5e7b2f1968732e",
+                  "bytes": 308770040}
 
 
 def log(msg):
