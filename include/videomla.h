@@ -104,12 +104,36 @@ typedef struct videomla_window {
  * otherwise, so the chunk overwrites the oldest non-sink frames; every other slot is left
  * untouched. With a sink, k_r receives the unrotated W_R^K x. Calling it again
  * before videomla_window_advance (the next denoising step) overwrites the same slots.
- * Requires d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0, d_c + d_rope <= 288.
+ * Requires d_model % 64 == 0, d_model <= 2048, d_c % 16 == 0, d_rope % 8 == 0,
+ * d_c + d_rope <= 288.
  */
 int videomla_cache_write(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                          const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
                          const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
                          int32_t* slots_out, void* stream);
+
+/*
+ * The same cache write with the layer's compression weights packed once, at model load, into
+ * the order the cache-write kernel consumes them (every token of every call reads the whole
+ * [W_down^KV; W_R^K] panel, Eq. 1 and Eq. 5; the packed order lets each GPU load fetch whole
+ * cache lines). The values are videomla_cache_write's, up to the order of the fp32 sums.
+ *
+ * videomla_write_weights_bytes -- size of the packed panel for these dims (0 if the dims are
+ *   invalid or not supported by the cache write).
+ * videomla_prepare_write_weights -- pack w_dkv [d_c][d_model] and w_kr [d_rope][d_model]
+ *   (bf16, as for videomla_cache_write) into w_packed, a caller-owned device buffer of at least
+ *   videomla_write_weights_bytes() bytes, 16-byte aligned. Enqueued on `stream`.
+ * videomla_cache_write_prepared -- videomla_cache_write with w_packed (as written by
+ *   videomla_prepare_write_weights for the same d_model, d_c and d_rope) in place of w_dkv and
+ *   w_kr. Same arguments, requirements and errors otherwise.
+ */
+size_t videomla_write_weights_bytes(const videomla_dims* dims);
+int videomla_prepare_write_weights(const videomla_dims* dims, const uint16_t* w_dkv,
+                                   const uint16_t* w_kr, uint16_t* w_packed, void* stream);
+int videomla_cache_write_prepared(const videomla_dims* dims, const videomla_window* win,
+                                  int32_t batch, const uint16_t* x, const uint16_t* w_packed,
+                                  const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
+                                  int32_t* slots_out, void* stream);
 
 /* Bytes of device workspace videomla_attend needs for this shape and batch. */
 size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch);

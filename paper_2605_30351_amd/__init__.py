@@ -13,6 +13,7 @@ from ._lib import (  # noqa: F401
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,
+    cache_write_prepared,
     dense_attend,
     dense_attend_workspace_bytes,
     dense_cache_bytes_per_token,
@@ -20,11 +21,13 @@ from ._lib import (  # noqa: F401
     layer_weights_bytes,
     make_dims,
     prepare_layer_weights,
+    prepare_write_weights,
     set_attend_workgroups,
     slot_of,
     timing_enable,
     timing_read,
     valid_tokens,
     window_advance,
+    write_weights_bytes,
 )
 from ._lib import LIB_PATH  # noqa: F401

@@ -22,7 +22,8 @@ _lib = ctypes.CDLL(LIB_PATH)
 OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
 
 EXPORTED = (
-    "videomla_cache_write", "videomla_attend_workspace_bytes", "videomla_attend",
+    "videomla_cache_write", "videomla_write_weights_bytes", "videomla_prepare_write_weights",
+    "videomla_cache_write_prepared", "videomla_attend_workspace_bytes", "videomla_attend",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
     "videomla_timing_enable", "videomla_timing_read",
@@ -55,6 +56,12 @@ _WP = ctypes.POINTER(VideomlaWindow)
 
 _lib.videomla_cache_write.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.videomla_cache_write.restype = ctypes.c_int
+_lib.videomla_write_weights_bytes.argtypes = [_DP]
+_lib.videomla_write_weights_bytes.restype = ctypes.c_size_t
+_lib.videomla_prepare_write_weights.argtypes = [_DP, _P, _P, _P, _P]
+_lib.videomla_prepare_write_weights.restype = ctypes.c_int
+_lib.videomla_cache_write_prepared.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P]
+_lib.videomla_cache_write_prepared.restype = ctypes.c_int
 _lib.videomla_attend_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
 _lib.videomla_attend_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
@@ -168,6 +175,46 @@ def cache_write(dims, frame_end: int, batch: int, x, w_dkv, w_kr, gamma, c_kv, k
         ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(x, "x"), _ptr(w_dkv, "w_dkv"),
         _ptr(w_kr, "w_kr"), _ptr(gamma, "gamma"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
         _ptr(slots, "slots", (torch.int32,)), _stream(stream)))
+
+
+def write_weights_bytes(dims) -> int:
+    return int(_lib.videomla_write_weights_bytes(ctypes.byref(make_dims(dims))))
+
+
+def prepare_write_weights(dims, w_dkv, w_kr, w_packed, stream=None):
+    """videomla_prepare_write_weights; `w_packed` is a bf16 or uint8 device tensor."""
+    d = make_dims(dims)
+    _need(w_dkv, "w_dkv", d.d_c * d.d_model)
+    _need(w_kr, "w_kr", d.d_rope * d.d_model)
+    nbytes = w_packed.numel() * w_packed.element_size()
+    if nbytes < write_weights_bytes(dims):
+        raise ValueError(f"w_packed holds {nbytes} bytes, needs {write_weights_bytes(dims)}")
+    _check(_lib.videomla_prepare_write_weights(
+        ctypes.byref(d), _ptr(w_dkv, "w_dkv"), _ptr(w_kr, "w_kr"),
+        _ptr(w_packed, "w_packed", (torch.bfloat16, torch.uint8)), _stream(stream)))
+
+
+def cache_write_prepared(dims, frame_end: int, batch: int, x, w_packed, gamma, c_kv, k_r,
+                         slots=None, stream=None):
+    """videomla_cache_write_prepared on torch tensors (bf16 data, int32 slots)."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    _need(x, "x", batch * d.chunk_frames * hw * d.d_model)
+    _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
+    _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
+    nbytes = w_packed.numel() * w_packed.element_size()
+    if nbytes < write_weights_bytes(dims):
+        raise ValueError(f"w_packed holds {nbytes} bytes, needs {write_weights_bytes(dims)}")
+    if gamma is not None:
+        _need(gamma, "gamma", d.d_c)
+    if slots is not None:
+        _need(slots, "slots", d.chunk_frames * hw)
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_cache_write_prepared(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(x, "x"),
+        _ptr(w_packed, "w_packed", (torch.bfloat16, torch.uint8)), _ptr(gamma, "gamma"),
+        _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"), _ptr(slots, "slots", (torch.int32,)),
+        _stream(stream)))
 
 
 def attend_workspace_bytes(dims, batch: int) -> int:

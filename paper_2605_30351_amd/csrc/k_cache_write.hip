@@ -2,18 +2,283 @@
 // (Eq. 5) rotated at the token's absolute (f, y, x) (kept unrotated when the cache has an
 // attention sink, Sec. "Decoupled 3D-RoPE"), and FIFO placement into the ring.
 //
-// One workgroup takes 32 chunk tokens of one batch element and all d_c + d_rope outputs:
-// out^T[o][token] = W[o][:] . x[token][:] with MFMA 32x32x16 (A = rows of [W_DKV; W_KR],
-// B = x rows). The contraction over d_model streams through a ring of kStages LDS stages of
-// kKC columns each, filled by direct global-to-LDS loads (no registers, several chunks in
-// flight) in an XOR-swizzled layout that makes the MFMA operand reads conflict-free. The four
-// waves share every staged chunk and split the 32-row output blocks between them. The epilogue
-// combines the RMSNorm sum of squares across waves in LDS, normalizes, rotates the RoPE block,
-// rounds to bf16 and stores each token's values to its ring slot.
+// The work is a skinny GEMM, out[token][o] = [W_DKV; W_KR][o][:] . x[token][:]: every token
+// needs the whole weight panel (d_c + d_rope rows of d_model), each token row is needed once.
+// Two kernels:
+//
+// cache_write_packed_kernel (weights packed once by pack_write_weights_kernel). A workgroup
+// takes a block of at most 32 consecutive tokens of the flat [batch][chunk] order, sized so
+// that the grid covers every CU once, and all outputs:
+//   * the block's x rows are loaded into LDS once, up front, by direct global-to-LDS loads
+//     (one memory latency, shared by all waves), in an XOR-swizzled layout that makes the
+//     MFMA operand reads conflict-free;
+//   * wave w owns outputs 32w .. 32w+31 and streams its slice of the packed panel from L2
+//     straight into registers, several MFMA k-steps ahead of use. The panel is stored in
+//     MFMA operand order, so each load reads 1 KB contiguous: full cache lines per
+//     instruction, which the L1 path delivers about three times faster than the 16- or
+//     32-row operand pattern read from the plain row-major weights;
+//   * MFMA 16x16x32: A = 16 weight rows x 32 columns, B = 32 columns x 16 tokens;
+//   * each workgroup starts its contraction at its own column offset, so that the
+//     workgroups of one L2 do not all ask for the same weight lines at the same time.
+//   The epilogue combines the RMSNorm sum of squares across waves in LDS, normalizes, rotates
+//   the RoPE block, rounds to bf16 into an LDS tile, and stores every token's c_kv and k_r
+//   rows whole (coalesced 16-byte stores) at its ring slot.
+//
+// cache_write_staged_kernel (plain row-major weights). One workgroup takes 32 chunk tokens and
+// all outputs: out^T[o][token] = W[o][:] . x[token][:] with MFMA 32x32x16 (A = rows of
+// [W_DKV; W_KR], B = x rows). The contraction over d_model streams through a ring of kStages
+// LDS stages of kKC columns each, filled by direct global-to-LDS loads in an XOR-swizzled
+// layout; the four waves share every staged chunk and split the 32-row output blocks between
+// them. Same epilogue steps, with 8-byte stores straight from the accumulators.
 #include "vmla_device.h"
 
 namespace vmla {
 namespace {
+
+constexpr int kTokTile = 32;   // token rows of the resident x tile: two 16-token MFMA blocks
+constexpr int kMaxWaves = 9;   // d_c + d_rope <= 288
+
+// D(16x16) += A(16x32) B(32x16). Lane l holds A[l%16][8(l/16) .. +8], B[8(l/16) .. +8][l%16];
+// accumulator element i of lane l is D[4(l/16) + i][l%16].
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// x tile layout: column blocks of 64 columns (8 chunks of 16 bytes); block b holds rows
+// 0 .. rows_pad-1 (rows_pad = the block's token count rounded up to 8) row-major, the chunk index
+// XOR-ed with (row / 2) mod 8, so 16 rows read at one chunk hit 16 distinct 16-byte bank groups.
+// A direct load fills 64 consecutive positions = 8 rows x 128 bytes of one block (whole lines).
+__device__ __forceinline__ int xpos(int b, int t, int cc, int rows_pad) {
+  return (b * rows_pad + t) * 8 + (cc ^ ((t >> 1) & 7));
+}
+
+// One wave per 32 outputs of d_c + d_rope. KPRE (weight k-steps of 32 columns in flight per
+// wave) divides d_model / 32, so the steady-state loop issues its loads unconditionally and
+// the compiler can count the outstanding loads exactly.
+template <int KPRE>
+__global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(const WriteArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t xs[kTokTile * kMaxWriteDModel];
+  __shared__ float ssq_part[kMaxWaves][kTokTile];
+  __shared__ int64_t tok_slot[kTokTile];
+  __shared__ f32x2 rope_cs[kTokTile][kMaxRopePairs];  // (cos, sin) of each token's pair angles
+
+  const int nwave = blockDim.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, q = lane >> 4;
+  const int dm = a.d_model, DC = a.d_c, DR = a.d_rope, NO = DC + DR;
+  const int n_tok = a.geo.chunk_tokens;
+  const int64_t M = (int64_t)a.batch * n_tok;    // tokens of the flat [batch][chunk] order
+  const int64_t g0 = (int64_t)blockIdx.x * a.tok_per_wg;
+  const int ntok = (int)(M - g0 < a.tok_per_wg ? M - g0 : a.tok_per_wg);  // >= 1 by the grid
+  const int rows_pad = (ntok + 7) & ~7;
+  const int ngrp = rows_pad / 8;                 // direct loads per column block
+
+  // RMSNorm gain of this lane's outputs 32 wave + 16 ob + 4q .. +3, fetched first
+  u32x2 gam[2] = {{0u, 0u}, {0u, 0u}};
+  if (a.gamma) {
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob) {
+      const int o = 32 * wave + 16 * ob + 4 * q;
+      if (o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
+    }
+  }
+
+  // ---- contraction order: k-step i of this workgroup is column k-step (i + rot) mod nks, rot
+  // a whole column block, so that the workgroups of one L2 start at different weight lines ----
+  const int nks = dm / 32, nblk = dm / 64;
+  const int rotb = (int)((blockIdx.x >> 3) % (unsigned)nblk);
+  const int rot = 2 * rotb;
+  auto kstep = [&](int i) { const int k = i + rot; return k < nks ? k : k - nks; };
+  // x arrives in two phases: k-steps [0, i_ph1) first, the rest during the first phase's work
+  const int i_ph1 = (nks / 2) / KPRE * KPRE;     // 0: a single phase
+  const int i_dma1 = i_ph1 > KPRE ? i_ph1 - KPRE : 0;
+
+  // direct loads of the column blocks ib_begin .. ib_end-1 (in contraction order), rows past
+  // the block's tokens repeating its last token (their results are never stored)
+  auto issue_x = [&](int ib_begin, int ib_end) {
+    const int n = (ib_end - ib_begin) * ngrp;
+    for (int j = wave; j < n; j += nwave) {
+      const int jb = j / ngrp, rg = j - jb * ngrp;
+      int b = rotb + ib_begin + jb;
+      if (b >= nblk) b -= nblk;
+      const int t = rg * 8 + (lane >> 3), cs = lane & 7;
+      const int cc = cs ^ ((t >> 1) & 7);
+      const int tt = t < ntok ? t : ntok - 1;
+      lds_dma16(a.x + (size_t)(g0 + tt) * dm + b * 64 + cc * 8,
+                __builtin_amdgcn_readfirstlane(lds_addr(xs + (b * rows_pad + rg * 8) * 64)));
+    }
+  };
+  issue_x(0, i_ph1 > 0 ? i_ph1 / 2 : nblk);
+
+  // ---- this wave's packed panel: k-step k holds its two A operands (outputs 32 wave + 16 ob
+  // + r, columns 32k + 8q ..) as 2 KB contiguous, lane-ordered ------------------------------
+  const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * 2) * 512 + lane * 8;
+  u32x4 wb[KPRE][2];
+#pragma unroll
+  for (int j = 0; j < KPRE; ++j) {
+    const int k = kstep(j);
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob) wb[j][ob] = ldg16(wpan + (2 * k + ob) * 512);
+  }
+  // while the first loads are in flight: each token's ring row (and slot), and the RoPE angles
+  // with the pair index uniform across a wave, so that the angle table is read by scalar loads
+  // (a per-lane index would turn them into vector loads that wait for every load in flight)
+  const int npair = DR / 2;
+  if (lane < ntok) {
+    const int g = (int)g0 + lane;  // batch * chunk_tokens < 2^31 (validated on the host)
+    const int b = g / n_tok, n = g - b * n_tok;
+    const TokenPos pos = token_pos(a.geo, n);
+    if (wave == 0) {
+      const int64_t slot = ring_slot(a.geo, pos);
+      tok_slot[lane] = (int64_t)b * a.geo.ring_tokens + slot;
+      if (b == 0 && a.slots) a.slots[n] = (int32_t)slot;
+    }
+    for (int pr = wave; pr < npair; pr += nwave) {
+      float u = 1.f, w = 0.f;  // rotating (1, 0) gives (cos, sin); identity with a sink
+      if (a.geo.sink_frames == 0) rope_rotate(a.rope, pr, pos, u, w);
+      rope_cs[lane][pr] = f32x2{u, w};
+    }
+  }
+  // loads complete in issue order: once at most the 2 KPRE weight loads issued after them are
+  // outstanding, this wave's first-phase x loads (and the gain) have landed
+  wait_vmcnt<2 * KPRE>();
+  __syncthreads();
+
+  f32x4 acc[2][2];  // [output block][token block]
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) acc[ob][tb] = f32x4{};
+
+  const int tmax = rows_pad - 1;
+  auto mma_step = [&](int i, const u32x4 (&w)[2]) {
+    const int k = kstep(i);
+    const int b = k >> 1, cc = 4 * (k & 1) + q;
+    bf16x8 xb[2];
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const int t = 16 * tb + r < tmax ? 16 * tb + r : tmax;
+      xb[tb] = as_bf16x8(*reinterpret_cast<const u32x4*>(&xs[xpos(b, t, cc, rows_pad) * 8]));
+    }
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+      for (int tb = 0; tb < 2; ++tb) acc[ob][tb] = mfma16(as_bf16x8(w[ob]), xb[tb], acc[ob][tb]);
+  };
+  auto steady = [&](int i0) {  // k-steps i0 .. i0+KPRE-1, refilling the ring KPRE ahead
+#pragma unroll
+    for (int j = 0; j < KPRE; ++j) {
+      mma_step(i0 + j, wb[j]);
+      const int kn = kstep(i0 + j + KPRE);
+#pragma unroll
+      for (int ob = 0; ob < 2; ++ob) wb[j][ob] = ldg16(wpan + (2 * kn + ob) * 512);
+    }
+  };
+  // the second phase's loads are issued KPRE k-steps before its first use, after the weight
+  // loads of the k-steps that precede it (so that those do not wait for them); at k-step
+  // i_ph1 the 2 KPRE weight loads issued since are the only ones that may still be pending
+  int i0 = 0;
+  for (; i0 < i_dma1; i0 += KPRE) steady(i0);
+  if (i_ph1 > 0) {
+    issue_x(i_ph1 / 2, nblk);
+    for (; i0 < i_ph1; i0 += KPRE) steady(i0);
+    wait_vmcnt<2 * KPRE>();
+    __syncthreads();
+  }
+  for (; i0 < nks - KPRE; i0 += KPRE) steady(i0);
+#pragma unroll
+  for (int j = 0; j < KPRE; ++j) mma_step(i0 + j, wb[j]);
+
+  // ---- epilogue. Lane (r, q) holds, for token 16 tb + r of the block, outputs
+  // 32 wave + 16 ob + 4q + e (e = 0..3) in acc[ob][tb][e] ----------------------------------
+  float ss[2] = {0.f, 0.f};
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int o = 32 * wave + 16 * ob + 4 * q + e;
+        if (o < DC) ss[tb] += acc[ob][tb][e] * acc[ob][tb][e];
+      }
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    ss[tb] += __shfl_xor(ss[tb], 16);
+    ss[tb] += __shfl_xor(ss[tb], 32);
+    if (q == 0) ssq_part[wave][16 * tb + r] = ss[tb];
+  }
+  __syncthreads();  // every wave is past its last x read: the tile area is reused below
+
+  // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
+  const int ots = NO + 8;  // row stride (elements): 16 bytes of padding per row
+  uint16_t* ot = xs;
+#pragma unroll
+  for (int tb = 0; tb < 2; ++tb) {
+    const int t = 16 * tb + r;
+    const int tc = t < ntok ? t : ntok - 1;
+    float tot = 0.f;
+    for (int w = 0; w < nwave; ++w) tot += ssq_part[w][t];
+    const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob) {
+      const int o = 32 * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
+      f32x4 v = acc[ob][tb];
+      if (o + 4 <= DC) {
+        v = v * rstd;
+        if (a.gamma) {
+          v[0] *= __uint_as_float(gam[ob][0] << 16);
+          v[1] *= __uint_as_float(gam[ob][0] & 0xffff0000u);
+          v[2] *= __uint_as_float(gam[ob][1] << 16);
+          v[3] *= __uint_as_float(gam[ob][1] & 0xffff0000u);
+        }
+      } else if (o < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
+        const f32x2 c0 = rope_cs[tc][(o - DC) / 2], c1 = rope_cs[tc][(o - DC) / 2 + 1];
+        v = f32x4{v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
+                  v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
+      } else {
+        continue;  // padding outputs past d_c + d_rope
+      }
+      *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(v);
+    }
+  }
+  __syncthreads();
+
+  // ---- stores: token t's row of NO/8 chunks (c_kv, then k_r) to its ring slot, coalesced ---
+  const int cpt = NO / 8;
+  for (int i = threadIdx.x; i < ntok * cpt; i += nwave * 64) {
+    const int t = i / cpt, ch = i - t * cpt;
+    const int64_t row = tok_slot[t];
+    const u32x4 val = *reinterpret_cast<const u32x4*>(&ot[t * ots + ch * 8]);
+    const int o = ch * 8;
+    if (o < DC) stg16(a.c_kv + (size_t)row * DC + o, val);
+    else stg16(a.k_r + (size_t)row * DR + (o - DC), val);
+  }
+}
+
+// Packed weight panel for cache_write_packed_kernel: W' = [W_DKV; W_KR; zero rows up to a whole
+// number of 32-row wave slices]. Entry ((w * nks + k) * 2 + ob) * 512 + 8 l + j holds
+// W'[32 w + 16 ob + l % 16][32 k + 8 (l / 16) + j]: the MFMA 16x16x32 A operand of lane l for
+// wave slice w, 16-row block ob and k-step k, so that every load of the kernel reads 1 KB
+// contiguous. One thread per 16-byte entry.
+__global__ __launch_bounds__(256) void pack_write_weights_kernel(const WriteArgs a) {
+  const int dm = a.d_model, DC = a.d_c, NO = a.d_c + a.d_rope;
+  const int nks = dm / 32;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;  // 16-byte entry
+  const int64_t n_entries = (int64_t)((NO + 31) / 32) * nks * 2 * 64;
+  if (e >= n_entries) return;
+  const int l = (int)(e & 63);
+  const int64_t blk = e >> 6;  // (w * nks + k) * 2 + ob
+  const int ob = (int)(blk & 1);
+  const int64_t wk = blk >> 1;
+  const int k = (int)(wk % nks), w = (int)(wk / nks);
+  const int o = 32 * w + 16 * ob + (l & 15);
+  const int col = 32 * k + 8 * (l >> 4);
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (o < DC) v = ldg16(a.w_dkv + (size_t)o * dm + col);
+  else if (o < NO) v = ldg16(a.w_kr + (size_t)(o - DC) * dm + col);
+  stg16(a.w_packed_out + e * 8, v);
+}
 
 constexpr int kTok = 32;     // tokens per workgroup
 constexpr int kWaves = 4;
@@ -24,7 +289,7 @@ constexpr int kKC = 64;      // contraction columns per stage: 8 chunks of 16 B 
 __device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
 
 template <int NB>  // 32-wide output blocks covering d_c + d_rope
-__global__ __launch_bounds__(kWaves * 64) void cache_write_kernel(const WriteArgs a) {
+__global__ __launch_bounds__(kWaves * 64) void cache_write_staged_kernel(const WriteArgs a) {
   constexpr int ROWS = NB * 32 + kTok;        // staged rows: weight rows, then x rows
   constexpr int INSTR = ROWS * 8 / 64;        // 1 KB load instructions per stage
   constexpr int PER_WAVE = (INSTR + kWaves - 1) / kWaves;
@@ -161,24 +426,59 @@ __global__ __launch_bounds__(kWaves * 64) void cache_write_kernel(const WriteArg
 
 }  // namespace
 
-hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s) {
+static hipError_t launch_cache_write_staged(const WriteArgs& a, hipStream_t s) {
   // validated by the caller: d_model % 64 == 0, d_c % 16 == 0, d_rope % 8 == 0,
   // d_c + d_rope <= 288
   const int nb = (a.d_c + a.d_rope + 31) / 32;
   const dim3 grid((a.geo.chunk_tokens + kTok - 1) / kTok, a.batch);
   const dim3 block(kWaves * 64);
   switch (nb) {
-    case 1: hipLaunchKernelGGL(cache_write_kernel<1>, grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL(cache_write_kernel<2>, grid, block, 0, s, a); break;
-    case 3: hipLaunchKernelGGL(cache_write_kernel<3>, grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL(cache_write_kernel<4>, grid, block, 0, s, a); break;
-    case 5: hipLaunchKernelGGL(cache_write_kernel<5>, grid, block, 0, s, a); break;
-    case 6: hipLaunchKernelGGL(cache_write_kernel<6>, grid, block, 0, s, a); break;
-    case 7: hipLaunchKernelGGL(cache_write_kernel<7>, grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL(cache_write_kernel<8>, grid, block, 0, s, a); break;
-    case 9: hipLaunchKernelGGL(cache_write_kernel<9>, grid, block, 0, s, a); break;
+    case 1: hipLaunchKernelGGL(cache_write_staged_kernel<1>, grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL(cache_write_staged_kernel<2>, grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL(cache_write_staged_kernel<3>, grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL(cache_write_staged_kernel<4>, grid, block, 0, s, a); break;
+    case 5: hipLaunchKernelGGL(cache_write_staged_kernel<5>, grid, block, 0, s, a); break;
+    case 6: hipLaunchKernelGGL(cache_write_staged_kernel<6>, grid, block, 0, s, a); break;
+    case 7: hipLaunchKernelGGL(cache_write_staged_kernel<7>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(cache_write_staged_kernel<8>, grid, block, 0, s, a); break;
+    case 9: hipLaunchKernelGGL(cache_write_staged_kernel<9>, grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+int cache_write_tokens_per_wg(int64_t tokens, int n_cu) {
+  // one workgroup per CU while that keeps blocks within the 32-row tile, else full tiles
+  const int64_t per = (tokens + n_cu - 1) / n_cu;
+  return (int)(per < 1 ? 1 : (per > kTokTile ? kTokTile : per));
+}
+
+size_t write_weights_packed_elems(int d_model, int d_c, int d_rope) {
+  return (size_t)((d_c + d_rope + 31) / 32) * (d_model / 32) * 2 * 512;
+}
+
+hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s) {
+  const int64_t entries = (int64_t)write_weights_packed_elems(a.d_model, a.d_c, a.d_rope) / 8;
+  hipLaunchKernelGGL(pack_write_weights_kernel, dim3((unsigned)((entries + 255) / 256)), dim3(256),
+                     0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s) {
+  if (!a.w_packed) return launch_cache_write_staged(a, s);
+  // validated by the caller: d_model % 64 == 0, d_model <= kMaxWriteDModel, d_c % 16 == 0,
+  // d_rope % 8 == 0, d_c + d_rope <= 288, 1 <= tok_per_wg <= 32
+  const int nw = (a.d_c + a.d_rope + 31) / 32;
+  const int nks = a.d_model / 32;  // even
+  const int64_t M = (int64_t)a.batch * a.geo.chunk_tokens;
+  const dim3 grid((unsigned)((M + a.tok_per_wg - 1) / a.tok_per_wg)), block(nw * 64);
+  if (nw > kMaxWaves) return hipErrorInvalidValue;
+  if (nks % 12 == 0)
+    hipLaunchKernelGGL(cache_write_packed_kernel<12>, grid, block, 0, s, a);
+  else if (nks % 8 == 0)
+    hipLaunchKernelGGL(cache_write_packed_kernel<8>, grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL(cache_write_packed_kernel<2>, grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -110,13 +110,14 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
 enum KernelId {
   K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
   K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW,
-  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_COUNT
+  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_PREPARE_WRITE, K_COUNT
 };
 const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
                                      "out_proj",          "dense_cache_write", "dense_q_prep",
                                      "dense_attend",      "dense_merge",  "rope_window",
                                      "q_down",            "q_up",         "latent_merge",
-                                     "out_mix",           "prepare_layer_weights"};
+                                     "out_mix",           "prepare_layer_weights",
+                                     "prepare_write_weights"};
 
 struct TimingRec {
   int kernel;
@@ -353,32 +354,89 @@ int videomla_set_attend_workgroups(int32_t n) {
   return ok();
 }
 
-int videomla_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                         const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
-                         const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
-                         int32_t* slots_out, void* stream) {
+namespace {
+
+// Shapes the cache-write kernels tile (shared by the plain and the packed-weight entry points).
+int check_write_dims(const videomla_dims* d) {
   if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
-  if (!x || !w_dkv || !w_kr || !c_kv || !k_r) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
   if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
+  if (d->d_model > kMaxWriteDModel)
+    return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be <= %d for the cache write, got %d", kMaxWriteDModel, d->d_model);
   if (d->d_c % 16) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 16, got %d", d->d_c);
   if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
   if (d->d_c + d->d_rope > 288) return fail(VIDEOMLA_EUNSUPPORTED, "d_c + d_rope must be <= 288");
-  if (!aligned16(x) || !aligned16(w_dkv) || !aligned16(w_kr) || !aligned16(c_kv) || !aligned16(k_r))
+  return 0;
+}
+
+// Validation and launch common to videomla_cache_write (w_packed == NULL) and
+// videomla_cache_write_prepared (w_dkv == w_kr == NULL).
+int cache_write_common(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                       const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
+                       const uint16_t* w_packed, const uint16_t* kv_norm_w, uint16_t* c_kv,
+                       uint16_t* k_r, int32_t* slots_out, void* stream) {
+  if (int e = check_write_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if ((int64_t)batch * d->chunk_frames * d->grid_h * d->grid_w >= ((int64_t)1 << 31))
+    return fail(VIDEOMLA_EUNSUPPORTED, "batch * chunk tokens must be < 2^31");
+  if (!x || !c_kv || !k_r || (!w_packed && (!w_dkv || !w_kr)))
+    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (!aligned16(x) || !aligned16(c_kv) || !aligned16(k_r) ||
+      (w_packed ? !aligned16(w_packed) : (!aligned16(w_dkv) || !aligned16(w_kr))))
     return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
   if (kv_norm_w && !aligned16(kv_norm_w)) return fail(VIDEOMLA_EALIGN, "kv_norm_w must be 16-byte aligned");
   WriteArgs a{};
-  a.x = x; a.w_dkv = w_dkv; a.w_kr = w_kr; a.gamma = kv_norm_w;
+  a.x = x; a.w_dkv = w_dkv; a.w_kr = w_kr; a.w_packed = w_packed; a.gamma = kv_norm_w;
   a.c_kv = c_kv; a.k_r = k_r; a.slots = slots_out;
   a.batch = batch; a.d_model = d->d_model; a.d_c = d->d_c; a.d_rope = d->d_rope;
   a.eps = d->kv_norm_eps;
   a.geo = make_geo(d, w);
   a.rope = make_rope(d);
+  a.tok_per_wg = cache_write_tokens_per_wg((int64_t)batch * a.geo.chunk_tokens, device_cu_count());
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const hipError_t e = timed(K_CACHE_WRITE, s, [&] { return launch_cache_write(a, s); });
   if (e != hipSuccess) return hip_fail(e, "cache_write");
   return ok();
+}
+
+}  // namespace
+
+int videomla_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                         const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
+                         const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
+                         int32_t* slots_out, void* stream) {
+  if (!w_dkv || !w_kr) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  return cache_write_common(d, w, batch, x, w_dkv, w_kr, nullptr, kv_norm_w, c_kv, k_r, slots_out,
+                            stream);
+}
+
+size_t videomla_write_weights_bytes(const videomla_dims* d) {
+  if (check_write_dims(d)) return 0;
+  return write_weights_packed_elems(d->d_model, d->d_c, d->d_rope) * 2;
+}
+
+int videomla_prepare_write_weights(const videomla_dims* d, const uint16_t* w_dkv,
+                                   const uint16_t* w_kr, uint16_t* w_packed, void* stream) {
+  if (int e = check_write_dims(d)) return e;
+  if (!w_dkv || !w_kr || !w_packed) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (!aligned16(w_dkv) || !aligned16(w_kr) || !aligned16(w_packed))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  WriteArgs a{};
+  a.w_dkv = w_dkv; a.w_kr = w_kr; a.w_packed_out = w_packed;
+  a.d_model = d->d_model; a.d_c = d->d_c; a.d_rope = d->d_rope;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = timed(K_PREPARE_WRITE, s, [&] { return launch_pack_write_weights(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "prepare_write_weights");
+  return ok();
+}
+
+int videomla_cache_write_prepared(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                                  const uint16_t* x, const uint16_t* w_packed,
+                                  const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
+                                  int32_t* slots_out, void* stream) {
+  if (!w_packed) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  return cache_write_common(d, w, batch, x, nullptr, nullptr, w_packed, kv_norm_w, c_kv, k_r,
+                            slots_out, stream);
 }
 
 size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {

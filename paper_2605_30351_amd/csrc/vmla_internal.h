@@ -7,6 +7,7 @@
 namespace vmla {
 
 constexpr int kMaxRopePairs = 64;  // a whole dense head of 128 channels
+constexpr int kMaxWriteDModel = 2048;  // cache write: 32 resident x rows of d_model fill 128 KB of LDS
 
 // Per RoPE pair p (interleaved channels 2p, 2p+1 of the d_rope vector): the axis whose
 // coordinate drives it (0 = t, 1 = h, 2 = w) and theta = base^(-2k / D_axis), in double.
@@ -37,7 +38,10 @@ struct WriteArgs {
   uint16_t* c_kv;         // [B][ring_tokens][d_c]
   uint16_t* k_r;          // [B][ring_tokens][d_rope]
   int32_t* slots;         // [chunk_tokens] or nullptr
+  const uint16_t* w_packed;  // packed [W_DKV; W_KR] panel (cache_write_packed_kernel), or nullptr
+  uint16_t* w_packed_out;    // pack_write_weights_kernel output
   int32_t batch, d_model, d_c, d_rope;
+  int32_t tok_per_wg;     // tokens of the flat [B][chunk] order per workgroup (1 .. 32)
   float eps;
   Geometry geo;
   RopeTable rope;
@@ -117,6 +121,9 @@ __host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_w
 
 // Launchers (one per kernel). Return the launch status.
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);
+int cache_write_tokens_per_wg(int64_t tokens, int n_cu);
+hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s);
+size_t write_weights_packed_elems(int d_model, int d_c, int d_rope);
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
 hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s);
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);

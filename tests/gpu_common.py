@@ -33,7 +33,8 @@ def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
 class Layer:
     """Device copies of one layer's inputs plus its ring."""
 
-    def __init__(self, vm, inp, sentinel=True):
+    def __init__(self, vm, inp, sentinel=True, packed=False):
+        """packed: write through videomla_cache_write_prepared with the packed weight panel."""
         self.vm, self.inp, d = vm, inp, inp.dims
         self.x = dev(inp.x)
         self.w_dkv, self.w_kr = dev(inp.w_dkv), dev(inp.w_kr)
@@ -49,12 +50,20 @@ class Layer:
         self.slots = torch.full((d.chunk_tokens,), -1, dtype=torch.int32, device="cuda")
         self.out = torch.zeros((B, d.chunk_tokens, d.n_heads, d.d_v), dtype=torch.bfloat16,
                                device="cuda")
+        self.w_packed = None
+        if packed:
+            self.w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device="cuda")
+            vm.prepare_write_weights(d, self.w_dkv, self.w_kr, self.w_packed)
 
     def write(self, fe):
         d = self.inp.dims
         xs = self.x[:, fe * d.hw:(fe + d.chunk_frames) * d.hw].contiguous()
-        self.vm.cache_write(d, fe, self.inp.batch, xs, self.w_dkv, self.w_kr, self.gamma,
-                            self.c_kv, self.k_r, self.slots)
+        if self.w_packed is not None:
+            self.vm.cache_write_prepared(d, fe, self.inp.batch, xs, self.w_packed, self.gamma,
+                                         self.c_kv, self.k_r, self.slots)
+        else:
+            self.vm.cache_write(d, fe, self.inp.batch, xs, self.w_dkv, self.w_kr, self.gamma,
+                                self.c_kv, self.k_r, self.slots)
 
     def attend(self, fe):
         d = self.inp.dims

@@ -110,6 +110,31 @@ def test_cache_write_rejects_bad_args():
     assert _write(d) == L.EINVAL
 
 
+def _write_prepared(d, fe=0, batch=1, x=FAKE, wp=FAKE):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_cache_write_prepared(ctypes.byref(d), ctypes.byref(w), batch, x, wp,
+                                                 None, FAKE, FAKE, None, None)
+
+
+def test_packed_write_weights_size_and_validation():
+    # one 2 KB block per (32-row wave slice, 32-column k-step): 7 x 48 x 2048 for Wan
+    assert vm.write_weights_bytes(WAN) == 7 * 48 * 2048
+    assert vm.write_weights_bytes(TINY) == 1 * 2 * 2048
+    assert L.raw().videomla_write_weights_bytes(ctypes.byref(_dims_struct(WAN, d_model=4096))) == 0
+    d = L.make_dims(WAN)
+    prep = L.raw().videomla_prepare_write_weights
+    assert prep(ctypes.byref(d), FAKE, FAKE, None, None) == L.EINVAL
+    assert prep(ctypes.byref(d), FAKE, MISALIGNED, FAKE, None) == L.EALIGN
+    assert prep(ctypes.byref(_dims_struct(WAN, d_c=100)), FAKE, FAKE, FAKE, None) == L.EUNSUPPORTED
+    assert _write_prepared(d, wp=None) == L.EINVAL
+    assert _write_prepared(d, wp=MISALIGNED) == L.EALIGN
+    assert _write_prepared(d, x=None) == L.EINVAL
+    assert _write_prepared(d, batch=0) == L.EINVAL
+    assert _write_prepared(d, fe=-1) == L.EINVAL
+    assert _write_prepared(_dims_struct(WAN, d_model=4096)) == L.EUNSUPPORTED
+    assert _write(_dims_struct(WAN, d_model=4096)) == L.EUNSUPPORTED
+
+
 def test_attend_rejects_bad_args():
     d = L.make_dims(WAN)
     assert _attend(d, q=None) == L.EINVAL

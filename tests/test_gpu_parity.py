@@ -46,10 +46,11 @@ from workloads import TINY, WAN, WAN_PAPER, make_layer_inputs  # noqa: E402
 # Tiny configuration: every write, partial and wrapped windows, batch 2, work partitions
 # -------------------------------------------------------------------------------------------
 
+@pytest.mark.parametrize("packed", [False, True], ids=["plain_weights", "packed_weights"])
 @pytest.mark.parametrize("norm", [True, False])
-def test_tiny_rollout_write_and_attend(vm, norm):
+def test_tiny_rollout_write_and_attend(vm, norm, packed):
     inp = make_layer_inputs(TINY, seed=0, n_frames=6, batch=2, norm=norm)
-    layer = Layer(vm, inp)
+    layer = Layer(vm, inp, packed=packed)
     exact = total = 0
     for fe in range(6):
         before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
@@ -84,11 +85,12 @@ def _roll(layer, upto_fe):
         layer.write(fe)
 
 
-def test_wan_cache_write_evicts_oldest_frames(vm):
+@pytest.mark.parametrize("packed", [False, True], ids=["plain_weights", "packed_weights"])
+def test_wan_cache_write_evicts_oldest_frames(vm, packed):
     """The 21-frame ring holds frames 0..20; writing frames 21..23 replaces frame slots 0..2
     and leaves the other 18 frames bitwise untouched."""
     inp = make_layer_inputs(WAN, seed=2, n_frames=24)
-    layer = Layer(vm, inp)
+    layer = Layer(vm, inp, packed=packed)
     _roll(layer, 18)
     before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
     layer.write(21)
@@ -97,6 +99,39 @@ def test_wan_cache_write_evicts_oldest_frames(vm):
     print(f"wan cache write exactly rounded fraction {exact:.6f}")
     assert exact >= 0.999
     assert np.array_equal(layer.slots.cpu().numpy()[[0, 4679]], [0, 3 * 1560 - 1])
+
+
+def test_packed_weight_panel_layout(vm):
+    """Every 16-byte entry of the packed panel is the documented slice of [W_DKV; W_KR; 0]:
+    entry ((w * nks + k) * 2 + ob) * 64 + l holds row 32 w + 16 ob + l % 16, columns
+    32 k + 8 (l / 16) .. +8 (bitwise, for both the tiny and the Wan shapes)."""
+    for dims in (TINY, WAN):
+        inp = make_layer_inputs(dims, seed=3, n_frames=dims.chunk_frames)
+        layer = Layer(vm, inp, packed=True)
+        torch.cuda.synchronize()
+        got = host_bits(layer.w_packed.view(torch.bfloat16)).reshape(-1, 8)
+        nks, no = dims.d_model // 32, dims.d_c + dims.d_rope
+        nw = (no + 31) // 32
+        panel = np.zeros((32 * nw, dims.d_model), np.uint16)
+        panel[:dims.d_c], panel[dims.d_c:no] = inp.w_dkv, inp.w_kr
+        e = np.arange(nw * nks * 2 * 64)
+        lane, blk = e % 64, e // 64
+        ob, k, w = blk % 2, (blk // 2) % nks, blk // 2 // nks
+        rows = 32 * w + 16 * ob + lane % 16
+        cols = 32 * k + 8 * (lane // 16)
+        want = panel[rows[:, None], cols[:, None] + np.arange(8)]
+        assert np.array_equal(got, want)
+
+
+def test_wan_batch4_packed_write_matches_oracle(vm):
+    """Batch 4 (18,720 tokens: full 32-token workgroups, blocks spanning batch elements)."""
+    inp = make_layer_inputs(WAN, seed=8, n_frames=3, batch=4)
+    layer = Layer(vm, inp, packed=True)
+    before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
+    layer.write(0)
+    stats = check_written_chunk(layer, 0, before_c, before_k)
+    exact = sum(e for e, _ in stats) / sum(n for _, n in stats)
+    assert exact >= 0.999
 
 
 @pytest.mark.parametrize("variant", ["wan", "peaked", "paper_dims"])
