@@ -524,6 +524,102 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
     }), flush=True)
 
 
+def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8):
+    """Per-kernel HIP-event averages of `steps` chunk-steps (packed cache write + attend) of
+    one layer with dims d at the wrapped full window (chunk at frame window_frames), batch
+    `batch`. Seeded synthetic bf16 drawn on the GPU; x cycles through `x_buffers` buffers."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq, B = d.chunk_tokens, batch
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    w_uk = normal((d.n_heads * d.d_nope, d.d_c), d.d_c ** -0.5)
+    w_uv = normal((d.n_heads * d.d_v, d.d_c), d.d_c ** -0.5)
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    q_nope, q_r = normal((B, nq, d.n_heads, d.d_nope)), normal((B, nq, d.n_heads, d.d_rope))
+    c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+    k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((B, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
+    w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
+    vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
+    for f in range(0, d.window_frames, d.chunk_frames):
+        vm.cache_write_prepared(d, f, B, normal((B, nq, d.d_model)), w_packed, gamma, c_kv, k_r)
+    fe = d.window_frames
+    xs = [normal((B, nq, d.d_model)) for _ in range(x_buffers)]
+    torch.cuda.synchronize()
+
+    def step(i):
+        vm.cache_write_prepared(d, fe, B, xs[i % len(xs)], w_packed, gamma, c_kv, k_r)
+        vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
+    vm.timing_enable(True)
+    for k in names:
+        vm.timing_read(k)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for i in range(steps):
+        step(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    kernels = {}
+    for k in names:
+        n, tot = vm.timing_read(k)
+        kernels[k] = round(1e3 * tot / max(n, 1), 3)
+    vm.timing_enable(False)
+    return ev0.elapsed_time(ev1) / steps, kernels
+
+
+def dc_sweep(args, vm, torch, d0):
+    """The paper's latent-width sweep (Table 5) at Wan geometry: one chunk-step (packed cache
+    write + attend of 4,680 x 12 query rows over the 32,760-key window) per d_c, batch 1, and
+    the few-query regime (1-frame chunks: 1,560 x 12 rows) at d_c = 192."""
+    from workloads import DC_SWEEP, WAN_1F
+    rows = []
+    for dc in DC_SWEEP:
+        d = d0.replace(d_c=dc)
+        entry = {"d_c": dc, "cache_bytes_per_token": 2 * (dc + d.d_rope),
+                 "vs_dense_cache": round(2 * d.n_heads * d.d_v / (dc + d.d_rope), 2)}
+        if vm.attend_workspace_bytes(d, 1) == 0:
+            entry["status"] = ("not built: 32 query rows x 512 fp32 latent accumulators per "
+                               "wave exceed the register file")
+            rows.append(entry)
+            continue
+        log(f"d_c {dc}")
+        ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=50)
+        W = work_model(d)
+        entry.update({"ms_per_step": round(ms, 4), "kernels_us": k,
+                      "latent_attend_tflops": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12, 1),
+                      "latent_attend_mfma_frac": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                      "cache_write_hbm_frac": round(W["write_bytes"] / (k["cache_write"] / 1e6) / 1e9 / HBM_PEAK_GBPS, 4)})
+        rows.append(entry)
+    log("1-frame chunks")
+    d = WAN_1F
+    ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=51)
+    W = work_model(d)
+    few = {"chunk_tokens": d.chunk_tokens, "ms_per_step": round(ms, 4), "kernels_us": k,
+           "latent_attend_tflops": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12, 1),
+           "latent_attend_mfma_frac": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)}
+    print(json.dumps({
+        "metric": "latent attend TFLOP/s and % MFMA peak per latent width d_c (Table 5 sweep)",
+        "value": next(r["latent_attend_tflops"] for r in rows if r["d_c"] == d0.d_c),
+        "unit": "TFLOP/s", "n_gpus": 1, "higher_is_better": True, "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic", "sweep": rows, "one_frame_chunks": few,
+        "config": {"workload": ("Wan2.1-1.3B layer chunk-step (3-frame chunk, 21-frame window, "
+                                "batch 1) at d_c in {64, 128, 192, 256, 512}, d_rope 32; plus "
+                                "1-frame chunks at d_c 192")},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -535,14 +631,16 @@ def main():
                     help="also run a 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="wan-layer-chunk-step",
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
-                             "wan-sink-chunk-step", "wan-full-layer-chunk-step"),
+                             "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
                          "chunks through 30 layers, latent path and dense comparator; "
                          "wan-sink-chunk-step: one chunk-step with a sink frame + 6 recent "
                          "frames late in a rollout; wan-full-layer-chunk-step: the whole "
-                         "attention layer in latent form (query path and W_O absorbed)")
+                         "attention layer in latent form (query path and W_O absorbed); "
+                         "wan-dc-sweep: chunk-steps at the latent widths of the paper's d_c "
+                         "sweep and with 1-frame chunks")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -564,6 +662,9 @@ def main():
         return
     if args.workload == "wan-full-layer-chunk-step":
         full_layer_chunk_step(args, vm, torch, WAN)
+        return
+    if args.workload == "wan-dc-sweep":
+        dc_sweep(args, vm, torch, WAN)
         return
     if args.workload == "wan-sink-chunk-step":
         from workloads import WAN_SINK

@@ -28,12 +28,19 @@ constexpr float kNegInf = -__builtin_huge_valf();
 // ---------------------------------------------------------------------------------------------
 constexpr int kMaxNope = 128;
 
+template <int DC> struct AbsorbChunk {  // W_UK_h columns staged in LDS per pass
+  static constexpr int DCP = (DC + 31) / 32 * 32;
+  static constexpr int CW = DCP <= 192 ? DCP : 128;
+  static_assert(DCP % CW == 0, "whole column chunks");
+};
+
 template <int DC, int DR>
 __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
-  constexpr int DCP = (DC + 31) / 32 * 32;
-  constexpr int WS = DCP + 8;  // LDS row stride (elements)
+  constexpr int DCP = AbsorbChunk<DC>::DCP;
+  constexpr int CW = AbsorbChunk<DC>::CW;  // columns per pass (LDS holds d_nope x CW)
+  constexpr int WS = CW + 8;               // LDS row stride (elements)
   constexpr int DQKP = (DC + DR + 15) / 16 * 16;
-  constexpr int NCB = DCP / 32;
+  constexpr int NCB = CW / 32;
   constexpr int KN = kMaxNope / 16;
   extern __shared__ __attribute__((aligned(16))) uint16_t wuk[];  // [d_nope][WS]
 
@@ -57,42 +64,46 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   for (int ks = 0; ks < KN; ++ks) bq[ks] = as_bf16x8(ok && ks < nks ? ldg16(qn + ks * 16 + 8 * g) : zero);
 
   const uint16_t* wsrc = a.w_uk + (size_t)h * dn * DC;
-  for (int c = tid; c < dn * (DC / 8); c += 256) {
-    const int r = c / (DC / 8), oc = c % (DC / 8);
-    *reinterpret_cast<u32x4*>(&wuk[r * WS + oc * 8]) = ldg16(wsrc + (size_t)r * DC + oc * 8);
-  }
-  __syncthreads();
-
   // tr-read addressing inside a 16-lane group
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  f32x16 acc[NCB];
-#pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x16{};
-#pragma unroll
-  for (int ks = 0; ks < KN; ++ks) {
-    if (ks < nks) {
-      const int k0 = ks * 16 + 8 * g;
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        const i16x4 lo = lds_read_tr(&wuk[(k0 + tr_row) * WS + cb * 32 + tr_col]);
-        const i16x4 hi = lds_read_tr(&wuk[(k0 + 4 + tr_row) * WS + cb * 32 + tr_col]);
-        acc[cb] = mfma32(join_bf16x8(lo, hi), bq[ks], acc[cb]);
-      }
+  for (int c0 = 0; c0 < DCP; c0 += CW) {
+    const int cw = DC - c0 < CW ? DC - c0 : CW;  // real columns of this pass
+    if (c0 > 0) __syncthreads();                 // the previous pass's reads are done
+    for (int c = tid; c < dn * (cw / 8); c += 256) {
+      const int r = c / (cw / 8), oc = c % (cw / 8);
+      *reinterpret_cast<u32x4*>(&wuk[r * WS + oc * 8]) = ldg16(wsrc + (size_t)r * DC + c0 + oc * 8);
     }
-  }
-  if (ok) {
+    __syncthreads();
+
+    f32x16 acc[NCB];
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x16{};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = cb * 32 + 8 * i + 4 * g;
-        if (c < DC) {
-          const f32x4 v = {acc[cb][4 * i] * a.qscale, acc[cb][4 * i + 1] * a.qscale,
-                           acc[cb][4 * i + 2] * a.qscale, acc[cb][4 * i + 3] * a.qscale};
-          *reinterpret_cast<bf16x4*>(dst + c) = to_bf16x4(v);
+    for (int ks = 0; ks < KN; ++ks) {
+      if (ks < nks) {
+        const int k0 = ks * 16 + 8 * g;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const i16x4 lo = lds_read_tr(&wuk[(k0 + tr_row) * WS + cb * 32 + tr_col]);
+          const i16x4 hi = lds_read_tr(&wuk[(k0 + 4 + tr_row) * WS + cb * 32 + tr_col]);
+          acc[cb] = mfma32(join_bf16x8(lo, hi), bq[ks], acc[cb]);
         }
       }
+    }
+    if (ok) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int c = c0 + cb * 32 + 8 * i + 4 * g;
+          if (c < DC) {
+            const f32x4 v = {acc[cb][4 * i] * a.qscale, acc[cb][4 * i + 1] * a.qscale,
+                             acc[cb][4 * i + 2] * a.qscale, acc[cb][4 * i + 3] * a.qscale};
+            *reinterpret_cast<bf16x4*>(dst + c) = to_bf16x4(v);
+          }
+        }
+    }
   }
 
   // RoPE part and zero padding: 32 tokens x (DR/2) pairs per wave.
@@ -689,6 +700,14 @@ template <int DC, int DR> struct AttShape;
 // per CU measured 6% slower than one 8-wave workgroup at the Wan shape.
 template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
 template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1; };
+// the latent widths of the paper's d_c sweep (Table 5), with the same 32-wide RoPE key
+template <> struct AttShape<64, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
+template <> struct AttShape<128, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
+// d_c = 256: 32 rows x 256 fp32 accumulators per wave need one wave per SIMD (8 waves spill)
+template <> struct AttShape<256, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1; };
+
+// Every (d_c, d_rope) the latent path is instantiated for.
+#define VMLA_LATENT_SHAPES(X) X(192, 32) X(16, 8) X(64, 32) X(128, 32) X(256, 32)
 
 template <int DC, int DR>
 hipError_t launch_attend_t(const AttendArgs& a, hipStream_t s) {
@@ -718,37 +737,55 @@ hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int DC, int DR> using ShapeCfg =
+    AttCfg<DC, DR, AttShape<DC, DR>::QB, AttShape<DC, DR>::NW, AttShape<DC, DR>::BN>;
+
 bool latent_attend_supported(int d_c, int d_rope) {
-  return (d_c == 192 && d_rope == 32) || (d_c == 16 && d_rope == 8);
+#define X(DC, DR) if (d_c == DC && d_rope == DR) return true;
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return false;
 }
 
 int latent_attend_rows_per_block(int d_c, int d_rope) {
-  if (d_c == 192 && d_rope == 32) return AttCfg<192, 32, AttShape<192, 32>::QB, AttShape<192, 32>::NW, AttShape<192, 32>::BN>::ROWS;
-  return AttCfg<16, 8, AttShape<16, 8>::QB, AttShape<16, 8>::NW, AttShape<16, 8>::BN>::ROWS;
+#define X(DC, DR) if (d_c == DC && d_rope == DR) return ShapeCfg<DC, DR>::ROWS;
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return 0;
 }
 
 int latent_attend_keys_per_tile(int d_c, int d_rope) {
-  if (d_c == 192 && d_rope == 32) return AttShape<192, 32>::BN;
-  return AttShape<16, 8>::BN;
+#define X(DC, DR) if (d_c == DC && d_rope == DR) return AttShape<DC, DR>::BN;
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return 0;
 }
 
 int latent_attend_wgs_per_cu(int d_c, int d_rope) {
-  if (d_c == 192 && d_rope == 32) return AttShape<192, 32>::WPC;
-  return AttShape<16, 8>::WPC;
+#define X(DC, DR) if (d_c == DC && d_rope == DR) return AttShape<DC, DR>::WPC;
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return 0;
+}
+
+size_t q_absorb_lds_bytes(int d_c, int d_nope) {
+#define X(DC, DR) if (d_c == DC) return (size_t)d_nope * (AbsorbChunk<DC>::CW + 8) * 2;
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return 0;
 }
 
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s) {
   const dim3 grid((a.geo.chunk_tokens + 127) / 128, a.n_heads, a.batch);
-  if (a.d_c == 192 && a.d_rope == 32) {
-    const size_t lds = (size_t)a.d_nope * (192 + 8) * 2;
-    hipLaunchKernelGGL((q_absorb_kernel<192, 32>), grid, dim3(256), lds, s, a);
-  } else if (a.d_c == 16 && a.d_rope == 8) {
-    const size_t lds = (size_t)a.d_nope * (32 + 8) * 2;
-    hipLaunchKernelGGL((q_absorb_kernel<16, 8>), grid, dim3(256), lds, s, a);
-  } else {
-    return hipErrorInvalidValue;
+  const size_t lds = q_absorb_lds_bytes(a.d_c, a.d_nope);
+#define X(DC, DR)                                                                    \
+  if (a.d_c == DC && a.d_rope == DR) {                                               \
+    hipLaunchKernelGGL((q_absorb_kernel<DC, DR>), grid, dim3(256), lds, s, a);       \
+    return hipGetLastError();                                                        \
   }
-  return hipGetLastError();
+  VMLA_LATENT_SHAPES(X)
+#undef X
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s) {
@@ -759,8 +796,9 @@ hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s) {
-  if (a.d_c == 192 && a.d_rope == 32) return launch_attend_t<192, 32>(a, s);
-  if (a.d_c == 16 && a.d_rope == 8) return launch_attend_t<16, 8>(a, s);
+#define X(DC, DR) if (a.d_c == DC && a.d_rope == DR) return launch_attend_t<DC, DR>(a, s);
+  VMLA_LATENT_SHAPES(X)
+#undef X
   return hipErrorInvalidValue;
 }
 
@@ -782,8 +820,9 @@ hipError_t launch_out_proj_t(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s) {
-  if (a.d_c == 192) return launch_out_proj_t<192>(a, s);
-  if (a.d_c == 16) return launch_out_proj_t<16>(a, s);
+#define X(DC, DR) if (a.d_c == DC && a.d_rope == DR) return launch_out_proj_t<DC>(a, s);
+  VMLA_LATENT_SHAPES(X)
+#undef X
   return hipErrorInvalidValue;
 }
 

@@ -301,14 +301,15 @@ int check_layer_shape(const videomla_dims* d, int32_t d_q) {
 int check_attend_shape(const videomla_dims* d) {
   if (!latent_attend_supported(d->d_c, d->d_rope))
     return fail(VIDEOMLA_EUNSUPPORTED,
-                "attention kernel is built for (d_c, d_rope) in {(192,32),(16,8)}, got (%d,%d)",
+                "attention kernel is built for (d_c, d_rope) in {(64,32),(128,32),(192,32),"
+                "(256,32),(16,8)}, got (%d,%d)",
                 d->d_c, d->d_rope);
   if (d->d_nope % 16 || d->d_nope > 128)
     return fail(VIDEOMLA_EUNSUPPORTED, "d_nope must be a multiple of 16 and <= 128, got %d", d->d_nope);
   if (d->d_v % 32 || d->d_v > 256)
     return fail(VIDEOMLA_EUNSUPPORTED, "d_v must be a multiple of 32 and <= 256, got %d", d->d_v);
-  const size_t lds = (size_t)d->d_nope * (round_up(d->d_c, 32) + 8) * 2;
-  if (lds > 64 * 1024) return fail(VIDEOMLA_EUNSUPPORTED, "d_nope %d too large for the query kernel", d->d_nope);
+  if (q_absorb_lds_bytes(d->d_c, d->d_nope) > 64 * 1024)
+    return fail(VIDEOMLA_EUNSUPPORTED, "d_nope %d too large for the query kernel", d->d_nope);
   return VIDEOMLA_OK;
 }
 

@@ -135,6 +135,18 @@ def test_packed_write_weights_size_and_validation():
     assert _write(_dims_struct(WAN, d_model=4096)) == L.EUNSUPPORTED
 
 
+def test_dc_sweep_shapes():
+    """The paper's Table 5 latent widths: 64, 128, 192 and 256 are built (with d_rope = 32);
+    512 needs more accumulator registers per query row than this kernel's layout has, and is
+    rejected by both calls."""
+    for dc in (64, 128, 192, 256):
+        assert vm.attend_workspace_bytes(WAN.replace(d_c=dc), 1) > 0
+        assert vm.write_weights_bytes(WAN.replace(d_c=dc)) > 0
+    assert vm.attend_workspace_bytes(WAN.replace(d_c=512), 1) == 0
+    assert _attend(_dims_struct(WAN, d_c=512)) == L.EUNSUPPORTED
+    assert _write(_dims_struct(WAN, d_c=512)) == L.EUNSUPPORTED
+
+
 def test_attend_rejects_bad_args():
     d = L.make_dims(WAN)
     assert _attend(d, q=None) == L.EINVAL
@@ -143,7 +155,7 @@ def test_attend_rejects_bad_args():
     assert need > 0
     assert _attend(d, ws=None) == L.EWORKSPACE
     assert _attend(d, ws_bytes=need - 1) == L.EWORKSPACE
-    assert _attend(_dims_struct(WAN, d_c=128)) == L.EUNSUPPORTED
+    assert _attend(_dims_struct(WAN, d_c=112)) == L.EUNSUPPORTED
     assert _attend(_dims_struct(WAN, d_v=100)) == L.EUNSUPPORTED
     assert _attend(_dims_struct(WAN, d_nope=100)) == L.EUNSUPPORTED
 
@@ -260,7 +272,7 @@ def test_layer_calls_validate_and_size():
     assert layer(weights_bytes=wb - 1) == L.EWORKSPACE
     assert layer(ws_ptr=None) == L.EWORKSPACE
     assert layer(ws_bytes=ws - 1) == L.EWORKSPACE
-    assert layer(d=_dims_struct(WAN, d_c=128)) == L.EUNSUPPORTED
+    assert layer(d=_dims_struct(WAN, d_c=112)) == L.EUNSUPPORTED
     assert layer(d=_dims_struct(WAN, d_model=1000)) == L.EUNSUPPORTED
     prep = L.raw().videomla_prepare_layer_weights
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, wb, None) == L.EINVAL

@@ -73,6 +73,18 @@ WAN_SINK = WAN.replace(window_frames=7, sink_frames=1)
 # Tiny sink case: one sink frame and three local frames, 1-frame chunks.
 TINY_SINK = TINY.replace(window_frames=4, sink_frames=1)
 
+# The latent widths of the paper's d_c sweep (Table 5), Wan geometry otherwise.
+DC_SWEEP = (64, 128, 192, 256, 512)
+WAN_DC = {dc: WAN.replace(d_c=dc) for dc in DC_SWEEP}
+
+# Few-query regime: 1-frame chunks (1,560 queries per call) over the 21-frame window.
+WAN_1F = WAN.replace(chunk_frames=1)
+
+# A small shape with Wan's head and RoPE widths: 2 heads, a 6x10 grid, a 5-frame window (300
+# keys: a ragged last key tile) and 2-frame chunks (120 queries); d_c is set per case.
+SMALL = Dims(d_model=256, n_heads=2, d_nope=128, d_rope=32, d_c=192, d_v=128, grid_h=6,
+             grid_w=10, window_frames=5, chunk_frames=2, rope_pairs=(8, 4, 4))
+
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (nearest, ties to even); returns the uint16 bit patterns."""
