@@ -524,10 +524,12 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
     }), flush=True)
 
 
-def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8):
+def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
+                       materialized=False):
     """Per-kernel HIP-event averages of `steps` chunk-steps (packed cache write + attend) of
     one layer with dims d at the wrapped full window (chunk at frame window_frames), batch
-    `batch`. Seeded synthetic bf16 drawn on the GPU; x cycles through `x_buffers` buffers."""
+    `batch`; the attend is the latent form, or the materialized-K/V form when `materialized`.
+    Seeded synthetic bf16 drawn on the GPU; x cycles through `x_buffers` buffers."""
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
@@ -545,7 +547,9 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8):
     c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
     k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
     out = torch.empty((B, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
-    ws = torch.empty(vm.attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
+    ws_bytes = (vm.attend_materialized_workspace_bytes if materialized
+                else vm.attend_workspace_bytes)(d, B)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
     vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
     for f in range(0, d.window_frames, d.chunk_frames):
@@ -556,12 +560,13 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8):
 
     def step(i):
         vm.cache_write_prepared(d, fe, B, xs[i % len(xs)], w_packed, gamma, c_kv, k_r)
-        vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+        vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, materialized=materialized)
 
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
+    names = (("cache_write", "mat_kv", "mat_q_prep", "mat_attend", "mat_merge") if materialized
+             else ("cache_write", "q_absorb", "latent_attend", "out_proj"))
     vm.timing_enable(True)
     for k in names:
         vm.timing_read(k)
@@ -577,6 +582,39 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8):
         kernels[k] = round(1e3 * tot / max(n, 1), 3)
     vm.timing_enable(False)
     return ev0.elapsed_time(ev1) / steps, kernels
+
+
+def latent_vs_materialized(args, vm, torch):
+    """The two exact forms of the attention at the paper's head split (d_nope 96 + d_rope 32,
+    Wan geometry, 3-frame chunk over the 32,760-key window, batch 1): the latent form
+    (absorbed queries, 2 d_c + d_rope = 416 multiply-adds per score) and the materialized form
+    (per-head K_h, V_h reconstructed for the window each call, then 96 + 32 + 128 = 256 per
+    score). Each step also writes the chunk's latents (packed cache write)."""
+    from workloads import WAN_PAPER
+    d = WAN_PAPER
+    steps = max(10, args.steps // 2)
+    res = {}
+    for name, mat in (("latent", False), ("materialized", True)):
+        log(name)
+        ms, k = chunk_step_kernels(vm, torch, d, 1, steps, args.warmup, seed=52, materialized=mat)
+        res[name] = {"ms_per_step": round(ms, 4), "kernels_us": k}
+    rows = d.chunk_tokens * d.n_heads
+    flop_lat = rows * d.window_tokens * 2 * (2 * d.d_c + d.d_rope)
+    flop_mat = rows * d.window_tokens * 2 * (d.d_nope + d.d_rope + d.d_v)
+    res["latent"]["attention_kernel_tflops"] = round(flop_lat / (res["latent"]["kernels_us"]["latent_attend"] / 1e6) / 1e12, 1)
+    res["materialized"]["attention_kernel_tflops"] = round(flop_mat / (res["materialized"]["kernels_us"]["mat_attend"] / 1e6) / 1e12, 1)
+    att_lat = sum(v for k2, v in res["latent"]["kernels_us"].items() if k2 != "cache_write")
+    att_mat = sum(v for k2, v in res["materialized"]["kernels_us"].items() if k2 != "cache_write")
+    print(json.dumps({
+        "metric": "attend us per call: latent form vs materialized per-head K/V (paper head split)",
+        "value": round(att_mat / att_lat, 4), "unit": "materialized / latent attend time",
+        "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "latent": res["latent"], "materialized": res["materialized"],
+        "attend_us": {"latent": round(att_lat, 2), "materialized": round(att_mat, 2)},
+        "config": {"workload": ("Wan2.1-1.3B geometry, paper head split d_nope 96 + d_rope 32, "
+                                "d_c 192: chunk of 3 frames (4,680 x 12 query rows) over the "
+                                "wrapped 32,760-key window, batch 1")},
+    }), flush=True)
 
 
 def dc_sweep(args, vm, torch, d0):
@@ -631,7 +669,8 @@ def main():
                     help="also run a 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="wan-layer-chunk-step",
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
-                             "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep"),
+                             "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
+                             "wan-paper-latent-vs-materialized"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -640,7 +679,8 @@ def main():
                          "frames late in a rollout; wan-full-layer-chunk-step: the whole "
                          "attention layer in latent form (query path and W_O absorbed); "
                          "wan-dc-sweep: chunk-steps at the latent widths of the paper's d_c "
-                         "sweep and with 1-frame chunks")
+                         "sweep and with 1-frame chunks; wan-paper-latent-vs-materialized: the "
+                         "latent and the materialized-K/V attention at the paper's head split")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -662,6 +702,9 @@ def main():
         return
     if args.workload == "wan-full-layer-chunk-step":
         full_layer_chunk_step(args, vm, torch, WAN)
+        return
+    if args.workload == "wan-paper-latent-vs-materialized":
+        latent_vs_materialized(args, vm, torch)
         return
     if args.workload == "wan-dc-sweep":
         dc_sweep(args, vm, torch, WAN)

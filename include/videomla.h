@@ -171,6 +171,27 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * videomla_attend_materialized -- the same attention computed in the training form (Eq. 2 and
+ * Eq. 7; App. "Inference-Time Reparameterization" states that the absorbed form equals it):
+ * per-head keys and values are reconstructed for every valid slot of the window,
+ *   K_h[j] = [W_up,h^K c_kv[j] ; k_r[j]]  (d_nope + d_rope),   V_h[j] = W_up,h^V c_kv[j]  (d_v),
+ * then standard softmax attention runs per head with q = [q_nope ; RoPE_3D(q_r)]. It trades the
+ * reconstruction (a GEMM over the window, once per call) for a cheaper score: d_nope + d_rope +
+ * d_v multiply-adds per (query, head, key) instead of the latent form's 2 d_c + d_rope.
+ * Arguments, layouts and result as videomla_attend; the workspace (at least
+ * videomla_attend_materialized_workspace_bytes() bytes) also holds the reconstructed rows.
+ * Requires d_nope + d_rope == d_v == 128 (the paper's 96 + 32), d_c % 64 == 0,
+ * sink_frames == 0; otherwise VIDEOMLA_EUNSUPPORTED. The work partition follows
+ * videomla_set_attend_workgroups.
+ */
+size_t videomla_attend_materialized_workspace_bytes(const videomla_dims* dims, int32_t batch);
+int videomla_attend_materialized(const videomla_dims* dims, const videomla_window* win,
+                                 int32_t batch, const uint16_t* q_nope, const uint16_t* q_r,
+                                 const uint16_t* w_uk, const uint16_t* w_uv,
+                                 const uint16_t* c_kv, const uint16_t* k_r, uint16_t* out,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * The whole attention layer in latent form (App. "Inference-Time Reparameterization",
  * Eqs. 8-11, and App. "VideoMLA Block"): from the chunk's attention input x to the output of
  * the output projection W_O, with the query path absorbed.

@@ -10,6 +10,8 @@ from ._lib import (  # noqa: F401
     attend,
     attend_layer,
     attend_layer_workspace_bytes,
+    attend_materialized,
+    attend_materialized_workspace_bytes,
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,

@@ -24,6 +24,7 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
 EXPORTED = (
     "videomla_cache_write", "videomla_write_weights_bytes", "videomla_prepare_write_weights",
     "videomla_cache_write_prepared", "videomla_attend_workspace_bytes", "videomla_attend",
+    "videomla_attend_materialized_workspace_bytes", "videomla_attend_materialized",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
     "videomla_timing_enable", "videomla_timing_read",
@@ -67,6 +68,11 @@ _lib.videomla_attend_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
                                  ctypes.c_size_t, _P]
 _lib.videomla_attend.restype = ctypes.c_int
+_lib.videomla_attend_materialized_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
+_lib.videomla_attend_materialized_workspace_bytes.restype = ctypes.c_size_t
+_lib.videomla_attend_materialized.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P,
+                                              _P, _P, ctypes.c_size_t, _P]
+_lib.videomla_attend_materialized.restype = ctypes.c_int
 _lib.videomla_window_advance.argtypes = [_DP, _WP]
 _lib.videomla_window_advance.restype = ctypes.c_int
 _lib.videomla_cache_bytes_per_token.argtypes = [_DP]
@@ -222,8 +228,9 @@ def attend_workspace_bytes(dims, batch: int) -> int:
 
 
 def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace,
-           stream=None):
-    """videomla_attend on torch tensors; `workspace` is a uint8 device tensor."""
+           stream=None, materialized=False):
+    """videomla_attend (or videomla_attend_materialized when `materialized`) on torch tensors;
+    `workspace` is a uint8 device tensor."""
     d = make_dims(dims)
     hw = d.grid_h * d.grid_w
     nq = d.chunk_frames * hw
@@ -236,10 +243,23 @@ def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r,
     _need(out, "out", batch * nq * d.n_heads * d.d_v)
     w = VideomlaWindow(int(frame_end))
     ws = _ptr(workspace, "workspace", (torch.uint8,))
-    _check(_lib.videomla_attend(
+    fn = _lib.videomla_attend_materialized if materialized else _lib.videomla_attend
+    _check(fn(
         ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
         _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
         _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
+
+
+def attend_materialized_workspace_bytes(dims, batch: int) -> int:
+    return int(_lib.videomla_attend_materialized_workspace_bytes(ctypes.byref(make_dims(dims)),
+                                                                 int(batch)))
+
+
+def attend_materialized(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out,
+                        workspace, stream=None):
+    """videomla_attend_materialized on torch tensors (arguments as attend)."""
+    attend(dims, frame_end, batch, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace, stream,
+           materialized=True)
 
 
 def dense_cache_bytes_per_token(dims) -> int:

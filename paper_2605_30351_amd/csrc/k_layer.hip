@@ -92,6 +92,32 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
   }
 
   // epilogue: lane holds token n0 + 32 wave + l32 and outputs o0 + 32 m + 8 i + 4 g + j
+  if constexpr (EPI == kEpiHeads) {
+    // through LDS, so that every store is a whole 16-byte chunk of 8 consecutive outputs of one
+    // token (head_w % 8 == 0 keeps a chunk inside one head): each wave's 32 token rows x 128
+    // outputs go to its own LDS tile, then its lanes copy them out row by row
+    constexpr int OTS = kGmOut + 8;  // tile row stride (elements)
+    __syncthreads();                 // every wave is done reading the stage buffers
+    uint16_t* ot = &stage[0][0] + wave * 32 * OTS;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 fv = {acc[m][4 * i], acc[m][4 * i + 1], acc[m][4 * i + 2], acc[m][4 * i + 3]};
+        *reinterpret_cast<bf16x4*>(&ot[l32 * OTS + m * 32 + 8 * i + 4 * g]) = to_bf16x4(fv);
+      }
+    __syncthreads();  // the tile rows are read by other lanes than the ones that wrote them
+#pragma unroll 4
+    for (int it = lane; it < 32 * (kGmOut / 8); it += 64) {
+      const int tr = it / (kGmOut / 8), ch = it % (kGmOut / 8);
+      const int tok = n0 + wave * 32 + tr, o = o0 + ch * 8;
+      if (tok < a.M && o < a.N)
+        stg16(a.out + (size_t)tok * a.ldo + (size_t)(o / a.head_w) * a.head_ld + a.col_off +
+                  o % a.head_w,
+              *reinterpret_cast<const u32x4*>(&ot[tr * OTS + ch * 8]));
+    }
+    return;
+  }
   const int t = n0 + wave * 32 + l32;
   float scale = 1.f;
   TokenPos pos{};
@@ -240,6 +266,8 @@ hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
   const dim3 grid((a.M + kGmTok - 1) / kGmTok, (a.N + kGmOut - 1) / kGmOut);
   if (a.epi == kEpiQcat)
     hipLaunchKernelGGL(gemm_nt_kernel<kEpiQcat>, grid, dim3(256), 0, s, a);
+  else if (a.epi == kEpiHeads)
+    hipLaunchKernelGGL(gemm_nt_kernel<kEpiHeads>, grid, dim3(256), 0, s, a);
   else
     hipLaunchKernelGGL(gemm_nt_kernel<kEpiStore>, grid, dim3(256), 0, s, a);
   return hipGetLastError();

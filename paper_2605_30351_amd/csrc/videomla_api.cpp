@@ -110,14 +110,17 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
 enum KernelId {
   K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
   K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW,
-  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_PREPARE_WRITE, K_COUNT
+  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_PREPARE_WRITE,
+  K_MAT_KV, K_MAT_Q_PREP, K_MAT_ATTEND, K_MAT_MERGE, K_COUNT
 };
 const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
                                      "out_proj",          "dense_cache_write", "dense_q_prep",
                                      "dense_attend",      "dense_merge",  "rope_window",
                                      "q_down",            "q_up",         "latent_merge",
                                      "out_mix",           "prepare_layer_weights",
-                                     "prepare_write_weights"};
+                                     "prepare_write_weights",
+                                     "mat_kv",            "mat_q_prep",   "mat_attend",
+                                     "mat_merge"};
 
 struct TimingRec {
   int kernel;
@@ -609,6 +612,119 @@ int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int3
   if (e != hipSuccess) return hip_fail(e, "dense_attend");
   e = timed(K_DENSE_MERGE, s, [&] { return launch_dense_merge(a, s); });
   if (e != hipSuccess) return hip_fail(e, "dense_merge");
+  return ok();
+}
+
+namespace {
+
+// Materialized-K/V path: the head rows [K_h | V_h] = [W_UK,h c ; k^R | W_UV,h c] must have the
+// dense attention kernel's width: d_nope + d_rope = d_v = its head width.
+int check_materialized_shape(const videomla_dims* d) {
+  if (!dense_attend_supported(d->d_v) || d->d_nope + d->d_rope != d->d_v)
+    return fail(VIDEOMLA_EUNSUPPORTED,
+                "materialized attention needs d_nope + d_rope = d_v = 128 (the head width of the "
+                "dense kernel), got %d + %d, %d", d->d_nope, d->d_rope, d->d_v);
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "materialized attention has no sink mode");
+  if (d->d_c % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 64, got %d", d->d_c);
+  if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
+  return 0;
+}
+
+// [B][ring][H][2 d_v] materialized rows, then the dense kernel's query rows and partials
+struct MatLayout {
+  size_t kv_off, dense_off, total;
+  WorkspaceLayout dense;
+};
+MatLayout mat_layout(const videomla_dims* d, int32_t batch) {
+  MatLayout m{};
+  const size_t kv = (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->n_heads * 2 *
+                    d->d_v * 2;
+  m.kv_off = 0;
+  m.dense_off = round_up(kv, 256);
+  m.dense = dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true));
+  m.total = m.dense_off + m.dense.total;
+  return m;
+}
+
+}  // namespace
+
+size_t videomla_attend_materialized_workspace_bytes(const videomla_dims* d, int32_t batch) {
+  if (check_dims(d) || batch <= 0 || check_materialized_shape(d)) return 0;
+  return mat_layout(d, batch).total;
+}
+
+int videomla_attend_materialized(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                                 const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                                 const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                                 uint16_t* out, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
+    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (int e = check_materialized_shape(d)) return e;
+  if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
+      !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const MatLayout L = mat_layout(d, batch);
+  if (!workspace || workspace_bytes < L.total)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
+                workspace ? workspace_bytes : (size_t)0);
+  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+
+  char* ws = static_cast<char*>(workspace);
+  uint16_t* kv = reinterpret_cast<uint16_t*>(ws + L.kv_off);
+  char* dws = ws + L.dense_off;
+  AttendArgs a{};
+  a.q_nope = q_nope; a.q_r = q_r; a.k_r = k_r; a.kv = kv; a.out = out;
+  a.qcat = reinterpret_cast<uint16_t*>(dws + L.dense.qcat_off);
+  a.o_part = reinterpret_cast<float*>(dws + L.dense.opart_off);
+  a.ml_part = reinterpret_cast<float*>(dws + L.dense.ml_off);
+  a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v;
+  a.d_nope = d->d_nope; a.d_rope = d->d_rope; a.d_c = d->d_v;
+  a.dqk_pad = d->d_v;
+  a.nq_pad = dense_nq_pad(d);
+  a.geo = make_geo(d, w);
+  a.rope = make_rope(d);
+  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
+  const Partition P = dense_partition(d, batch, a.n_valid);
+  a.n_wg = P.G;
+  a.att_rows = P.rows;
+  a.row_blocks = P.RB;
+  a.tiles_per_row = P.T;
+  a.units = P.U;
+  a.max_seg = P.max_seg;
+  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
+                                              : 1.0 / std::sqrt((double)(d->d_nope + d->d_rope));
+  a.qscale = (float)(scale * 1.4426950408889634);
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int64_t ring = a.geo.ring_tokens, H = d->n_heads, ld = 2 * (int64_t)d->d_v;
+  hipError_t e = timed(K_MAT_KV, s, [&] {
+    // per batch element: K_h no-RoPE part = W_UK,h c and V_h = W_UV,h c of the valid slots
+    for (int b = 0; b < batch; ++b) {
+      GemmArgs g{};
+      g.b = c_kv + (size_t)b * ring * d->d_c;
+      g.out = kv + (size_t)b * ring * H * ld;
+      g.M = a.n_valid; g.K = d->d_c; g.ldo = (int32_t)(H * ld); g.epi = kEpiHeads;
+      g.head_ld = (int32_t)ld;
+      g.a = w_uk; g.N = (int32_t)(H * d->d_nope); g.head_w = d->d_nope; g.col_off = 0;
+      hipError_t r = launch_gemm_nt(g, s);
+      if (r != hipSuccess) return r;
+      g.a = w_uv; g.N = (int32_t)(H * d->d_v); g.head_w = d->d_v; g.col_off = d->d_v;
+      r = launch_gemm_nt(g, s);
+      if (r != hipSuccess) return r;
+    }
+    return launch_mat_rope_fill(a, kv, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "mat_kv");
+  e = timed(K_MAT_Q_PREP, s, [&] { return launch_mat_q_prep(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "mat_q_prep");
+  e = timed(K_MAT_ATTEND, s, [&] { return launch_dense_attend(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "mat_attend");
+  e = timed(K_MAT_MERGE, s, [&] { return launch_dense_merge(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "mat_merge");
   return ok();
 }
 

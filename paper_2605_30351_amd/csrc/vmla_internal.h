@@ -94,6 +94,7 @@ struct DenseWriteArgs {
 // Plain bf16 GEMM out^T[o][token] = a[o][:] . b[token][:] (a [N][K], b [M][K], K % 64 == 0).
 constexpr int kEpiStore = 0;  // out[token][o] (row stride ldo), bf16
 constexpr int kEpiQcat = 1;   // q_cat rows (token, head): RMSNorm factor, RoPE, scale; see k_layer.hip
+constexpr int kEpiHeads = 2;  // out[token][(o / head_w) head_ld + col_off + o % head_w], bf16, head_w % 8 == 0
 struct GemmArgs {
   const uint16_t* a;       // [N][K] weight rows
   const uint16_t* b;       // [M][K] token rows
@@ -102,6 +103,8 @@ struct GemmArgs {
   int32_t epi;
   // q_cat epilogue: output column o = h (q_dc + q_dr) + c; row (token, h) of width ldo
   int32_t q_heads, q_dc, q_dr, q_norm_dim;
+  // per-head epilogue: output column o goes to head o / head_w, column col_off + o % head_w
+  int32_t head_w, head_ld, col_off;
   float qscale, eps;
   Geometry geo;            // token t of the flat [B][Nq] order sits at chunk index t % Nq
   RopeTable rope;
@@ -132,6 +135,8 @@ hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);
 hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s);
+hipError_t launch_mat_q_prep(const AttendArgs& a, hipStream_t s);
+hipError_t launch_mat_rope_fill(const AttendArgs& a, uint16_t* kv, hipStream_t s);
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
 hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat, hipStream_t s);
 hipError_t launch_prepare_weights(const PrepArgs& a, hipStream_t s);

@@ -65,12 +65,14 @@ class Layer:
             self.vm.cache_write(d, fe, self.inp.batch, xs, self.w_dkv, self.w_kr, self.gamma,
                                 self.c_kv, self.k_r, self.slots)
 
-    def attend(self, fe):
+    def attend(self, fe, materialized=False):
+        """videomla_attend, or videomla_attend_materialized (per-head K/V reconstructed)."""
         d = self.inp.dims
-        ws = torch.empty(self.vm.attend_workspace_bytes(d, self.inp.batch), dtype=torch.uint8,
-                         device="cuda")
+        size = (self.vm.attend_materialized_workspace_bytes if materialized
+                else self.vm.attend_workspace_bytes)(d, self.inp.batch)
+        ws = torch.empty(size, dtype=torch.uint8, device="cuda")
         self.vm.attend(d, fe, self.inp.batch, self.q_nope, self.q_r, self.w_uk, self.w_uv,
-                       self.c_kv, self.k_r, self.out, ws)
+                       self.c_kv, self.k_r, self.out, ws, materialized=materialized)
         torch.cuda.synchronize()
         return bf16_to_f64(host_bits(self.out))
 

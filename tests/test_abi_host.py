@@ -147,6 +147,29 @@ def test_dc_sweep_shapes():
     assert _write(_dims_struct(WAN, d_c=512)) == L.EUNSUPPORTED
 
 
+def test_materialized_attend_validation():
+    """The materialized form needs the dense kernel's head width: d_nope + d_rope = d_v = 128
+    (the paper's 96 + 32), no sink."""
+    assert vm.attend_materialized_workspace_bytes(WAN_PAPER, 1) > 0
+    assert vm.attend_materialized_workspace_bytes(WAN, 1) == 0       # 128 + 32 != 128
+    mat = L.raw().videomla_attend_materialized
+
+    def call(d, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+        w = L.VideomlaWindow(0)
+        return mat(ctypes.byref(d), ctypes.byref(w), 1, q, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                   ws, ws_bytes, None)
+    d = L.make_dims(WAN_PAPER)
+    assert call(L.make_dims(WAN)) == L.EUNSUPPORTED
+    assert call(_dims_struct(WAN_PAPER, sink_frames=1, window_frames=7)) == L.EUNSUPPORTED
+    assert call(d, q=None) == L.EINVAL
+    assert call(d, q=MISALIGNED) == L.EALIGN
+    need = vm.attend_materialized_workspace_bytes(WAN_PAPER, 1)
+    assert call(d, ws=None) == L.EWORKSPACE
+    assert call(d, ws_bytes=need - 1) == L.EWORKSPACE
+    # the reconstructed rows dominate: ring x heads x (K_h | V_h) in bf16
+    assert need >= 32760 * 12 * 256 * 2
+
+
 def test_attend_rejects_bad_args():
     d = L.make_dims(WAN)
     assert _attend(d, q=None) == L.EINVAL

@@ -85,6 +85,9 @@ WAN_1F = WAN.replace(chunk_frames=1)
 SMALL = Dims(d_model=256, n_heads=2, d_nope=128, d_rope=32, d_c=192, d_v=128, grid_h=6,
              grid_w=10, window_frames=5, chunk_frames=2, rope_pairs=(8, 4, 4))
 
+# SMALL with the paper's own head split (d_nope 96 + d_rope 32 = d_v = 128).
+SMALL_PAPER = SMALL.replace(d_nope=96, rope_pairs=(6, 5, 5), rope_band_dim=(44, 42, 42))
+
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round float32 values to bf16 (nearest, ties to even); returns the uint16 bit patterns."""
