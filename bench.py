@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "527b467b623a1fe6e1e27d7548f6c7c452ef2e288252b113ac5e7b2f1968732e",
-                  "bytes": 308770040}
+                  "sha256": "604f0720719f5b3e8a6ecbbf7549611116b8c60823bf7fc4337b2fe296d675d4",
+                  "bytes": 308651281}
 
 
 def log(msg):
