@@ -585,35 +585,37 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
 
 
 def latent_vs_materialized(args, vm, torch):
-    """The two exact forms of the attention at the paper's head split (d_nope 96 + d_rope 32,
-    Wan geometry, 3-frame chunk over the 32,760-key window, batch 1): the latent form
-    (absorbed queries, 2 d_c + d_rope = 416 multiply-adds per score) and the materialized form
-    (per-head K_h, V_h reconstructed for the window each call, then 96 + 32 + 128 = 256 per
-    score). Each step also writes the chunk's latents (packed cache write)."""
-    from workloads import WAN_PAPER
-    d = WAN_PAPER
+    """The two exact forms of the attention at Wan geometry (3-frame chunk of 4,680 x 12 query
+    rows over the wrapped 32,760-key window, batch 1, d_c 192), for both head splits: the
+    paper's d_nope 96 + d_rope 32 and the measured configuration's 128 + 32. Latent form:
+    absorbed queries, 2 d_c + d_rope = 416 multiply-adds per score. Materialized form: per-head
+    K_h, V_h reconstructed for the window each call, then d_nope + d_rope + d_v = 256 or 288
+    per score. Each step also writes the chunk's latents (packed cache write)."""
+    from workloads import WAN, WAN_PAPER
     steps = max(10, args.steps // 2)
-    res = {}
-    for name, mat in (("latent", False), ("materialized", True)):
-        log(name)
-        ms, k = chunk_step_kernels(vm, torch, d, 1, steps, args.warmup, seed=52, materialized=mat)
-        res[name] = {"ms_per_step": round(ms, 4), "kernels_us": k}
-    rows = d.chunk_tokens * d.n_heads
-    flop_lat = rows * d.window_tokens * 2 * (2 * d.d_c + d.d_rope)
-    flop_mat = rows * d.window_tokens * 2 * (d.d_nope + d.d_rope + d.d_v)
-    res["latent"]["attention_kernel_tflops"] = round(flop_lat / (res["latent"]["kernels_us"]["latent_attend"] / 1e6) / 1e12, 1)
-    res["materialized"]["attention_kernel_tflops"] = round(flop_mat / (res["materialized"]["kernels_us"]["mat_attend"] / 1e6) / 1e12, 1)
-    att_lat = sum(v for k2, v in res["latent"]["kernels_us"].items() if k2 != "cache_write")
-    att_mat = sum(v for k2, v in res["materialized"]["kernels_us"].items() if k2 != "cache_write")
+    out = {}
+    for label, d in (("d_nope 96 (paper)", WAN_PAPER), ("d_nope 128", WAN)):
+        res = {}
+        for name, mat in (("latent", False), ("materialized", True)):
+            log(f"{label}: {name}")
+            ms, k = chunk_step_kernels(vm, torch, d, 1, steps, args.warmup, seed=52, materialized=mat)
+            res[name] = {"ms_per_step": round(ms, 4), "kernels_us": k}
+        rows = d.chunk_tokens * d.n_heads
+        flop_lat = rows * d.window_tokens * 2 * (2 * d.d_c + d.d_rope)
+        flop_mat = rows * d.window_tokens * 2 * (d.d_nope + d.d_rope + d.d_v)
+        res["latent"]["attention_kernel_tflops"] = round(flop_lat / (res["latent"]["kernels_us"]["latent_attend"] / 1e6) / 1e12, 1)
+        res["materialized"]["attention_kernel_tflops"] = round(flop_mat / (res["materialized"]["kernels_us"]["mat_attend"] / 1e6) / 1e12, 1)
+        att = {n: round(sum(v for k2, v in res[n]["kernels_us"].items() if k2 != "cache_write"), 2)
+               for n in res}
+        out[label] = {**res, "attend_us": att, "materialized_over_latent": round(att["materialized"] / att["latent"], 4)}
     print(json.dumps({
-        "metric": "attend us per call: latent form vs materialized per-head K/V (paper head split)",
-        "value": round(att_mat / att_lat, 4), "unit": "materialized / latent attend time",
+        "metric": "attend us per call: latent form vs materialized per-head K/V",
+        "value": out["d_nope 128"]["materialized_over_latent"], "unit": "materialized / latent attend time (d_nope 128)",
         "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic", "latent": res["latent"], "materialized": res["materialized"],
-        "attend_us": {"latent": round(att_lat, 2), "materialized": round(att_mat, 2)},
-        "config": {"workload": ("Wan2.1-1.3B geometry, paper head split d_nope 96 + d_rope 32, "
-                                "d_c 192: chunk of 3 frames (4,680 x 12 query rows) over the "
-                                "wrapped 32,760-key window, batch 1")},
+        "data": "synthetic", "results": out,
+        "config": {"workload": ("Wan2.1-1.3B geometry, d_c 192, d_rope 32, d_nope 96 and 128: "
+                                "chunk of 3 frames (4,680 x 12 query rows) over the wrapped "
+                                "32,760-key window, batch 1")},
     }), flush=True)
 
 
@@ -670,7 +672,7 @@ def main():
     ap.add_argument("--workload", default="wan-layer-chunk-step",
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
                              "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
-                             "wan-paper-latent-vs-materialized"),
+                             "wan-latent-vs-materialized"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -679,8 +681,8 @@ def main():
                          "frames late in a rollout; wan-full-layer-chunk-step: the whole "
                          "attention layer in latent form (query path and W_O absorbed); "
                          "wan-dc-sweep: chunk-steps at the latent widths of the paper's d_c "
-                         "sweep and with 1-frame chunks; wan-paper-latent-vs-materialized: the "
-                         "latent and the materialized-K/V attention at the paper's head split")
+                         "sweep and with 1-frame chunks; wan-latent-vs-materialized: the "
+                         "latent and the materialized-K/V attention at both head splits")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -703,7 +705,7 @@ def main():
     if args.workload == "wan-full-layer-chunk-step":
         full_layer_chunk_step(args, vm, torch, WAN)
         return
-    if args.workload == "wan-paper-latent-vs-materialized":
+    if args.workload == "wan-latent-vs-materialized":
         latent_vs_materialized(args, vm, torch)
         return
     if args.workload == "wan-dc-sweep":

@@ -180,8 +180,8 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
  * d_v multiply-adds per (query, head, key) instead of the latent form's 2 d_c + d_rope.
  * Arguments, layouts and result as videomla_attend; the workspace (at least
  * videomla_attend_materialized_workspace_bytes() bytes) also holds the reconstructed rows.
- * Requires d_nope + d_rope == d_v == 128 (the paper's 96 + 32), d_c % 64 == 0,
- * sink_frames == 0; otherwise VIDEOMLA_EUNSUPPORTED. The work partition follows
+ * Requires d_v == 128 and d_nope + d_rope in {128 (the paper's 96 + 32), 160 (128 + 32)},
+ * d_c % 64 == 0, sink_frames == 0; otherwise VIDEOMLA_EUNSUPPORTED. The work partition follows
  * videomla_set_attend_workgroups.
  */
 size_t videomla_attend_materialized_workspace_bytes(const videomla_dims* dims, int32_t batch);

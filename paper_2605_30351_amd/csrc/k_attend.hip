@@ -185,23 +185,26 @@ constexpr float kLazyMax = 8.0f;
 
 
 // Tile layouts. Latent (DENSE = false): a tile row is [c_kv (DC) | k_r (DR) | pad], the scores
-// contract over all of it and V is its first DC columns. Dense comparator (DENSE = true, DC =
-// head width, DR = 0): a tile row is [K_h | V_h] of one head, the scores contract over K_h and V
-// is the second half.
-template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false>
+// contract over all of it and V is its first DC columns. Per-head rows (DENSE = true, DC = key
+// width, DR = 0, DVW = value width, 0 meaning DC): a tile row is [K_h | V_h] of one head, the
+// scores contract over K_h and V is the rest (the dense comparator: 128 | 128; the materialized
+// form: [W_UK,h c ; k^R] | W_UV,h c = 128 | 128 or 160 | 128).
+template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false, int DVW = 0>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
   static constexpr int DQKP = (DQK + 15) / 16 * 16;
   static constexpr int KSTEPS = DQKP / 16;
-  static constexpr int DVB = (DC + 31) / 32;
+  static constexpr int OW = DENSE && DVW ? DVW : DC;  // value (and partial-result) width
+  static constexpr int DVB = (OW + 31) / 32;
   static constexpr int KB = BN / 32;       // 32-key blocks per tile
   static constexpr int VOFF = DENSE ? DQKP : 0;  // first V column of a tile row
-  // Tile rows have no padding. Latent rows (DQKP elements): the 16-byte chunks of row r sit at
-  // chunk index XOR ((r / 4) mod 4). Dense rows (2 DQKP = 32 chunks, a multiple of 16 bank
-  // groups): chunk index XOR (4 (r mod 4) + (r / 4) mod 4) within groups of 16. Either way the
-  // 16-row operand reads of the score MFMA and the 4-row transpose reads of the PV MFMA hit 16
-  // distinct 4-bank groups each.
-  static constexpr int STRIDE = DENSE ? 2 * DQKP : DQKP;
+  // Tile rows have no padding. Rows whose chunk count is a multiple of 16 bank groups (the
+  // dense 128 | 128 rows, 32 chunks): chunk index XOR (4 (r mod 4) + (r / 4) mod 4) within
+  // groups of 16. Other rows (latent DQKP elements; 160 | 128 = 36 chunks): chunk index XOR
+  // ((r / 4) mod 4) within groups of 4. Either way the 16-row operand reads of the score MFMA
+  // and the 4-row transpose reads of the PV MFMA hit 16 distinct 4-bank groups each (checked by
+  // enumeration on the host for every layout instantiated here).
+  static constexpr int STRIDE = DENSE ? DQKP + OW : DQKP;
   static constexpr int NT = NW * 64;
   static constexpr int ROWS = NW * QB * 32;
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
@@ -214,12 +217,13 @@ struct AttCfg {
   static_assert(BN % 32 == 0, "key tile must be a multiple of 32");
   static_assert(VOFF + DVB * 32 <= STRIDE, "transpose reads must stay inside a tile row");
   static_assert(DQKP % 32 == 0, "the swizzle permutes chunks within aligned groups of four");
-  static_assert(!DENSE || (CPR % 16 == 0 && DR == 0 && DC % 32 == 0), "dense tile layout");
+  static_assert(!DENSE || (DR == 0 && DC % 32 == 0 && OW % 32 == 0), "per-head tile layout");
   static_assert(BN * CPR % 64 == 0, "a tile is a whole number of 64-lane loads");
+  static constexpr bool SW16 = DENSE && CPR % 16 == 0;
   // chunk position of logical chunk c in row r (an involution: it also maps back)
   __device__ static constexpr int pos(int r, int c) {
-    return DENSE ? ((c & ~15) | ((c ^ (((r & 3) << 2) | ((r >> 2) & 3))) & 15))
-                 : ((c & ~3) | ((c ^ (r >> 2)) & 3));
+    return SW16 ? ((c & ~15) | ((c ^ (((r & 3) << 2) | ((r >> 2) & 3))) & 15))
+                : ((c & ~3) | ((c ^ (r >> 2)) & 3));
   }
   // element offset of (row r, column c) inside a tile
   __device__ static constexpr int at(int r, int c) {
@@ -227,9 +231,9 @@ struct AttCfg {
   }
 };
 
-template <int DC, int DR, int QB, int NW, int BN, int WPC, bool DENSE = false>
+template <int DC, int DR, int QB, int NW, int BN, int WPC, bool DENSE = false, int DVW = 0>
 __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const AttendArgs a) {
-  using C = AttCfg<DC, DR, QB, NW, BN, DENSE>;
+  using C = AttCfg<DC, DR, QB, NW, BN, DENSE, DVW>;
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
 
@@ -565,13 +569,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     const int r = row0 + qb * 32 + l32;
     if (r >= rows_b) continue;
     const size_t grow_i = (size_t)b * rows_b + r;
-    float* op = a.o_part + ((size_t)split * total_rows + grow_i) * DC;
+    float* op = a.o_part + ((size_t)split * total_rows + grow_i) * C::OW;
 #pragma unroll
     for (int d = 0; d < C::DVB; ++d)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int c = d * 32 + 8 * i + 4 * g;
-        if (c < DC) {
+        if (c < C::OW) {
           const f32x4 v = {o[qb][d][4 * i], o[qb][d][4 * i + 1], o[qb][d][4 * i + 2], o[qb][d][4 * i + 3]};
           *reinterpret_cast<f32x4*>(op + c) = v;
         }
@@ -733,6 +737,22 @@ hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s) {
   if (a.d_v != kDenseHead) return hipErrorInvalidValue;
   hipLaunchKernelGGL((latent_attend_kernel<kDenseHead, 0, DenseShape::QB, DenseShape::NW,
                                            DenseShape::BN, DenseShape::WPC, true>),
+                     dim3(a.n_wg), dim3(DenseCfg::NT), 0, s, a);
+  return hipGetLastError();
+}
+
+// Materialized form: per-head rows [K_h | V_h] with K_h = [W_UK,h c ; k^R] of width d_nope +
+// d_rope (a.dqk_pad) and V_h of width d_v = 128: 128 | 128 is the dense comparator's
+// instantiation, 160 | 128 (d_nope 128 + d_rope 32) its own.
+bool mat_attend_supported(int d_k, int d_v) {
+  return d_v == kDenseHead && (d_k == kDenseHead || d_k == 160);
+}
+
+hipError_t launch_mat_attend(const AttendArgs& a, hipStream_t s) {
+  if (!mat_attend_supported(a.dqk_pad, a.d_v)) return hipErrorInvalidValue;
+  if (a.dqk_pad == kDenseHead) return launch_dense_attend(a, s);
+  hipLaunchKernelGGL((latent_attend_kernel<160, 0, DenseShape::QB, DenseShape::NW,
+                                           DenseShape::BN, DenseShape::WPC, true, kDenseHead>),
                      dim3(a.n_wg), dim3(DenseCfg::NT), 0, s, a);
   return hipGetLastError();
 }

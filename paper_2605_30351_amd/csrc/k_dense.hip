@@ -148,39 +148,40 @@ __global__ __launch_bounds__(256) void dense_q_prep_kernel(const AttendArgs a) {
 
 // ---------------------------------------------------------------------------------------------
 // mat_q_prep (materialized-K/V path): per-head query rows [q_nope ; RoPE_3D(q_R)] * scale *
-// log2 e (Eq. 4 and Eq. 6, the training form), head-major and padded like dense_q_prep's.
-// Grid (nq_pad / 4, B), 256 threads = 4 tokens x 64 channel pairs of the d_nope + d_rope = d_v
-// wide head row; a RoPE pair takes its angle once and applies it to every head.
+// log2 e (Eq. 4 and Eq. 6, the training form), d_nope + d_rope wide, head-major and padded like
+// dense_q_prep's. Grid (nq_pad / 4, B), 256 threads = 4 tokens x 64 lanes over the row's channel
+// pairs; a RoPE pair takes its angle once and applies it to every head.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void mat_q_prep_kernel(const AttendArgs a) {
-  const int t = threadIdx.x >> 6, p = threadIdx.x & 63;
+  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + t, b = blockIdx.y;
-  const int H = a.n_heads, DN = a.d_nope, DR = a.d_rope, DH = DN + DR, Nq = a.geo.chunk_tokens;
-  if (2 * p >= DH) return;
-  const bool rope = 2 * p >= DN;
-  const int pr = p - DN / 2;  // RoPE pair (when rope)
-  float cs = 1.f, sn = 0.f;
-  if (rope && n < Nq) rope_rotate(a.rope, pr, token_pos(a.geo, n), cs, sn);  // (1,0) -> (cos, sin)
-  for (int h = 0; h < H; ++h) {
-    uint32_t packed = 0;
-    if (n < Nq) {
-      const size_t row = ((size_t)b * Nq + n) * H + h;
-      const uint32_t raw = rope ? *reinterpret_cast<const uint32_t*>(a.q_r + row * DR + 2 * pr)
-                                : *reinterpret_cast<const uint32_t*>(a.q_nope + row * DN + 2 * p);
-      const float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff));
-      const float v = bf16_bits_to_f32((uint16_t)(raw >> 16));
-      packed = (uint32_t)to_bf16_bits((u * cs - v * sn) * a.qscale) |
-               ((uint32_t)to_bf16_bits((u * sn + v * cs) * a.qscale) << 16);
+  const int H = a.n_heads, DN = a.d_nope, DR = a.d_rope, DH = a.dqk_pad, Nq = a.geo.chunk_tokens;
+  for (int p = lane; 2 * p < DH; p += 64) {  // channel pair p of the d_nope + d_rope wide row
+    const bool rope = 2 * p >= DN;
+    const int pr = p - DN / 2;  // RoPE pair (when rope)
+    float cs = 1.f, sn = 0.f;
+    if (rope && n < Nq) rope_rotate(a.rope, pr, token_pos(a.geo, n), cs, sn);  // (1,0) -> (cos, sin)
+    for (int h = 0; h < H; ++h) {
+      uint32_t packed = 0;
+      if (n < Nq) {
+        const size_t row = ((size_t)b * Nq + n) * H + h;
+        const uint32_t raw = rope ? *reinterpret_cast<const uint32_t*>(a.q_r + row * DR + 2 * pr)
+                                  : *reinterpret_cast<const uint32_t*>(a.q_nope + row * DN + 2 * p);
+        const float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff));
+        const float v = bf16_bits_to_f32((uint16_t)(raw >> 16));
+        packed = (uint32_t)to_bf16_bits((u * cs - v * sn) * a.qscale) |
+                 ((uint32_t)to_bf16_bits((u * sn + v * cs) * a.qscale) << 16);
+      }
+      *reinterpret_cast<uint32_t*>(a.qcat + (((size_t)b * H + h) * a.nq_pad + n) * DH + 2 * p) = packed;
     }
-    *reinterpret_cast<uint32_t*>(a.qcat + (((size_t)b * H + h) * a.nq_pad + n) * DH + 2 * p) = packed;
   }
 }
 
 // mat_rope_fill: the head-shared RoPE key of every valid slot (rotated at write) copied into
 // channels d_nope .. d_nope + d_rope of every head's K_h row of the materialized ring
-// [B][ring][H][2 d_v]. One thread per (batch, slot, head, 16-byte chunk).
+// [B][ring][H][d_nope + d_rope + d_v]. One thread per (batch, slot, head, 16-byte chunk).
 __global__ __launch_bounds__(256) void mat_rope_fill_kernel(const AttendArgs a, uint16_t* kv) {
-  const int H = a.n_heads, DR = a.d_rope, cpk = DR / 8, DH = a.d_v;
+  const int H = a.n_heads, DR = a.d_rope, cpk = DR / 8, LD = a.dqk_pad + a.d_v;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t per_b = (int64_t)a.n_valid * H * cpk;
   if (e >= per_b * a.batch) return;
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(256) void mat_rope_fill_kernel(const AttendArgs a, 
   const int h = (int)(jh % H);
   const int64_t j = jh / H;
   const size_t slot = (size_t)b * a.geo.ring_tokens + j;
-  stg16(kv + (slot * H + h) * 2 * DH + a.d_nope + ch * 8, ldg16(a.k_r + slot * DR + ch * 8));
+  stg16(kv + (slot * H + h) * LD + a.d_nope + ch * 8, ldg16(a.k_r + slot * DR + ch * 8));
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -251,7 +252,7 @@ hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_mat_q_prep(const AttendArgs& a, hipStream_t s) {
-  // validated by the caller: d_nope + d_rope = d_v <= 128, nq_pad % 4 == 0
+  // validated by the caller: dqk_pad = d_nope + d_rope, both even, nq_pad % 4 == 0
   hipLaunchKernelGGL(mat_q_prep_kernel, dim3(a.nq_pad / 4, a.batch), dim3(256), 0, s, a);
   return hipGetLastError();
 }

@@ -617,31 +617,38 @@ int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int3
 
 namespace {
 
-// Materialized-K/V path: the head rows [K_h | V_h] = [W_UK,h c ; k^R | W_UV,h c] must have the
-// dense attention kernel's width: d_nope + d_rope = d_v = its head width.
+// Materialized-K/V path: head rows [K_h | V_h] = [W_UK,h c ; k^R | W_UV,h c], keys of width
+// d_nope + d_rope, values of width d_v; the attention kernel is built for 128 | 128 and 160 | 128.
 int check_materialized_shape(const videomla_dims* d) {
-  if (!dense_attend_supported(d->d_v) || d->d_nope + d->d_rope != d->d_v)
+  if (!mat_attend_supported(d->d_nope + d->d_rope, d->d_v))
     return fail(VIDEOMLA_EUNSUPPORTED,
-                "materialized attention needs d_nope + d_rope = d_v = 128 (the head width of the "
-                "dense kernel), got %d + %d, %d", d->d_nope, d->d_rope, d->d_v);
+                "materialized attention is built for d_v = 128 and d_nope + d_rope in {128, 160}, "
+                "got %d + %d, %d", d->d_nope, d->d_rope, d->d_v);
   if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "materialized attention has no sink mode");
   if (d->d_c % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 64, got %d", d->d_c);
   if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
   return 0;
 }
 
-// [B][ring][H][2 d_v] materialized rows, then the dense kernel's query rows and partials
+// [B][ring][H][d_k + d_v] materialized rows (d_k = d_nope + d_rope), then the per-head query
+// rows (d_k wide), the partial results (d_v wide) and (max, sum) pairs
 struct MatLayout {
   size_t kv_off, dense_off, total;
   WorkspaceLayout dense;
 };
 MatLayout mat_layout(const videomla_dims* d, int32_t batch) {
   MatLayout m{};
-  const size_t kv = (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->n_heads * 2 *
-                    d->d_v * 2;
+  const size_t dk = (size_t)d->d_nope + d->d_rope;
+  const size_t kv = (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->n_heads *
+                    (dk + d->d_v) * 2;
   m.kv_off = 0;
   m.dense_off = round_up(kv, 256);
-  m.dense = dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true));
+  const int n_seg = workspace_max_seg(d, batch, true);
+  const size_t rows = (size_t)batch * d->n_heads * dense_nq_pad(d);
+  m.dense.qcat_off = 0;
+  m.dense.opart_off = round_up(rows * dk * 2, 256);
+  m.dense.ml_off = m.dense.opart_off + round_up((size_t)n_seg * rows * d->d_v * 4, 256);
+  m.dense.total = m.dense.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
   m.total = m.dense_off + m.dense.total;
   return m;
 }
@@ -683,7 +690,7 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
   a.ml_part = reinterpret_cast<float*>(dws + L.dense.ml_off);
   a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v;
   a.d_nope = d->d_nope; a.d_rope = d->d_rope; a.d_c = d->d_v;
-  a.dqk_pad = d->d_v;
+  a.dqk_pad = d->d_nope + d->d_rope;  // key width
   a.nq_pad = dense_nq_pad(d);
   a.geo = make_geo(d, w);
   a.rope = make_rope(d);
@@ -700,7 +707,7 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
   a.qscale = (float)(scale * 1.4426950408889634);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int64_t ring = a.geo.ring_tokens, H = d->n_heads, ld = 2 * (int64_t)d->d_v;
+  const int64_t ring = a.geo.ring_tokens, H = d->n_heads, ld = (int64_t)a.dqk_pad + d->d_v;
   hipError_t e = timed(K_MAT_KV, s, [&] {
     // per batch element: K_h no-RoPE part = W_UK,h c and V_h = W_UV,h c of the valid slots
     for (int b = 0; b < batch; ++b) {
@@ -712,7 +719,7 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
       g.a = w_uk; g.N = (int32_t)(H * d->d_nope); g.head_w = d->d_nope; g.col_off = 0;
       hipError_t r = launch_gemm_nt(g, s);
       if (r != hipSuccess) return r;
-      g.a = w_uv; g.N = (int32_t)(H * d->d_v); g.head_w = d->d_v; g.col_off = d->d_v;
+      g.a = w_uv; g.N = (int32_t)(H * d->d_v); g.head_w = d->d_v; g.col_off = a.dqk_pad;
       r = launch_gemm_nt(g, s);
       if (r != hipSuccess) return r;
     }
@@ -721,7 +728,7 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
   if (e != hipSuccess) return hip_fail(e, "mat_kv");
   e = timed(K_MAT_Q_PREP, s, [&] { return launch_mat_q_prep(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_q_prep");
-  e = timed(K_MAT_ATTEND, s, [&] { return launch_dense_attend(a, s); });
+  e = timed(K_MAT_ATTEND, s, [&] { return launch_mat_attend(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_attend");
   e = timed(K_MAT_MERGE, s, [&] { return launch_dense_merge(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_merge");

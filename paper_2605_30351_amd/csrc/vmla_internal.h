@@ -136,6 +136,8 @@ hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s);
 hipError_t launch_mat_q_prep(const AttendArgs& a, hipStream_t s);
+hipError_t launch_mat_attend(const AttendArgs& a, hipStream_t s);
+bool mat_attend_supported(int d_k, int d_v);
 hipError_t launch_mat_rope_fill(const AttendArgs& a, uint16_t* kv, hipStream_t s);
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
 hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat, hipStream_t s);

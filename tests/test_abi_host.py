@@ -148,10 +148,11 @@ def test_dc_sweep_shapes():
 
 
 def test_materialized_attend_validation():
-    """The materialized form needs the dense kernel's head width: d_nope + d_rope = d_v = 128
-    (the paper's 96 + 32), no sink."""
+    """The materialized form is built for d_v = 128 with keys of d_nope + d_rope = 128 (the
+    paper's 96 + 32) or 160 (128 + 32), no sink."""
     assert vm.attend_materialized_workspace_bytes(WAN_PAPER, 1) > 0
-    assert vm.attend_materialized_workspace_bytes(WAN, 1) == 0       # 128 + 32 != 128
+    assert vm.attend_materialized_workspace_bytes(WAN, 1) > 0
+    assert vm.attend_materialized_workspace_bytes(WAN.replace(d_nope=112), 1) == 0
     mat = L.raw().videomla_attend_materialized
 
     def call(d, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
@@ -159,7 +160,7 @@ def test_materialized_attend_validation():
         return mat(ctypes.byref(d), ctypes.byref(w), 1, q, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                    ws, ws_bytes, None)
     d = L.make_dims(WAN_PAPER)
-    assert call(L.make_dims(WAN)) == L.EUNSUPPORTED
+    assert call(_dims_struct(WAN, d_nope=112)) == L.EUNSUPPORTED
     assert call(_dims_struct(WAN_PAPER, sink_frames=1, window_frames=7)) == L.EUNSUPPORTED
     assert call(d, q=None) == L.EINVAL
     assert call(d, q=MISALIGNED) == L.EALIGN
@@ -168,6 +169,7 @@ def test_materialized_attend_validation():
     assert call(d, ws_bytes=need - 1) == L.EWORKSPACE
     # the reconstructed rows dominate: ring x heads x (K_h | V_h) in bf16
     assert need >= 32760 * 12 * 256 * 2
+    assert vm.attend_materialized_workspace_bytes(WAN, 1) >= 32760 * 12 * 288 * 2
 
 
 def test_attend_rejects_bad_args():

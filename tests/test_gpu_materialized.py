@@ -1,7 +1,8 @@
 """GPU parity of the materialized-K/V attention (videomla_attend_materialized: per-head keys
 and values reconstructed from the latent ring, then standard attention) against the fp64
 oracle, whose reference is that same training form. Bars as in tests/test_gpu_parity.py.
-The paper's head split is required: d_nope + d_rope = d_v = 128."""
+Both head splits it is built for: the paper's d_nope 96 + d_rope 32 (keys as wide as the
+128-wide values) and d_nope 128 + d_rope 32 (160-wide keys)."""
 import numpy as np
 import pytest
 import torch
@@ -23,14 +24,14 @@ def vm():
 
 from oracle import videomla_oracle as O  # noqa: E402
 from tests.gpu_common import Layer, assert_attention_close, sample_rows  # noqa: E402
-from workloads import SMALL_PAPER, WAN_PAPER, make_layer_inputs  # noqa: E402
+from workloads import SMALL, SMALL_PAPER, WAN, WAN_PAPER, make_layer_inputs  # noqa: E402
 
 
-def test_small_every_output(vm):
+@pytest.mark.parametrize("dims", [SMALL_PAPER, SMALL], ids=["nope96", "nope128"])
+def test_small_every_output(vm, dims):
     """Every output of a 7-chunk rollout (partial windows, ring wrap, ragged last key tile),
     batch 2, 1, 3, 7 and the default number of workgroups, against the oracle and against the
     latent path on the same ring."""
-    dims = SMALL_PAPER
     inp = make_layer_inputs(dims, seed=60, n_frames=14, batch=2)
     layer = Layer(vm, inp, packed=True)
     for fe in range(0, 14, dims.chunk_frames):
@@ -46,12 +47,13 @@ def test_small_every_output(vm):
         vm.set_attend_workgroups(0)
 
 
-def test_wan_paper_dims(vm):
-    """Wan geometry with the paper's head split: the chunk alone (frame 0) and the wrapped
-    32,760-key window (frames 3..23), sampled rows."""
-    inp = make_layer_inputs(WAN_PAPER, seed=61, n_frames=24)
+@pytest.mark.parametrize("dims", [WAN_PAPER, WAN], ids=["nope96", "nope128"])
+def test_wan_geometry(vm, dims):
+    """Wan geometry: the chunk alone (frame 0) and the wrapped 32,760-key window (frames
+    3..23), sampled rows."""
+    inp = make_layer_inputs(dims, seed=61, n_frames=24)
     layer = Layer(vm, inp, packed=True)
-    rows = sample_rows(WAN_PAPER.chunk_tokens, k=24, seed=5)
+    rows = sample_rows(dims.chunk_tokens, k=24, seed=5)
     layer.write(0)
     got = layer.attend(0, materialized=True)
     assert_attention_close(got[0][rows], O.chunk_attention(inp, 0, 0, rows=rows), "wan fe=0")
