@@ -105,7 +105,7 @@ typedef struct videomla_window {
  * untouched. With a sink, k_r receives the unrotated W_R^K x. Calling it again
  * before videomla_window_advance (the next denoising step) overwrites the same slots.
  * Requires d_model % 64 == 0, d_model <= 2048, d_c % 16 == 0, d_rope % 8 == 0,
- * d_c + d_rope <= 288.
+ * d_c + d_rope <= 288 (videomla_cache_write_prepared below takes up to 576).
  */
 int videomla_cache_write(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                          const uint16_t* x, const uint16_t* w_dkv, const uint16_t* w_kr,
@@ -125,7 +125,8 @@ int videomla_cache_write(const videomla_dims* dims, const videomla_window* win, 
  *   videomla_write_weights_bytes() bytes, 16-byte aligned. Enqueued on `stream`.
  * videomla_cache_write_prepared -- videomla_cache_write with w_packed (as written by
  *   videomla_prepare_write_weights for the same d_model, d_c and d_rope) in place of w_dkv and
- *   w_kr. Same arguments, requirements and errors otherwise.
+ *   w_kr. Same arguments, requirements and errors otherwise, except that d_c + d_rope may be
+ *   up to 576 (the d_c = 512 latent of the paper's sweep).
  */
 size_t videomla_write_weights_bytes(const videomla_dims* dims);
 int videomla_prepare_write_weights(const videomla_dims* dims, const uint16_t* w_dkv,
@@ -162,8 +163,8 @@ size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch)
  *   workspace  device buffer of at least videomla_attend_workspace_bytes() bytes
  * Arithmetic: bf16 operands, fp32 accumulation and softmax, bf16 round-to-nearest-even output.
  * Requires d_nope % 16 == 0 and d_nope <= 128, d_v % 32 == 0 and d_v <= 256,
- * (d_c, d_rope) in {(192, 32), (16, 8)},
- * otherwise VIDEOMLA_EUNSUPPORTED.
+ * (d_c, d_rope) in {(64, 32), (128, 32), (192, 32), (256, 32), (512, 32), (16, 8)} (the widths
+ * of the paper's d_c sweep, Table 5, and a tiny test shape), otherwise VIDEOMLA_EUNSUPPORTED.
  */
 int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                     const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,

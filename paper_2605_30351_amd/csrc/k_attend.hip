@@ -189,13 +189,20 @@ constexpr float kLazyMax = 8.0f;
 // width, DR = 0, DVW = value width, 0 meaning DC): a tile row is [K_h | V_h] of one head, the
 // scores contract over K_h and V is the rest (the dense comparator: 128 | 128; the materialized
 // form: [W_UK,h c ; k^R] | W_UV,h c = 128 | 128 or 160 | 128).
-template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false, int DVW = 0>
+//
+// Value split (VS = 2, latent rows only): the waves of a pair share their 32 query rows; each
+// computes the same scores and softmax (so both hold identical running max and sum) and the
+// PV product for its half of the value columns. This halves the accumulator registers per
+// wave, at the cost of computing the scores twice, for latent widths whose 32 x d_c fp32
+// accumulators would not fit one wave.
+template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false, int DVW = 0, int VS = 1>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
   static constexpr int DQKP = (DQK + 15) / 16 * 16;
   static constexpr int KSTEPS = DQKP / 16;
   static constexpr int OW = DENSE && DVW ? DVW : DC;  // value (and partial-result) width
   static constexpr int DVB = (OW + 31) / 32;
+  static constexpr int DVBW = DVB / VS;               // value blocks per wave
   static constexpr int KB = BN / 32;       // 32-key blocks per tile
   static constexpr int VOFF = DENSE ? DQKP : 0;  // first V column of a tile row
   // Tile rows have no padding. Rows whose chunk count is a multiple of 16 bank groups (the
@@ -206,7 +213,8 @@ struct AttCfg {
   // enumeration on the host for every layout instantiated here).
   static constexpr int STRIDE = DENSE ? DQKP + OW : DQKP;
   static constexpr int NT = NW * 64;
-  static constexpr int ROWS = NW * QB * 32;
+  static constexpr int ROWS = NW / VS * QB * 32;
+  static_assert(VS == 1 || (!DENSE && DVB % VS == 0 && NW % VS == 0), "value split");
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
   static constexpr int CPR = STRIDE / 8;          // 16-byte chunks per tile row
   static constexpr int NDMA = BN * CPR / 64;      // 1 KB direct-to-LDS loads per tile
@@ -231,9 +239,10 @@ struct AttCfg {
   }
 };
 
-template <int DC, int DR, int QB, int NW, int BN, int WPC, bool DENSE = false, int DVW = 0>
+template <int DC, int DR, int QB, int NW, int BN, int WPC, bool DENSE = false, int DVW = 0,
+          int VS = 1>
 __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const AttendArgs a) {
-  using C = AttCfg<DC, DR, QB, NW, BN, DENSE, DVW>;
+  using C = AttCfg<DC, DR, QB, NW, BN, DENSE, DVW, VS>;
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
 
@@ -261,7 +270,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   u = seg_lo;
   const int b = (int)(rbg / a.row_blocks), rb = (int)(rbg % a.row_blocks);
   const int split = (int)blockIdx.x - attend_owner(rbg * T, U, G);
-  const int row0 = rb * C::ROWS + wave * QB * 32;
+  const int vpar = VS > 1 ? wave % VS : 0;  // value-column half of this wave (value split)
+  const int row0 = rb * C::ROWS + wave / VS * QB * 32;
   const int key_begin = kt0 * BN;
   const int key_end = min(a.n_valid, kt1 * BN);
   const int n_tiles = kt1 - kt0;
@@ -320,14 +330,14 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       q[qb][ks] = as_bf16x8(r < rows_b ? ldg16(src + ks * 16 + 8 * g) : zero);
   }
 
-  f32x16 o[QB][C::DVB];
+  f32x16 o[QB][C::DVBW];
   float m_run[QB], l_run[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     m_run[qb] = kNegInf;
     l_run[qb] = 0.f;
 #pragma unroll
-    for (int d = 0; d < C::DVB; ++d) o[qb][d] = f32x16{};
+    for (int d = 0; d < C::DVBW; ++d) o[qb][d] = f32x16{};
   }
 
   auto dma_tile = [&](int k0, uint16_t* buf) {
@@ -414,7 +424,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
         m_run[qb] = m_new;
         l_run[qb] *= alpha;
 #pragma unroll
-        for (int d = 0; d < C::DVB; ++d) {
+        for (int d = 0; d < C::DVBW; ++d) {
           *slot = o[qb][d];
           asm volatile("" ::: "memory");
           f32x16 tmp = *slot;
@@ -431,8 +441,10 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // column tr_col (+32 d); rows 4g.. have swizzle g, rows 4g+8.. have g+2, for every kk
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int vofs_lo = C::at(4 * g + tr_row, C::VOFF + tr_col);
-  const int vofs_hi = C::at(4 * g + tr_row + 8, C::VOFF + tr_col);
+  // (the latent swizzle permutes chunks within 32-column groups, so a whole number of 32-column
+  // blocks is a plain offset: this wave's value half starts vpar * DVBW blocks in)
+  const int vofs_lo = C::at(4 * g + tr_row, C::VOFF + tr_col) + vpar * C::DVBW * 32;
+  const int vofs_hi = C::at(4 * g + tr_row + 8, C::VOFF + tr_col) + vpar * C::DVBW * 32;
   // dense: the 4-bit XOR also permutes the 32-column blocks d, so one offset per (half, d)
   int vofs_d[2][DENSE ? C::DVB : 1];
   if constexpr (DENSE) {
@@ -459,7 +471,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     dma_tile(kbase + 2 * BN, stg);  // buffer of tile t-1, free since the last barrier
     static_assert(C::KB == 1, "the step is laid out for 32-key tiles");
     constexpr int NS = C::KSTEPS;
-    constexpr int NPV = 2 * C::DVB;  // PV operand reads per tile (each feeds QB MFMAs)
+    constexpr int NPV = 2 * C::DVBW;  // PV operand reads per tile (each feeds QB MFMAs)
     constexpr int NSLOT = NS > NPV + 2 ? NS : NPV + 2;
     constexpr int NSM = NS < 4 ? NS : 4;  // slots carrying the softmax; pairs 0-3 precede PV
     auto kread = [&](int ks) {
@@ -467,8 +479,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     };
     const lds_u16* vlo = as_lds(cur) + vofs_lo;
     const lds_u16* vhi = as_lds(cur) + vofs_hi;
-    auto vread = [&](int j) {  // A operand of PV MFMA j: kk = j / DVB, d = j % DVB
-      const int kk = j / C::DVB, d = j % C::DVB;
+    auto vread = [&](int j) {  // A operand of PV MFMA j: kk = j / DVBW, d = j % DVBW
+      const int kk = j / C::DVBW, d = j % C::DVBW;
       if constexpr (DENSE)
         return join_bf16x8(lds_read_tr(as_lds(cur) + vofs_d[0][d] + kk * 16 * C::STRIDE),
                            lds_read_tr(as_lds(cur) + vofs_d[1][d] + kk * 16 * C::STRIDE));
@@ -512,7 +524,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
           for (int p = ks * 8 / NSM; p < (ks + 1) * 8 / NSM; ++p) sm_pair(qb, p);
       }
       if (j >= 0 && j < NPV) {
-        const int kk = j / C::DVB, d = j % C::DVB;
+        const int kk = j / C::DVBW, d = j % C::DVBW;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
           const bf16x8 pb = as_bf16x8(kk == 0 ? u32x4{pk[qb][0], pk[qb][1], pk[qb][2], pk[qb][3]}
@@ -571,16 +583,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     const size_t grow_i = (size_t)b * rows_b + r;
     float* op = a.o_part + ((size_t)split * total_rows + grow_i) * C::OW;
 #pragma unroll
-    for (int d = 0; d < C::DVB; ++d)
+    for (int d = 0; d < C::DVBW; ++d)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int c = d * 32 + 8 * i + 4 * g;
+        const int c = (vpar * C::DVBW + d) * 32 + 8 * i + 4 * g;
         if (c < C::OW) {
           const f32x4 v = {o[qb][d][4 * i], o[qb][d][4 * i + 1], o[qb][d][4 * i + 2], o[qb][d][4 * i + 3]};
           *reinterpret_cast<f32x4*>(op + c) = v;
         }
       }
-    if (g == 0) {
+    if (g == 0 && vpar == 0) {
       float* ml = a.ml_part + ((size_t)split * total_rows + grow_i) * 2;
       ml[0] = m_run[qb];
       ml[1] = l_tot;
@@ -702,23 +714,26 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
 template <int DC, int DR> struct AttShape;
 // WPC = resident workgroups per CU (the grid is WPC workgroups per CU). Two 4-wave workgroups
 // per CU measured 6% slower than one 8-wave workgroup at the Wan shape.
-template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
-template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1; };
+template <> struct AttShape<192, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1, VS = 1; };
+template <> struct AttShape<16, 8> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1, VS = 1; };
 // the latent widths of the paper's d_c sweep (Table 5), with the same 32-wide RoPE key
-template <> struct AttShape<64, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
-template <> struct AttShape<128, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1; };
+template <> struct AttShape<64, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1, VS = 1; };
+template <> struct AttShape<128, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1, VS = 1; };
 // d_c = 256: 32 rows x 256 fp32 accumulators per wave need one wave per SIMD (8 waves spill)
-template <> struct AttShape<256, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1; };
+template <> struct AttShape<256, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1, VS = 1; };
+// d_c = 512: wave pairs split the value columns (256 each), one wave per SIMD
+template <> struct AttShape<512, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1, VS = 2; };
 
 // Every (d_c, d_rope) the latent path is instantiated for.
-#define VMLA_LATENT_SHAPES(X) X(192, 32) X(16, 8) X(64, 32) X(128, 32) X(256, 32)
+#define VMLA_LATENT_SHAPES(X) X(192, 32) X(16, 8) X(64, 32) X(128, 32) X(256, 32) X(512, 32)
 
 template <int DC, int DR>
 hipError_t launch_attend_t(const AttendArgs& a, hipStream_t s) {
   using S = AttShape<DC, DR>;
-  using C = AttCfg<DC, DR, S::QB, S::NW, S::BN>;
+  using C = AttCfg<DC, DR, S::QB, S::NW, S::BN, false, 0, S::VS>;
   const dim3 grid(a.n_wg);
-  hipLaunchKernelGGL((latent_attend_kernel<DC, DR, S::QB, S::NW, S::BN, S::WPC>), grid, dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((latent_attend_kernel<DC, DR, S::QB, S::NW, S::BN, S::WPC, false, 0, S::VS>),
+                     grid, dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -758,7 +773,8 @@ hipError_t launch_mat_attend(const AttendArgs& a, hipStream_t s) {
 }
 
 template <int DC, int DR> using ShapeCfg =
-    AttCfg<DC, DR, AttShape<DC, DR>::QB, AttShape<DC, DR>::NW, AttShape<DC, DR>::BN>;
+    AttCfg<DC, DR, AttShape<DC, DR>::QB, AttShape<DC, DR>::NW, AttShape<DC, DR>::BN, false, 0,
+           AttShape<DC, DR>::VS>;
 
 bool latent_attend_supported(int d_c, int d_rope) {
 #define X(DC, DR) if (d_c == DC && d_rope == DR) return true;

@@ -36,7 +36,7 @@ namespace vmla {
 namespace {
 
 constexpr int kTokTile = 32;   // token rows of the resident x tile: two 16-token MFMA blocks
-constexpr int kMaxWaves = 9;   // d_c + d_rope <= 288
+constexpr int kMaxWaves = 9;   // d_c + d_rope <= 288 with 32 outputs per wave, 576 with 64
 
 // D(16x16) += A(16x32) B(32x16). Lane l holds A[l%16][8(l/16) .. +8], B[8(l/16) .. +8][l%16];
 // accumulator element i of lane l is D[4(l/16) + i][l%16].
@@ -52,10 +52,10 @@ __device__ __forceinline__ int xpos(int b, int t, int cc, int rows_pad) {
   return (b * rows_pad + t) * 8 + (cc ^ ((t >> 1) & 7));
 }
 
-// One wave per 32 outputs of d_c + d_rope. KPRE (weight k-steps of 32 columns in flight per
-// wave) divides d_model / 32, so the steady-state loop issues its loads unconditionally and
-// the compiler can count the outstanding loads exactly.
-template <int KPRE>
+// One wave per 16 OB outputs of d_c + d_rope (OB = 2, or 4 beyond 288 outputs). KPRE (weight
+// k-steps of 32 columns in flight per wave) divides d_model / 32, so the steady-state loop
+// issues its loads unconditionally and the compiler can count the outstanding loads exactly.
+template <int KPRE, int OB>
 __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(const WriteArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t xs[kTokTile * kMaxWriteDModel];
   __shared__ float ssq_part[kMaxWaves][kTokTile];
@@ -75,11 +75,13 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   const int ngrp = rows_pad / 8;                 // direct loads per column block
 
   // RMSNorm gain of this lane's outputs 32 wave + 16 ob + 4q .. +3, fetched first
-  u32x2 gam[2] = {{0u, 0u}, {0u, 0u}};
+  constexpr int OPW = 16 * OB;  // outputs per wave
+  u32x2 gam[OB];
   if (a.gamma) {
 #pragma unroll
-    for (int ob = 0; ob < 2; ++ob) {
-      const int o = 32 * wave + 16 * ob + 4 * q;
+    for (int ob = 0; ob < OB; ++ob) {
+      const int o = OPW * wave + 16 * ob + 4 * q;
+      gam[ob] = u32x2{0u, 0u};
       if (o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
     }
   }
@@ -113,13 +115,13 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
 
   // ---- this wave's packed panel: k-step k holds its two A operands (outputs 32 wave + 16 ob
   // + r, columns 32k + 8q ..) as 2 KB contiguous, lane-ordered ------------------------------
-  const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * 2) * 512 + lane * 8;
-  u32x4 wb[KPRE][2];
+  const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * OB) * 512 + lane * 8;
+  u32x4 wb[KPRE][OB];
 #pragma unroll
   for (int j = 0; j < KPRE; ++j) {
     const int k = kstep(j);
 #pragma unroll
-    for (int ob = 0; ob < 2; ++ob) wb[j][ob] = ldg16(wpan + (2 * k + ob) * 512);
+    for (int ob = 0; ob < OB; ++ob) wb[j][ob] = ldg16(wpan + (OB * k + ob) * 512);
   }
   // while the first loads are in flight: each token's ring row (and slot), and the RoPE angles
   // with the pair index uniform across a wave, so that the angle table is read by scalar loads
@@ -140,19 +142,19 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
       rope_cs[lane][pr] = f32x2{u, w};
     }
   }
-  // loads complete in issue order: once at most the 2 KPRE weight loads issued after them are
+  // loads complete in issue order: once at most the OB KPRE weight loads issued after them are
   // outstanding, this wave's first-phase x loads (and the gain) have landed
-  wait_vmcnt<2 * KPRE>();
+  wait_vmcnt<OB * KPRE>();
   __syncthreads();
 
-  f32x4 acc[2][2];  // [output block][token block]
+  f32x4 acc[OB][2];  // [output block][token block]
 #pragma unroll
-  for (int ob = 0; ob < 2; ++ob)
+  for (int ob = 0; ob < OB; ++ob)
 #pragma unroll
     for (int tb = 0; tb < 2; ++tb) acc[ob][tb] = f32x4{};
 
   const int tmax = rows_pad - 1;
-  auto mma_step = [&](int i, const u32x4 (&w)[2]) {
+  auto mma_step = [&](int i, const u32x4 (&w)[OB]) {
     const int k = kstep(i);
     const int b = k >> 1, cc = 4 * (k & 1) + q;
     bf16x8 xb[2];
@@ -162,7 +164,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
       xb[tb] = as_bf16x8(*reinterpret_cast<const u32x4*>(&xs[xpos(b, t, cc, rows_pad) * 8]));
     }
 #pragma unroll
-    for (int ob = 0; ob < 2; ++ob)
+    for (int ob = 0; ob < OB; ++ob)
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) acc[ob][tb] = mfma16(as_bf16x8(w[ob]), xb[tb], acc[ob][tb]);
   };
@@ -172,18 +174,18 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
       mma_step(i0 + j, wb[j]);
       const int kn = kstep(i0 + j + KPRE);
 #pragma unroll
-      for (int ob = 0; ob < 2; ++ob) wb[j][ob] = ldg16(wpan + (2 * kn + ob) * 512);
+      for (int ob = 0; ob < OB; ++ob) wb[j][ob] = ldg16(wpan + (OB * kn + ob) * 512);
     }
   };
   // the second phase's loads are issued KPRE k-steps before its first use, after the weight
   // loads of the k-steps that precede it (so that those do not wait for them); at k-step
-  // i_ph1 the 2 KPRE weight loads issued since are the only ones that may still be pending
+  // i_ph1 the OB KPRE weight loads issued since are the only ones that may still be pending
   int i0 = 0;
   for (; i0 < i_dma1; i0 += KPRE) steady(i0);
   if (i_ph1 > 0) {
     issue_x(i_ph1 / 2, nblk);
     for (; i0 < i_ph1; i0 += KPRE) steady(i0);
-    wait_vmcnt<2 * KPRE>();
+    wait_vmcnt<OB * KPRE>();
     __syncthreads();
   }
   for (; i0 < nks - KPRE; i0 += KPRE) steady(i0);
@@ -191,15 +193,15 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   for (int j = 0; j < KPRE; ++j) mma_step(i0 + j, wb[j]);
 
   // ---- epilogue. Lane (r, q) holds, for token 16 tb + r of the block, outputs
-  // 32 wave + 16 ob + 4q + e (e = 0..3) in acc[ob][tb][e] ----------------------------------
+  // OPW wave + 16 ob + 4q + e (e = 0..3) in acc[ob][tb][e] ---------------------------------
   float ss[2] = {0.f, 0.f};
 #pragma unroll
-  for (int ob = 0; ob < 2; ++ob)
+  for (int ob = 0; ob < OB; ++ob)
 #pragma unroll
     for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int o = 32 * wave + 16 * ob + 4 * q + e;
+        const int o = OPW * wave + 16 * ob + 4 * q + e;
         if (o < DC) ss[tb] += acc[ob][tb][e] * acc[ob][tb][e];
       }
 #pragma unroll
@@ -221,8 +223,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
     for (int w = 0; w < nwave; ++w) tot += ssq_part[w][t];
     const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
 #pragma unroll
-    for (int ob = 0; ob < 2; ++ob) {
-      const int o = 32 * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
+    for (int ob = 0; ob < OB; ++ob) {
+      const int o = OPW * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
       f32x4 v = acc[ob][tb];
       if (o + 4 <= DC) {
         v = v * rstd;
@@ -257,22 +259,23 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
 }
 
 // Packed weight panel for cache_write_packed_kernel: W' = [W_DKV; W_KR; zero rows up to a whole
-// number of 32-row wave slices]. Entry ((w * nks + k) * 2 + ob) * 512 + 8 l + j holds
-// W'[32 w + 16 ob + l % 16][32 k + 8 (l / 16) + j]: the MFMA 16x16x32 A operand of lane l for
+// number of wave slices of 16 OB rows]. Entry ((w * nks + k) * OB + ob) * 512 + 8 l + j holds
+// W'[16 OB w + 16 ob + l % 16][32 k + 8 (l / 16) + j]: the MFMA 16x16x32 A operand of lane l for
 // wave slice w, 16-row block ob and k-step k, so that every load of the kernel reads 1 KB
 // contiguous. One thread per 16-byte entry.
 __global__ __launch_bounds__(256) void pack_write_weights_kernel(const WriteArgs a) {
   const int dm = a.d_model, DC = a.d_c, NO = a.d_c + a.d_rope;
   const int nks = dm / 32;
+  const int OB = write_blocks_per_wave(NO), OPW = 16 * OB;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;  // 16-byte entry
-  const int64_t n_entries = (int64_t)((NO + 31) / 32) * nks * 2 * 64;
+  const int64_t n_entries = (int64_t)((NO + OPW - 1) / OPW) * nks * OB * 64;
   if (e >= n_entries) return;
   const int l = (int)(e & 63);
-  const int64_t blk = e >> 6;  // (w * nks + k) * 2 + ob
-  const int ob = (int)(blk & 1);
-  const int64_t wk = blk >> 1;
+  const int64_t blk = e >> 6;  // (w * nks + k) * OB + ob
+  const int ob = (int)(blk % OB);
+  const int64_t wk = blk / OB;
   const int k = (int)(wk % nks), w = (int)(wk / nks);
-  const int o = 32 * w + 16 * ob + (l & 15);
+  const int o = OPW * w + 16 * ob + (l & 15);
   const int col = 32 * k + 8 * (l >> 4);
   u32x4 v = {0u, 0u, 0u, 0u};
   if (o < DC) v = ldg16(a.w_dkv + (size_t)o * dm + col);
@@ -454,7 +457,8 @@ int cache_write_tokens_per_wg(int64_t tokens, int n_cu) {
 }
 
 size_t write_weights_packed_elems(int d_model, int d_c, int d_rope) {
-  return (size_t)((d_c + d_rope + 31) / 32) * (d_model / 32) * 2 * 512;
+  const int ob = write_blocks_per_wave(d_c + d_rope), opw = 16 * ob;
+  return (size_t)((d_c + d_rope + opw - 1) / opw) * (d_model / 32) * ob * 512;
 }
 
 hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s) {
@@ -467,18 +471,26 @@ hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s) {
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s) {
   if (!a.w_packed) return launch_cache_write_staged(a, s);
   // validated by the caller: d_model % 64 == 0, d_model <= kMaxWriteDModel, d_c % 16 == 0,
-  // d_rope % 8 == 0, d_c + d_rope <= 288, 1 <= tok_per_wg <= 32
-  const int nw = (a.d_c + a.d_rope + 31) / 32;
+  // d_rope % 8 == 0, d_c + d_rope <= 576, 1 <= tok_per_wg <= 32
+  const int ob = write_blocks_per_wave(a.d_c + a.d_rope);
+  const int nw = (a.d_c + a.d_rope + 16 * ob - 1) / (16 * ob);
   const int nks = a.d_model / 32;  // even
   const int64_t M = (int64_t)a.batch * a.geo.chunk_tokens;
   const dim3 grid((unsigned)((M + a.tok_per_wg - 1) / a.tok_per_wg)), block(nw * 64);
   if (nw > kMaxWaves) return hipErrorInvalidValue;
-  if (nks % 12 == 0)
-    hipLaunchKernelGGL(cache_write_packed_kernel<12>, grid, block, 0, s, a);
-  else if (nks % 8 == 0)
-    hipLaunchKernelGGL(cache_write_packed_kernel<8>, grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL(cache_write_packed_kernel<2>, grid, block, 0, s, a);
+  if (ob == 2) {
+    if (nks % 12 == 0)
+      hipLaunchKernelGGL((cache_write_packed_kernel<12, 2>), grid, block, 0, s, a);
+    else if (nks % 8 == 0)
+      hipLaunchKernelGGL((cache_write_packed_kernel<8, 2>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((cache_write_packed_kernel<2, 2>), grid, block, 0, s, a);
+  } else {  // 64 outputs per wave: fewer k-steps in flight keep the register count in bounds
+    if (nks % 4 == 0)
+      hipLaunchKernelGGL((cache_write_packed_kernel<4, 4>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((cache_write_packed_kernel<2, 4>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 

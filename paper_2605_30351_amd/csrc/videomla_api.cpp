@@ -305,7 +305,7 @@ int check_attend_shape(const videomla_dims* d) {
   if (!latent_attend_supported(d->d_c, d->d_rope))
     return fail(VIDEOMLA_EUNSUPPORTED,
                 "attention kernel is built for (d_c, d_rope) in {(64,32),(128,32),(192,32),"
-                "(256,32),(16,8)}, got (%d,%d)",
+                "(256,32),(512,32),(16,8)}, got (%d,%d)",
                 d->d_c, d->d_rope);
   if (d->d_nope % 16 || d->d_nope > 128)
     return fail(VIDEOMLA_EUNSUPPORTED, "d_nope must be a multiple of 16 and <= 128, got %d", d->d_nope);
@@ -368,7 +368,8 @@ int check_write_dims(const videomla_dims* d) {
     return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be <= %d for the cache write, got %d", kMaxWriteDModel, d->d_model);
   if (d->d_c % 16) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 16, got %d", d->d_c);
   if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
-  if (d->d_c + d->d_rope > 288) return fail(VIDEOMLA_EUNSUPPORTED, "d_c + d_rope must be <= 288");
+  if (d->d_c + d->d_rope > kMaxWriteOutPacked)
+    return fail(VIDEOMLA_EUNSUPPORTED, "d_c + d_rope must be <= %d", kMaxWriteOutPacked);
   return 0;
 }
 
@@ -379,6 +380,10 @@ int cache_write_common(const videomla_dims* d, const videomla_window* w, int32_t
                        const uint16_t* w_packed, const uint16_t* kv_norm_w, uint16_t* c_kv,
                        uint16_t* k_r, int32_t* slots_out, void* stream) {
   if (int e = check_write_dims(d)) return e;
+  if (!w_packed && d->d_c + d->d_rope > kMaxWriteOutPlain)
+    return fail(VIDEOMLA_EUNSUPPORTED,
+                "d_c + d_rope must be <= %d for the plain-weight cache write (the packed-weight "
+                "one takes up to %d)", kMaxWriteOutPlain, kMaxWriteOutPacked);
   if (int e = check_window(w)) return e;
   if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
   if ((int64_t)batch * d->chunk_frames * d->grid_h * d->grid_w >= ((int64_t)1 << 31))

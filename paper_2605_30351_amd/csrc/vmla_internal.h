@@ -8,6 +8,11 @@ namespace vmla {
 
 constexpr int kMaxRopePairs = 64;  // a whole dense head of 128 channels
 constexpr int kMaxWriteDModel = 2048;  // cache write: 32 resident x rows of d_model fill 128 KB of LDS
+constexpr int kMaxWriteOutPlain = 288;   // d_c + d_rope of the plain-weight cache write
+constexpr int kMaxWriteOutPacked = 576;  // d_c + d_rope of the packed-weight cache write
+// 16-row output blocks per wave of the packed-weight cache write: 2 (32 outputs) up to 288
+// outputs, else 4 (64 outputs), so that at most 9 waves cover d_c + d_rope
+__host__ __device__ inline int write_blocks_per_wave(int outputs) { return outputs <= kMaxWriteOutPlain ? 2 : 4; }
 
 // Per RoPE pair p (interleaved channels 2p, 2p+1 of the d_rope vector): the axis whose
 // coordinate drives it (0 = t, 1 = h, 2 = w) and theta = base^(-2k / D_axis), in double.

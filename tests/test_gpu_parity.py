@@ -103,21 +103,23 @@ def test_wan_cache_write_evicts_oldest_frames(vm, packed):
 
 def test_packed_weight_panel_layout(vm):
     """Every 16-byte entry of the packed panel is the documented slice of [W_DKV; W_KR; 0]:
-    entry ((w * nks + k) * 2 + ob) * 64 + l holds row 32 w + 16 ob + l % 16, columns
-    32 k + 8 (l / 16) .. +8 (bitwise, for both the tiny and the Wan shapes)."""
-    for dims in (TINY, WAN):
+    with OB 16-row blocks per wave slice (2, or 4 beyond 288 outputs), entry
+    ((w * nks + k) * OB + ob) * 64 + l holds row 16 OB w + 16 ob + l % 16, columns
+    32 k + 8 (l / 16) .. +8 (bitwise, for the tiny, the Wan and the d_c = 512 shapes)."""
+    for dims in (TINY, WAN, WAN.replace(d_c=512)):
         inp = make_layer_inputs(dims, seed=3, n_frames=dims.chunk_frames)
         layer = Layer(vm, inp, packed=True)
         torch.cuda.synchronize()
         got = host_bits(layer.w_packed.view(torch.bfloat16)).reshape(-1, 8)
         nks, no = dims.d_model // 32, dims.d_c + dims.d_rope
-        nw = (no + 31) // 32
-        panel = np.zeros((32 * nw, dims.d_model), np.uint16)
+        OB = 2 if no <= 288 else 4
+        nw = (no + 16 * OB - 1) // (16 * OB)
+        panel = np.zeros((16 * OB * nw, dims.d_model), np.uint16)
         panel[:dims.d_c], panel[dims.d_c:no] = inp.w_dkv, inp.w_kr
-        e = np.arange(nw * nks * 2 * 64)
+        e = np.arange(nw * nks * OB * 64)
         lane, blk = e % 64, e // 64
-        ob, k, w = blk % 2, (blk // 2) % nks, blk // 2 // nks
-        rows = 32 * w + 16 * ob + lane % 16
+        ob, k, w = blk % OB, (blk // OB) % nks, blk // OB // nks
+        rows = 16 * OB * w + 16 * ob + lane % 16
         cols = 32 * k + 8 * (lane // 16)
         want = panel[rows[:, None], cols[:, None] + np.arange(8)]
         assert np.array_equal(got, want)
