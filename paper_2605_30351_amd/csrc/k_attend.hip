@@ -190,16 +190,19 @@ constexpr float kLazyMax = 8.0f;
 // scores contract over K_h and V is the rest (the dense comparator: 128 | 128; the materialized
 // form: [W_UK,h c ; k^R] | W_UV,h c = 128 | 128 or 160 | 128).
 //
-// Value split (VS = 2, latent rows only): the waves of a pair share their 32 query rows; each
-// computes the same scores and softmax (so both hold identical running max and sum) and the
-// PV product for its half of the value columns. This halves the accumulator registers per
-// wave, at the cost of computing the scores twice, for latent widths whose 32 x d_c fp32
-// accumulators would not fit one wave.
+// Pair split (VS = 2, latent rows only): the waves of a pair share their 32 query rows. Each
+// contracts the scores over its half of the [c_kv | k_r] columns, the two partial score tiles
+// are exchanged through LDS at the step's barrier and summed (in the same order of operands on
+// both sides, so both hold bitwise identical scores, running max and sum), and each wave
+// accumulates the PV product for its half of the value columns. This halves the accumulator and
+// query registers per wave, for latent widths whose 32 x d_c fp32 accumulators would not fit
+// one wave, without computing any score twice.
 template <int DC, int DR, int QB, int NW, int BN, bool DENSE = false, int DVW = 0, int VS = 1>
 struct AttCfg {
   static constexpr int DQK = DC + DR;
   static constexpr int DQKP = (DQK + 15) / 16 * 16;
   static constexpr int KSTEPS = DQKP / 16;
+  static constexpr int NSH = KSTEPS / VS;  // score steps of one wave
   static constexpr int OW = DENSE && DVW ? DVW : DC;  // value (and partial-result) width
   static constexpr int DVB = (OW + 31) / 32;
   static constexpr int DVBW = DVB / VS;               // value blocks per wave
@@ -214,7 +217,8 @@ struct AttCfg {
   static constexpr int STRIDE = DENSE ? DQKP + OW : DQKP;
   static constexpr int NT = NW * 64;
   static constexpr int ROWS = NW / VS * QB * 32;
-  static_assert(VS == 1 || (!DENSE && DVB % VS == 0 && NW % VS == 0), "value split");
+  static_assert(VS == 1 || (VS == 2 && !DENSE && DVB % VS == 0 && NW % VS == 0 &&
+                            KSTEPS % VS == 0 && QB == 1 && BN == 32), "pair split");
   static constexpr int OCT_C = DC / 8, OCT_R = DR / 8;
   static constexpr int CPR = STRIDE / 8;          // 16-byte chunks per tile row
   static constexpr int NDMA = BN * CPR / 64;      // 1 KB direct-to-LDS loads per tile
@@ -245,6 +249,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   using C = AttCfg<DC, DR, QB, NW, BN, DENSE, DVW, VS>;
   __shared__ __attribute__((aligned(16))) uint16_t tile[C::NBUF][C::TILE];
   __shared__ __attribute__((aligned(16))) float resc[NW][64 * 16];
+  // pair split: partial score tiles, [tile parity][wave][4 chunks][64 lanes][4]
+  __shared__ __attribute__((aligned(16))) float xch[VS > 1 ? 2 : 1][VS > 1 ? NW : 1][64 * 16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -270,7 +276,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   u = seg_lo;
   const int b = (int)(rbg / a.row_blocks), rb = (int)(rbg % a.row_blocks);
   const int split = (int)blockIdx.x - attend_owner(rbg * T, U, G);
-  const int vpar = VS > 1 ? wave % VS : 0;  // value-column half of this wave (value split)
+  const int vpar = VS > 1 ? wave % VS : 0;  // column half of this wave (pair split)
   const int row0 = rb * C::ROWS + wave / VS * QB * 32;
   const int key_begin = kt0 * BN;
   const int key_end = min(a.n_valid, kt1 * BN);
@@ -319,14 +325,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   }
 
 
-  // queries of this wave, B-operand layout: lane holds row l32, dims ks*16 + 8g .. +8
-  bf16x8 q[QB][C::KSTEPS];
+  // queries of this wave, B-operand layout: lane holds row l32, dims ks*16 + 8g .. +8 (of the
+  // wave's NSH score steps, which start at step vpar * NSH)
+  bf16x8 q[QB][C::NSH];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int r = row0 + qb * 32 + l32;
-    const uint16_t* src = a.qcat + ((size_t)b * rows_b + (r < rows_b ? r : 0)) * C::DQKP;
+    const uint16_t* src = a.qcat + ((size_t)b * rows_b + (r < rows_b ? r : 0)) * C::DQKP +
+                          vpar * C::NSH * 16;
 #pragma unroll
-    for (int ks = 0; ks < C::KSTEPS; ++ks)
+    for (int ks = 0; ks < C::NSH; ++ks)
       q[qb][ks] = as_bf16x8(r < rows_b ? ldg16(src + ks * 16 + 8 * g) : zero);
   }
 
@@ -356,9 +364,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // K operand of step ks: row l32 (+32 kb), chunk 2 ks + g, i.e. C::at(). Latent: the XOR folded
   // into one of two per-lane bases (ks even / odd) so that ks and kb become immediate offsets;
   // dense: one offset per step (its 4-bit XOR reaches every chunk of a group).
+  // With the pair split, local step ks is global step vpar * NSH + ks, whose parity picks the base.
   const int hk = (l32 >> 2) & 3;
-  const int koff_e = l32 * C::STRIDE + ((g ^ hk) << 3);
-  const int koff_o = l32 * C::STRIDE + (((2 + g) ^ hk) << 3) - 16;
+  const int koff_ev = l32 * C::STRIDE + ((g ^ hk) << 3);
+  const int koff_od = l32 * C::STRIDE + (((2 + g) ^ hk) << 3) - 16;
+  const bool kflip = (vpar * C::NSH) & 1;
+  const int koff_e = (kflip ? koff_od : koff_ev) + vpar * C::NSH * 16;
+  const int koff_o = (kflip ? koff_ev : koff_od) + vpar * C::NSH * 16;
   int koff_d[DENSE ? C::KSTEPS : 1];
   if constexpr (DENSE) {
 #pragma unroll
@@ -375,11 +387,36 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) s[qb][kb] = f32x16{};
 #pragma unroll
-      for (int ks = 0; ks < C::KSTEPS; ++ks) {
+      for (int ks = 0; ks < C::NSH; ++ks) {
         const bf16x8 k = as_bf16x8(*reinterpret_cast<const u32x4*>(
             &buf[koff(ks) + kb * 32 * C::STRIDE]));
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) s[qb][kb] = mfma32(k, q[qb][ks], s[qb][kb]);
+      }
+    }
+  };
+  // Pair split: publish this wave's partial scores of tile parity `par` (before a barrier), then
+  // (after it) add the partner's. Chunk j of lane l sits at (64 j + l) * 4 floats, so every
+  // 16-byte access of a wave covers consecutive addresses.
+  auto xch_put = [&](int par, const f32x16 (&s)[QB][C::KB]) {
+    if constexpr (VS > 1) {
+      float* dst = &xch[par][wave][lane * 4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<f32x4*>(dst + 256 * j) =
+            f32x4{s[0][0][4 * j], s[0][0][4 * j + 1], s[0][0][4 * j + 2], s[0][0][4 * j + 3]};
+    }
+  };
+  auto xch_add = [&](int par, f32x16 (&s)[QB][C::KB]) {
+    if constexpr (VS > 1) {
+      const float* src = &xch[par][wave ^ 1][lane * 4];
+      // vpar 0 computes mine + partner's and vpar 1 partner's + mine: the same sum either way
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(src + 256 * j);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          s[0][0][4 * j + i] = vpar == 0 ? s[0][0][4 * j + i] + v[i] : v[i] + s[0][0][4 * j + i];
       }
     }
   };
@@ -470,7 +507,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     // so the wave's LDS traffic and VALU work are spread evenly under its MFMAs.
     dma_tile(kbase + 2 * BN, stg);  // buffer of tile t-1, free since the last barrier
     static_assert(C::KB == 1, "the step is laid out for 32-key tiles");
-    constexpr int NS = C::KSTEPS;
+    constexpr int NS = C::NSH;
     constexpr int NPV = 2 * C::DVBW;  // PV operand reads per tile (each feeds QB MFMAs)
     constexpr int NSLOT = NS > NPV + 2 ? NS : NPV + 2;
     constexpr int NSM = NS < 4 ? NS : 4;  // slots carrying the softmax; pairs 0-3 precede PV
@@ -539,8 +576,10 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       s_nxt[qb][0] = acc[qb];
       l_run[qb] = lsum[qb];
     }
+    xch_put((t + 1) & 1, s_nxt);
     wait_vmcnt<0>();  // this wave's part of tile t+2 is in LDS
     __syncthreads();
+    xch_add((t + 1) & 1, s_nxt);
     if (kbase + 2 * BN > key_end) mask_tail(kbase + BN, s_nxt);  // only near the split's end
     own_max_of(s_nxt);
     raise_max_if_needed();
@@ -554,8 +593,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   __syncthreads();
 
   f32x16 s_a[QB][C::KB], s_b[QB][C::KB];
+  if (n_tiles > 0) scores(tile[0], s_a);
+  if constexpr (VS > 1) {
+    if (n_tiles > 0) xch_put(0, s_a);
+    __syncthreads();
+    if (n_tiles > 0) xch_add(0, s_a);
+  }
   if (n_tiles > 0) {
-    scores(tile[0], s_a);
     if (key_begin + BN > key_end) mask_tail(key_begin, s_a);
     own_max_of(s_a);
     raise_max_if_needed();  // sets the running max from the first tile
@@ -721,7 +765,8 @@ template <> struct AttShape<64, 32> { static constexpr int QB = 1, NW = 8, BN = 
 template <> struct AttShape<128, 32> { static constexpr int QB = 1, NW = 8, BN = 32, WPC = 1, VS = 1; };
 // d_c = 256: 32 rows x 256 fp32 accumulators per wave need one wave per SIMD (8 waves spill)
 template <> struct AttShape<256, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1, VS = 1; };
-// d_c = 512: wave pairs split the value columns (256 each), one wave per SIMD
+// d_c = 512: wave pairs split the score contraction and the value columns (pair split), one
+// wave per SIMD
 template <> struct AttShape<512, 32> { static constexpr int QB = 1, NW = 4, BN = 32, WPC = 1, VS = 2; };
 
 // Every (d_c, d_rope) the latent path is instantiated for.
