@@ -549,7 +549,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       if (ks + 2 < NS) kq[(ks + 2) % 3] = kread(ks + 2);
       const int j = ks - 2;  // PV operand of this slot
       if (j + 1 >= 0 && j + 1 < NPV) vq[(j + 1) & 1] = vread(j + 1);
+      // Issue priority 1 for the first half of the slots, 0 for the second: of the two waves
+      // sharing a SIMD's matrix pipe, the one that is behind wins it more often, so they
+      // finish their streams closer together (the older wave otherwise takes the pipe first
+      // and the younger one ends the step alone, at a lower MFMA rate).
       __builtin_amdgcn_sched_barrier(0);
+      if (ks == 0) __builtin_amdgcn_s_setprio(1);
+      if (ks == NSLOT / 2) __builtin_amdgcn_s_setprio(0);
       if (ks < NS) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) acc[qb] = mfma32(kq[ks % 3], q[qb][ks], acc[qb]);
