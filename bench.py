@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "5639735ea275bc2c2758ff95b3fabf07060ecee220a12a0f3ee1f82b8fab09ab",
-                  "bytes": 308878869}
+                  "sha256": "f4b697e68789265dece3b39d957860660bc9a148a67a66ff36500676abe0ad32",
+                  "bytes": 308002154}
 
 
 def log(msg):

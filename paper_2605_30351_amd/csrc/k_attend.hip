@@ -440,11 +440,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   auto own_max_of = [&](const f32x16 (&s)[QB][C::KB]) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
+      // a tree of three-input maxima (depth 3) rather than a chain of 16
       float m = kNegInf;
 #pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[qb][kb][r]);
+      for (int kb = 0; kb < C::KB; ++kb) {
+        const f32x16& v = s[qb][kb];
+        const float a0 = fmaxf(fmaxf(v[0], v[1]), v[2]), a1 = fmaxf(fmaxf(v[3], v[4]), v[5]);
+        const float a2 = fmaxf(fmaxf(v[6], v[7]), v[8]), a3 = fmaxf(fmaxf(v[9], v[10]), v[11]);
+        const float a4 = fmaxf(fmaxf(v[12], v[13]), v[14]);
+        m = fmaxf(m, fmaxf(fmaxf(fmaxf(a0, a1), a2), fmaxf(fmaxf(a3, a4), v[15])));
+      }
       own_max[qb] = m;
     }
   };
