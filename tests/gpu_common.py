@@ -30,6 +30,13 @@ def ulp_distance(a_bits: np.ndarray, b_bits: np.ndarray) -> np.ndarray:
     return np.abs(ordered(a_bits) - ordered(b_bits))
 
 
+def layer_for(vm, inp, mode, **kw):
+    """Layer whose cache write takes plain ("plain_weights") or packed ("packed_weights")
+    weights."""
+    assert mode in ("plain_weights", "packed_weights"), mode
+    return Layer(vm, inp, packed=mode == "packed_weights", **kw)
+
+
 class Layer:
     """Device copies of one layer's inputs plus its ring."""
 
