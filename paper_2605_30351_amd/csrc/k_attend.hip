@@ -70,9 +70,19 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   for (int c0 = 0; c0 < DCP; c0 += CW) {
     const int cw = DC - c0 < CW ? DC - c0 : CW;  // real columns of this pass
     if (c0 > 0) __syncthreads();                 // the previous pass's reads are done
-    for (int c = tid; c < dn * (cw / 8); c += 256) {
-      const int r = c / (cw / 8), oc = c % (cw / 8);
-      *reinterpret_cast<u32x4*>(&wuk[r * WS + oc * 8]) = ldg16(wsrc + (size_t)r * DC + c0 + oc * 8);
+    {  // every staging load of this thread issued, then stored
+      constexpr int PER = kMaxNope * (CW / 8) / 256;
+      u32x4 wv[PER];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = tid + 256 * i;
+        if (c < dn * (cw / 8)) wv[i] = ldg16(wsrc + (size_t)(c / (cw / 8)) * DC + c0 + (c % (cw / 8)) * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = tid + 256 * i;
+        if (c < dn * (cw / 8)) *reinterpret_cast<u32x4*>(&wuk[(c / (cw / 8)) * WS + (c % (cw / 8)) * 8]) = wv[i];
+      }
     }
     __syncthreads();
 
@@ -657,57 +667,109 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 }
 
 // ---------------------------------------------------------------------------------------------
-// out_proj: grid (ceil(Nq/128), H, B), 4 waves x 32 tokens, one head per workgroup. Each wave
-// handles the rows (token n, head h) of its 32 tokens:
-//   1. merge scale of every row over its key splits s: M = max_s m_s, 1/L with
-//      L = sum_s 2^(m_s - M) l_s
-//   2. o_lat = (1/L) sum_s 2^(m_s - M) O_s, streamed as 16-byte chunks that cover the rows'
-//      partial results contiguously, rounded to bf16 into an LDS tile [32][DC]
-//   3. out^T[v][token] = W_UV_h[v][:] . o_lat[token][:] with MFMA (A = W_UV rows from global
-//      memory, B = o_lat rows from LDS)
+// out_proj: grid (ceil(Nq / (32 NW)), H, B), NW waves x 32 tokens, one head per workgroup.
+// Each wave handles the rows (token n, head h) of its 32 tokens:
+//   1. merge coefficients of every row over its key splits s: M = max_s m_s,
+//      L = sum_s 2^(m_s - M) l_s, coef_s = 2^(m_s - M) / L (kept in LDS for up to kMergeSplits
+//      splits, so that the partial rows' loads below do not wait on per-row scalars)
+//   2. o_lat = sum_s coef_s O_s, streamed as 16-byte chunks that cover the rows' partial results
+//      contiguously, rounded to bf16 into an LDS tile [32][DC]
+//   3. out^T[v][token] = W_UV_h[v][:] . o_lat[token][:] with MFMA (A = W_UV rows, B = o_lat
+//      rows from LDS). Where it fits (WL), W_UV_h is staged in LDS once per workgroup with
+//      whole-line loads, all issued before the first is stored; otherwise every wave reads its
+//      A operands from global memory.
 //   4. the bf16 result is staged through the same LDS tile so that every output row is stored
 //      as whole 16-byte chunks.
 // Lanes of tokens past the chunk work on the chunk's last token and store nothing.
 // ---------------------------------------------------------------------------------------------
-template <int DC, int NVB>  // NVB = d_v / 32
-__global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
+constexpr int kMergeSplits = 4;
+
+template <int DC, int NVB>
+struct OutProjShape {
+  static constexpr int DV = NVB * 32;
+  static constexpr int LS = (DC > DV ? DC : DV) + 8;  // LDS row stride (elements); +16 B per row
+  static constexpr int ROWB = 32 * (4 + 4 + 4 + 4 * kMergeSplits);  // per-wave row scalars
+  static constexpr int BUDGET = 160 * 1024 - 512;
+  static constexpr int need(int nw, bool wl) { return nw * (32 * LS * 2 + ROWB) + (wl ? DV * LS * 2 : 0); }
+  // eight waves with W_UV_h in LDS, else four with it, else four reading it from global memory
+  static constexpr int NW = need(8, true) <= BUDGET ? 8 : 4;
+  static constexpr bool WL = need(NW, true) <= BUDGET;
+};
+
+template <int DC, int NVB, int NW, bool WL>
+__global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   constexpr int KS = DC / 16;
   constexpr int DV = NVB * 32;
-  constexpr int LS = (DC > DV ? DC : DV) + 8;  // LDS row stride (elements); +16 B per row
+  constexpr int LS = OutProjShape<DC, NVB>::LS;
   constexpr int CH = DC / 4;                   // fp32 chunks of 16 B per partial row
+  constexpr int NT = NW * 64;
   static_assert((32 * CH) % 64 == 0 && (32 * DV / 8) % 64 == 0, "whole 64-lane passes");
-  __shared__ __attribute__((aligned(16))) uint16_t tileo[4][32 * LS];
-  __shared__ float row_m[4][32], row_il[4][32];
-  __shared__ int row_ns[4][32];
+  __shared__ __attribute__((aligned(16))) uint16_t tileo[NW][32 * LS];
+  __shared__ __attribute__((aligned(16))) uint16_t wlds[WL ? DV * LS : 8];
+  __shared__ float row_m[NW][32], row_il[NW][32];
+  __shared__ float row_coef[NW][32][kMergeSplits];
+  __shared__ int row_ns[NW][32];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int h = blockIdx.y, b = blockIdx.z;
   const int H = a.n_heads, Nq = a.geo.chunk_tokens;
-  const int n0 = blockIdx.x * 128 + wave * 32;
+  const int n0 = blockIdx.x * (NW * 32) + wave * 32;
   const size_t total_rows = (size_t)a.batch * Nq * H;
   auto row_of = [&](int t) {  // global row of the wave's token t
     const int n = min(n0 + t, Nq - 1);
     return ((size_t)b * Nq + n) * H + h;
   };
   uint16_t* tw = tileo[wave];
+  const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
 
-  // 1. merge scale per row (lanes 0..31, one row each)
+  // 0. W_UV_h [DV][DC] into LDS: every load of this thread issued, then stored
+  if constexpr (WL) {
+    constexpr int CPR = DC / 8, PER = (DV * CPR + NT - 1) / NT;
+    u32x4 wv[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + NT * i;
+      if (c < DV * CPR) wv[i] = ldg16(w + (size_t)(c / CPR) * DC + (c % CPR) * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + NT * i;
+      if (c < DV * CPR) *reinterpret_cast<u32x4*>(&wlds[(c / CPR) * LS + (c % CPR) * 8]) = wv[i];
+    }
+  }
+
+  // 1. merge coefficients per row (lanes 0..31, one row each)
   if (lane < 32) {
     const size_t row = row_of(lane);
     const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
     const int ns = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
                    attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
+    // the (max, sum) pairs of the first kMergeSplits splits, all loads issued together
+    f32x2 ml[kMergeSplits];
+#pragma unroll
+    for (int s = 0; s < kMergeSplits; ++s)
+      ml[s] = s < ns ? *reinterpret_cast<const f32x2*>(a.ml_part + ((size_t)s * total_rows + row) * 2)
+                     : f32x2{kNegInf, 0.f};
     float M = kNegInf;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
+#pragma unroll
+    for (int s = 0; s < kMergeSplits; ++s) M = fmaxf(M, ml[s][0]);
+    for (int s = kMergeSplits; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
     float L = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float* ml = a.ml_part + ((size_t)s * total_rows + row) * 2;
-      L += fast_exp2(ml[0] - M) * ml[1];
+#pragma unroll
+    for (int s = 0; s < kMergeSplits; ++s)
+      if (s < ns) L += fast_exp2(ml[s][0] - M) * ml[s][1];
+    for (int s = kMergeSplits; s < ns; ++s) {
+      const float* p = a.ml_part + ((size_t)s * total_rows + row) * 2;
+      L += fast_exp2(p[0] - M) * p[1];
     }
+    const float il = 1.f / L;
+#pragma unroll
+    for (int s = 0; s < kMergeSplits; ++s)
+      row_coef[wave][lane][s] = s < ns ? fast_exp2(ml[s][0] - M) * il : 0.f;
     row_m[wave][lane] = M;
-    row_il[wave][lane] = 1.f / L;
+    row_il[wave][lane] = il;
     row_ns[wave][lane] = ns;
   }
   __syncthreads();
@@ -718,20 +780,28 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
     const int q = it * 64 + lane;
     const int t = q / CH, k = q % CH;
     const size_t row = row_of(t);
-    const float M = row_m[wave][t], il = row_il[wave][t];
     const int ns = row_ns[wave][t];
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ns; ++s) {
-      const float coef = fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * il;
-      const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
-      acc += coef * v;
+#pragma unroll
+    for (int s = 0; s < kMergeSplits; ++s) {
+      if (s < ns) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
+        acc += row_coef[wave][t][s] * v;
+      }
+    }
+    if (ns > kMergeSplits) {  // rare: more splits than the coefficient table holds
+      const float M = row_m[wave][t], il = row_il[wave][t];
+      for (int s = kMergeSplits; s < ns; ++s) {
+        const float coef = fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * il;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
+        acc += coef * v;
+      }
     }
     *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
   }
-  __syncthreads();
+  __syncthreads();  // the o_lat tiles and (WL) the W_UV_h tile are complete
 
   // 3. out^T = W_UV_h o_lat^T
-  const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
   f32x16 acc[NVB];
 #pragma unroll
   for (int vb = 0; vb < NVB; ++vb) acc[vb] = f32x16{};
@@ -740,7 +810,8 @@ __global__ __launch_bounds__(256) void out_proj_kernel(const AttendArgs a) {
     const bf16x8 bo = as_bf16x8(*reinterpret_cast<const u32x4*>(&tw[l32 * LS + ks * 16 + 8 * g]));
 #pragma unroll
     for (int vb = 0; vb < NVB; ++vb) {
-      const bf16x8 aw = as_bf16x8(ldg16(w + (size_t)(vb * 32 + l32) * DC + ks * 16 + 8 * g));
+      const bf16x8 aw = WL ? as_bf16x8(*reinterpret_cast<const u32x4*>(&wlds[(vb * 32 + l32) * LS + ks * 16 + 8 * g]))
+                           : as_bf16x8(ldg16(w + (size_t)(vb * 32 + l32) * DC + ks * 16 + 8 * g));
       acc[vb] = mfma32(aw, bo, acc[vb]);
     }
   }
@@ -894,21 +965,27 @@ hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+template <int DC, int NVB>
+hipError_t launch_out_proj_v(const AttendArgs& a, hipStream_t s) {
+  using P = OutProjShape<DC, NVB>;
+  const dim3 grid((a.geo.chunk_tokens + 32 * P::NW - 1) / (32 * P::NW), a.n_heads, a.batch);
+  hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL>), grid, dim3(64 * P::NW), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int DC>
 hipError_t launch_out_proj_t(const AttendArgs& a, hipStream_t s) {
-  const dim3 grid((a.geo.chunk_tokens + 127) / 128, a.n_heads, a.batch);
   switch (a.d_v / 32) {
-    case 1: hipLaunchKernelGGL((out_proj_kernel<DC, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((out_proj_kernel<DC, 2>), grid, dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((out_proj_kernel<DC, 3>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((out_proj_kernel<DC, 4>), grid, dim3(256), 0, s, a); break;
-    case 5: hipLaunchKernelGGL((out_proj_kernel<DC, 5>), grid, dim3(256), 0, s, a); break;
-    case 6: hipLaunchKernelGGL((out_proj_kernel<DC, 6>), grid, dim3(256), 0, s, a); break;
-    case 7: hipLaunchKernelGGL((out_proj_kernel<DC, 7>), grid, dim3(256), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((out_proj_kernel<DC, 8>), grid, dim3(256), 0, s, a); break;
+    case 1: return launch_out_proj_v<DC, 1>(a, s);
+    case 2: return launch_out_proj_v<DC, 2>(a, s);
+    case 3: return launch_out_proj_v<DC, 3>(a, s);
+    case 4: return launch_out_proj_v<DC, 4>(a, s);
+    case 5: return launch_out_proj_v<DC, 5>(a, s);
+    case 6: return launch_out_proj_v<DC, 6>(a, s);
+    case 7: return launch_out_proj_v<DC, 7>(a, s);
+    case 8: return launch_out_proj_v<DC, 8>(a, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s) {
