@@ -331,9 +331,13 @@ int videomla_set_attend_workgroups(int32_t n_workgroups);
  * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj",
  * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge", "rope_window", "q_down",
  * "q_up", "latent_merge", "out_mix", "prepare_layer_weights") into
- * *count and *total_ms, and forgets them. Timing state is process-wide and not thread-safe.
+ * *count and *total_ms, and forgets them. videomla_timing_only restricts the bracketing to the
+ * launches of one kernel (NULL: every kernel again), so that a timed loop carries the events of
+ * that kernel only; VIDEOMLA_EINVAL for an unknown name. Timing state is process-wide and not
+ * thread-safe.
  */
 int videomla_timing_enable(int32_t enable);
+int videomla_timing_only(const char* kernel);
 int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms);
 
 #ifdef __cplusplus

@@ -27,6 +27,7 @@ from ._lib import (  # noqa: F401
     set_attend_workgroups,
     slot_of,
     timing_enable,
+    timing_only,
     timing_read,
     valid_tokens,
     window_advance,

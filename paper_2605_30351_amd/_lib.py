@@ -27,7 +27,7 @@ EXPORTED = (
     "videomla_attend_materialized_workspace_bytes", "videomla_attend_materialized",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
-    "videomla_timing_enable", "videomla_timing_read",
+    "videomla_timing_enable", "videomla_timing_only", "videomla_timing_read",
     "videomla_dense_cache_bytes_per_token", "videomla_dense_cache_write",
     "videomla_dense_attend_workspace_bytes", "videomla_dense_attend",
     "videomla_layer_weights_bytes", "videomla_prepare_layer_weights",
@@ -87,6 +87,8 @@ _lib.videomla_set_attend_workgroups.argtypes = [ctypes.c_int32]
 _lib.videomla_set_attend_workgroups.restype = ctypes.c_int
 _lib.videomla_timing_enable.argtypes = [ctypes.c_int32]
 _lib.videomla_timing_enable.restype = ctypes.c_int
+_lib.videomla_timing_only.argtypes = [ctypes.c_char_p]
+_lib.videomla_timing_only.restype = ctypes.c_int
 _lib.videomla_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
                                       ctypes.POINTER(ctypes.c_double)]
 _lib.videomla_timing_read.restype = ctypes.c_int
@@ -381,6 +383,11 @@ def set_attend_workgroups(n: int):
 
 def timing_enable(on: bool = True):
     _check(_lib.videomla_timing_enable(1 if on else 0))
+
+
+def timing_only(kernel: str | None = None):
+    """videomla_timing_only: bracket only this kernel's launches (None: every kernel)."""
+    _check(_lib.videomla_timing_only(None if kernel is None else kernel.encode()))
 
 
 def timing_read(kernel: str) -> tuple[int, float]:

@@ -127,6 +127,7 @@ struct TimingRec {
   hipEvent_t start, stop;
 };
 bool g_timing = false;
+int g_timing_only = -1;  // >= 0: time only this kernel
 std::vector<TimingRec> g_pending;
 std::vector<hipEvent_t> g_event_pool;
 
@@ -137,13 +138,14 @@ hipEvent_t take_event() {
     return e;
   }
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  // timing only: GPU-side intervals on one device, so no system-scope fence (a lighter marker)
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
 template <class F>
 hipError_t timed(int kernel, hipStream_t s, F&& launch) {
-  if (!g_timing) return launch();
+  if (!g_timing || (g_timing_only >= 0 && kernel != g_timing_only)) return launch();
   hipEvent_t e0 = take_event(), e1 = take_event();
   if (!e0 || !e1) return launch();
   hipEventRecord(e0, s);
@@ -858,6 +860,19 @@ int videomla_attend_layer(const videomla_dims* d, const videomla_window* w, int3
 int videomla_timing_enable(int32_t enable) {
   g_timing = enable != 0;
   return ok();
+}
+
+int videomla_timing_only(const char* kernel) {
+  if (!kernel) {
+    g_timing_only = -1;
+    return ok();
+  }
+  for (int k = 0; k < K_COUNT; ++k)
+    if (std::strcmp(kernel, kKernelNames[k]) == 0) {
+      g_timing_only = k;
+      return ok();
+    }
+  return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
 }
 
 int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms) {

@@ -135,6 +135,14 @@ def test_packed_write_weights_size_and_validation():
     assert _write(_dims_struct(WAN, d_model=4096)) == L.EUNSUPPORTED
 
 
+def test_timing_selection():
+    """videomla_timing_only takes the kernel names that videomla_timing_read knows, or NULL."""
+    vm.timing_only("latent_attend")
+    vm.timing_only(None)
+    assert L.raw().videomla_timing_only(b"no_such_kernel") == L.EINVAL
+    assert L.raw().videomla_timing_only(None) == L.OK
+
+
 def test_dc_sweep_shapes():
     """The paper's Table 5 latent widths 64, 128, 192, 256 and 512 are built (with d_rope = 32).
     d_c + d_rope = 544 exceeds the plain-weight cache write (288 outputs): only the packed-weight
