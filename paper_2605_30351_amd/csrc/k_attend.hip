@@ -32,6 +32,9 @@ template <int DC> struct AbsorbChunk {  // W_UK_h columns staged in LDS per pass
   static constexpr int DCP = (DC + 31) / 32 * 32;
   static constexpr int CW = DCP <= 192 ? DCP : 128;
   static_assert(DCP % CW == 0, "whole column chunks");
+  // single pass: the output rows go through an LDS tile (per wave 32 rows of DQKP + 8) that
+  // reuses the W_UK_h area, and are stored whole
+  static constexpr bool STAGE = DCP == CW;
 };
 
 template <int DC, int DR>
@@ -64,6 +67,9 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   for (int ks = 0; ks < KN; ++ks) bq[ks] = as_bf16x8(ok && ks < nks ? ldg16(qn + ks * 16 + 8 * g) : zero);
 
   const uint16_t* wsrc = a.w_uk + (size_t)h * dn * DC;
+  constexpr bool STAGE = AbsorbChunk<DC>::STAGE;
+  constexpr int OS = DQKP + 8;  // output tile row stride (elements)
+  uint16_t* ot = wuk + wave * 32 * OS;
   // tr-read addressing inside a 16-lane group
   const int tr_row = (lane & 15) >> 2;
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -101,7 +107,8 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
         }
       }
     }
-    if (ok) {
+    if (STAGE) __syncthreads();  // every wave is done reading W_UK_h: its area holds the rows
+    if (ok || STAGE) {
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -110,7 +117,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
           if (c < DC) {
             const f32x4 v = {acc[cb][4 * i] * a.qscale, acc[cb][4 * i + 1] * a.qscale,
                              acc[cb][4 * i + 2] * a.qscale, acc[cb][4 * i + 3] * a.qscale};
-            *reinterpret_cast<bf16x4*>(dst + c) = to_bf16x4(v);
+            *reinterpret_cast<bf16x4*>(STAGE ? ot + l32 * OS + c : dst + c) = to_bf16x4(v);
           }
         }
     }
@@ -127,12 +134,26 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
     rope_rotate(a.rope, p, rope_pos(a.geo, token_pos(a.geo, t)), u, v);
     const uint32_t packed =
         (uint32_t)to_bf16_bits(u * a.qscale) | ((uint32_t)to_bf16_bits(v * a.qscale) << 16);
-    *reinterpret_cast<uint32_t*>(a.qcat + r * DQKP + DC + 2 * p) = packed;
+    *reinterpret_cast<uint32_t*>(STAGE ? ot + (t - tok0) * OS + DC + 2 * p
+                                       : a.qcat + r * DQKP + DC + 2 * p) = packed;
   }
   if (DQKP > DC + DR) {
     for (int t = tok0 + lane; t < tok0 + 32 && t < Nq; t += 64) {
       const size_t r = ((size_t)b * Nq + t) * H + h;
-      for (int c = DC + DR; c < DQKP; ++c) a.qcat[r * DQKP + c] = 0;
+      for (int c = DC + DR; c < DQKP; ++c) {
+        if (STAGE) ot[(t - tok0) * OS + c] = 0;
+        else a.qcat[r * DQKP + c] = 0;
+      }
+    }
+  }
+  if constexpr (STAGE) {
+    __syncthreads();  // the wave's rows are complete in its tile
+    constexpr int CPR = DQKP / 8;  // 16-byte chunks per row
+    for (int i = lane; i < 32 * CPR; i += 64) {
+      const int t = i / CPR, k = i - t * CPR;
+      if (tok0 + t < Nq)
+        *reinterpret_cast<u32x4*>(a.qcat + (((size_t)b * Nq + tok0 + t) * H + h) * DQKP + k * 8) =
+            *reinterpret_cast<const u32x4*>(&ot[t * OS + k * 8]);
     }
   }
 }
@@ -676,8 +697,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 //      contiguously, rounded to bf16 into an LDS tile [32][DC]
 //   3. out^T[v][token] = W_UV_h[v][:] . o_lat[token][:] with MFMA (A = W_UV rows, B = o_lat
 //      rows from LDS). Where it fits (WL), W_UV_h is staged in LDS once per workgroup with
-//      whole-line loads, all issued before the first is stored; otherwise every wave reads its
-//      A operands from global memory.
+//      whole-line loads, issued at the start and stored after the merge (their latency passes
+//      under it); otherwise every wave reads its A operands from global memory.
 //   4. the bf16 result is staged through the same LDS tile so that every output row is stored
 //      as whole 16-byte chunks.
 // Lanes of tokens past the chunk work on the chunk's last token and store nothing.
@@ -724,19 +745,14 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   uint16_t* tw = tileo[wave];
   const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
 
-  // 0. W_UV_h [DV][DC] into LDS: every load of this thread issued, then stored
+  // 0. W_UV_h [DV][DC] for LDS: every load of this thread issued now, stored after the merge
+  constexpr int WCPR = DC / 8, WPER = WL ? (DV * WCPR + NT - 1) / NT : 1;
+  u32x4 wv[WPER];
   if constexpr (WL) {
-    constexpr int CPR = DC / 8, PER = (DV * CPR + NT - 1) / NT;
-    u32x4 wv[PER];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
+    for (int i = 0; i < WPER; ++i) {
       const int c = tid + NT * i;
-      if (c < DV * CPR) wv[i] = ldg16(w + (size_t)(c / CPR) * DC + (c % CPR) * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + NT * i;
-      if (c < DV * CPR) *reinterpret_cast<u32x4*>(&wlds[(c / CPR) * LS + (c % CPR) * 8]) = wv[i];
+      if (c < DV * WCPR) wv[i] = ldg16(w + (size_t)(c / WCPR) * DC + (c % WCPR) * 8);
     }
   }
 
@@ -798,6 +814,13 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       }
     }
     *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
+  }
+  if constexpr (WL) {
+#pragma unroll
+    for (int i = 0; i < WPER; ++i) {
+      const int c = tid + NT * i;
+      if (c < DV * WCPR) *reinterpret_cast<u32x4*>(&wlds[(c / WCPR) * LS + (c % WCPR) * 8]) = wv[i];
+    }
   }
   __syncthreads();  // the o_lat tiles and (WL) the W_UV_h tile are complete
 
@@ -931,8 +954,13 @@ int latent_attend_wgs_per_cu(int d_c, int d_rope) {
   return 0;
 }
 
-size_t q_absorb_lds_bytes(int d_c, int d_nope) {
-#define X(DC, DR) if (d_c == DC) return (size_t)d_nope * (AbsorbChunk<DC>::CW + 8) * 2;
+size_t q_absorb_lds_bytes(int d_c, int d_rope, int d_nope) {
+#define X(DC, DR)                                                                      \
+  if (d_c == DC && d_rope == DR) {                                                     \
+    const size_t w = (size_t)d_nope * (AbsorbChunk<DC>::CW + 8);                       \
+    const size_t o = AbsorbChunk<DC>::STAGE ? 4 * 32 * ((DC + DR + 15) / 16 * 16 + 8) : 0; \
+    return (w > o ? w : o) * 2;                                                        \
+  }
   VMLA_LATENT_SHAPES(X)
 #undef X
   return 0;
@@ -940,7 +968,7 @@ size_t q_absorb_lds_bytes(int d_c, int d_nope) {
 
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s) {
   const dim3 grid((a.geo.chunk_tokens + 127) / 128, a.n_heads, a.batch);
-  const size_t lds = q_absorb_lds_bytes(a.d_c, a.d_nope);
+  const size_t lds = q_absorb_lds_bytes(a.d_c, a.d_rope, a.d_nope);
 #define X(DC, DR)                                                                    \
   if (a.d_c == DC && a.d_rope == DR) {                                               \
     hipLaunchKernelGGL((q_absorb_kernel<DC, DR>), grid, dim3(256), lds, s, a);       \

@@ -313,7 +313,7 @@ int check_attend_shape(const videomla_dims* d) {
     return fail(VIDEOMLA_EUNSUPPORTED, "d_nope must be a multiple of 16 and <= 128, got %d", d->d_nope);
   if (d->d_v % 32 || d->d_v > 256)
     return fail(VIDEOMLA_EUNSUPPORTED, "d_v must be a multiple of 32 and <= 256, got %d", d->d_v);
-  if (q_absorb_lds_bytes(d->d_c, d->d_nope) > 64 * 1024)
+  if (q_absorb_lds_bytes(d->d_c, d->d_rope, d->d_nope) > 64 * 1024)
     return fail(VIDEOMLA_EUNSUPPORTED, "d_nope %d too large for the query kernel", d->d_nope);
   return VIDEOMLA_OK;
 }

@@ -150,7 +150,7 @@ hipError_t launch_prepare_weights(const PrepArgs& a, hipStream_t s);
 
 // Shapes the attention kernel is instantiated for.
 bool latent_attend_supported(int d_c, int d_rope);
-size_t q_absorb_lds_bytes(int d_c, int d_nope);
+size_t q_absorb_lds_bytes(int d_c, int d_rope, int d_nope);
 int latent_attend_rows_per_block(int d_c, int d_rope);
 int latent_attend_keys_per_tile(int d_c, int d_rope);
 int latent_attend_wgs_per_cu(int d_c, int d_rope);
