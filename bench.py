@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "1063a283cec0501cebef87c385acadc80f5d1706dda944c249457c3cc83aff99",
-                  "bytes": 308443603}
+                  "sha256": "4ff261cbe52b5d5618d3428ce2a34e8f819ccfc18c38b6ceb6789c2a214b77f0",
+                  "bytes": 307580504}
 
 
 def log(msg):
@@ -118,6 +118,36 @@ def copy_probe(torch, dev, nbytes=1 << 28, reps=3):
         b.copy_(a)
     torch.cuda.synchronize()
     del a, b
+
+
+def timed_steps(vm, torch, step, n, names):
+    """Milliseconds per step from n steps that carry no library timing events, their per-step
+    times, then per-kernel HIP-event averages ({name: {"launches", "avg_us"}}) from a second
+    pass of n steps with every kernel bracketed (each event pair adds a few microseconds)."""
+    import numpy as np
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    marks[0].record()
+    for i in range(n):
+        step(i)
+        marks[i + 1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(n)])
+    vm.timing_enable(True)
+    vm.timing_only(None)
+    for k in names:
+        vm.timing_read(k)
+    for i in range(n):
+        step(i)
+    torch.cuda.synchronize()
+    kernels = {}
+    for k in names:
+        c, tot = vm.timing_read(k)
+        kernels[k] = {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3)}
+    vm.timing_enable(False)
+    return 1e3 * elapsed / n, step_ms, kernels
 
 
 def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
@@ -248,29 +278,12 @@ def sink_chunk_step(args, vm, torch, d, fe=237):
         step(i)
     torch.cuda.synchronize()
     names = ("cache_write", "q_absorb", "rope_window", "latent_attend", "out_proj")
-    vm.timing_enable(True)
-    for k in names:
-        vm.timing_read(k)
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    marks[0].record()
-    for i in range(args.steps):
-        step(i)
-        marks[i + 1].record()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
-    kernels = {}
-    for k in names:
-        n, tot = vm.timing_read(k)
-        kernels[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 3)}
-    vm.timing_enable(False)
+    ms, step_ms, kernels = timed_steps(vm, torch, step, args.steps, names)
     S = vm.valid_tokens(d, fe)
     rows = nq * d.n_heads
     attend_core = rows * S * (2 * (d.d_c + d.d_rope) + 2 * d.d_c)
     attend_flop = attend_core + rows * 2 * (d.d_nope * d.d_c + d.d_c * d.d_v)
     write_flop = nq * 2 * d.d_model * (d.d_c + d.d_rope)
-    ms = 1e3 * elapsed / args.steps
     k3 = kernels["latent_attend"]["avg_us"] / 1e6
     print(json.dumps({
         "metric": "ms/chunk-step & TFLOP/s, sink frame + 6-frame local window (window-local RoPE)",
@@ -335,23 +348,7 @@ def full_layer_chunk_step(args, vm, torch, d, d_q=768, fe=21):
         step(i)
     torch.cuda.synchronize()
     names = ("cache_write", "q_down", "q_up", "latent_attend", "latent_merge", "out_mix")
-    vm.timing_enable(True)
-    for k in names:
-        vm.timing_read(k)
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    marks[0].record()
-    for i in range(args.steps):
-        step(i)
-        marks[i + 1].record()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
-    kernels = {}
-    for k in names:
-        n, tot = vm.timing_read(k)
-        kernels[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 3)}
-    vm.timing_enable(False)
+    ms, step_ms, kernels = timed_steps(vm, torch, step, args.steps, names)
     S = d.window_tokens
     rows = nq * H
     flop = {"cache_write": nq * 2 * d.d_model * (d.d_c + d.d_rope),
@@ -361,7 +358,6 @@ def full_layer_chunk_step(args, vm, torch, d, d_q=768, fe=21):
             "out_mix": nq * 2 * H * d.d_c * d.d_model}
     for k, f in flop.items():
         kernels[k]["tflops"] = round(f / (kernels[k]["avg_us"] / 1e6) / 1e12, 1)
-    ms = 1e3 * elapsed / args.steps
     print(json.dumps({
         "metric": "ms/chunk-step & TFLOP/s, whole attention layer in latent form (x -> W_O output)",
         "value": round(sum(flop.values()) / (ms / 1e3) / 1e12, 2), "unit": "TFLOP/s",
@@ -567,21 +563,8 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
     torch.cuda.synchronize()
     names = (("cache_write", "mat_kv", "mat_q_prep", "mat_attend", "mat_merge") if materialized
              else ("cache_write", "q_absorb", "latent_attend", "out_proj"))
-    vm.timing_enable(True)
-    for k in names:
-        vm.timing_read(k)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record()
-    for i in range(steps):
-        step(i)
-    ev1.record()
-    torch.cuda.synchronize()
-    kernels = {}
-    for k in names:
-        n, tot = vm.timing_read(k)
-        kernels[k] = round(1e3 * tot / max(n, 1), 3)
-    vm.timing_enable(False)
-    return ev0.elapsed_time(ev1) / steps, kernels
+    ms, _, kernels = timed_steps(vm, torch, step, steps, names)
+    return ms, {k: v["avg_us"] for k, v in kernels.items()}
 
 
 def latent_vs_materialized(args, vm, torch):
