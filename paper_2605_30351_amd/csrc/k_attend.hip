@@ -712,9 +712,13 @@ struct OutProjShape {
   static constexpr int ROWB = 32 * (4 + 4 + 4 + 4 * kMergeSplits);  // per-wave row scalars
   static constexpr int BUDGET = 160 * 1024 - 512;
   static constexpr int need(int nw, bool wl) { return nw * (32 * LS * 2 + ROWB) + (wl ? DV * LS * 2 : 0); }
-  // eight waves with W_UV_h in LDS, else four with it, else four reading it from global memory
+  // the most waves per workgroup (8, else 4) that fit with W_UV_h in LDS, else 4 reading it
+  // from global memory; fewer waves (down to 2) are launched when the grid would otherwise
+  // leave most compute units idle
   static constexpr int NW = need(8, true) <= BUDGET ? 8 : 4;
   static constexpr bool WL = need(NW, true) <= BUDGET;
+  static constexpr bool WL4 = need(4, true) <= BUDGET;
+  static constexpr bool WL2 = need(2, true) <= BUDGET;
 };
 
 template <int DC, int NVB, int NW, bool WL>
@@ -993,11 +997,29 @@ hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+int out_proj_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+    return n;
+  return 256;
+}
+
 template <int DC, int NVB>
 hipError_t launch_out_proj_v(const AttendArgs& a, hipStream_t s) {
   using P = OutProjShape<DC, NVB>;
-  const dim3 grid((a.geo.chunk_tokens + 32 * P::NW - 1) / (32 * P::NW), a.n_heads, a.batch);
-  hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL>), grid, dim3(64 * P::NW), 0, s, a);
+  // waves per workgroup: the largest of P::NW, 4, 2 whose grid covers at least half of the CUs
+  // (four waves with W_UV_h in LDS hold one workgroup per CU, so a grid of more than one
+  // workgroup per CU would run in two rounds)
+  auto wgs = [&](int nw) { return (int64_t)((a.geo.chunk_tokens + 32 * nw - 1) / (32 * nw)) * a.n_heads * a.batch; };
+  const int n_cu = out_proj_cu_count();
+  int nw = P::NW;
+  if (2 * wgs(nw) < n_cu && nw > 4) nw = 4;
+  if (2 * wgs(nw) < n_cu && nw > 2) nw = 2;
+  const dim3 grid((a.geo.chunk_tokens + 32 * nw - 1) / (32 * nw), a.n_heads, a.batch);
+  if (nw == P::NW) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL>), grid, dim3(64 * nw), 0, s, a);
+  else if (nw == 4) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 4, P::WL4>), grid, dim3(64 * nw), 0, s, a);
+  else hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 2, P::WL2>), grid, dim3(64 * nw), 0, s, a);
   return hipGetLastError();
 }
 
