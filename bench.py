@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "4ff261cbe52b5d5618d3428ce2a34e8f819ccfc18c38b6ceb6789c2a214b77f0",
-                  "bytes": 307580504}
+                  "sha256": "8a196967a7f65a1709372373c7e1d33f1c6497b72c4625c1d72c031da4021847",
+                  "bytes": 308558416}
 
 
 def log(msg):
