@@ -12,67 +12,92 @@
 //   gemm (store)      y = sum_h B_h o_lat_h = [B_1 .. B_H] o_lat
 //
 // gemm: out^T[o][token] = A[o][:] . B[token][:], A = weight rows [N][K], B = token rows [M][K],
-// both row-major with K % 64 == 0. A workgroup (4 waves) takes 128 tokens x 128 outputs, wave w
-// the tokens 32 w .. 32 w + 31 with MFMA 32x32x16; the contraction streams through three LDS
-// stages of 64 columns filled by direct global-to-LDS loads (chunk index XOR (row / 2) mod 8).
-// Rows past M or N are clamped to the last row and their results discarded.
+// both row-major with K % 64 == 0. A workgroup of 8 waves (two per SIMD) takes 128 tokens and
+// 128 or 256 outputs, each wave 32 tokens x 64 or 128 outputs with MFMA 32x32x16; the
+// contraction streams through LDS stages of 64 columns filled by direct global-to-LDS loads
+// (chunk index XOR (row / 2) mod 8). Tiles are numbered token-block-major and dealt to the XCDs
+// in contiguous ranges. Rows past M or N are clamped to the last row and their results discarded.
 #include "vmla_device.h"
 
 namespace vmla {
 namespace {
 
-constexpr int kGmTok = 128, kGmOut = 128, kGmKC = 64, kGmStages = 3;
-constexpr int kGmRows = kGmTok + kGmOut;
-constexpr int kGmLoads = kGmRows * 8 / 64;  // 1 KB loads per stage (32)
-
 __device__ __forceinline__ int gm_swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
+constexpr int kGmKC = 64;  // contraction columns per LDS stage
 
-template <int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t stage[kGmStages][kGmRows * kGmKC];
+// Tile shape: TT token rows x TO outputs per workgroup, WT x WO waves (each 32 tokens x TO / WO
+// outputs), ST stages of 64 columns, at least MINB workgroups resident per CU. XCD: tiles are
+// numbered token-block-major and each XCD takes a contiguous range of them (workgroup w runs on
+// XCD w mod 8), so that the workgroups sharing a token block share that XCD's L2.
+template <int TT, int TO, int WT, int WO, int ST, int MINB, bool XCD = false>
+struct GemmShape {
+  static constexpr int kTok = TT, kOut = TO, kWT = WT, kWO = WO, kStages = ST, kMinBlocks = MINB;
+  static constexpr bool kXcdMap = XCD;
+  static constexpr int kWaves = WT * WO, kThreads = 64 * kWaves;
+  static constexpr int kRows = TT + TO;              // LDS rows per stage (tokens, then outputs)
+  static constexpr int kLoadsPerWave = kRows * 8 / 64 / kWaves;  // 1 KB loads per wave per stage
+  static constexpr int kMO = TO / WO / 32;           // 32x32 output blocks per wave
+  static_assert(TT == 32 * WT && TO % (32 * WO) == 0, "wave tiling");
+  static_assert(kRows * 8 % (64 * kWaves) == 0, "stage loads split evenly over the waves");
+  static constexpr size_t kLdsBytes = (size_t)ST * kRows * kGmKC * 2;
+};
+
+template <int EPI, class P>
+__global__ __launch_bounds__(P::kThreads, P::kMinBlocks) void gemm_nt_kernel(const GemmArgs a) {
+  constexpr int TT = P::kTok, TO = P::kOut, ST = P::kStages, NW = P::kWaves, MO = P::kMO;
+  constexpr int LPW = P::kLoadsPerWave, WOUT = 32 * MO;
+  __shared__ __attribute__((aligned(16))) uint16_t stage[ST][P::kRows * kGmKC];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wt = wave % P::kWT, wo = wave / P::kWT;
   const int g = lane >> 5, l32 = lane & 31;
-  const int n0 = blockIdx.x * kGmTok, o0 = blockIdx.y * kGmOut;
+  int tx = blockIdx.x, ty = blockIdx.y;
+  if constexpr (P::kXcdMap) {
+    const int nty = (a.N + TO - 1) / TO, G = gridDim.x, id = blockIdx.x;
+    const int xcd = id & 7, L = xcd * (G >> 3) + min(xcd, G & 7) + (id >> 3);
+    tx = L / nty;
+    ty = L % nty;
+  }
+  const int n0 = tx * TT, o0 = ty * TO;
   const int K = a.K;
 
-  const uint16_t* src[kGmLoads / 4];
+  const uint16_t* src[LPW];
 #pragma unroll
-  for (int i = 0; i < kGmLoads / 4; ++i) {
-    const int p = (wave + 4 * i) * 64 + lane;
+  for (int i = 0; i < LPW; ++i) {
+    const int p = (wave + NW * i) * 64 + lane;
     const int r = p >> 3, cs = p & 7;
     const int c = cs ^ ((r >> 1) & 7);
-    const uint16_t* row = r < kGmTok ? a.b + (size_t)min(n0 + r, a.M - 1) * K
-                                     : a.a + (size_t)min(o0 + r - kGmTok, a.N - 1) * K;
+    const uint16_t* row = r < TT ? a.b + (size_t)min(n0 + r, a.M - 1) * K
+                                 : a.a + (size_t)min(o0 + r - TT, a.N - 1) * K;
     src[i] = row + c * 8;
   }
   auto issue = [&](int chunk) {
-    uint16_t* st = stage[chunk % kGmStages];
+    uint16_t* st = stage[chunk % ST];
 #pragma unroll
-    for (int i = 0; i < kGmLoads / 4; ++i)
+    for (int i = 0; i < LPW; ++i)
       lds_dma16(src[i] + chunk * kGmKC,
-                __builtin_amdgcn_readfirstlane(lds_addr(st + (wave + 4 * i) * 512)));
+                __builtin_amdgcn_readfirstlane(lds_addr(st + (wave + NW * i) * 512)));
   };
 
-  f32x16 acc[4];
+  f32x16 acc[MO];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) acc[m] = f32x16{};
+  for (int m = 0; m < MO; ++m) acc[m] = f32x16{};
   float ssq = 0.f;  // q_cat epilogue: this lane's half of the token row's sum of squares
   const int nchunks = K / kGmKC;
 #pragma unroll
-  for (int c = 0; c < kGmStages - 1; ++c)
+  for (int c = 0; c < ST - 1; ++c)
     if (c < nchunks) issue(c);
   for (int i = 0; i < nchunks; ++i) {
-    if (i + kGmStages - 2 < nchunks) wait_vmcnt<(kGmStages - 2) * (kGmLoads / 4)>();
+    if (i + ST - 2 < nchunks) wait_vmcnt<(ST - 2) * LPW>();
     else wait_vmcnt<0>();
     __syncthreads();  // chunk i is in LDS for every wave; chunk i-1 is no longer read
-    if (i + kGmStages - 1 < nchunks) issue(i + kGmStages - 1);
-    const uint16_t* st = stage[i % kGmStages];
+    if (i + ST - 1 < nchunks) issue(i + ST - 1);
+    const uint16_t* st = stage[i % ST];
 #pragma unroll
     for (int ks = 0; ks < kGmKC / 16; ++ks) {
       const int c = ks * 2 + g;
       const bf16x8 bx =
-          as_bf16x8(*reinterpret_cast<const u32x4*>(&st[gm_swz(wave * 32 + l32, c) * 8]));
+          as_bf16x8(*reinterpret_cast<const u32x4*>(&st[gm_swz(wt * 32 + l32, c) * 8]));
       if constexpr (EPI == kEpiQcat) {  // widen each bf16 by its bit pattern, square in fp32
         const u32x4 w = as_u32x4(bx);
 #pragma unroll
@@ -83,24 +108,26 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
         }
       }
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const bf16x8 aw = as_bf16x8(
-            *reinterpret_cast<const u32x4*>(&st[gm_swz(kGmTok + m * 32 + l32, c) * 8]));
+      for (int m = 0; m < MO; ++m) {
+        const bf16x8 aw = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            &st[gm_swz(TT + wo * WOUT + m * 32 + l32, c) * 8]));
         acc[m] = mfma32(aw, bx, acc[m]);
       }
     }
   }
 
-  // epilogue: lane holds token n0 + 32 wave + l32 and outputs o0 + 32 m + 8 i + 4 g + j
+  // epilogue: lane holds token n0 + 32 wt + l32 and outputs o0 + wo WOUT + 32 m + 8 i + 4 g + j
+  const int ob = o0 + wo * WOUT;
   if constexpr (EPI == kEpiHeads) {
     // through LDS, so that every store is a whole 16-byte chunk of 8 consecutive outputs of one
-    // token (head_w % 8 == 0 keeps a chunk inside one head): each wave's 32 token rows x 128
+    // token (head_w % 8 == 0 keeps a chunk inside one head): each wave's 32 token rows x WOUT
     // outputs go to its own LDS tile, then its lanes copy them out row by row
-    constexpr int OTS = kGmOut + 8;  // tile row stride (elements)
-    __syncthreads();                 // every wave is done reading the stage buffers
+    constexpr int OTS = WOUT + 8;  // tile row stride (elements)
+    static_assert(NW * 32 * OTS <= ST * P::kRows * kGmKC, "output tiles fit the stage buffers");
+    __syncthreads();               // every wave is done reading the stage buffers
     uint16_t* ot = &stage[0][0] + wave * 32 * OTS;
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < MO; ++m)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const f32x4 fv = {acc[m][4 * i], acc[m][4 * i + 1], acc[m][4 * i + 2], acc[m][4 * i + 3]};
@@ -108,9 +135,9 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
       }
     __syncthreads();  // the tile rows are read by other lanes than the ones that wrote them
 #pragma unroll 4
-    for (int it = lane; it < 32 * (kGmOut / 8); it += 64) {
-      const int tr = it / (kGmOut / 8), ch = it % (kGmOut / 8);
-      const int tok = n0 + wave * 32 + tr, o = o0 + ch * 8;
+    for (int it = lane; it < 32 * (WOUT / 8); it += 64) {
+      const int tr = it / (WOUT / 8), ch = it % (WOUT / 8);
+      const int tok = n0 + wt * 32 + tr, o = ob + ch * 8;
       if (tok < a.M && o < a.N)
         stg16(a.out + (size_t)tok * a.ldo + (size_t)(o / a.head_w) * a.head_ld + a.col_off +
                   o % a.head_w,
@@ -118,7 +145,7 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
     }
     return;
   }
-  const int t = n0 + wave * 32 + l32;
+  const int t = n0 + wt * 32 + l32;
   float scale = 1.f;
   TokenPos pos{};
   if constexpr (EPI == kEpiQcat) {
@@ -128,10 +155,10 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
   }
   if (t >= a.M) return;
 #pragma unroll
-  for (int m = 0; m < 4; ++m)
+  for (int m = 0; m < MO; ++m)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int o = o0 + m * 32 + 8 * i + 4 * g;
+      const int o = ob + m * 32 + 8 * i + 4 * g;
       if (o >= a.N) continue;
       float v[4] = {acc[m][4 * i], acc[m][4 * i + 1], acc[m][4 * i + 2], acc[m][4 * i + 3]};
       uint16_t* dst;
@@ -153,7 +180,7 @@ __global__ __launch_bounds__(256, 1) void gemm_nt_kernel(const GemmArgs a) {
     }
   if constexpr (EPI == kEpiQcat) {  // zero padding of each head's q_cat row
     const int dqk = a.q_dc + a.q_dr;
-    if (blockIdx.y == 0 && g == 0)
+    if (ty == 0 && wo == 0 && g == 0)
       for (int h = 0; h < a.q_heads; ++h)
         for (int c = dqk; c < a.ldo; ++c) a.out[((size_t)t * a.q_heads + h) * a.ldo + c] = 0;
   }
@@ -261,16 +288,31 @@ __global__ __launch_bounds__(256) void prepare_weights_kernel(const PrepArgs a) 
 
 }  // namespace
 
+template <class P>
+hipError_t launch_gemm_shape(const GemmArgs& a, hipStream_t s) {
+  const int ntx = (a.M + P::kTok - 1) / P::kTok, nty = (a.N + P::kOut - 1) / P::kOut;
+  const dim3 grid = P::kXcdMap ? dim3(ntx * nty) : dim3(ntx, nty);
+  if (a.epi == kEpiQcat)
+    hipLaunchKernelGGL((gemm_nt_kernel<kEpiQcat, P>), grid, dim3(P::kThreads), 0, s, a);
+  else if (a.epi == kEpiHeads)
+    hipLaunchKernelGGL((gemm_nt_kernel<kEpiHeads, P>), grid, dim3(P::kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((gemm_nt_kernel<kEpiStore, P>), grid, dim3(P::kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+// Wide tiles (128 tokens x 256 outputs) carry twice the MFMA work per byte a CU takes in, and
+// win once they fill most of the chip (Wan shape: q_up 58 -> 45 us, out_mix 57 -> 46 us); below
+// that the 128 x 128 tiles keep every CU busy (q_down, 111 wide tiles: 21 -> 20 us).
+using GemmWide = GemmShape<128, 256, 4, 2, 3, 1, true>;
+using GemmSquare = GemmShape<128, 128, 4, 2, 4, 1, true>;
+
 hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
   // validated by the caller: K % 64 == 0, N % 4 == 0, M >= 1, N >= 1
-  const dim3 grid((a.M + kGmTok - 1) / kGmTok, (a.N + kGmOut - 1) / kGmOut);
-  if (a.epi == kEpiQcat)
-    hipLaunchKernelGGL(gemm_nt_kernel<kEpiQcat>, grid, dim3(256), 0, s, a);
-  else if (a.epi == kEpiHeads)
-    hipLaunchKernelGGL(gemm_nt_kernel<kEpiHeads>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(gemm_nt_kernel<kEpiStore>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  const int64_t wide_tiles = (int64_t)((a.M + GemmWide::kTok - 1) / GemmWide::kTok) *
+                             ((a.N + GemmWide::kOut - 1) / GemmWide::kOut);
+  if (wide_tiles >= 192) return launch_gemm_shape<GemmWide>(a, s);
+  return launch_gemm_shape<GemmSquare>(a, s);
 }
 
 hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat, hipStream_t s) {
