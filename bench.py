@@ -667,6 +667,8 @@ def main():
                          "sweep and with 1-frame chunks; wan-latent-vs-materialized: the "
                          "latent and the materialized-K/V attention at both head splits")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
+    ap.add_argument("--attend-balance", type=int, choices=(0, 1), default=1,
+                    help="1 (default): adaptive per-XCD work partition of the latent attention; 0: even split")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -678,6 +680,8 @@ def main():
 
     import paper_2605_30351_amd as vm
     from workloads import WAN, make_layer_inputs
+
+    vm.set_attend_balance(bool(args.attend_balance))
 
     if args.workload == "wan-30-layer-chunk":
         thirty_layer_chunk(args, vm, torch, WAN)
@@ -817,6 +821,7 @@ def main():
             "d_model": d.d_model, "heads": d.n_heads, "d_nope": d.d_nope, "d_rope": d.d_rope,
             "d_c": d.d_c, "d_v": d.d_v, "chunk_tokens": d.chunk_tokens,
             "window_tokens": d.window_tokens, "rope_pairs": list(d.rope_pairs), "seed": 1,
+            "attend_partition": "adaptive per-XCD" if args.attend_balance else "even",
         },
         "attend": {
             "ms": round(att_ms, 4),

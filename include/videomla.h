@@ -325,6 +325,22 @@ const char* videomla_last_error(void);
 int videomla_set_attend_workgroups(int32_t n_workgroups);
 
 /*
+ * Tuning knob: adaptive work partition of the latent attention (videomla_attend and
+ * videomla_attend_layer; 0 = the even split, the default; 1 = adaptive). Workgroup k runs on XCD
+ * k mod 8, and the XCDs of one device can run at different clocks under this load; the call
+ * then waits for the slowest. In adaptive mode each call gives each XCD's workgroups a share of
+ * the units proportional to the work per time that XCD achieved in the previous adaptive call
+ * on the same workspace (each weight within [0.8, 1.25] of the mean), recorded in a 33 KB state
+ * area at the end of the workspace. The first call, or one after a call with another workgroup
+ * count, splits evenly. The merge of the partial results stays exact, but the split points, and
+ * so the rounding of the outputs, can differ from call to call: outputs are not bitwise
+ * reproducible in this mode. Shapes whose ranges could get too short for the workspace's
+ * partial-result slots keep the even split. Process-wide; calls that share a workspace must be
+ * ordered on one stream, as in the default mode.
+ */
+int videomla_set_attend_balance(int32_t on);
+
+/*
  * Kernel timing with HIP events, for benchmarks. When enabled, every kernel the library
  * launches is bracketed by two events recorded on the same stream. After the caller has
  * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed

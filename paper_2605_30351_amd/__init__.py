@@ -24,6 +24,7 @@ from ._lib import (  # noqa: F401
     make_dims,
     prepare_layer_weights,
     prepare_write_weights,
+    set_attend_balance,
     set_attend_workgroups,
     slot_of,
     timing_enable,

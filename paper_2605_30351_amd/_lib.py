@@ -27,6 +27,7 @@ EXPORTED = (
     "videomla_attend_materialized_workspace_bytes", "videomla_attend_materialized",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
+    "videomla_set_attend_balance",
     "videomla_timing_enable", "videomla_timing_only", "videomla_timing_read",
     "videomla_dense_cache_bytes_per_token", "videomla_dense_cache_write",
     "videomla_dense_attend_workspace_bytes", "videomla_dense_attend",
@@ -85,6 +86,8 @@ _lib.videomla_last_error.argtypes = []
 _lib.videomla_last_error.restype = ctypes.c_char_p
 _lib.videomla_set_attend_workgroups.argtypes = [ctypes.c_int32]
 _lib.videomla_set_attend_workgroups.restype = ctypes.c_int
+_lib.videomla_set_attend_balance.argtypes = [ctypes.c_int32]
+_lib.videomla_set_attend_balance.restype = ctypes.c_int
 _lib.videomla_timing_enable.argtypes = [ctypes.c_int32]
 _lib.videomla_timing_enable.restype = ctypes.c_int
 _lib.videomla_timing_only.argtypes = [ctypes.c_char_p]
@@ -379,6 +382,11 @@ def slot_of(dims, f: int, y: int, x: int) -> int:
 def set_attend_workgroups(n: int):
     """Workgroup count of the attention kernel (0 = one per compute unit)."""
     _check(_lib.videomla_set_attend_workgroups(int(n)))
+
+
+def set_attend_balance(on: bool):
+    """Adaptive per-XCD work partition of the latent attention (off by default)."""
+    _check(_lib.videomla_set_attend_balance(1 if on else 0))
 
 
 def timing_enable(on: bool = True):

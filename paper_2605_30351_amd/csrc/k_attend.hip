@@ -294,7 +294,46 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // tiles of one row block is a segment with its own partial result.
   const int64_t U = a.units;
   const int G = a.n_wg, T = a.tiles_per_row;
-  const int64_t u_begin = (int64_t)blockIdx.x * U / G, u_end = (int64_t)(blockIdx.x + 1) * U / G;
+  int64_t u_begin = (int64_t)blockIdx.x * U / G, u_end = (int64_t)(blockIdx.x + 1) * U / G;
+  // Adaptive split: each XCD's weight is proportional to the units per time its workgroups
+  // achieved in the previous call (slot (bal_seq - 1) & 1); equal weights if that slot does not
+  // hold a consistent record for this G.
+  __shared__ uint32_t bal_t[8];
+  uint32_t bw[8];
+  uint64_t bal_t0 = 0;
+  if (a.bal_on) {
+    bal_t0 = __builtin_amdgcn_s_memrealtime();
+    const uint32_t* prev = a.bal_state + ((a.bal_seq + 1) & 1) * kBalSlot;
+    uint32_t* next = a.bal_state + (a.bal_seq & 1) * kBalSlot;
+    if (tid < 8) bal_t[tid] = 0;
+    __syncthreads();
+    const bool hdr = prev[9] == kBalMark && prev[8] == (uint32_t)G;
+    if (hdr)
+      for (int k = tid; k < G; k += NW * 64) atomicMax(&bal_t[k & 7], prev[kBalHead + k]);
+    __syncthreads();
+    bool ok = hdr;
+    double sp[8], tot = 0.0;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const int nx = G > x ? (G - x + 7) / 8 : 0;  // workgroups on XCD x
+      const uint32_t w = prev[x], t = bal_t[x];
+      sp[x] = 0.0;
+      if (nx > 0) {
+        ok = ok && w >= kBalMin && w <= kBalMax && t > 0u && t < 1000000000u;
+        sp[x] = (double)w / (double)(t > 0u ? t : 1u);
+        tot += nx * sp[x];
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const double v = ok && sp[x] > 0.0 ? kBalOne * sp[x] * G / tot : (double)kBalOne;
+      bw[x] = __builtin_amdgcn_readfirstlane(
+          (uint32_t)fmin(fmax(rint(v), (double)kBalMin), (double)kBalMax));
+    }
+    u_begin = bal_start(bw, G, U, blockIdx.x);
+    u_end = bal_start(bw, G, U, blockIdx.x + 1);
+    if (blockIdx.x == 0 && tid < 10) next[tid] = tid < 8 ? bw[tid] : tid == 8 ? (uint32_t)G : kBalMark;
+  }
   // Segments are taken last to first: a workgroup's last segment is the head of a row block
   // (keys from 0) and its first the tail of another, so in this order every workgroup walks the
   // keys at about the same position at the same time (all ranges have the same length), and
@@ -306,7 +345,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   const int kt1 = (int)(u - rbg * T);
   u = seg_lo;
   const int b = (int)(rbg / a.row_blocks), rb = (int)(rbg % a.row_blocks);
-  const int split = (int)blockIdx.x - attend_owner(rbg * T, U, G);
+  const int split = (int)blockIdx.x - (a.bal_on ? bal_owner(bw, G, U, rbg * T) : attend_owner(rbg * T, U, G));
   const int vpar = VS > 1 ? wave % VS : 0;  // column half of this wave (pair split)
   const int row0 = rb * C::ROWS + wave / VS * QB * 32;
   const int key_begin = kt0 * BN;
@@ -685,6 +724,9 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     }
   }
   }  // segments
+  if (a.bal_on && tid == 0)
+    a.bal_state[(a.bal_seq & 1) * kBalSlot + kBalHead + blockIdx.x] =
+        (uint32_t)(__builtin_amdgcn_s_memrealtime() - bal_t0);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -764,8 +806,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   if (lane < 32) {
     const size_t row = row_of(lane);
     const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
-    const int ns = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
-                   attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
+    const int ns = attend_split_count(a, rbg);
     // the (max, sum) pairs of the first kMergeSplits splits, all loads issued together
     f32x2 ml[kMergeSplits];
 #pragma unroll

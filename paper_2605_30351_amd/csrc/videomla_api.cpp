@@ -160,6 +160,8 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 int g_attend_wg = 0;  // 0 = as many workgroups as the compute units hold at once
+int g_attend_balance = 0;  // adaptive per-XCD partition of the latent attention
+uint32_t g_bal_seq = 0;    // sequence number of adaptive attention calls
 
 int device_cu_count() {
   int dev = 0, n = 0;
@@ -227,7 +229,8 @@ int workspace_max_seg(const videomla_dims* d, int32_t batch, bool dense = false)
 }
 
 struct WorkspaceLayout {
-  size_t qcat_off, opart_off, ml_off, krot_off, total;
+  size_t qcat_off, opart_off, ml_off, krot_off, bal_off, total;
+  int n_seg;  // partial-result slots
 };
 
 WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
@@ -242,7 +245,10 @@ WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_se
   const size_t krot = d->sink_frames > 0
                           ? (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->d_rope * 2
                           : 0;
-  w.total = w.krot_off + round_up(krot, 256);
+  // the adaptive partition's two state slots
+  w.bal_off = w.krot_off + round_up(krot, 256);
+  w.total = w.bal_off + round_up((size_t)2 * kBalSlot * 4, 256);
+  w.n_seg = n_seg;
   return w;
 }
 
@@ -351,6 +357,12 @@ int videomla_window_advance(const videomla_dims* d, videomla_window* w) {
   if (int e = check_dims(d)) return e;
   if (int e = check_window(w)) return e;
   w->frame_end += d->chunk_frames;
+  return ok();
+}
+
+int videomla_set_attend_balance(int32_t on) {
+  if (on != 0 && on != 1) return fail(VIDEOMLA_EINVAL, "attend balance must be 0 or 1, got %d", on);
+  g_attend_balance = on;
   return ok();
 }
 
@@ -482,6 +494,14 @@ AttendArgs attend_args(const videomla_dims* d, const videomla_window* w, int32_t
   a.tiles_per_row = P.T;
   a.units = P.U;
   a.max_seg = P.max_seg;
+  // adaptive only where every range keeps at least one unit under any weights and the
+  // workspace holds the partial results such ranges can leave
+  a.bal_state = reinterpret_cast<uint32_t*>(ws + L.bal_off);
+  a.bal_on = g_attend_balance && P.G <= kBalMaxWg && bal_max_seg(P.G, P.U, P.T) <= L.n_seg;
+  if (a.bal_on) {
+    a.max_seg = L.n_seg;
+    a.bal_seq = (int32_t)(g_bal_seq++ & 0x7fffffff);
+  }
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
   a.qscale = (float)(scale * 1.4426950408889634);

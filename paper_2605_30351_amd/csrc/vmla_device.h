@@ -152,4 +152,16 @@ __device__ __forceinline__ void rope_rotate(const RopeTable& t, int pair, const 
   v = rv;
 }
 
+// Partial results of row block rbg: the workgroups owning its first and last units, under the
+// even split or (bal_on) the adaptive one whose weights the attention call stored.
+__device__ inline int attend_split_count(const AttendArgs& a, int64_t rbg) {
+  const int64_t lo = rbg * a.tiles_per_row, hi = lo + a.tiles_per_row - 1;
+  if (!a.bal_on) return attend_owner(hi, a.units, a.n_wg) - attend_owner(lo, a.units, a.n_wg) + 1;
+  const uint32_t* st = a.bal_state + (a.bal_seq & 1) * kBalSlot;
+  uint32_t w[8];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) w[x] = st[x];
+  return bal_owner(w, a.n_wg, a.units, hi) - bal_owner(w, a.n_wg, a.units, lo) + 1;
+}
+
 }  // namespace vmla

@@ -76,6 +76,11 @@ struct AttendArgs {
   int64_t units;           // U = batch * row_blocks * T
   int32_t max_seg;         // partial-result slots the workspace holds
   float qscale;            // softmax scale * log2(e), folded into the absorbed query
+  // Adaptive partition (latent path, optional): two state slots of kBalSlot words in the
+  // workspace; the call with sequence number bal_seq reads slot (bal_seq - 1) & 1 and writes
+  // slot bal_seq & 1 (see bal_* below). bal_on = 0: the even split above.
+  uint32_t* bal_state;
+  int32_t bal_on, bal_seq;
   Geometry geo;
   RopeTable rope;
   // dense per-head comparator only (rows are (head, token) pairs, each head padded to nq_pad)
@@ -125,6 +130,48 @@ struct PrepArgs {
 // Workgroup whose unit range [w*U/G, (w+1)*U/G) contains `unit`.
 __host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_wg) {
   return (int)(((unit + 1) * (int64_t)n_wg - 1) / units);
+}
+
+// Adaptive partition of the attention units. Workgroup k runs on XCD k mod 8 and gets a share of
+// the units proportional to its XCD's integer weight w[k mod 8] in [kBalMin, kBalMax]:
+// workgroup k takes [start(k), start(k+1)) with start(k) = floor(U cum(k) / cum(G)), cum(k) the
+// summed weights of workgroups 0 .. k-1. Equal weights give the even split. A state slot holds
+// the weights a call used (words 0..7), its G (8), a marker (9) and each workgroup's duration in
+// 100 MHz ticks (kBalHead + k); the next call sets each XCD's weight proportional to the work per
+// time that XCD achieved. Any slot content that fails the checks means equal weights.
+constexpr uint32_t kBalMin = 820, kBalMax = 1280, kBalOne = 1024, kBalMark = 0x564d4c42u;
+constexpr int kBalHead = 16, kBalMaxWg = 4096, kBalSlot = kBalHead + kBalMaxWg;
+
+__host__ __device__ inline int64_t bal_cum(const uint32_t* w, int k) {
+  int64_t s = 0;
+  for (int x = 0; x < 8; ++x) s += (int64_t)w[x] * (k > x ? (k - x + 7) / 8 : 0);
+  return s;
+}
+__host__ __device__ inline int64_t bal_start(const uint32_t* w, int G, int64_t U, int k) {
+  return U * bal_cum(w, k) / bal_cum(w, G);
+}
+// The workgroup whose range contains `unit`: the largest k < G with start(k) <= unit, i.e.
+// with cum(k) <= C = floor(((unit + 1) cum(G) - 1) / U); cum(8q + j) = q S + w[0] + .. + w[j-1]
+// with S the sum of the 8 weights, so k = 8 (C / S) + the number of leading weights whose sum
+// stays within C mod S.
+__host__ __device__ inline int bal_owner(const uint32_t* w, int G, int64_t U, int64_t unit) {
+  const int64_t C = ((unit + 1) * bal_cum(w, G) - 1) / U;
+  int64_t S = 0;
+  for (int x = 0; x < 8; ++x) S += w[x];
+  int64_t r = C % S, k = C / S * 8;
+  for (int x = 0; x < 7 && r >= (int64_t)w[x]; ++x) {
+    r -= w[x];
+    ++k;
+  }
+  return (int)(k < G - 1 ? k : G - 1);
+}
+// Partial-result slots a row block of T units can need under any weights: every range holds at
+// least floor(U kBalMin / (kBalMin + (G - 1) kBalMax)) - 1 units.
+__host__ __device__ inline int bal_max_seg(int G, int64_t U, int T) {
+  const int64_t min_len = U * kBalMin / (kBalMin + (int64_t)(G - 1) * kBalMax) - 1;
+  if (min_len < 1) return G + 1;  // some range could be empty: never adaptive
+  const int64_t n = (T + min_len - 1) / min_len + 1;
+  return (int)(n < G ? n : G);
 }
 
 // Launchers (one per kernel). Return the launch status.
