@@ -30,8 +30,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "8a196967a7f65a1709372373c7e1d33f1c6497b72c4625c1d72c031da4021847",
-                  "bytes": 308558416}
+                  "sha256": "8de7e93d05bf8b1b8520b2f0acaccd79cd1bc7ce7820a71a15bff42475157e13",
+                  "bytes": 305102101}
 
 
 def log(msg):
