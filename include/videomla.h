@@ -325,8 +325,9 @@ const char* videomla_last_error(void);
 int videomla_set_attend_workgroups(int32_t n_workgroups);
 
 /*
- * Tuning knob: adaptive work partition of the latent attention (videomla_attend and
- * videomla_attend_layer; 0 = the even split, the default; 1 = adaptive). Workgroup k runs on XCD
+ * Tuning knob: adaptive work partition of the attention kernels (videomla_attend,
+ * videomla_attend_layer, videomla_attend_materialized and videomla_dense_attend; 0 = the even
+ * split, the default; 1 = adaptive). Workgroup k runs on XCD
  * k mod 8, and the XCDs of one device can run at different clocks under this load; the call
  * then waits for the slowest. In adaptive mode each call gives each XCD's workgroups a share of
  * the units proportional to the work per time that XCD achieved in the previous adaptive call

@@ -215,8 +215,7 @@ __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
   const size_t total_rows = (size_t)a.batch * rows_b;
   const size_t orow = (size_t)b * rows_b + r;
   const int64_t rbg = (int64_t)b * a.row_blocks + r / a.att_rows;
-  const int ns = attend_owner(rbg * a.tiles_per_row + a.tiles_per_row - 1, a.units, a.n_wg) -
-                 attend_owner(rbg * a.tiles_per_row, a.units, a.n_wg) + 1;
+  const int ns = attend_split_count(a, rbg);
   float M = kNegInfD;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + orow) * 2]);
   float L = 0.f;

@@ -252,6 +252,18 @@ WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_se
   return w;
 }
 
+// The adaptive partition (videomla_set_attend_balance) for a call: only where every range keeps
+// at least one unit under any weights and the workspace holds the partial results such ranges
+// can leave.
+void set_balance(AttendArgs& a, const Partition& P, char* ws, const WorkspaceLayout& L) {
+  a.bal_state = reinterpret_cast<uint32_t*>(ws + L.bal_off);
+  a.bal_on = g_attend_balance && P.G <= kBalMaxWg && bal_max_seg(P.G, P.U, P.T) <= L.n_seg;
+  if (a.bal_on) {
+    a.max_seg = L.n_seg;
+    a.bal_seq = (int32_t)(g_bal_seq++ & 0x7fffffff);
+  }
+}
+
 // Dense comparator workspace: q_cat [B][H][nq_pad][d_v] bf16, then the partial results.
 WorkspaceLayout dense_workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
   const size_t rows = (size_t)batch * d->n_heads * dense_nq_pad(d);
@@ -259,7 +271,9 @@ WorkspaceLayout dense_workspace_layout(const videomla_dims* d, int32_t batch, in
   w.qcat_off = 0;
   w.opart_off = round_up(rows * d->d_v * 2, 256);
   w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_v * 4, 256);
-  w.total = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
+  w.bal_off = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
+  w.total = w.bal_off + round_up((size_t)2 * kBalSlot * 4, 256);
+  w.n_seg = n_seg;
   return w;
 }
 
@@ -494,14 +508,7 @@ AttendArgs attend_args(const videomla_dims* d, const videomla_window* w, int32_t
   a.tiles_per_row = P.T;
   a.units = P.U;
   a.max_seg = P.max_seg;
-  // adaptive only where every range keeps at least one unit under any weights and the
-  // workspace holds the partial results such ranges can leave
-  a.bal_state = reinterpret_cast<uint32_t*>(ws + L.bal_off);
-  a.bal_on = g_attend_balance && P.G <= kBalMaxWg && bal_max_seg(P.G, P.U, P.T) <= L.n_seg;
-  if (a.bal_on) {
-    a.max_seg = L.n_seg;
-    a.bal_seq = (int32_t)(g_bal_seq++ & 0x7fffffff);
-  }
+  set_balance(a, P, ws, L);
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
   a.qscale = (float)(scale * 1.4426950408889634);
@@ -629,6 +636,7 @@ int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int3
   a.tiles_per_row = P.T;
   a.units = P.U;
   a.max_seg = P.max_seg;
+  set_balance(a, P, ws, L);
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale : 1.0 / std::sqrt((double)d->d_v);
   a.qscale = (float)(scale * 1.4426950408889634);
 
@@ -729,6 +737,7 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
   a.tiles_per_row = P.T;
   a.units = P.U;
   a.max_seg = P.max_seg;
+  set_balance(a, P, dws, L.dense);
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)(d->d_nope + d->d_rope));
   a.qscale = (float)(scale * 1.4426950408889634);

@@ -119,3 +119,31 @@ def test_wan_layer_adaptive_calls(vm):
             assert_attention_close(got[0][rows], want, f"adaptive layer call {call}")
     finally:
         vm.set_attend_balance(False)
+
+
+def test_dense_and_materialized_adaptive_calls(vm):
+    """The dense comparator and the materialized form in adaptive mode (their merge reads the
+    adaptive split points): two consecutive calls each at Wan geometry, sampled rows."""
+    from tests.test_gpu_dense import DenseLayer
+    from workloads import make_dense_inputs
+    d = WAN
+    rows = sample_rows(d.chunk_tokens, k=16, seed=34)
+    dinp = make_dense_inputs(d, seed=34, n_frames=21)
+    dense = DenseLayer(vm, dinp)
+    for f in range(0, 21, d.chunk_frames):
+        dense.write(f)
+    want_d = O.dense_chunk_attention(dinp, 0, 18, rows=rows)
+    inp = make_layer_inputs(d, seed=35, n_frames=21)
+    layer = Layer(vm, inp, packed=True)
+    for f in range(0, 21, d.chunk_frames):
+        layer.write(f)
+    want_m = O.chunk_attention(inp, 0, 18, rows=rows)
+    vm.set_attend_balance(True)
+    try:
+        for call in range(2):
+            got = dense.attend(18)
+            assert_attention_close(got[0][rows], want_d, f"adaptive dense call {call}")
+            got = layer.attend(18, materialized=True)
+            assert_attention_close(got[0][rows], want_m, f"adaptive materialized call {call}")
+    finally:
+        vm.set_attend_balance(False)
