@@ -29,8 +29,9 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 # (FETCH_SIZE, WRITE_SIZE) scaled by the same counters on a plain copy of known size; valid only
 # for the kernel source it was measured on (sha256 of the listed files), else reported as null.
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
-                              "paper_2605_30351_amd/csrc/vmla_device.h"),
-                  "sha256": "8de7e93d05bf8b1b8520b2f0acaccd79cd1bc7ce7820a71a15bff42475157e13",
+                              "paper_2605_30351_amd/csrc/vmla_device.h",
+                              "paper_2605_30351_amd/csrc/vmla_internal.h"),
+                  "sha256": "59c3d7765eb75c2a5da2dda30a98fae6d87d67188d758e2af198677a38427a54",
                   "bytes": 305102101}
 
 
