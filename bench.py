@@ -14,6 +14,7 @@ roofline of the dominant kernel and the CPU oracle's throughput on a bounded sam
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -122,33 +123,52 @@ def copy_probe(torch, dev, nbytes=1 << 28, reps=3):
 
 
 def timed_steps(vm, torch, step, n, names):
-    """Milliseconds per step from n steps that carry no library timing events, their per-step
-    times, then per-kernel HIP-event averages ({name: {"launches", "avg_us"}}) from a second
-    pass of n steps with every kernel bracketed (each event pair adds a few microseconds)."""
+    """Milliseconds per step from n steps that carry no timing events, their per-step times,
+    then per-kernel HIP-event averages ({name: {"launches", "avg_us"}}) from a second pass of n
+    steps with every kernel bracketed (each event pair adds a few microseconds).
+
+    step(i, timer) runs one step; the attention call passes `timer` (a videomla Timer or None)
+    in its options, and the cache write is bracketed by the same timer's begin / end."""
     import numpy as np
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     marks[0].record()
     for i in range(n):
-        step(i)
+        step(i, None)
         marks[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(n)])
-    vm.timing_enable(True)
-    vm.timing_only(None)
-    for k in names:
-        vm.timing_read(k)
+    timer = vm.Timer()
     for i in range(n):
-        step(i)
+        step(i, timer)
     torch.cuda.synchronize()
     kernels = {}
     for k in names:
-        c, tot = vm.timing_read(k)
+        c, tot = timer.read(k)
         kernels[k] = {"launches": c, "avg_us": round(1e3 * tot / max(c, 1), 3)}
-    vm.timing_enable(False)
+    timer.close()
     return 1e3 * elapsed / n, step_ms, kernels
+
+
+def bracket(timer, name, launch):
+    """Run `launch` between timer.begin(name) and timer.end(name) on the current stream, or
+    plainly when `timer` is None."""
+    if timer is None:
+        return launch()
+    timer.begin(name)
+    r = launch()
+    timer.end(name)
+    return r
+
+
+def calibrate(vm, torch, call, n=3):
+    """A few adaptive calls on the workspace the timed calls use: they set the per-XCD weights
+    of the partition, which the timed (frozen) calls then reuse unchanged."""
+    for _ in range(n):
+        call(vm.AttendOpts(partition="adaptive"))
+    torch.cuda.synchronize()
 
 
 def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
@@ -191,6 +211,7 @@ def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
     torch.cuda.synchronize()
 
     frame = [d.window_frames]  # the chunk being generated: frames 21..23, then 24..26, ...
+    opts = vm.AttendOpts(partition=args.partition)
 
     def chunk():
         fe = frame[0]
@@ -199,8 +220,13 @@ def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
                 vm.cache_write_prepared(d, fe, 1, L["x"], L["w_packed"], L["gamma"], L["c_kv"],
                                         L["k_r"])
                 vm.attend(d, fe, 1, L["q_nope"], L["q_r"], L["w_uk"], L["w_uv"], L["c_kv"],
-                          L["k_r"], out, ws)
+                          L["k_r"], out, ws, opts=opts)
         frame[0] = vm.window_advance(d, fe)
+
+    if args.partition == "frozen":
+        L = layers[0]
+        calibrate(vm, torch, lambda o: vm.attend(d, frame[0], 1, L["q_nope"], L["q_r"], L["w_uk"],
+                                                 L["w_uv"], L["c_kv"], L["k_r"], out, ws, opts=o))
 
     n_warm, n_time = max(1, min(args.warmup, 3)), max(1, min(args.steps, 10))
     log(f"warmup {n_warm} chunks, timing {n_time}")
@@ -235,7 +261,8 @@ def thirty_layer_chunk(args, vm, torch, d, n_layers=30, n_steps=4):
         "config": {"workload": ("Wan2.1-1.3B, one 3-frame chunk (4,680 tokens x 12 heads) "
                                 "through 30 attention layers x 4 denoising steps over a "
                                 "32,760-token 21-frame window each, then the window advance"),
-                   "layers": n_layers, "denoising_steps": n_steps, "seed": 3},
+                   "layers": n_layers, "denoising_steps": n_steps, "seed": 3,
+                   "attend_partition": args.partition},
     }), flush=True)
 
 
@@ -271,12 +298,18 @@ def sink_chunk_step(args, vm, torch, d, fe=237):
     xs = [normal((1, nq, d.d_model)) for _ in range(args.x_buffers)]
     torch.cuda.synchronize()
 
-    def step(i):
-        vm.cache_write_prepared(d, fe, 1, xs[i % len(xs)], w_packed, gamma, c_kv, k_r)
-        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+    def attend(o):
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, opts=o)
+
+    def step(i, timer=None):
+        bracket(timer, "cache_write", lambda: vm.cache_write_prepared(d, fe, 1, xs[i % len(xs)], w_packed,
+                                                            gamma, c_kv, k_r))
+        attend(vm.AttendOpts(partition=args.partition, timer=timer))
 
     for i in range(args.warmup):
         step(i)
+    if args.partition == "frozen":
+        calibrate(vm, torch, attend)
     torch.cuda.synchronize()
     names = ("cache_write", "q_absorb", "rope_window", "latent_attend", "out_proj")
     ms, step_ms, kernels = timed_steps(vm, torch, step, args.steps, names)
@@ -300,7 +333,7 @@ def sink_chunk_step(args, vm, torch, d, fe=237):
                                 f"of 4,680 x 12 query rows over {S:,} keys (1 sink frame + 6 "
                                 "recent frames), batch 1"),
                    "sink_frames": d.sink_frames, "window_frames": d.window_frames,
-                   "window_tokens": S, "seed": 9},
+                   "window_tokens": S, "seed": 9, "attend_partition": args.partition},
     }), flush=True)
 
 
@@ -340,13 +373,20 @@ def full_layer_chunk_step(args, vm, torch, d, d_q=768, fe=21):
     xs = [normal((1, nq, d.d_model)) for _ in range(args.x_buffers)]
     torch.cuda.synchronize()
 
-    def step(i):
+    def layer(o, x=None):
+        vm.attend_layer(d, fe, 1, d_q, xs[0] if x is None else x, weights, c_kv, k_r, y, ws,
+                        opts=o)
+
+    def step(i, timer=None):
         x = xs[i % len(xs)]
-        vm.cache_write_prepared(d, fe, 1, x, w_packed, gamma, c_kv, k_r)
-        vm.attend_layer(d, fe, 1, d_q, x, weights, c_kv, k_r, y, ws)
+        bracket(timer, "cache_write", lambda: vm.cache_write_prepared(d, fe, 1, x, w_packed, gamma, c_kv,
+                                                            k_r))
+        layer(vm.AttendOpts(partition=args.partition, timer=timer), x)
 
     for i in range(args.warmup):
         step(i)
+    if args.partition == "frozen":
+        calibrate(vm, torch, layer)
     torch.cuda.synchronize()
     names = ("cache_write", "q_down", "q_up", "latent_attend", "latent_merge", "out_mix")
     ms, step_ms, kernels = timed_steps(vm, torch, step, args.steps, names)
@@ -370,7 +410,7 @@ def full_layer_chunk_step(args, vm, torch, d, d_q=768, fe=21):
                                 "of 4,680 tokens, then c^Q = RMSNorm(W_DQ x) (d_q = 768), "
                                 "absorbed queries, latent attend over 32,760 keys x 12 heads, "
                                 "y = sum_h B_h o_lat_h; batch 1"),
-                   "d_q": d_q, "seed": 12},
+                   "d_q": d_q, "seed": 12, "attend_partition": args.partition},
     }), flush=True)
 
 
@@ -431,34 +471,39 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
             ws = torch.empty(vm.dense_attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
             names = ("dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge")
 
-        def call(L, fe, x):
+        def call(L, fe, x, part, timer=None):
+            o = vm.AttendOpts(partition=part, timer=timer)
             if path == "latent":
-                vm.cache_write_prepared(d, fe, B, x, L["w_packed"], L["gamma"], L["c_kv"],
-                                        L["k_r"])
+                bracket(timer, "cache_write", lambda: vm.cache_write_prepared(
+                    d, fe, B, x, L["w_packed"], L["gamma"], L["c_kv"], L["k_r"]))
                 vm.attend(d, fe, B, L["q_nope"], L["q_r"], L["w_uk"], L["w_uv"], L["c_kv"],
-                          L["k_r"], out, ws)
+                          L["k_r"], out, ws, opts=o)
             else:
-                vm.dense_cache_write(d, fe, B, x, L["w_k"], L["w_v"], L["kv"])
-                vm.dense_attend(d, fe, B, L["q"], L["kv"], out, ws)
+                bracket(timer, "dense_cache_write", lambda: vm.dense_cache_write(
+                    d, fe, B, x, L["w_k"], L["w_v"], L["kv"]))
+                vm.dense_attend(d, fe, B, L["q"], L["kv"], out, ws, opts=o)
 
-        # warm-up: one chunk-step of every layer at frame 0 (rewritten by chunk 0 below)
+        # warm-up: one chunk-step of every layer at frame 0 (rewritten by chunk 0 below); with
+        # the frozen partition, adaptive calls at the full window first set its weights
+        if args.partition == "frozen":
+            for li in range(3):
+                call(layers[li], d.window_frames, x_of(0, 0, li), "adaptive")
         for li, L in enumerate(layers):
-            call(L, 0, x_of(0, 0, li))
+            call(L, 0, x_of(0, 0, li), args.partition)
         torch.cuda.synchronize()
         log(f"{path}: timing {n_chunks} chunks")
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_chunks + 1)]
         fe = 0
         t0 = time.perf_counter()
         ev[0].record()
+        timer = None
         for c in range(n_chunks):
             if c == n_chunks - 1:
                 torch.cuda.synchronize()
-                vm.timing_enable(True)
-                for k in names:
-                    vm.timing_read(k)
+                timer = vm.Timer()
             for s in range(n_steps):
                 for li, L in enumerate(layers):
-                    call(L, fe, x_of(c, s, li))
+                    call(L, fe, x_of(c, s, li), args.partition, timer)
             ev[c + 1].record()
             fe = vm.window_advance(d, fe)
             if c % 10 == 9:
@@ -467,9 +512,9 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
         wall = time.perf_counter() - t0
         kern = {}
         for k in names:
-            n, tot = vm.timing_read(k)
+            n, tot = timer.read(k)
             kern[k] = {"launches": n, "avg_us": round(1e3 * tot / max(n, 1), 2)}
-        vm.timing_enable(False)
+        timer.close()
         ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(n_chunks)]
         full = ms[(d.window_frames - 1) // d.chunk_frames:] or ms
         del layers, out, ws
@@ -517,12 +562,12 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
                                 "steps, 21-frame window; latent path and dense per-head "
                                 "comparator on the same schedule"),
                    "batch": B, "layers": n_layers, "denoising_steps": n_steps,
-                   "chunks": n_chunks, "seed": 4},
+                   "chunks": n_chunks, "seed": 4, "attend_partition": args.partition},
     }), flush=True)
 
 
 def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
-                       materialized=False):
+                       materialized=False, partition="frozen"):
     """Per-kernel HIP-event averages of `steps` chunk-steps (packed cache write + attend) of
     one layer with dims d at the wrapped full window (chunk at frame window_frames), batch
     `batch`; the attend is the latent form, or the materialized-K/V form when `materialized`.
@@ -544,9 +589,9 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
     c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
     k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
     out = torch.empty((B, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
-    ws_bytes = (vm.attend_materialized_workspace_bytes if materialized
-                else vm.attend_workspace_bytes)(d, B)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    form = "materialized" if materialized else "latent"
+    ws = torch.empty(vm.attend_workspace_bytes(d, B, vm.AttendOpts(form=form)), dtype=torch.uint8,
+                     device=dev)
     w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
     vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
     for f in range(0, d.window_frames, d.chunk_frames):
@@ -555,12 +600,18 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
     xs = [normal((B, nq, d.d_model)) for _ in range(x_buffers)]
     torch.cuda.synchronize()
 
-    def step(i):
-        vm.cache_write_prepared(d, fe, B, xs[i % len(xs)], w_packed, gamma, c_kv, k_r)
-        vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, materialized=materialized)
+    def attend(o):
+        vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, opts=o)
+
+    def step(i, timer=None):
+        bracket(timer, "cache_write", lambda: vm.cache_write_prepared(d, fe, B, xs[i % len(xs)], w_packed,
+                                                            gamma, c_kv, k_r))
+        attend(vm.AttendOpts(partition=partition, form=form, timer=timer))
 
     for i in range(warmup):
         step(i)
+    if partition == "frozen":
+        calibrate(vm, torch, lambda o: attend(dataclasses.replace(o, form=form)))
     torch.cuda.synchronize()
     names = (("cache_write", "mat_kv", "mat_q_prep", "mat_attend", "mat_merge") if materialized
              else ("cache_write", "q_absorb", "latent_attend", "out_proj"))
@@ -582,7 +633,8 @@ def latent_vs_materialized(args, vm, torch):
         res = {}
         for name, mat in (("latent", False), ("materialized", True)):
             log(f"{label}: {name}")
-            ms, k = chunk_step_kernels(vm, torch, d, 1, steps, args.warmup, seed=52, materialized=mat)
+            ms, k = chunk_step_kernels(vm, torch, d, 1, steps, args.warmup, seed=52, materialized=mat,
+                                       partition=args.partition)
             res[name] = {"ms_per_step": round(ms, 4), "kernels_us": k}
         rows = d.chunk_tokens * d.n_heads
         flop_lat = rows * d.window_tokens * 2 * (2 * d.d_c + d.d_rope)
@@ -619,7 +671,8 @@ def dc_sweep(args, vm, torch, d0):
             rows.append(entry)
             continue
         log(f"d_c {dc}")
-        ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=50)
+        ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=50,
+                                   partition=args.partition)
         W = work_model(d)
         entry.update({"ms_per_step": round(ms, 4), "kernels_us": k,
                       "latent_attend_tflops": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12, 1),
@@ -628,7 +681,8 @@ def dc_sweep(args, vm, torch, d0):
         rows.append(entry)
     log("1-frame chunks")
     d = WAN_1F
-    ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=51)
+    ms, k = chunk_step_kernels(vm, torch, d, 1, max(10, args.steps // 2), args.warmup, seed=51,
+                               partition=args.partition)
     W = work_model(d)
     few = {"chunk_tokens": d.chunk_tokens, "ms_per_step": round(ms, 4), "kernels_us": k,
            "latent_attend_tflops": round(W["attend_core"] / (k["latent_attend"] / 1e6) / 1e12, 1),
@@ -668,8 +722,11 @@ def main():
                          "sweep and with 1-frame chunks; wan-latent-vs-materialized: the "
                          "latent and the materialized-K/V attention at both head splits")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
-    ap.add_argument("--attend-balance", type=int, choices=(0, 1), default=1,
-                    help="1 (default): adaptive per-XCD work partition of the latent attention; 0: even split")
+    ap.add_argument("--partition", choices=("frozen", "even", "adaptive"), default="frozen",
+                    help="work partition of the attention calls: frozen (default; per-XCD "
+                         "weights calibrated by a few adaptive calls before the timed region, "
+                         "then fixed: bitwise reproducible), even, or adaptive (re-weighted "
+                         "every call)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -681,8 +738,6 @@ def main():
 
     import paper_2605_30351_amd as vm
     from workloads import WAN, make_layer_inputs
-
-    vm.set_attend_balance(bool(args.attend_balance))
 
     if args.workload == "wan-30-layer-chunk":
         thirty_layer_chunk(args, vm, torch, WAN)
@@ -734,13 +789,19 @@ def main():
     del x_all
     torch.cuda.synchronize()
 
-    def step(i):
-        vm.cache_write_prepared(d, fe, 1, xs[i % len(xs)], w_packed, gamma, c_kv, k_r)
-        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws)
+    def attend(o):
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, opts=o)
+
+    def step(i, timer=None, partition=args.partition):
+        bracket(timer, "cache_write", lambda: vm.cache_write_prepared(d, fe, 1, xs[i % len(xs)], w_packed,
+                                                            gamma, c_kv, k_r))
+        attend(vm.AttendOpts(partition=partition, timer=timer))
 
     log(f"warmup {args.warmup}")
     for i in range(args.warmup):
         step(i)
+    if args.partition == "frozen":
+        calibrate(vm, torch, attend)  # per-XCD weights for the frozen calls below
     torch.cuda.synchronize()
 
     if args.copy_probe:
@@ -750,48 +811,58 @@ def main():
     # The timed region carries HIP events around the roofline kernel (latent_attend) only: every
     # event pair adds a few microseconds to the step. The per-kernel breakdown comes from a
     # second pass of the same steps with every kernel bracketed.
-    names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
     log(f"timing {args.steps} steps")
-    vm.timing_enable(True)
-    vm.timing_only("latent_attend")
-    for k in names:
-        vm.timing_read(k)  # drop anything recorded before the timed region
+    k3_timer = vm.Timer()
+    k3_timer.only("latent_attend")
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     marks[0].record()
     for i in range(args.steps):
-        step(i)
+        step(i, k3_timer)
         marks[i + 1].record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     step_ms = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)])
-    n_k3, t_k3 = vm.timing_read("latent_attend")
+    n_k3, t_k3 = k3_timer.read("latent_attend")
     log("timed region done")
+    frozen_out = out.clone() if args.partition == "frozen" else None
 
-    vm.timing_only(None)
+    names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
     kernels = {}
+    all_timer = vm.Timer()
     for i in range(args.steps):
-        step(i)
+        step(i, all_timer)
     torch.cuda.synchronize()
     for k in names:
-        n, tot = vm.timing_read(k)
+        n, tot = all_timer.read(k)
         kernels[k] = {"launches": n, "avg_us": 1e3 * tot / max(n, 1)}
-    vm.timing_enable(False)
-
-    # the cache write alone with one x buffer, which then stays in the 256 MB Infinity Cache
-    vm.timing_enable(True)
-    vm.timing_read("cache_write")
-    for _ in range(20):
-        vm.cache_write_prepared(d, fe, 1, xs[0], w_packed, gamma, c_kv, k_r)
+    # the same steps with the even split, for comparison with the measured partition
+    for i in range(args.steps):
+        step(i, all_timer, "even")
     torch.cuda.synchronize()
-    n_warm_mall, t_warm_mall = vm.timing_read("cache_write")
+    n_even, t_even = all_timer.read("latent_attend")
+    if frozen_out is not None:  # frozen calls repeat bitwise
+        attend(vm.AttendOpts(partition="frozen"))
+        torch.cuda.synchronize()
+        repeat_ok = bool(torch.equal(out.view(torch.int16), frozen_out.view(torch.int16)))
+    all_timer.read("cache_write")
+    # the cache write alone with one x buffer, which then stays in the 256 MB Infinity Cache
+    for _ in range(20):
+        bracket(all_timer, "cache_write", lambda: vm.cache_write_prepared(
+            d, fe, 1, xs[0], w_packed, gamma, c_kv, k_r))
+    torch.cuda.synchronize()
+    n_w, t_w = all_timer.read("cache_write")
+    warm_mall_us = 1e3 * t_w / max(n_w, 1)
     # the same write from the plain row-major weights (videomla_cache_write), rotating x buffers
     for i in range(50):
-        vm.cache_write(d, fe, 1, xs[i % len(xs)], w_dkv, w_kr, gamma, c_kv, k_r)
+        x = xs[i % len(xs)]
+        bracket(all_timer, "cache_write", lambda: vm.cache_write(d, fe, 1, x, w_dkv, w_kr, gamma,
+                                                                 c_kv, k_r))
     torch.cuda.synchronize()
-    n_plain, t_plain = vm.timing_read("cache_write")
-    vm.timing_enable(False)
+    n_p, t_p = all_timer.read("cache_write")
+    plain_us = 1e3 * t_p / max(n_p, 1)
+    all_timer.close()
 
     ms = 1e3 * elapsed / args.steps
     W = work_model(d)
@@ -800,6 +871,7 @@ def main():
     k3_s = t_k3 / max(n_k3, 1) / 1e3  # from the timed region
     k3_tflops = W["attend_core"] / k3_s / 1e12
     wr_s = kernels["cache_write"]["avg_us"] / 1e6
+    even_s = t_even / max(n_even, 1) / 1e3
 
     result = {
         "metric": "ms/chunk-step & TFLOP/s for latent-MLA attend (Wan-1.3B shape); % MFMA peak",
@@ -822,7 +894,7 @@ def main():
             "d_model": d.d_model, "heads": d.n_heads, "d_nope": d.d_nope, "d_rope": d.d_rope,
             "d_c": d.d_c, "d_v": d.d_v, "chunk_tokens": d.chunk_tokens,
             "window_tokens": d.window_tokens, "rope_pairs": list(d.rope_pairs), "seed": 1,
-            "attend_partition": "adaptive per-XCD" if args.attend_balance else "even",
+            "attend_partition": args.partition,
         },
         "attend": {
             "ms": round(att_ms, 4),
@@ -833,14 +905,17 @@ def main():
             "us": round(wr_s * 1e6, 3),
             "gbps": round(W["write_bytes"] / wr_s / 1e9, 1),
             "hbm_frac": round(W["write_bytes"] / wr_s / 1e9 / HBM_PEAK_GBPS, 4),
-            "warm_infinity_cache_us": round(1e3 * t_warm_mall / max(n_warm_mall, 1), 3),
+            "warm_infinity_cache_us": round(warm_mall_us, 3),
             "weights": "packed once (videomla_prepare_write_weights)",
-            "plain_weights_us": round(1e3 * t_plain / max(n_plain, 1), 3),
+            "plain_weights_us": round(plain_us, 3),
         },
         "kernels": {k: {"launches": v["launches"], "avg_us": round(v["avg_us"], 3)}
                     for k, v in kernels.items()},
         "kernels_pass": "a second pass of the same steps with every kernel bracketed by events; "
                         "the timed region brackets latent_attend only",
+        "latent_attend_even_split": {"avg_us": round(even_s * 1e6, 3),
+                                     "frac": round(W["attend_core"] / even_s / 1e12
+                                                   / MFMA_BF16_PEAK_TFLOPS, 4)},
         "roofline": {
             "kernel": "latent_attend",
             "bound": "mfma",
@@ -853,6 +928,8 @@ def main():
             "traffic": attend_traffic(),
         },
     }
+    if frozen_out is not None:
+        result["frozen_repeat_bitwise_equal"] = repeat_ok
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         del xs

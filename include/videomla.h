@@ -88,6 +88,69 @@ typedef struct videomla_window {
 } videomla_window;
 
 /*
+ * Options of the attention calls (videomla_attend_ex, videomla_attend_layer,
+ * videomla_dense_attend and their workspace-size queries). A NULL options pointer, or a
+ * zero-initialized struct, gives the defaults. The library keeps no state between calls: every
+ * choice a call depends on is in its arguments, and the adaptive partition keeps its record in
+ * the caller's workspace.
+ *
+ *   n_workgroups   workgroups of the attention kernel; 0 = one per compute unit. The
+ *                  (batch, row block, key tile) units are split over them; a row block shared by
+ *                  several workgroups leaves one partial result per workgroup, merged exactly by
+ *                  their running maxima and sums (the online-softmax merge). Changes the
+ *                  workspace size.
+ *   partition      VIDEOMLA_PARTITION_EVEN (default): the units are split evenly; outputs are
+ *                    bitwise reproducible.
+ *                  VIDEOMLA_PARTITION_ADAPTIVE: workgroup k runs on XCD k mod 8, and the XCDs of
+ *                    one device can run at different clocks under this load. Each call gives
+ *                    each XCD's workgroups a share of the units proportional to the work per
+ *                    time that XCD achieved in the previous adaptive call on the same workspace
+ *                    (each weight within [0.8, 1.25] of the mean), and records its own times
+ *                    there. Split points, and so the rounding of the outputs, can change from
+ *                    call to call.
+ *                  VIDEOMLA_PARTITION_FROZEN: the weights the last adaptive call on this
+ *                    workspace computed (equal weights if there was none), recording nothing:
+ *                    outputs are bitwise reproducible from call to call. Calibrate with a few
+ *                    adaptive calls, then freeze.
+ *                  The state takes 16.4 KB at the end of the workspace. Shapes whose ranges could
+ *                  get too short for the workspace's partial-result slots keep the even split.
+ *                  Calls that share a workspace must be ordered on one stream.
+ *   form           VIDEOMLA_FORM_LATENT (default): the absorbed form (App. "Inference-Time
+ *                    Reparameterization", Eqs. 8-11).
+ *                  VIDEOMLA_FORM_MATERIALIZED: the training form (Eq. 2, Eq. 7), per-head keys and
+ *                    values reconstructed for the window each call (videomla_attend_ex only).
+ *                  VIDEOMLA_FORM_AUTO: whichever of the two the library's cost model predicts to
+ *                    be faster for (dims, batch, query rows) over a full window; the latent form
+ *                    where the materialized one is not built. The choice does not depend on
+ *                    frame_end, so the workspace-size query sees the same form.
+ *                  Both forms compute the same attention; they differ in rounding only.
+ *   query_begin,   the call attends the queries of chunk tokens query_begin ..
+ *   query_count      query_begin + query_count - 1 (query_count 0 = to the end of the chunk):
+ *                  a block of the chunk's query rows, as one GPU's share of a query-sharded
+ *                  chunk, or the few-query regime. q_nope, q_r (q, x) and out (y) then hold
+ *                  query_count tokens per batch element, at their chunk positions.
+ *   timer          a caller-owned timer (videomla_timer_create), or NULL: each kernel the call
+ *                  launches is bracketed by two HIP events recorded on its stream.
+ */
+#define VIDEOMLA_PARTITION_EVEN 0
+#define VIDEOMLA_PARTITION_ADAPTIVE 1
+#define VIDEOMLA_PARTITION_FROZEN 2
+#define VIDEOMLA_FORM_LATENT 0
+#define VIDEOMLA_FORM_MATERIALIZED 1
+#define VIDEOMLA_FORM_AUTO 2
+
+typedef struct videomla_timer videomla_timer;
+
+typedef struct videomla_attend_opts {
+  int32_t n_workgroups;
+  int32_t partition;
+  int32_t form;
+  int32_t query_begin;
+  int32_t query_count;
+  videomla_timer* timer;
+} videomla_attend_opts;
+
+/*
  * videomla_cache_write -- compress the chunk's tokens and write them into the ring
  * (Eq. 1: c = W_down^KV x; RMSNorm of c when kv_norm_w != NULL; Eq. 5: k^R = W_R^K x rotated by
  * RoPE_3D at the token's absolute (f, y, x); FIFO placement of whole frames).
@@ -136,8 +199,12 @@ int videomla_cache_write_prepared(const videomla_dims* dims, const videomla_wind
                                   const uint16_t* kv_norm_w, uint16_t* c_kv, uint16_t* k_r,
                                   int32_t* slots_out, void* stream);
 
-/* Bytes of device workspace videomla_attend needs for this shape and batch. */
+/* Bytes of device workspace videomla_attend needs for this shape and batch (0 if the dims are
+ * invalid or not supported); videomla_attend_workspace_bytes_ex for videomla_attend_ex with
+ * these options (the form, work partition and query rows change it). */
 size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch);
+size_t videomla_attend_workspace_bytes_ex(const videomla_dims* dims, int32_t batch,
+                                          const videomla_attend_opts* opts);
 
 /*
  * videomla_attend -- latent multi-head attention of the chunk's queries over the window.
@@ -165,6 +232,8 @@ size_t videomla_attend_workspace_bytes(const videomla_dims* dims, int32_t batch)
  * Requires d_nope % 16 == 0 and d_nope <= 128, d_v % 32 == 0 and d_v <= 256,
  * (d_c, d_rope) in {(64, 32), (128, 32), (192, 32), (256, 32), (512, 32), (16, 8)} (the widths
  * of the paper's d_c sweep, Table 5, and a tiny test shape), otherwise VIDEOMLA_EUNSUPPORTED.
+ * The work is split evenly over one workgroup per compute unit, so outputs are bitwise
+ * reproducible; videomla_attend_ex takes other choices.
  */
 int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                     const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
@@ -172,25 +241,28 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * videomla_attend_materialized -- the same attention computed in the training form (Eq. 2 and
+ * videomla_attend_ex -- videomla_attend with options (videomla_attend_opts; NULL = the
+ * defaults, which make it videomla_attend). With query_begin / query_count, q_nope, q_r and out
+ * hold [batch][query_count][n_heads][...] and the queries sit at chunk tokens query_begin ..;
+ * the window is the same.
+ * With form VIDEOMLA_FORM_MATERIALIZED the attention is computed in the training form (Eq. 2 and
  * Eq. 7; App. "Inference-Time Reparameterization" states that the absorbed form equals it):
  * per-head keys and values are reconstructed for every valid slot of the window,
  *   K_h[j] = [W_up,h^K c_kv[j] ; k_r[j]]  (d_nope + d_rope),   V_h[j] = W_up,h^V c_kv[j]  (d_v),
  * then standard softmax attention runs per head with q = [q_nope ; RoPE_3D(q_r)]. It trades the
  * reconstruction (a GEMM over the window, once per call) for a cheaper score: d_nope + d_rope +
- * d_v multiply-adds per (query, head, key) instead of the latent form's 2 d_c + d_rope.
- * Arguments, layouts and result as videomla_attend; the workspace (at least
- * videomla_attend_materialized_workspace_bytes() bytes) also holds the reconstructed rows.
- * Requires d_v == 128 and d_nope + d_rope in {128 (the paper's 96 + 32), 160 (128 + 32)},
- * d_c % 64 == 0, sink_frames == 0; otherwise VIDEOMLA_EUNSUPPORTED. The work partition follows
- * videomla_set_attend_workgroups.
+ * d_v multiply-adds per (query, head, key) instead of the latent form's 2 d_c + d_rope; the
+ * workspace also holds the reconstructed rows. That form requires d_v == 128, d_nope + d_rope in
+ * {128 (the paper's 96 + 32), 160 (128 + 32)}, d_c % 64 == 0 and sink_frames == 0, otherwise
+ * VIDEOMLA_EUNSUPPORTED. The workspace must be at least videomla_attend_workspace_bytes_ex()
+ * bytes for the same options. EINVAL for options out of range (partition or form unknown,
+ * n_workgroups outside [0, 2^20], a query range outside the chunk).
  */
-size_t videomla_attend_materialized_workspace_bytes(const videomla_dims* dims, int32_t batch);
-int videomla_attend_materialized(const videomla_dims* dims, const videomla_window* win,
-                                 int32_t batch, const uint16_t* q_nope, const uint16_t* q_r,
-                                 const uint16_t* w_uk, const uint16_t* w_uv,
-                                 const uint16_t* c_kv, const uint16_t* k_r, uint16_t* out,
-                                 void* workspace, size_t workspace_bytes, void* stream);
+int videomla_attend_ex(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                       const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                       const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                       uint16_t* out, void* workspace, size_t workspace_bytes,
+                       const videomla_attend_opts* opts, void* stream);
 
 /*
  * The whole attention layer in latent form (App. "Inference-Time Reparameterization",
@@ -228,9 +300,9 @@ int videomla_prepare_layer_weights(const videomla_dims* dims, int32_t d_q, const
                                    const uint16_t* w_uv, const uint16_t* w_o, void* weights,
                                    size_t weights_bytes, void* stream);
 
-/* Bytes of device workspace videomla_attend_layer needs for this shape, d_q and batch. */
+/* Bytes of device workspace videomla_attend_layer needs for this shape, d_q, batch and options. */
 size_t videomla_attend_layer_workspace_bytes(const videomla_dims* dims, int32_t d_q,
-                                             int32_t batch);
+                                             int32_t batch, const videomla_attend_opts* opts);
 
 /*
  * videomla_attend_layer -- the layer above for the chunk at win->frame_end, over the same
@@ -241,12 +313,15 @@ size_t videomla_attend_layer_workspace_bytes(const videomla_dims* dims, int32_t 
  *   y        [batch][chunk_frames * HW][d_model]   bf16, output of the output projection
  * Arithmetic: bf16 operands (c^Q before its normalization, q_cat, o_lat and the packed weights
  * are rounded to bf16), fp32 accumulation, softmax and normalization factors.
- * Requirements of videomla_attend and of videomla_prepare_layer_weights.
+ * Requirements of videomla_attend and of videomla_prepare_layer_weights. opts (or NULL) as for
+ * videomla_attend_ex, except that the form is always the latent one (form must be LATENT or
+ * AUTO); with a query range x and y hold query_count tokens per batch element.
  */
 int videomla_attend_layer(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                           int32_t d_q, const uint16_t* x, const void* weights,
                           size_t weights_bytes, const uint16_t* c_kv, const uint16_t* k_r,
-                          uint16_t* y, void* workspace, size_t workspace_bytes, void* stream);
+                          uint16_t* y, void* workspace, size_t workspace_bytes,
+                          const videomla_attend_opts* opts, void* stream);
 
 /*
  * Dense per-head comparator: the cache VideoMLA replaces, built only to measure the latent
@@ -279,8 +354,9 @@ int videomla_dense_cache_write(const videomla_dims* dims, const videomla_window*
                                const uint16_t* w_v, uint16_t* kv, int32_t* slots_out,
                                void* stream);
 
-/* Bytes of device workspace videomla_dense_attend needs for this shape and batch. */
-size_t videomla_dense_attend_workspace_bytes(const videomla_dims* dims, int32_t batch);
+/* Bytes of device workspace videomla_dense_attend needs for this shape, batch and options. */
+size_t videomla_dense_attend_workspace_bytes(const videomla_dims* dims, int32_t batch,
+                                             const videomla_attend_opts* opts);
 
 /*
  * videomla_dense_attend -- standard per-head softmax attention of the chunk's queries over the
@@ -292,70 +368,64 @@ size_t videomla_dense_attend_workspace_bytes(const videomla_dims* dims, int32_t 
  *   kv    the ring as written by videomla_dense_cache_write
  *   out   [batch][chunk_frames * HW][n_heads][d_v]   bf16
  *   workspace  device buffer of at least videomla_dense_attend_workspace_bytes() bytes
- * Arithmetic as videomla_attend. Requires d_v == 128 and sink_frames == 0. The work
- * partition follows videomla_set_attend_workgroups.
+ * Arithmetic as videomla_attend. Requires d_v == 128 and sink_frames == 0. opts (or NULL) as
+ * for videomla_attend_ex (form ignored); with a query range q and out hold query_count tokens.
  */
 int videomla_dense_attend(const videomla_dims* dims, const videomla_window* win, int32_t batch,
                           const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
-                          size_t workspace_bytes, void* stream);
+                          size_t workspace_bytes, const videomla_attend_opts* opts,
+                          void* stream);
 
-/* Slide the window after the last denoising step of a chunk: frame_end += chunk_frames.
- * Host only; eviction is implicit (the next chunk's write overwrites the oldest frames). */
+/* Slide the window after the last denoising step of a chunk (App. "Chunk-Causal Sliding-Window
+ * Attention": each chunk's frames join the window and the oldest frames leave it, first in first
+ * out): frame_end += chunk_frames. Host only; the eviction itself is implicit, since the next
+ * chunk's videomla_cache_write overwrites the frame slots of the oldest frames. EINVAL for
+ * invalid dims or a NULL / negative window. */
 int videomla_window_advance(const videomla_dims* dims, videomla_window* win);
 
-/* Bytes the ring holds per token and layer: 2 * (d_c + d_rope) (224 scalars = 448 B for Wan). */
+/* Bytes the ring holds per token and layer: 2 * (d_c + d_rope), one bf16 latent c^KV and one
+ * bf16 decoupled key k^R (Sec. "Compressed KV Cache Construction", Eq. 1 and Eq. 5; the cache
+ * traffic per cached token of Eqs. 15-16): 224 scalars = 448 B for Wan against 2 n_h d_h = 3,072
+ * for per-head keys and values. 0 for invalid dims. */
 size_t videomla_cache_bytes_per_token(const videomla_dims* dims);
 
-/* Number of valid ring slots the chunk at win->frame_end attends over:
- * min(window_frames, frame_end + chunk_frames) * HW. Negative on invalid arguments. */
+/* Number of valid ring slots the chunk at win->frame_end attends over (App. "Chunk-Causal
+ * Sliding-Window Attention": the window holds at most window_frames frames, the chunk
+ * included): min(window_frames, frame_end + chunk_frames) * HW. Negative on invalid arguments. */
 int64_t videomla_valid_tokens(const videomla_dims* dims, const videomla_window* win);
 
-/* Slot of the token at absolute position (f, y, x); negative on invalid arguments. */
+/* Ring slot of the token at absolute position (f, y, x), as videomla_cache_write places it
+ * (first-in first-out frame slots, App. "Chunk-Causal Sliding-Window Attention"); negative on
+ * invalid arguments. */
 int64_t videomla_slot_of(const videomla_dims* dims, int64_t f, int32_t y, int32_t x);
 
 /* Message describing the last non-zero return on this thread ("" if none). */
 const char* videomla_last_error(void);
 
 /*
- * Tuning knob: number of workgroups the attention kernel uses (0 = one per compute unit, the
- * default). The (batch, 256-row block, key tile) work is split evenly over them; a row block
- * shared by several workgroups leaves one partial result per workgroup, merged exactly by
- * their running maxima and sums. Changes videomla_attend_workspace_bytes. Process-wide.
+ * Kernel timing with HIP events, for benchmarks. A timer is a caller-owned host object; an
+ * attention call whose options name it brackets every kernel it launches (or, after
+ * videomla_timer_only, the launches of one kernel) with two events recorded on its stream.
+ * videomla_timer_begin / videomla_timer_end bracket whatever the caller enqueues between them on
+ * `stream` under one of the names, in the same way (the cache writes, which take no options,
+ * are timed like this as "cache_write" and "dense_cache_write"); a begin without its end is
+ * dropped by the next begin. After the caller has synchronized the stream, videomla_timer_read
+ * accumulates the elapsed time of all completed intervals of one name ("q_absorb",
+ * "latent_attend", "out_proj", "rope_window", "bal_prep", "mat_kv", "mat_q_prep", "mat_attend",
+ * "mat_merge", "dense_q_prep", "dense_attend", "dense_merge", "q_down", "q_up", "latent_merge",
+ * "out_mix", "cache_write", "dense_cache_write") into *count and *total_ms, and forgets them.
+ * videomla_timer_only(timer, NULL) times every kernel again; EINVAL for an unknown name or a
+ * NULL timer. The events are created without the system-scope fence (GPU-side intervals on one
+ * device). A timer may be used by one thread at a time; destroying it releases its events (the
+ * caller must have synchronized the streams they were recorded on).
  */
-int videomla_set_attend_workgroups(int32_t n_workgroups);
-
-/*
- * Tuning knob: adaptive work partition of the attention kernels (videomla_attend,
- * videomla_attend_layer, videomla_attend_materialized and videomla_dense_attend; 0 = the even
- * split, the default; 1 = adaptive). Workgroup k runs on XCD
- * k mod 8, and the XCDs of one device can run at different clocks under this load; the call
- * then waits for the slowest. In adaptive mode each call gives each XCD's workgroups a share of
- * the units proportional to the work per time that XCD achieved in the previous adaptive call
- * on the same workspace (each weight within [0.8, 1.25] of the mean), recorded in a 33 KB state
- * area at the end of the workspace. The first call, or one after a call with another workgroup
- * count, splits evenly. The merge of the partial results stays exact, but the split points, and
- * so the rounding of the outputs, can differ from call to call: outputs are not bitwise
- * reproducible in this mode. Shapes whose ranges could get too short for the workspace's
- * partial-result slots keep the even split. Process-wide; calls that share a workspace must be
- * ordered on one stream, as in the default mode.
- */
-int videomla_set_attend_balance(int32_t on);
-
-/*
- * Kernel timing with HIP events, for benchmarks. When enabled, every kernel the library
- * launches is bracketed by two events recorded on the same stream. After the caller has
- * synchronized the stream, videomla_timing_read accumulates the elapsed time of all completed
- * launches of one kernel ("cache_write", "q_absorb", "latent_attend", "out_proj",
- * "dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge", "rope_window", "q_down",
- * "q_up", "latent_merge", "out_mix", "prepare_layer_weights") into
- * *count and *total_ms, and forgets them. videomla_timing_only restricts the bracketing to the
- * launches of one kernel (NULL: every kernel again), so that a timed loop carries the events of
- * that kernel only; VIDEOMLA_EINVAL for an unknown name. Timing state is process-wide and not
- * thread-safe.
- */
-int videomla_timing_enable(int32_t enable);
-int videomla_timing_only(const char* kernel);
-int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms);
+int videomla_timer_create(videomla_timer** timer);
+int videomla_timer_destroy(videomla_timer* timer);
+int videomla_timer_only(videomla_timer* timer, const char* kernel);
+int videomla_timer_begin(videomla_timer* timer, const char* kernel, void* stream);
+int videomla_timer_end(videomla_timer* timer, const char* kernel, void* stream);
+int videomla_timer_read(videomla_timer* timer, const char* kernel, int64_t* count,
+                        double* total_ms);
 
 #ifdef __cplusplus
 }

@@ -6,12 +6,12 @@ streams; importing it fails if the library has not been built.
 """
 from ._lib import (  # noqa: F401
     EXPORTED,
+    AttendOpts,
+    Timer,
     VideomlaError,
     attend,
     attend_layer,
     attend_layer_workspace_bytes,
-    attend_materialized,
-    attend_materialized_workspace_bytes,
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,
@@ -24,12 +24,7 @@ from ._lib import (  # noqa: F401
     make_dims,
     prepare_layer_weights,
     prepare_write_weights,
-    set_attend_balance,
-    set_attend_workgroups,
     slot_of,
-    timing_enable,
-    timing_only,
-    timing_read,
     valid_tokens,
     window_advance,
     write_weights_bytes,

@@ -7,6 +7,7 @@ at import time if the shared library has not been built, and never falls back to
 from __future__ import annotations
 
 import ctypes
+import dataclasses
 import os
 
 import torch
@@ -24,16 +25,19 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
 EXPORTED = (
     "videomla_cache_write", "videomla_write_weights_bytes", "videomla_prepare_write_weights",
     "videomla_cache_write_prepared", "videomla_attend_workspace_bytes", "videomla_attend",
-    "videomla_attend_materialized_workspace_bytes", "videomla_attend_materialized",
+    "videomla_attend_workspace_bytes_ex", "videomla_attend_ex",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
-    "videomla_slot_of", "videomla_last_error", "videomla_set_attend_workgroups",
-    "videomla_set_attend_balance",
-    "videomla_timing_enable", "videomla_timing_only", "videomla_timing_read",
+    "videomla_slot_of", "videomla_last_error",
+    "videomla_timer_create", "videomla_timer_destroy", "videomla_timer_only",
+    "videomla_timer_begin", "videomla_timer_end", "videomla_timer_read",
     "videomla_dense_cache_bytes_per_token", "videomla_dense_cache_write",
     "videomla_dense_attend_workspace_bytes", "videomla_dense_attend",
     "videomla_layer_weights_bytes", "videomla_prepare_layer_weights",
     "videomla_attend_layer_workspace_bytes", "videomla_attend_layer",
 )
+
+PARTITION = {"even": 0, "adaptive": 1, "frozen": 2}
+FORM = {"latent": 0, "materialized": 1, "auto": 2}
 
 
 class VideomlaDims(ctypes.Structure):
@@ -52,9 +56,16 @@ class VideomlaWindow(ctypes.Structure):
     _fields_ = [("frame_end", ctypes.c_int64)]
 
 
+class VideomlaAttendOpts(ctypes.Structure):
+    _fields_ = [("n_workgroups", ctypes.c_int32), ("partition", ctypes.c_int32),
+                ("form", ctypes.c_int32), ("query_begin", ctypes.c_int32),
+                ("query_count", ctypes.c_int32), ("timer", ctypes.c_void_p)]
+
+
 _P = ctypes.c_void_p
 _DP = ctypes.POINTER(VideomlaDims)
 _WP = ctypes.POINTER(VideomlaWindow)
+_OP = ctypes.POINTER(VideomlaAttendOpts)
 
 _lib.videomla_cache_write.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P]
 _lib.videomla_cache_write.restype = ctypes.c_int
@@ -69,11 +80,11 @@ _lib.videomla_attend_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
                                  ctypes.c_size_t, _P]
 _lib.videomla_attend.restype = ctypes.c_int
-_lib.videomla_attend_materialized_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
-_lib.videomla_attend_materialized_workspace_bytes.restype = ctypes.c_size_t
-_lib.videomla_attend_materialized.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P,
-                                              _P, _P, ctypes.c_size_t, _P]
-_lib.videomla_attend_materialized.restype = ctypes.c_int
+_lib.videomla_attend_workspace_bytes_ex.argtypes = [_DP, ctypes.c_int32, _OP]
+_lib.videomla_attend_workspace_bytes_ex.restype = ctypes.c_size_t
+_lib.videomla_attend_ex.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
+                                    ctypes.c_size_t, _OP, _P]
+_lib.videomla_attend_ex.restype = ctypes.c_int
 _lib.videomla_window_advance.argtypes = [_DP, _WP]
 _lib.videomla_window_advance.restype = ctypes.c_int
 _lib.videomla_cache_bytes_per_token.argtypes = [_DP]
@@ -84,35 +95,37 @@ _lib.videomla_slot_of.argtypes = [_DP, ctypes.c_int64, ctypes.c_int32, ctypes.c_
 _lib.videomla_slot_of.restype = ctypes.c_int64
 _lib.videomla_last_error.argtypes = []
 _lib.videomla_last_error.restype = ctypes.c_char_p
-_lib.videomla_set_attend_workgroups.argtypes = [ctypes.c_int32]
-_lib.videomla_set_attend_workgroups.restype = ctypes.c_int
-_lib.videomla_set_attend_balance.argtypes = [ctypes.c_int32]
-_lib.videomla_set_attend_balance.restype = ctypes.c_int
-_lib.videomla_timing_enable.argtypes = [ctypes.c_int32]
-_lib.videomla_timing_enable.restype = ctypes.c_int
-_lib.videomla_timing_only.argtypes = [ctypes.c_char_p]
-_lib.videomla_timing_only.restype = ctypes.c_int
-_lib.videomla_timing_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
-                                      ctypes.POINTER(ctypes.c_double)]
-_lib.videomla_timing_read.restype = ctypes.c_int
+_lib.videomla_timer_create.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+_lib.videomla_timer_create.restype = ctypes.c_int
+_lib.videomla_timer_destroy.argtypes = [_P]
+_lib.videomla_timer_destroy.restype = ctypes.c_int
+_lib.videomla_timer_only.argtypes = [_P, ctypes.c_char_p]
+_lib.videomla_timer_only.restype = ctypes.c_int
+_lib.videomla_timer_begin.argtypes = [_P, ctypes.c_char_p, _P]
+_lib.videomla_timer_begin.restype = ctypes.c_int
+_lib.videomla_timer_end.argtypes = [_P, ctypes.c_char_p, _P]
+_lib.videomla_timer_end.restype = ctypes.c_int
+_lib.videomla_timer_read.argtypes = [_P, ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_double)]
+_lib.videomla_timer_read.restype = ctypes.c_int
 _lib.videomla_dense_cache_bytes_per_token.argtypes = [_DP]
 _lib.videomla_dense_cache_bytes_per_token.restype = ctypes.c_size_t
 _lib.videomla_dense_cache_write.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P]
 _lib.videomla_dense_cache_write.restype = ctypes.c_int
-_lib.videomla_dense_attend_workspace_bytes.argtypes = [_DP, ctypes.c_int32]
+_lib.videomla_dense_attend_workspace_bytes.argtypes = [_DP, ctypes.c_int32, _OP]
 _lib.videomla_dense_attend_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_dense_attend.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, ctypes.c_size_t,
-                                       _P]
+                                       _OP, _P]
 _lib.videomla_dense_attend.restype = ctypes.c_int
 _lib.videomla_layer_weights_bytes.argtypes = [_DP, ctypes.c_int32]
 _lib.videomla_layer_weights_bytes.restype = ctypes.c_size_t
 _lib.videomla_prepare_layer_weights.argtypes = [_DP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P,
                                                 _P, ctypes.c_size_t, _P]
 _lib.videomla_prepare_layer_weights.restype = ctypes.c_int
-_lib.videomla_attend_layer_workspace_bytes.argtypes = [_DP, ctypes.c_int32, ctypes.c_int32]
+_lib.videomla_attend_layer_workspace_bytes.argtypes = [_DP, ctypes.c_int32, ctypes.c_int32, _OP]
 _lib.videomla_attend_layer_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_attend_layer.argtypes = [_DP, _WP, ctypes.c_int32, ctypes.c_int32, _P, _P,
-                                       ctypes.c_size_t, _P, _P, _P, _P, ctypes.c_size_t, _P]
+                                       ctypes.c_size_t, _P, _P, _P, _P, ctypes.c_size_t, _OP, _P]
 _lib.videomla_attend_layer.restype = ctypes.c_int
 
 
@@ -141,6 +154,87 @@ def make_dims(d) -> VideomlaDims:
     s.kv_norm_eps = float(d.kv_norm_eps)
     s.sink_frames = int(getattr(d, "sink_frames", 0))
     return s
+
+
+class Timer:
+    """A caller-owned videomla_timer: kernels of the attention calls whose options name it are
+    bracketed by HIP events on their stream."""
+
+    def __init__(self):
+        h = ctypes.c_void_p()
+        _check(_lib.videomla_timer_create(ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def only(self, kernel: str | None = None):
+        """Bracket only this kernel's launches (None: every kernel)."""
+        _check(_lib.videomla_timer_only(self._h, None if kernel is None else kernel.encode()))
+
+    def begin(self, kernel: str, stream=None):
+        """videomla_timer_begin on the stream (default: torch's current stream)."""
+        _check(_lib.videomla_timer_begin(self._h, kernel.encode(), _stream(stream)))
+
+    def end(self, kernel: str, stream=None):
+        """videomla_timer_end on the stream (default: torch's current stream)."""
+        _check(_lib.videomla_timer_end(self._h, kernel.encode(), _stream(stream)))
+
+    def read(self, kernel: str) -> tuple[int, float]:
+        """(launches, total ms) of the completed launches of `kernel` since the last read."""
+        c, t = ctypes.c_int64(0), ctypes.c_double(0.0)
+        _check(_lib.videomla_timer_read(self._h, kernel.encode(), ctypes.byref(c),
+                                        ctypes.byref(t)))
+        return int(c.value), float(t.value)
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            _lib.videomla_timer_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+@dataclasses.dataclass
+class AttendOpts:
+    """videomla_attend_opts: workgroups (0 = one per compute unit), partition ("even",
+    "adaptive", "frozen"), form ("latent", "materialized", "auto"), the block of query tokens
+    [query_begin, query_begin + query_count) of the chunk (query_count 0 = to its end), timer."""
+
+    n_workgroups: int = 0
+    partition: str = "even"
+    form: str = "latent"
+    query_begin: int = 0
+    query_count: int = 0
+    timer: Timer | None = None
+
+    def struct(self) -> VideomlaAttendOpts:
+        o = VideomlaAttendOpts()
+        o.n_workgroups = int(self.n_workgroups)
+        o.partition = PARTITION[self.partition]
+        o.form = FORM[self.form]
+        o.query_begin = int(self.query_begin)
+        o.query_count = int(self.query_count)
+        o.timer = self.timer.handle if self.timer is not None else None
+        return o
+
+    def n_queries(self, dims) -> int:
+        """Query tokens per batch element of a call with these options."""
+        chunk = int(dims.chunk_frames) * int(dims.grid_h) * int(dims.grid_w)
+        return int(self.query_count) if self.query_count else chunk - int(self.query_begin)
+
+
+def _opts(opts: AttendOpts | None):
+    return ctypes.byref(opts.struct()) if opts is not None else None
+
+
+def _nq(dims, opts):
+    return (opts or AttendOpts()).n_queries(dims)
 
 
 def _ptr(t: torch.Tensor | None, name: str, dtypes=(torch.bfloat16, torch.int16, torch.uint16)):
@@ -228,17 +322,22 @@ def cache_write_prepared(dims, frame_end: int, batch: int, x, w_packed, gamma, c
         _stream(stream)))
 
 
-def attend_workspace_bytes(dims, batch: int) -> int:
-    return int(_lib.videomla_attend_workspace_bytes(ctypes.byref(make_dims(dims)), int(batch)))
+def attend_workspace_bytes(dims, batch: int, opts: AttendOpts | None = None) -> int:
+    """videomla_attend_workspace_bytes, or videomla_attend_workspace_bytes_ex with opts."""
+    d = make_dims(dims)
+    if opts is None:
+        return int(_lib.videomla_attend_workspace_bytes(ctypes.byref(d), int(batch)))
+    o = opts.struct()
+    return int(_lib.videomla_attend_workspace_bytes_ex(ctypes.byref(d), int(batch), ctypes.byref(o)))
 
 
 def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace,
-           stream=None, materialized=False):
-    """videomla_attend (or videomla_attend_materialized when `materialized`) on torch tensors;
+           stream=None, opts: AttendOpts | None = None):
+    """videomla_attend on torch tensors, or videomla_attend_ex when `opts` is given;
     `workspace` is a uint8 device tensor."""
     d = make_dims(dims)
     hw = d.grid_h * d.grid_w
-    nq = d.chunk_frames * hw
+    nq = _nq(dims, opts)
     _need(q_nope, "q_nope", batch * nq * d.n_heads * d.d_nope)
     _need(q_r, "q_r", batch * nq * d.n_heads * d.d_rope)
     _need(w_uk, "w_uk", d.n_heads * d.d_nope * d.d_c)
@@ -248,23 +347,14 @@ def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r,
     _need(out, "out", batch * nq * d.n_heads * d.d_v)
     w = VideomlaWindow(int(frame_end))
     ws = _ptr(workspace, "workspace", (torch.uint8,))
-    fn = _lib.videomla_attend_materialized if materialized else _lib.videomla_attend
-    _check(fn(
-        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
-        _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
-        _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
-
-
-def attend_materialized_workspace_bytes(dims, batch: int) -> int:
-    return int(_lib.videomla_attend_materialized_workspace_bytes(ctypes.byref(make_dims(dims)),
-                                                                 int(batch)))
-
-
-def attend_materialized(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out,
-                        workspace, stream=None):
-    """videomla_attend_materialized on torch tensors (arguments as attend)."""
-    attend(dims, frame_end, batch, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace, stream,
-           materialized=True)
+    args = [ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
+            _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
+            _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0]
+    if opts is None:
+        _check(_lib.videomla_attend(*args, _stream(stream)))
+    else:
+        o = opts.struct()
+        _check(_lib.videomla_attend_ex(*args, ctypes.byref(o), _stream(stream)))
 
 
 def dense_cache_bytes_per_token(dims) -> int:
@@ -288,23 +378,28 @@ def dense_cache_write(dims, frame_end: int, batch: int, x, w_k, w_v, kv, slots=N
         _ptr(w_v, "w_v"), _ptr(kv, "kv"), _ptr(slots, "slots", (torch.int32,)), _stream(stream)))
 
 
-def dense_attend_workspace_bytes(dims, batch: int) -> int:
-    return int(_lib.videomla_dense_attend_workspace_bytes(ctypes.byref(make_dims(dims)), int(batch)))
+def dense_attend_workspace_bytes(dims, batch: int, opts: AttendOpts | None = None) -> int:
+    o = opts.struct() if opts is not None else None
+    return int(_lib.videomla_dense_attend_workspace_bytes(
+        ctypes.byref(make_dims(dims)), int(batch), ctypes.byref(o) if o is not None else None))
 
 
-def dense_attend(dims, frame_end: int, batch: int, q, kv, out, workspace, stream=None):
+def dense_attend(dims, frame_end: int, batch: int, q, kv, out, workspace, stream=None,
+                 opts: AttendOpts | None = None):
     """videomla_dense_attend on torch tensors; `workspace` is a uint8 device tensor."""
     d = make_dims(dims)
     hw = d.grid_h * d.grid_w
-    nq = d.chunk_frames * hw
+    nq = _nq(dims, opts)
     _need(q, "q", batch * nq * d.n_heads * d.d_v)
     _need(kv, "kv", batch * d.window_frames * hw * d.n_heads * 2 * d.d_v)
     _need(out, "out", batch * nq * d.n_heads * d.d_v)
     w = VideomlaWindow(int(frame_end))
     ws = _ptr(workspace, "workspace", (torch.uint8,))
+    o = opts.struct() if opts is not None else None
     _check(_lib.videomla_dense_attend(
         ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q, "q"), _ptr(kv, "kv"),
-        _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0, _stream(stream)))
+        _ptr(out, "out"), ws, workspace.numel() if workspace is not None else 0,
+        ctypes.byref(o) if o is not None else None, _stream(stream)))
 
 
 def layer_weights_bytes(dims, d_q: int) -> int:
@@ -331,27 +426,31 @@ def prepare_layer_weights(dims, d_q: int, w_dq, gamma_q, w_uq, w_qr, w_uk, w_uv,
         _stream(stream)))
 
 
-def attend_layer_workspace_bytes(dims, d_q: int, batch: int) -> int:
-    return int(_lib.videomla_attend_layer_workspace_bytes(ctypes.byref(make_dims(dims)), int(d_q),
-                                                          int(batch)))
+def attend_layer_workspace_bytes(dims, d_q: int, batch: int, opts: AttendOpts | None = None) -> int:
+    o = opts.struct() if opts is not None else None
+    return int(_lib.videomla_attend_layer_workspace_bytes(
+        ctypes.byref(make_dims(dims)), int(d_q), int(batch),
+        ctypes.byref(o) if o is not None else None))
 
 
 def attend_layer(dims, frame_end: int, batch: int, d_q: int, x, weights, c_kv, k_r, y, workspace,
-                 stream=None):
+                 stream=None, opts: AttendOpts | None = None):
     """videomla_attend_layer on torch tensors; `weights` and `workspace` are uint8 device tensors."""
     d = make_dims(dims)
     hw = d.grid_h * d.grid_w
-    nq = d.chunk_frames * hw
+    nq = _nq(dims, opts)
     _need(x, "x", batch * nq * d.d_model)
     _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
     _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
     _need(y, "y", batch * nq * d.d_model)
     w = VideomlaWindow(int(frame_end))
+    o = opts.struct() if opts is not None else None
     _check(_lib.videomla_attend_layer(
         ctypes.byref(d), ctypes.byref(w), int(batch), int(d_q), _ptr(x, "x"),
         _ptr(weights, "weights", (torch.uint8,)), weights.numel(), _ptr(c_kv, "c_kv"),
         _ptr(k_r, "k_r"), _ptr(y, "y"), _ptr(workspace, "workspace", (torch.uint8,)),
-        workspace.numel() if workspace is not None else 0, _stream(stream)))
+        workspace.numel() if workspace is not None else 0,
+        ctypes.byref(o) if o is not None else None, _stream(stream)))
 
 
 def window_advance(dims, frame_end: int) -> int:
@@ -377,31 +476,6 @@ def slot_of(dims, f: int, y: int, x: int) -> int:
     if v < 0:
         raise VideomlaError(EINVAL, _lib.videomla_last_error().decode())
     return v
-
-
-def set_attend_workgroups(n: int):
-    """Workgroup count of the attention kernel (0 = one per compute unit)."""
-    _check(_lib.videomla_set_attend_workgroups(int(n)))
-
-
-def set_attend_balance(on: bool):
-    """Adaptive per-XCD work partition of the latent attention (off by default)."""
-    _check(_lib.videomla_set_attend_balance(1 if on else 0))
-
-
-def timing_enable(on: bool = True):
-    _check(_lib.videomla_timing_enable(1 if on else 0))
-
-
-def timing_only(kernel: str | None = None):
-    """videomla_timing_only: bracket only this kernel's launches (None: every kernel)."""
-    _check(_lib.videomla_timing_only(None if kernel is None else kernel.encode()))
-
-
-def timing_read(kernel: str) -> tuple[int, float]:
-    c, t = ctypes.c_int64(0), ctypes.c_double(0.0)
-    _check(_lib.videomla_timing_read(kernel.encode(), ctypes.byref(c), ctypes.byref(t)))
-    return int(c.value), float(t.value)
 
 
 def raw():

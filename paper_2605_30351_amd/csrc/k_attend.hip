@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int h = blockIdx.y, b = blockIdx.z;
-  const int H = a.n_heads, dn = a.d_nope, Nq = a.geo.chunk_tokens;
+  const int H = a.n_heads, dn = a.d_nope, Nq = a.geo.q_count;
   const int nks = dn / 16;
 
   const int n = blockIdx.x * 128 + wave * 32 + l32;
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
     const size_t r = ((size_t)b * Nq + t) * H + h;
     const uint32_t raw = *reinterpret_cast<const uint32_t*>(a.q_r + r * DR + 2 * p);
     float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff)), v = bf16_bits_to_f32((uint16_t)(raw >> 16));
-    rope_rotate(a.rope, p, rope_pos(a.geo, token_pos(a.geo, t)), u, v);
+    rope_rotate(a.rope, p, rope_pos(a.geo, query_pos(a.geo, t)), u, v);
     const uint32_t packed =
         (uint32_t)to_bf16_bits(u * a.qscale) | ((uint32_t)to_bf16_bits(v * a.qscale) << 16);
     *reinterpret_cast<uint32_t*>(STAGE ? ot + (t - tok0) * OS + DC + 2 * p
@@ -192,6 +192,58 @@ __global__ __launch_bounds__(256) void rope_window_kernel(const AttendArgs a) {
   rope_rotate(a.rope, p, pos, u, v);
   *reinterpret_cast<uint32_t*>(a.k_rot + off) =
       (uint32_t)to_bf16_bits(u) | ((uint32_t)to_bf16_bits(v) << 16);
+}
+
+// ---------------------------------------------------------------------------------------------
+// bal_prep (adaptive partition only): one wave, launched before the attention kernel of an
+// adaptive call. It reads the weights and per-workgroup durations the previous adaptive call on
+// this workspace left, and sets each XCD's weight proportional to the units per time its
+// workgroups achieved there (weight over the XCD's slowest workgroup time), normalized to a
+// mean of kBalOne and clamped to [kBalMin, kBalMax]; equal weights when the record is missing,
+// was made for another G, or lacks a duration. It then writes G and the marker, and clears the
+// durations, which the attention kernel of this call fills in. Lane l reads and clears the
+// durations of workgroups k = l mod 64 (XCD k mod 8 = l mod 8), so every duration is read and
+// cleared by the same lane.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void bal_prep_kernel(uint32_t* st, int G) {
+  const int lane = threadIdx.x;
+  uint32_t w_prev[8];
+  bal_weights(st, G, w_prev);
+  const bool hdr = st[9] == kBalMark && st[8] == (uint32_t)G;
+  uint32_t tmax = 0, tmin = 0xffffffffu;
+  for (int k = lane; k < G; k += 64) {
+    const uint32_t t = st[kBalHead + k];
+    tmax = max(tmax, t);
+    tmin = min(tmin, t);
+  }
+  // combine the lanes of one XCD (lanes x, x + 8, .., x + 56)
+#pragma unroll
+  for (int sh = 8; sh < 64; sh <<= 1) {
+    tmax = max(tmax, (uint32_t)__shfl_xor((int)tmax, sh));
+    tmin = min(tmin, (uint32_t)__shfl_xor((int)tmin, sh));
+  }
+  // every lane gathers the 8 per-XCD results (XCD x from lane x)
+  bool ok = hdr;
+  double sp[8], tot = 0.0;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const uint32_t mx = (uint32_t)__shfl((int)tmax, x), mn = (uint32_t)__shfl((int)tmin, x);
+    const int nx = G > x ? (G - x + 7) / 8 : 0;  // workgroups on XCD x
+    sp[x] = 0.0;
+    if (nx > 0) {
+      ok = ok && mn > 0u && mx < 1000000000u;
+      sp[x] = (double)w_prev[x] / (double)(mx > 0u ? mx : 1u);
+      tot += nx * sp[x];
+    }
+  }
+  uint32_t w_new[8];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const double v = ok && sp[x] > 0.0 ? kBalOne * sp[x] * G / tot : (double)kBalOne;
+    w_new[x] = (uint32_t)fmin(fmax(rint(v), (double)kBalMin), (double)kBalMax);
+  }
+  for (int k = lane; k < G; k += 64) st[kBalHead + k] = 0u;
+  if (lane < 10) st[lane] = lane < 8 ? w_new[lane] : lane == 8 ? (uint32_t)G : kBalMark;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -288,51 +340,25 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   const int g = lane >> 5, l32 = lane & 31;
   // query rows per batch element: (token, head) pairs, head-minor (latent); (head, token)
   // pairs with every head padded to whole row blocks (dense: a row block is one head's)
-  const int rows_b = DENSE ? a.n_heads * a.nq_pad : a.geo.chunk_tokens * a.n_heads;
+  const int rows_b = DENSE ? a.n_heads * a.nq_pad : a.geo.q_count * a.n_heads;
 
   // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
   // tiles of one row block is a segment with its own partial result.
   const int64_t U = a.units;
   const int G = a.n_wg, T = a.tiles_per_row;
   int64_t u_begin = (int64_t)blockIdx.x * U / G, u_end = (int64_t)(blockIdx.x + 1) * U / G;
-  // Adaptive split: each XCD's weight is proportional to the units per time its workgroups
-  // achieved in the previous call (slot (bal_seq - 1) & 1); equal weights if that slot does not
-  // hold a consistent record for this G.
-  __shared__ uint32_t bal_t[8];
+  // Weighted split: the per-XCD weights the partition state holds (set by bal_prep_kernel for an
+  // adaptive call, left as they are for a frozen one); an adaptive call records each
+  // workgroup's duration for the next one.
   uint32_t bw[8];
   uint64_t bal_t0 = 0;
   if (a.bal_on) {
-    bal_t0 = __builtin_amdgcn_s_memrealtime();
-    const uint32_t* prev = a.bal_state + ((a.bal_seq + 1) & 1) * kBalSlot;
-    uint32_t* next = a.bal_state + (a.bal_seq & 1) * kBalSlot;
-    if (tid < 8) bal_t[tid] = 0;
-    __syncthreads();
-    const bool hdr = prev[9] == kBalMark && prev[8] == (uint32_t)G;
-    if (hdr)
-      for (int k = tid; k < G; k += NW * 64) atomicMax(&bal_t[k & 7], prev[kBalHead + k]);
-    __syncthreads();
-    bool ok = hdr;
-    double sp[8], tot = 0.0;
+    bal_weights(a.bal_state, G, bw);
 #pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      const int nx = G > x ? (G - x + 7) / 8 : 0;  // workgroups on XCD x
-      const uint32_t w = prev[x], t = bal_t[x];
-      sp[x] = 0.0;
-      if (nx > 0) {
-        ok = ok && w >= kBalMin && w <= kBalMax && t > 0u && t < 1000000000u;
-        sp[x] = (double)w / (double)(t > 0u ? t : 1u);
-        tot += nx * sp[x];
-      }
-    }
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      const double v = ok && sp[x] > 0.0 ? kBalOne * sp[x] * G / tot : (double)kBalOne;
-      bw[x] = __builtin_amdgcn_readfirstlane(
-          (uint32_t)fmin(fmax(rint(v), (double)kBalMin), (double)kBalMax));
-    }
+    for (int x = 0; x < 8; ++x) bw[x] = __builtin_amdgcn_readfirstlane(bw[x]);
     u_begin = bal_start(bw, G, U, blockIdx.x);
     u_end = bal_start(bw, G, U, blockIdx.x + 1);
-    if (blockIdx.x == 0 && tid < 10) next[tid] = tid < 8 ? bw[tid] : tid == 8 ? (uint32_t)G : kBalMark;
+    if (a.bal_rec) bal_t0 = __builtin_amdgcn_s_memrealtime();
   }
   // Segments are taken last to first: a workgroup's last segment is the head of a row block
   // (keys from 0) and its first the tail of another, so in this order every workgroup walks the
@@ -724,9 +750,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     }
   }
   }  // segments
-  if (a.bal_on && tid == 0)
-    a.bal_state[(a.bal_seq & 1) * kBalSlot + kBalHead + blockIdx.x] =
-        (uint32_t)(__builtin_amdgcn_s_memrealtime() - bal_t0);
+  if (a.bal_rec && tid == 0)
+    a.bal_state[kBalHead + blockIdx.x] = (uint32_t)(__builtin_amdgcn_s_memrealtime() - bal_t0);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -781,7 +806,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, l32 = lane & 31;
   const int h = blockIdx.y, b = blockIdx.z;
-  const int H = a.n_heads, Nq = a.geo.chunk_tokens;
+  const int H = a.n_heads, Nq = a.geo.q_count;
   const int n0 = blockIdx.x * (NW * 32) + wave * 32;
   const size_t total_rows = (size_t)a.batch * Nq * H;
   auto row_of = [&](int t) {  // global row of the wave's token t
@@ -1012,7 +1037,7 @@ size_t q_absorb_lds_bytes(int d_c, int d_rope, int d_nope) {
 }
 
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s) {
-  const dim3 grid((a.geo.chunk_tokens + 127) / 128, a.n_heads, a.batch);
+  const dim3 grid((a.geo.q_count + 127) / 128, a.n_heads, a.batch);
   const size_t lds = q_absorb_lds_bytes(a.d_c, a.d_rope, a.d_nope);
 #define X(DC, DR)                                                                    \
   if (a.d_c == DC && a.d_rope == DR) {                                               \
@@ -1028,6 +1053,11 @@ hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s) {
   const int64_t threads = (int64_t)a.n_valid * (a.d_rope / 2);
   hipLaunchKernelGGL(rope_window_kernel, dim3((unsigned)((threads + 255) / 256), a.batch),
                      dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_bal_prep(const AttendArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(bal_prep_kernel, dim3(1), dim3(64), 0, s, a.bal_state, a.n_wg);
   return hipGetLastError();
 }
 
@@ -1052,12 +1082,12 @@ hipError_t launch_out_proj_v(const AttendArgs& a, hipStream_t s) {
   // waves per workgroup: the largest of P::NW, 4, 2 whose grid covers at least half of the CUs
   // (four waves with W_UV_h in LDS hold one workgroup per CU, so a grid of more than one
   // workgroup per CU would run in two rounds)
-  auto wgs = [&](int nw) { return (int64_t)((a.geo.chunk_tokens + 32 * nw - 1) / (32 * nw)) * a.n_heads * a.batch; };
+  auto wgs = [&](int nw) { return (int64_t)((a.geo.q_count + 32 * nw - 1) / (32 * nw)) * a.n_heads * a.batch; };
   const int n_cu = out_proj_cu_count();
   int nw = P::NW;
   if (2 * wgs(nw) < n_cu && nw > 4) nw = 4;
   if (2 * wgs(nw) < n_cu && nw > 2) nw = 2;
-  const dim3 grid((a.geo.chunk_tokens + 32 * nw - 1) / (32 * nw), a.n_heads, a.batch);
+  const dim3 grid((a.geo.q_count + 32 * nw - 1) / (32 * nw), a.n_heads, a.batch);
   if (nw == P::NW) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL>), grid, dim3(64 * nw), 0, s, a);
   else if (nw == 4) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 4, P::WL4>), grid, dim3(64 * nw), 0, s, a);
   else hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 2, P::WL2>), grid, dim3(64 * nw), 0, s, a);

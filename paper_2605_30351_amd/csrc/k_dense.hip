@@ -128,10 +128,10 @@ __global__ __launch_bounds__(256, 1) void dense_cache_write_kernel(const DenseWr
 __global__ __launch_bounds__(256) void dense_q_prep_kernel(const AttendArgs a) {
   const int t = threadIdx.x >> 6, p = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + t, b = blockIdx.y;
-  const int H = a.n_heads, DH = a.d_v, Nq = a.geo.chunk_tokens;
+  const int H = a.n_heads, DH = a.d_v, Nq = a.geo.q_count;
   if (2 * p >= DH) return;
   float cs = 1.f, sn = 0.f;
-  if (n < Nq) rope_rotate(a.rope, p, token_pos(a.geo, n), cs, sn);  // (1, 0) -> (cos, sin)
+  if (n < Nq) rope_rotate(a.rope, p, query_pos(a.geo, n), cs, sn);  // (1, 0) -> (cos, sin)
   for (int h = 0; h < H; ++h) {
     uint32_t packed = 0;
     if (n < Nq) {
@@ -155,12 +155,12 @@ __global__ __launch_bounds__(256) void dense_q_prep_kernel(const AttendArgs a) {
 __global__ __launch_bounds__(256) void mat_q_prep_kernel(const AttendArgs a) {
   const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int n = blockIdx.x * 4 + t, b = blockIdx.y;
-  const int H = a.n_heads, DN = a.d_nope, DR = a.d_rope, DH = a.dqk_pad, Nq = a.geo.chunk_tokens;
+  const int H = a.n_heads, DN = a.d_nope, DR = a.d_rope, DH = a.dqk_pad, Nq = a.geo.q_count;
   for (int p = lane; 2 * p < DH; p += 64) {  // channel pair p of the d_nope + d_rope wide row
     const bool rope = 2 * p >= DN;
     const int pr = p - DN / 2;  // RoPE pair (when rope)
     float cs = 1.f, sn = 0.f;
-    if (rope && n < Nq) rope_rotate(a.rope, pr, token_pos(a.geo, n), cs, sn);  // (1,0) -> (cos, sin)
+    if (rope && n < Nq) rope_rotate(a.rope, pr, query_pos(a.geo, n), cs, sn);  // (1,0) -> (cos, sin)
     for (int h = 0; h < H; ++h) {
       uint32_t packed = 0;
       if (n < Nq) {
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(256) void mat_rope_fill_kernel(const AttendArgs a, 
 __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
   const int DH = a.d_v, gpr = DH / 8;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int H = a.n_heads, Nq = a.geo.chunk_tokens;
+  const int H = a.n_heads, Nq = a.geo.q_count;
   const int64_t n_out = (int64_t)a.batch * Nq * H;
   const int64_t R = e / gpr;
   const int grp = (int)(e % gpr);
@@ -264,7 +264,7 @@ hipError_t launch_mat_rope_fill(const AttendArgs& a, uint16_t* kv, hipStream_t s
 }
 
 hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s) {
-  const int64_t threads = (int64_t)a.batch * a.geo.chunk_tokens * a.n_heads * (a.d_v / 8);
+  const int64_t threads = (int64_t)a.batch * a.geo.q_count * a.n_heads * (a.d_v / 8);
   hipLaunchKernelGGL(dense_merge_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                      a);
   return hipGetLastError();

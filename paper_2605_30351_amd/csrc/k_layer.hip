@@ -151,7 +151,7 @@ __global__ __launch_bounds__(P::kThreads, P::kMinBlocks) void gemm_nt_kernel(con
   if constexpr (EPI == kEpiQcat) {
     ssq = half_swap_sum(ssq);
     scale = a.qscale * rsqrtf(ssq / (float)a.q_norm_dim + a.eps);
-    if (t < a.M) pos = rope_pos(a.geo, token_pos(a.geo, t % a.geo.chunk_tokens));
+    if (t < a.M) pos = rope_pos(a.geo, query_pos(a.geo, t % a.geo.q_count));
   }
   if (t >= a.M) return;
 #pragma unroll
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(P::kThreads, P::kMinBlocks) void gemm_nt_kernel(con
 __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, uint16_t* o_lat,
                                                            int ld_olat) {
   const int DC = a.d_c, gpr = DC / 8, H = a.n_heads;
-  const int Nq = a.geo.chunk_tokens;
+  const int Nq = a.geo.q_count;
   const int rows_b = Nq * H;
   const int64_t n_rows = (int64_t)a.batch * rows_b;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -315,8 +315,8 @@ hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat, hipStream_t s) {
-  const int64_t rows = (int64_t)a.batch * a.geo.chunk_tokens * a.n_heads;
-  const int64_t pad = (int64_t)a.batch * a.geo.chunk_tokens * ((ld_olat - a.n_heads * a.d_c) / 8);
+  const int64_t rows = (int64_t)a.batch * a.geo.q_count * a.n_heads;
+  const int64_t pad = (int64_t)a.batch * a.geo.q_count * ((ld_olat - a.n_heads * a.d_c) / 8);
   const int64_t threads = rows * (a.d_c / 8) + pad;
   hipLaunchKernelGGL(latent_merge_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                      a, o_lat, ld_olat);

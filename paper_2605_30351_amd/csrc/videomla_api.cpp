@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -95,6 +96,8 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
   g.grid_w = d->grid_w;
   g.window_frames = d->window_frames;
   g.chunk_tokens = d->chunk_frames * d->grid_h * d->grid_w;
+  g.q_begin = 0;
+  g.q_count = g.chunk_tokens;
   g.frame_end = w->frame_end;
   g.ring_tokens = (int64_t)d->window_frames * d->grid_h * d->grid_w;
   g.sink_frames = d->sink_frames;
@@ -106,35 +109,47 @@ Geometry make_geo(const videomla_dims* d, const videomla_window* w) {
   return g;
 }
 
-// ---- timing -------------------------------------------------------------------------------
+}  // namespace
+
+// ---- timing ---------------------------------------------------------------------------------
+// A caller-owned timer: the event pairs of the launches it bracketed, not yet read, and a pool of
+// events to reuse. Used by one thread at a time.
+struct videomla_timer {
+  struct Rec {
+    int kernel;
+    hipEvent_t start, stop;
+  };
+  int only = -1;  // >= 0: time only this kernel
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  Rec open{-1, nullptr, nullptr};  // videomla_timer_begin without its end yet
+};
+
+namespace {
+
 enum KernelId {
-  K_CACHE_WRITE = 0, K_Q_ABSORB, K_LATENT_ATTEND, K_OUT_PROJ,
-  K_DENSE_CACHE_WRITE, K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE, K_ROPE_WINDOW,
-  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_PREPARE, K_PREPARE_WRITE,
-  K_MAT_KV, K_MAT_Q_PREP, K_MAT_ATTEND, K_MAT_MERGE, K_COUNT
+  K_Q_ABSORB = 0, K_LATENT_ATTEND, K_OUT_PROJ, K_ROPE_WINDOW, K_BAL_PREP,
+  K_MAT_KV, K_MAT_Q_PREP, K_MAT_ATTEND, K_MAT_MERGE,
+  K_DENSE_Q_PREP, K_DENSE_ATTEND, K_DENSE_MERGE,
+  K_Q_DOWN, K_Q_UP, K_LATENT_MERGE, K_OUT_MIX, K_CACHE_WRITE, K_DENSE_CACHE_WRITE, K_COUNT
 };
-const char* kKernelNames[K_COUNT] = {"cache_write",       "q_absorb",     "latent_attend",
-                                     "out_proj",          "dense_cache_write", "dense_q_prep",
-                                     "dense_attend",      "dense_merge",  "rope_window",
-                                     "q_down",            "q_up",         "latent_merge",
-                                     "out_mix",           "prepare_layer_weights",
-                                     "prepare_write_weights",
-                                     "mat_kv",            "mat_q_prep",   "mat_attend",
-                                     "mat_merge"};
+const char* kKernelNames[K_COUNT] = {"q_absorb",     "latent_attend", "out_proj",
+                                     "rope_window",  "bal_prep",      "mat_kv",
+                                     "mat_q_prep",   "mat_attend",    "mat_merge",
+                                     "dense_q_prep", "dense_attend",  "dense_merge",
+                                     "q_down",       "q_up",          "latent_merge",
+                                     "out_mix",      "cache_write",   "dense_cache_write"};
 
-struct TimingRec {
-  int kernel;
-  hipEvent_t start, stop;
-};
-bool g_timing = false;
-int g_timing_only = -1;  // >= 0: time only this kernel
-std::vector<TimingRec> g_pending;
-std::vector<hipEvent_t> g_event_pool;
+int kernel_id(const char* name) {
+  for (int k = 0; k < K_COUNT; ++k)
+    if (std::strcmp(name, kKernelNames[k]) == 0) return k;
+  return -1;
+}
 
-hipEvent_t take_event() {
-  if (!g_event_pool.empty()) {
-    hipEvent_t e = g_event_pool.back();
-    g_event_pool.pop_back();
+hipEvent_t take_event(videomla_timer* t) {
+  if (!t->pool.empty()) {
+    hipEvent_t e = t->pool.back();
+    t->pool.pop_back();
     return e;
   }
   hipEvent_t e = nullptr;
@@ -144,24 +159,32 @@ hipEvent_t take_event() {
 }
 
 template <class F>
-hipError_t timed(int kernel, hipStream_t s, F&& launch) {
-  if (!g_timing || (g_timing_only >= 0 && kernel != g_timing_only)) return launch();
-  hipEvent_t e0 = take_event(), e1 = take_event();
-  if (!e0 || !e1) return launch();
-  hipEventRecord(e0, s);
+hipError_t timed(videomla_timer* t, int kernel, hipStream_t s, F&& launch) {
+  if (!t || (t->only >= 0 && kernel != t->only)) return launch();
+  hipEvent_t e0 = take_event(t), e1 = take_event(t);
+  if (!e0 || !e1) {
+    if (e0) t->pool.push_back(e0);
+    if (e1) t->pool.push_back(e1);
+    return launch();
+  }
+  if (hipEventRecord(e0, s) != hipSuccess) {
+    t->pool.push_back(e0);
+    t->pool.push_back(e1);
+    return launch();
+  }
   const hipError_t err = launch();
-  hipEventRecord(e1, s);
-  g_pending.push_back({kernel, e0, e1});
+  if (hipEventRecord(e1, s) != hipSuccess) {
+    t->pool.push_back(e0);
+    t->pool.push_back(e1);
+    return err;
+  }
+  t->pending.push_back({kernel, e0, e1});
   return err;
 }
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(VIDEOMLA_EHIP, "%s launch failed: %s", what, hipGetErrorString(e));
 }
-
-int g_attend_wg = 0;  // 0 = as many workgroups as the compute units hold at once
-int g_attend_balance = 0;  // adaptive per-XCD partition of the latent attention
-uint32_t g_bal_seq = 0;    // sequence number of adaptive attention calls
 
 int device_cu_count() {
   int dev = 0, n = 0;
@@ -171,6 +194,40 @@ int device_cu_count() {
   return 256;  // MI355X; used only when no device is visible (host-side size queries)
 }
 
+// ---- options ----------------------------------------------------------------------------------
+// The options of one attention call, validated, with the query range resolved.
+struct Opts {
+  int n_wg;       // requested workgroups (0 = one per compute unit, or per resident slot)
+  int partition;  // VIDEOMLA_PARTITION_*
+  int form;       // VIDEOMLA_FORM_* (AUTO resolved by the caller)
+  int q_begin, q_count;
+  videomla_timer* timer;
+};
+
+int resolve_opts(const videomla_dims* d, const videomla_attend_opts* o, Opts& r) {
+  const int chunk = d->chunk_frames * d->grid_h * d->grid_w;
+  r = Opts{0, VIDEOMLA_PARTITION_EVEN, VIDEOMLA_FORM_LATENT, 0, chunk, nullptr};
+  if (!o) return VIDEOMLA_OK;
+  if (o->n_workgroups < 0 || o->n_workgroups > (1 << 20))
+    return fail(VIDEOMLA_EINVAL, "n_workgroups must be in [0, 2^20], got %d", o->n_workgroups);
+  if (o->partition < VIDEOMLA_PARTITION_EVEN || o->partition > VIDEOMLA_PARTITION_FROZEN)
+    return fail(VIDEOMLA_EINVAL, "unknown partition mode %d", o->partition);
+  if (o->form < VIDEOMLA_FORM_LATENT || o->form > VIDEOMLA_FORM_AUTO)
+    return fail(VIDEOMLA_EINVAL, "unknown attention form %d", o->form);
+  if (o->query_begin < 0 || o->query_begin >= chunk || o->query_count < 0 ||
+      o->query_count > chunk - o->query_begin)
+    return fail(VIDEOMLA_EINVAL, "query range [%d, %d + %d) outside the chunk's %d tokens",
+                o->query_begin, o->query_begin, o->query_count, chunk);
+  r.n_wg = o->n_workgroups;
+  r.partition = o->partition;
+  r.form = o->form;
+  r.q_begin = o->query_begin;
+  r.q_count = o->query_count > 0 ? o->query_count : chunk - o->query_begin;
+  r.timer = o->timer;
+  return VIDEOMLA_OK;
+}
+
+// ---- work partition ---------------------------------------------------------------------------
 // Work partition of the attention kernel for a window of n_valid keys (see AttendArgs).
 struct Partition {
   int G, rows, RB, T, max_seg;
@@ -178,14 +235,15 @@ struct Partition {
 };
 
 // rows: query rows per row block; RB: row blocks per batch element; bn: keys per tile;
-// wpc: resident workgroups per compute unit.
-Partition make_partition(int rows, int RB, int bn, int wpc, int32_t batch, int64_t n_valid) {
+// wpc: resident workgroups per compute unit; n_wg: requested workgroups (0 = wpc per CU).
+Partition make_partition(int rows, int RB, int bn, int wpc, int32_t batch, int64_t n_valid,
+                         int n_wg) {
   Partition p{};
   p.rows = rows;
   p.RB = RB;
   p.T = (int)((n_valid + bn - 1) / bn);
   p.U = (int64_t)batch * p.RB * p.T;
-  const int64_t G = g_attend_wg > 0 ? g_attend_wg : (int64_t)device_cu_count() * wpc;
+  const int64_t G = n_wg > 0 ? n_wg : (int64_t)device_cu_count() * wpc;
   p.G = (int)(G < p.U ? G : p.U);
   p.max_seg = 1;
   for (int64_t rbg = 0; rbg < (int64_t)batch * p.RB; ++rbg) {
@@ -195,86 +253,102 @@ Partition make_partition(int rows, int RB, int bn, int wpc, int32_t batch, int64
   return p;
 }
 
-Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+Partition attend_partition(const videomla_dims* d, int32_t batch, int64_t n_valid, const Opts& o) {
   const int rows = latent_attend_rows_per_block(d->d_c, d->d_rope);
-  const int64_t rows_b = (int64_t)d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
+  const int64_t rows_b = (int64_t)o.q_count * d->n_heads;
   return make_partition(rows, (int)((rows_b + rows - 1) / rows),
                         latent_attend_keys_per_tile(d->d_c, d->d_rope),
-                        latent_attend_wgs_per_cu(d->d_c, d->d_rope), batch, n_valid);
+                        latent_attend_wgs_per_cu(d->d_c, d->d_rope), batch, n_valid, o.n_wg);
 }
 
-// Dense comparator: every head's chunk rows padded to whole row blocks.
-int dense_nq_pad(const videomla_dims* d) {
+// Per-head forms (the dense comparator and the materialized form): every head's query rows
+// padded to whole row blocks.
+int head_nq_pad(const Opts& o) {
   const int rows = dense_attend_rows_per_block();
-  const int nq = d->chunk_frames * d->grid_h * d->grid_w;
-  return (nq + rows - 1) / rows * rows;
+  return (o.q_count + rows - 1) / rows * rows;
 }
 
-Partition dense_partition(const videomla_dims* d, int32_t batch, int64_t n_valid) {
+Partition head_partition(const videomla_dims* d, int32_t batch, int64_t n_valid, const Opts& o) {
   const int rows = dense_attend_rows_per_block();
-  return make_partition(rows, d->n_heads * (dense_nq_pad(d) / rows), dense_attend_keys_per_tile(),
-                        1, batch, n_valid);
+  return make_partition(rows, d->n_heads * (head_nq_pad(o) / rows), dense_attend_keys_per_tile(),
+                        1, batch, n_valid, o.n_wg);
 }
 
-// Slots the workspace must hold for any window this shape can attend over (chunk_frames up to
-// window_frames valid frames).
-int workspace_max_seg(const videomla_dims* d, int32_t batch, bool dense = false) {
+// Partial-result slots the workspace must hold for any window this shape can attend over
+// (chunk_frames up to window_frames valid frames).
+int workspace_max_seg(const videomla_dims* d, int32_t batch, const Opts& o, bool per_head) {
   int m = 1;
   for (int f = d->chunk_frames; f <= d->window_frames; ++f) {
     const int64_t n_valid = (int64_t)f * d->grid_h * d->grid_w;
-    const int s = (dense ? dense_partition(d, batch, n_valid) : attend_partition(d, batch, n_valid)).max_seg;
+    const int s = (per_head ? head_partition(d, batch, n_valid, o)
+                            : attend_partition(d, batch, n_valid, o)).max_seg;
     if (s > m) m = s;
   }
   return m;
 }
 
+// Workspace of the attention kernels: q rows [rows][q_width] bf16, the partial results
+// [n_seg][rows][o_width] fp32 and (max, sum) pairs [n_seg][rows][2] fp32, the rotated window keys
+// (latent form with a sink), then the partition state.
 struct WorkspaceLayout {
   size_t qcat_off, opart_off, ml_off, krot_off, bal_off, total;
   int n_seg;  // partial-result slots
 };
 
-WorkspaceLayout workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
-  const size_t rows = (size_t)batch * d->chunk_frames * d->grid_h * d->grid_w * d->n_heads;
-  const size_t dqkp = round_up((size_t)d->d_c + d->d_rope, 16);
+WorkspaceLayout make_layout(size_t base, size_t rows, size_t q_width, size_t o_width, int n_seg,
+                            size_t krot_bytes) {
   WorkspaceLayout w{};
-  w.qcat_off = 0;
-  w.opart_off = round_up(rows * dqkp * 2, 256);
-  w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_c * 4, 256);
+  w.qcat_off = base;
+  w.opart_off = w.qcat_off + round_up(rows * q_width * 2, 256);
+  w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * o_width * 4, 256);
   w.krot_off = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
-  // with a sink: the window's keys rotated at window-local time, [B][ring][d_rope]
+  w.bal_off = w.krot_off + round_up(krot_bytes, 256);
+  w.total = w.bal_off + round_up((size_t)kBalSlot * 4, 256);
+  w.n_seg = n_seg;
+  return w;
+}
+
+WorkspaceLayout latent_layout(const videomla_dims* d, int32_t batch, const Opts& o) {
+  const size_t rows = (size_t)batch * o.q_count * d->n_heads;
   const size_t krot = d->sink_frames > 0
                           ? (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->d_rope * 2
                           : 0;
-  // the adaptive partition's two state slots
-  w.bal_off = w.krot_off + round_up(krot, 256);
-  w.total = w.bal_off + round_up((size_t)2 * kBalSlot * 4, 256);
-  w.n_seg = n_seg;
-  return w;
+  return make_layout(0, rows, round_up((size_t)d->d_c + d->d_rope, 16), d->d_c,
+                     workspace_max_seg(d, batch, o, false), krot);
 }
 
-// The adaptive partition (videomla_set_attend_balance) for a call: only where every range keeps
-// at least one unit under any weights and the workspace holds the partial results such ranges
-// can leave.
-void set_balance(AttendArgs& a, const Partition& P, char* ws, const WorkspaceLayout& L) {
+// Dense comparator: q rows [B][H][nq_pad][d_v].
+WorkspaceLayout dense_layout(const videomla_dims* d, int32_t batch, const Opts& o) {
+  const size_t rows = (size_t)batch * d->n_heads * head_nq_pad(o);
+  return make_layout(0, rows, d->d_v, d->d_v, workspace_max_seg(d, batch, o, true), 0);
+}
+
+// Materialized form: the reconstructed rows [B][ring][H][d_k + d_v] (d_k = d_nope + d_rope),
+// then per-head q rows [B][H][nq_pad][d_k] and the rest as for the dense comparator.
+struct MatLayout {
+  size_t kv_off;
+  WorkspaceLayout att;
+};
+MatLayout mat_layout(const videomla_dims* d, int32_t batch, const Opts& o) {
+  const size_t dk = (size_t)d->d_nope + d->d_rope;
+  const size_t kv = (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->n_heads *
+                    (dk + d->d_v) * 2;
+  const size_t rows = (size_t)batch * d->n_heads * head_nq_pad(o);
+  MatLayout m{};
+  m.kv_off = 0;
+  m.att = make_layout(round_up(kv, 256), rows, dk, d->d_v, workspace_max_seg(d, batch, o, true), 0);
+  return m;
+}
+
+// The weighted partition for a call (adaptive or frozen): only where every range keeps at least
+// one unit under any weights and the workspace holds the partial results such ranges can leave.
+void set_balance(AttendArgs& a, const Partition& P, char* ws, const WorkspaceLayout& L,
+                 const Opts& o) {
   a.bal_state = reinterpret_cast<uint32_t*>(ws + L.bal_off);
-  a.bal_on = g_attend_balance && P.G <= kBalMaxWg && bal_max_seg(P.G, P.U, P.T) <= L.n_seg;
-  if (a.bal_on) {
-    a.max_seg = L.n_seg;
-    a.bal_seq = (int32_t)(g_bal_seq++ & 0x7fffffff);
-  }
-}
-
-// Dense comparator workspace: q_cat [B][H][nq_pad][d_v] bf16, then the partial results.
-WorkspaceLayout dense_workspace_layout(const videomla_dims* d, int32_t batch, int n_seg) {
-  const size_t rows = (size_t)batch * d->n_heads * dense_nq_pad(d);
-  WorkspaceLayout w{};
-  w.qcat_off = 0;
-  w.opart_off = round_up(rows * d->d_v * 2, 256);
-  w.ml_off = w.opart_off + round_up((size_t)n_seg * rows * d->d_v * 4, 256);
-  w.bal_off = w.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
-  w.total = w.bal_off + round_up((size_t)2 * kBalSlot * 4, 256);
-  w.n_seg = n_seg;
-  return w;
+  a.bal_on = o.partition != VIDEOMLA_PARTITION_EVEN && P.G <= kBalMaxWg &&
+             bal_max_seg(P.G, P.U, P.T) <= L.n_seg;
+  a.bal_rec = a.bal_on && o.partition == VIDEOMLA_PARTITION_ADAPTIVE;
+  if (a.bal_on) a.max_seg = L.n_seg;
 }
 
 // Full-head RoPE of the dense comparator: channels (d - 4 floor(d/6), 2 floor(d/6),
@@ -374,18 +448,6 @@ int videomla_window_advance(const videomla_dims* d, videomla_window* w) {
   return ok();
 }
 
-int videomla_set_attend_balance(int32_t on) {
-  if (on != 0 && on != 1) return fail(VIDEOMLA_EINVAL, "attend balance must be 0 or 1, got %d", on);
-  g_attend_balance = on;
-  return ok();
-}
-
-int videomla_set_attend_workgroups(int32_t n) {
-  if (n < 0 || n > (1 << 20)) return fail(VIDEOMLA_EINVAL, "workgroup count must be in [0, 2^20], got %d", n);
-  g_attend_wg = n;
-  return ok();
-}
-
 namespace {
 
 // Shapes the cache-write kernels tile (shared by the plain and the packed-weight entry points).
@@ -431,7 +493,7 @@ int cache_write_common(const videomla_dims* d, const videomla_window* w, int32_t
   a.rope = make_rope(d);
   a.tok_per_wg = cache_write_tokens_per_wg((int64_t)batch * a.geo.chunk_tokens, device_cu_count());
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const hipError_t e = timed(K_CACHE_WRITE, s, [&] { return launch_cache_write(a, s); });
+  const hipError_t e = launch_cache_write(a, s);
   if (e != hipSuccess) return hip_fail(e, "cache_write");
   return ok();
 }
@@ -462,7 +524,7 @@ int videomla_prepare_write_weights(const videomla_dims* d, const uint16_t* w_dkv
   a.w_dkv = w_dkv; a.w_kr = w_kr; a.w_packed_out = w_packed;
   a.d_model = d->d_model; a.d_c = d->d_c; a.d_rope = d->d_rope;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const hipError_t e = timed(K_PREPARE_WRITE, s, [&] { return launch_pack_write_weights(a, s); });
+  const hipError_t e = launch_pack_write_weights(a, s);
   if (e != hipSuccess) return hip_fail(e, "prepare_write_weights");
   return ok();
 }
@@ -476,18 +538,86 @@ int videomla_cache_write_prepared(const videomla_dims* d, const videomla_window*
                             slots_out, stream);
 }
 
-size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
-  if (check_dims(d) || batch <= 0) return 0;
-  if (!latent_attend_supported(d->d_c, d->d_rope)) return 0;
-  return workspace_layout(d, batch, workspace_max_seg(d, batch)).total;
-}
-
 namespace {
 
-// Attention arguments common to videomla_attend and videomla_attend_layer (shapes, window,
-// work partition, workspace carving); the caller sets the query and projection pointers.
+// ---- attention ----------------------------------------------------------------------------------
+
+int check_attend_args(const videomla_dims* d, const videomla_window* w, int32_t batch) {
+  if (int e = check_dims(d)) return e;
+  if (int e = check_window(w)) return e;
+  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+  return VIDEOMLA_OK;
+}
+
+int check_workspace(const void* ws, size_t have, size_t need) {
+  if (!ws || have < need)
+    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                ws ? have : (size_t)0);
+  if (!aligned16(ws)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+  return VIDEOMLA_OK;
+}
+
+// Materialized-K/V form: head rows [K_h | V_h] = [W_UK,h c ; k^R | W_UV,h c], keys of width
+// d_nope + d_rope, values of width d_v; the attention kernel is built for 128 | 128 and 160 | 128.
+bool materialized_supported(const videomla_dims* d) {
+  return mat_attend_supported(d->d_nope + d->d_rope, d->d_v) && d->sink_frames == 0 &&
+         d->d_c % 64 == 0 && d->d_rope % 8 == 0;
+}
+
+int check_materialized_shape(const videomla_dims* d) {
+  if (!mat_attend_supported(d->d_nope + d->d_rope, d->d_v))
+    return fail(VIDEOMLA_EUNSUPPORTED,
+                "materialized attention is built for d_v = 128 and d_nope + d_rope in {128, 160}, "
+                "got %d + %d, %d", d->d_nope, d->d_rope, d->d_v);
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "materialized attention has no sink mode");
+  if (d->d_c % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 64, got %d", d->d_c);
+  if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
+  return VIDEOMLA_OK;
+}
+
+// Cost model behind VIDEOMLA_FORM_AUTO, over a full window of S keys and R = batch x query
+// tokens x heads query rows (each head's rows padded to whole row blocks in the materialized
+// form). Latent: R S (2 d_c + d_rope) multiply-adds at kLatentMacRate. Materialized: the
+// reconstruction, bound by writing the batch x S x H x (d_k + d_v) bf16 rows at kMatKvRate
+// bytes/s, then R_pad S (d_k + d_v) multiply-adds at kMatMacRate. Both add the per-call cost of
+// their query preparation and merge, which scales with R. The rates are the ones measured on
+// MI355X at the Wan shape (latent 1190 us, materialized attention 1001 us and reconstruction
+// 99 us for 56,160 rows x 32,760 keys at d_nope 128).
+constexpr double kLatentMacRate = 6.43e14;   // multiply-adds per second, latent attention
+constexpr double kMatMacRate = 5.29e14;      // multiply-adds per second, per-head attention
+constexpr double kMatKvRate = 2.28e12;       // bytes per second written by the reconstruction
+constexpr double kLatentRowCost = 9.8e-10;   // seconds per query row: absorption + merge
+constexpr double kMatRowCost = 6.8e-10;      // seconds per query row: query prep + merge
+
+bool prefer_materialized(const videomla_dims* d, int32_t batch, const Opts& o) {
+  if (!materialized_supported(d)) return false;
+  const double S = (double)d->window_frames * d->grid_h * d->grid_w;
+  const double R = (double)batch * o.q_count * d->n_heads;
+  const double R_pad = (double)batch * head_nq_pad(o) * d->n_heads;
+  const double dk = d->d_nope + d->d_rope;
+  const double t_lat = R * S * (2.0 * d->d_c + d->d_rope) / kLatentMacRate + R * kLatentRowCost;
+  const double t_mat = (double)batch * S * d->n_heads * (dk + d->d_v) * 2.0 / kMatKvRate +
+                       R_pad * S * (dk + d->d_v) / kMatMacRate + R * kMatRowCost;
+  return t_mat < t_lat;
+}
+
+// The form a videomla_attend_ex call runs (AUTO resolved); -1 with the error set if the options
+// ask for the materialized form on a shape it is not built for.
+int attend_form(const videomla_dims* d, int32_t batch, const Opts& o) {
+  if (o.form == VIDEOMLA_FORM_MATERIALIZED) {
+    if (check_materialized_shape(d)) return -1;
+    return VIDEOMLA_FORM_MATERIALIZED;
+  }
+  if (o.form == VIDEOMLA_FORM_AUTO && prefer_materialized(d, batch, o))
+    return VIDEOMLA_FORM_MATERIALIZED;
+  return VIDEOMLA_FORM_LATENT;
+}
+
+// Attention arguments common to the latent form of videomla_attend_ex and videomla_attend_layer
+// (shapes, window, query range, work partition, workspace carving); the caller sets the query
+// and projection pointers.
 AttendArgs attend_args(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                       const WorkspaceLayout& L, char* ws, const uint16_t* c_kv,
+                       const Opts& o, const WorkspaceLayout& L, char* ws, const uint16_t* c_kv,
                        const uint16_t* k_r) {
   AttendArgs a{};
   a.c_kv = c_kv; a.k_r = k_r;
@@ -499,252 +629,126 @@ AttendArgs attend_args(const videomla_dims* d, const videomla_window* w, int32_t
   a.d_c = d->d_c; a.d_v = d->d_v;
   a.dqk_pad = (int32_t)round_up((size_t)d->d_c + d->d_rope, 16);
   a.geo = make_geo(d, w);
+  a.geo.q_begin = o.q_begin;
+  a.geo.q_count = o.q_count;
   a.rope = make_rope(d);
   a.n_valid = (int32_t)videomla_valid_tokens(d, w);
-  const Partition P = attend_partition(d, batch, a.n_valid);
+  const Partition P = attend_partition(d, batch, a.n_valid, o);
   a.n_wg = P.G;
   a.att_rows = P.rows;
   a.row_blocks = P.RB;
   a.tiles_per_row = P.T;
   a.units = P.U;
   a.max_seg = P.max_seg;
-  set_balance(a, P, ws, L);
+  set_balance(a, P, ws, L, o);
   const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
                                               : 1.0 / std::sqrt((double)d->d_nope + d->d_rope);
   a.qscale = (float)(scale * 1.4426950408889634);
   return a;
 }
 
-// The window keys at window-local time (sink only), then the attention kernel.
-int run_attention(AttendArgs& a, hipStream_t s) {
+// Arguments of the per-head forms (dense comparator: head width d_v, queries q; materialized:
+// keys d_nope + d_rope wide). Rows are (head, token) pairs, each head padded to nq_pad.
+AttendArgs head_args(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                     const Opts& o, const WorkspaceLayout& L, char* ws, bool materialized) {
+  AttendArgs a{};
+  a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
+  a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
+  a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
+  a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v; a.d_c = d->d_v;
+  a.d_nope = materialized ? d->d_nope : 0;
+  a.d_rope = materialized ? d->d_rope : 0;
+  a.dqk_pad = materialized ? d->d_nope + d->d_rope : d->d_v;  // key width
+  a.nq_pad = head_nq_pad(o);
+  a.geo = make_geo(d, w);
+  a.geo.q_begin = o.q_begin;
+  a.geo.q_count = o.q_count;
+  a.rope = materialized ? make_rope(d) : make_dense_rope(d);
+  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
+  const Partition P = head_partition(d, batch, a.n_valid, o);
+  a.n_wg = P.G;
+  a.att_rows = P.rows;
+  a.row_blocks = P.RB;
+  a.tiles_per_row = P.T;
+  a.units = P.U;
+  a.max_seg = P.max_seg;
+  set_balance(a, P, ws, L, o);
+  const double dk = materialized ? (double)(d->d_nope + d->d_rope) : (double)d->d_v;
+  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale : 1.0 / std::sqrt(dk);
+  a.qscale = (float)(scale * 1.4426950408889634);
+  return a;
+}
+
+// The weights of an adaptive call (before its attention kernel), then the attention kernel.
+int run_partition_prep(AttendArgs& a, videomla_timer* t, hipStream_t s) {
+  if (!a.bal_rec) return VIDEOMLA_OK;
+  const hipError_t e = timed(t, K_BAL_PREP, s, [&] { return launch_bal_prep(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "bal_prep");
+  return VIDEOMLA_OK;
+}
+
+// The window keys at window-local time (sink only), the partition weights (adaptive only), then
+// the attention kernel.
+int run_attention(AttendArgs& a, videomla_timer* t, hipStream_t s) {
   hipError_t e;
   if (a.k_rot) {
-    e = timed(K_ROPE_WINDOW, s, [&] { return launch_rope_window(a, s); });
+    e = timed(t, K_ROPE_WINDOW, s, [&] { return launch_rope_window(a, s); });
     if (e != hipSuccess) return hip_fail(e, "rope_window");
     a.k_r = a.k_rot;
   }
-  e = timed(K_LATENT_ATTEND, s, [&] { return launch_latent_attend(a, s); });
+  if (int r = run_partition_prep(a, t, s)) return r;
+  e = timed(t, K_LATENT_ATTEND, s, [&] { return launch_latent_attend(a, s); });
   if (e != hipSuccess) return hip_fail(e, "latent_attend");
   return VIDEOMLA_OK;
 }
 
-}  // namespace
+// Workspace of a videomla_attend_ex call (0 with the error set when unsupported).
+size_t attend_workspace(const videomla_dims* d, int32_t batch, const Opts& o, int form) {
+  if (form == VIDEOMLA_FORM_MATERIALIZED) return mat_layout(d, batch, o).att.total;
+  return latent_layout(d, batch, o).total;
+}
 
-int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
-                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
-                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+int attend_impl(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r, uint16_t* out,
+                void* workspace, size_t workspace_bytes, const videomla_attend_opts* opts,
+                void* stream) {
+  if (int e = check_attend_args(d, w, batch)) return e;
+  Opts o;
+  if (int e = resolve_opts(d, opts, o)) return e;
   if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
     return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
   if (int e = check_attend_shape(d)) return e;
+  const int form = attend_form(d, batch, o);
+  if (form < 0) return VIDEOMLA_EUNSUPPORTED;
   if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
       !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
     return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  const WorkspaceLayout L = workspace_layout(d, batch, workspace_max_seg(d, batch));
-  if (!workspace || workspace_bytes < L.total)
-    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
-
-  AttendArgs a = attend_args(d, w, batch, L, static_cast<char*>(workspace), c_kv, k_r);
-  a.q_nope = q_nope; a.q_r = q_r; a.w_uk = w_uk; a.w_uv = w_uv; a.out = out;
-
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = timed(K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "q_absorb");
-  if (int r = run_attention(a, s)) return r;
-  e = timed(K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "out_proj");
-  return ok();
-}
-
-size_t videomla_dense_cache_bytes_per_token(const videomla_dims* d) {
-  if (check_dims(d)) return 0;
-  return 2 * (size_t)d->n_heads * d->d_v * 2;
-}
-
-int videomla_dense_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                               const uint16_t* x, const uint16_t* w_k, const uint16_t* w_v,
-                               uint16_t* kv, int32_t* slots_out, void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
-  if (!x || !w_k || !w_v || !kv) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
-  if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
-  if (int e = check_dense_head(d)) return e;
-  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
-  if ((2 * d->n_heads * d->d_v) % 128)
-    return fail(VIDEOMLA_EUNSUPPORTED, "2 * n_heads * d_v must be a multiple of 128, got %d",
-                2 * d->n_heads * d->d_v);
-  if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) || !aligned16(kv))
-    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  DenseWriteArgs a{};
-  a.x = x; a.w_k = w_k; a.w_v = w_v; a.kv = kv; a.slots = slots_out;
-  a.batch = batch; a.d_model = d->d_model; a.n_heads = d->n_heads; a.d_head = d->d_v;
-  a.geo = make_geo(d, w);
-  a.rope = make_dense_rope(d);
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const hipError_t e = timed(K_DENSE_CACHE_WRITE, s, [&] { return launch_dense_cache_write(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "dense_cache_write");
-  return ok();
-}
-
-size_t videomla_dense_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
-  if (check_dims(d) || batch <= 0) return 0;
-  if (!dense_attend_supported(d->d_v)) return 0;
-  return dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true)).total;
-}
-
-int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                          const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
-                          size_t workspace_bytes, void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
-  if (!q || !kv || !out) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
-  if (!dense_attend_supported(d->d_v))
-    return fail(VIDEOMLA_EUNSUPPORTED, "dense attention is built for d_v = 128, got %d", d->d_v);
-  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
-  if (!aligned16(q) || !aligned16(kv) || !aligned16(out))
-    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  const WorkspaceLayout L = dense_workspace_layout(d, batch, workspace_max_seg(d, batch, true));
-  if (!workspace || workspace_bytes < L.total)
-    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
-
-  AttendArgs a{};
-  a.q = q; a.kv = kv; a.out = out;
   char* ws = static_cast<char*>(workspace);
-  a.qcat = reinterpret_cast<uint16_t*>(ws + L.qcat_off);
-  a.o_part = reinterpret_cast<float*>(ws + L.opart_off);
-  a.ml_part = reinterpret_cast<float*>(ws + L.ml_off);
-  a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v;
-  a.d_c = d->d_v; a.d_rope = 0; a.d_nope = 0;
-  a.dqk_pad = d->d_v;
-  a.nq_pad = dense_nq_pad(d);
-  a.geo = make_geo(d, w);
-  a.rope = make_dense_rope(d);
-  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
-  const Partition P = dense_partition(d, batch, a.n_valid);
-  a.n_wg = P.G;
-  a.att_rows = P.rows;
-  a.row_blocks = P.RB;
-  a.tiles_per_row = P.T;
-  a.units = P.U;
-  a.max_seg = P.max_seg;
-  set_balance(a, P, ws, L);
-  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale : 1.0 / std::sqrt((double)d->d_v);
-  a.qscale = (float)(scale * 1.4426950408889634);
+  videomla_timer* t = o.timer;
 
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = timed(K_DENSE_Q_PREP, s, [&] { return launch_dense_q_prep(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "dense_q_prep");
-  e = timed(K_DENSE_ATTEND, s, [&] { return launch_dense_attend(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "dense_attend");
-  e = timed(K_DENSE_MERGE, s, [&] { return launch_dense_merge(a, s); });
-  if (e != hipSuccess) return hip_fail(e, "dense_merge");
-  return ok();
-}
+  if (form == VIDEOMLA_FORM_LATENT) {
+    const WorkspaceLayout L = latent_layout(d, batch, o);
+    if (int e = check_workspace(workspace, workspace_bytes, L.total)) return e;
+    AttendArgs a = attend_args(d, w, batch, o, L, ws, c_kv, k_r);
+    a.q_nope = q_nope; a.q_r = q_r; a.w_uk = w_uk; a.w_uv = w_uv; a.out = out;
+    hipError_t e = timed(t, K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
+    if (e != hipSuccess) return hip_fail(e, "q_absorb");
+    if (int r = run_attention(a, t, s)) return r;
+    e = timed(t, K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
+    if (e != hipSuccess) return hip_fail(e, "out_proj");
+    return ok();
+  }
 
-namespace {
-
-// Materialized-K/V path: head rows [K_h | V_h] = [W_UK,h c ; k^R | W_UV,h c], keys of width
-// d_nope + d_rope, values of width d_v; the attention kernel is built for 128 | 128 and 160 | 128.
-int check_materialized_shape(const videomla_dims* d) {
-  if (!mat_attend_supported(d->d_nope + d->d_rope, d->d_v))
-    return fail(VIDEOMLA_EUNSUPPORTED,
-                "materialized attention is built for d_v = 128 and d_nope + d_rope in {128, 160}, "
-                "got %d + %d, %d", d->d_nope, d->d_rope, d->d_v);
-  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "materialized attention has no sink mode");
-  if (d->d_c % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_c must be a multiple of 64, got %d", d->d_c);
-  if (d->d_rope % 8) return fail(VIDEOMLA_EUNSUPPORTED, "d_rope must be a multiple of 8, got %d", d->d_rope);
-  return 0;
-}
-
-// [B][ring][H][d_k + d_v] materialized rows (d_k = d_nope + d_rope), then the per-head query
-// rows (d_k wide), the partial results (d_v wide) and (max, sum) pairs
-struct MatLayout {
-  size_t kv_off, dense_off, total;
-  WorkspaceLayout dense;
-};
-MatLayout mat_layout(const videomla_dims* d, int32_t batch) {
-  MatLayout m{};
-  const size_t dk = (size_t)d->d_nope + d->d_rope;
-  const size_t kv = (size_t)batch * d->window_frames * d->grid_h * d->grid_w * d->n_heads *
-                    (dk + d->d_v) * 2;
-  m.kv_off = 0;
-  m.dense_off = round_up(kv, 256);
-  const int n_seg = workspace_max_seg(d, batch, true);
-  const size_t rows = (size_t)batch * d->n_heads * dense_nq_pad(d);
-  m.dense.qcat_off = 0;
-  m.dense.opart_off = round_up(rows * dk * 2, 256);
-  m.dense.ml_off = m.dense.opart_off + round_up((size_t)n_seg * rows * d->d_v * 4, 256);
-  m.dense.total = m.dense.ml_off + round_up((size_t)n_seg * rows * 2 * 4, 256);
-  m.total = m.dense_off + m.dense.total;
-  return m;
-}
-
-}  // namespace
-
-size_t videomla_attend_materialized_workspace_bytes(const videomla_dims* d, int32_t batch) {
-  if (check_dims(d) || batch <= 0 || check_materialized_shape(d)) return 0;
-  return mat_layout(d, batch).total;
-}
-
-int videomla_attend_materialized(const videomla_dims* d, const videomla_window* w, int32_t batch,
-                                 const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
-                                 const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
-                                 uint16_t* out, void* workspace, size_t workspace_bytes,
-                                 void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
-  if (!q_nope || !q_r || !w_uk || !w_uv || !c_kv || !k_r || !out)
-    return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
-  if (int e = check_materialized_shape(d)) return e;
-  if (!aligned16(q_nope) || !aligned16(q_r) || !aligned16(w_uk) || !aligned16(w_uv) ||
-      !aligned16(c_kv) || !aligned16(k_r) || !aligned16(out))
-    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
-  const MatLayout L = mat_layout(d, batch);
-  if (!workspace || workspace_bytes < L.total)
-    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
-
-  char* ws = static_cast<char*>(workspace);
-  uint16_t* kv = reinterpret_cast<uint16_t*>(ws + L.kv_off);
-  char* dws = ws + L.dense_off;
-  AttendArgs a{};
+  // materialized: per-head K_h, V_h of every valid slot, then per-head attention
+  const MatLayout M = mat_layout(d, batch, o);
+  if (int e = check_workspace(workspace, workspace_bytes, M.att.total)) return e;
+  uint16_t* kv = reinterpret_cast<uint16_t*>(ws + M.kv_off);
+  AttendArgs a = head_args(d, w, batch, o, M.att, ws, true);
   a.q_nope = q_nope; a.q_r = q_r; a.k_r = k_r; a.kv = kv; a.out = out;
-  a.qcat = reinterpret_cast<uint16_t*>(dws + L.dense.qcat_off);
-  a.o_part = reinterpret_cast<float*>(dws + L.dense.opart_off);
-  a.ml_part = reinterpret_cast<float*>(dws + L.dense.ml_off);
-  a.batch = batch; a.n_heads = d->n_heads; a.d_v = d->d_v;
-  a.d_nope = d->d_nope; a.d_rope = d->d_rope; a.d_c = d->d_v;
-  a.dqk_pad = d->d_nope + d->d_rope;  // key width
-  a.nq_pad = dense_nq_pad(d);
-  a.geo = make_geo(d, w);
-  a.rope = make_rope(d);
-  a.n_valid = (int32_t)videomla_valid_tokens(d, w);
-  const Partition P = dense_partition(d, batch, a.n_valid);
-  a.n_wg = P.G;
-  a.att_rows = P.rows;
-  a.row_blocks = P.RB;
-  a.tiles_per_row = P.T;
-  a.units = P.U;
-  a.max_seg = P.max_seg;
-  set_balance(a, P, dws, L.dense);
-  const double scale = d->softmax_scale > 0.f ? (double)d->softmax_scale
-                                              : 1.0 / std::sqrt((double)(d->d_nope + d->d_rope));
-  a.qscale = (float)(scale * 1.4426950408889634);
-
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int64_t ring = a.geo.ring_tokens, H = d->n_heads, ld = (int64_t)a.dqk_pad + d->d_v;
-  hipError_t e = timed(K_MAT_KV, s, [&] {
+  hipError_t e = timed(t, K_MAT_KV, s, [&] {
     // per batch element: K_h no-RoPE part = W_UK,h c and V_h = W_UV,h c of the valid slots
     for (int b = 0; b < batch; ++b) {
       GemmArgs g{};
@@ -762,14 +766,121 @@ int videomla_attend_materialized(const videomla_dims* d, const videomla_window* 
     return launch_mat_rope_fill(a, kv, s);
   });
   if (e != hipSuccess) return hip_fail(e, "mat_kv");
-  e = timed(K_MAT_Q_PREP, s, [&] { return launch_mat_q_prep(a, s); });
+  e = timed(t, K_MAT_Q_PREP, s, [&] { return launch_mat_q_prep(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_q_prep");
-  e = timed(K_MAT_ATTEND, s, [&] { return launch_mat_attend(a, s); });
+  if (int r = run_partition_prep(a, t, s)) return r;
+  e = timed(t, K_MAT_ATTEND, s, [&] { return launch_mat_attend(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_attend");
-  e = timed(K_MAT_MERGE, s, [&] { return launch_dense_merge(a, s); });
+  e = timed(t, K_MAT_MERGE, s, [&] { return launch_dense_merge(a, s); });
   if (e != hipSuccess) return hip_fail(e, "mat_merge");
   return ok();
 }
+
+}  // namespace
+
+size_t videomla_attend_workspace_bytes_ex(const videomla_dims* d, int32_t batch,
+                                          const videomla_attend_opts* opts) {
+  if (check_dims(d) || batch <= 0) return 0;
+  Opts o;
+  if (resolve_opts(d, opts, o)) return 0;
+  if (check_attend_shape(d)) return 0;
+  const int form = attend_form(d, batch, o);
+  if (form < 0) return 0;
+  return attend_workspace(d, batch, o, form);
+}
+
+size_t videomla_attend_workspace_bytes(const videomla_dims* d, int32_t batch) {
+  return videomla_attend_workspace_bytes_ex(d, batch, nullptr);
+}
+
+int videomla_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                    const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                    const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                    uint16_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return attend_impl(d, w, batch, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace,
+                     workspace_bytes, nullptr, stream);
+}
+
+int videomla_attend_ex(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                       const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                       const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                       uint16_t* out, void* workspace, size_t workspace_bytes,
+                       const videomla_attend_opts* opts, void* stream) {
+  return attend_impl(d, w, batch, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, workspace,
+                     workspace_bytes, opts, stream);
+}
+
+// ---- dense comparator ---------------------------------------------------------------------------
+
+size_t videomla_dense_cache_bytes_per_token(const videomla_dims* d) {
+  if (check_dims(d)) return 0;
+  return 2 * (size_t)d->n_heads * d->d_v * 2;
+}
+
+int videomla_dense_cache_write(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                               const uint16_t* x, const uint16_t* w_k, const uint16_t* w_v,
+                               uint16_t* kv, int32_t* slots_out, void* stream) {
+  if (int e = check_attend_args(d, w, batch)) return e;
+  if (!x || !w_k || !w_v || !kv) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (d->d_model % 64) return fail(VIDEOMLA_EUNSUPPORTED, "d_model must be a multiple of 64, got %d", d->d_model);
+  if (int e = check_dense_head(d)) return e;
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
+  if ((2 * d->n_heads * d->d_v) % 128)
+    return fail(VIDEOMLA_EUNSUPPORTED, "2 * n_heads * d_v must be a multiple of 128, got %d",
+                2 * d->n_heads * d->d_v);
+  if (!aligned16(x) || !aligned16(w_k) || !aligned16(w_v) || !aligned16(kv))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  DenseWriteArgs a{};
+  a.x = x; a.w_k = w_k; a.w_v = w_v; a.kv = kv; a.slots = slots_out;
+  a.batch = batch; a.d_model = d->d_model; a.n_heads = d->n_heads; a.d_head = d->d_v;
+  a.geo = make_geo(d, w);
+  a.rope = make_dense_rope(d);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = launch_dense_cache_write(a, s);
+  if (e != hipSuccess) return hip_fail(e, "dense_cache_write");
+  return ok();
+}
+
+size_t videomla_dense_attend_workspace_bytes(const videomla_dims* d, int32_t batch,
+                                             const videomla_attend_opts* opts) {
+  if (check_dims(d) || batch <= 0) return 0;
+  Opts o;
+  if (resolve_opts(d, opts, o)) return 0;
+  if (!dense_attend_supported(d->d_v)) return 0;
+  return dense_layout(d, batch, o).total;
+}
+
+int videomla_dense_attend(const videomla_dims* d, const videomla_window* w, int32_t batch,
+                          const uint16_t* q, const uint16_t* kv, uint16_t* out, void* workspace,
+                          size_t workspace_bytes, const videomla_attend_opts* opts,
+                          void* stream) {
+  if (int e = check_attend_args(d, w, batch)) return e;
+  Opts o;
+  if (int e = resolve_opts(d, opts, o)) return e;
+  if (!q || !kv || !out) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
+  if (!dense_attend_supported(d->d_v))
+    return fail(VIDEOMLA_EUNSUPPORTED, "dense attention is built for d_v = 128, got %d", d->d_v);
+  if (d->sink_frames) return fail(VIDEOMLA_EUNSUPPORTED, "the dense comparator has no sink mode");
+  if (!aligned16(q) || !aligned16(kv) || !aligned16(out))
+    return fail(VIDEOMLA_EALIGN, "tensor pointers must be 16-byte aligned");
+  const WorkspaceLayout L = dense_layout(d, batch, o);
+  if (int e = check_workspace(workspace, workspace_bytes, L.total)) return e;
+
+  AttendArgs a = head_args(d, w, batch, o, L, static_cast<char*>(workspace), false);
+  a.q = q; a.kv = kv; a.out = out;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  videomla_timer* t = o.timer;
+  hipError_t e = timed(t, K_DENSE_Q_PREP, s, [&] { return launch_dense_q_prep(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_q_prep");
+  if (int r = run_partition_prep(a, t, s)) return r;
+  e = timed(t, K_DENSE_ATTEND, s, [&] { return launch_dense_attend(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_attend");
+  e = timed(t, K_DENSE_MERGE, s, [&] { return launch_dense_merge(a, s); });
+  if (e != hipSuccess) return hip_fail(e, "dense_merge");
+  return ok();
+}
+
+// ---- the whole attention layer ---------------------------------------------------------------
 
 size_t videomla_layer_weights_bytes(const videomla_dims* d, int32_t d_q) {
   if (check_dims(d) || check_layer_shape(d, d_q)) return 0;
@@ -799,44 +910,56 @@ int videomla_prepare_layer_weights(const videomla_dims* d, int32_t d_q, const ui
   a.n_heads = d->n_heads; a.d_model = d->d_model; a.d_nope = d->d_nope; a.d_rope = d->d_rope;
   a.d_c = d->d_c; a.d_v = d->d_v; a.d_q = d_q; a.d_q_pad = L.d_q_pad; a.k_out_pad = L.k_out_pad;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const hipError_t e = timed(K_PREPARE, s, [&] { return launch_prepare_weights(a, s); });
+  const hipError_t e = launch_prepare_weights(a, s);
   if (e != hipSuccess) return hip_fail(e, "prepare_layer_weights");
   return ok();
 }
 
 namespace {
-// attention workspace, then u = W_down^Q x [B Nq][d_q_pad] and o_lat [B Nq][k_out_pad], bf16
+// attention workspace, then u = W_down^Q x [B q_count][d_q_pad] and o_lat [B q_count][k_out_pad],
+// bf16
 struct LayerWorkspace {
   WorkspaceLayout att;
   size_t u_off, olat_off, total;
 };
 
-LayerWorkspace layer_workspace(const videomla_dims* d, int32_t d_q, int32_t batch) {
+LayerWorkspace layer_workspace(const videomla_dims* d, int32_t d_q, int32_t batch, const Opts& o) {
   const LayerWeightsLayout W = layer_weights_layout(d, d_q);
   LayerWorkspace L{};
-  L.att = workspace_layout(d, batch, workspace_max_seg(d, batch));
-  const size_t tokens = (size_t)batch * d->chunk_frames * d->grid_h * d->grid_w;
+  L.att = latent_layout(d, batch, o);
+  const size_t tokens = (size_t)batch * o.q_count;
   L.u_off = L.att.total;
   L.olat_off = L.u_off + round_up(tokens * W.d_q_pad * 2, 256);
   L.total = L.olat_off + round_up(tokens * W.k_out_pad * 2, 256);
   return L;
 }
+
+int resolve_layer_opts(const videomla_dims* d, const videomla_attend_opts* opts, Opts& o) {
+  if (int e = resolve_opts(d, opts, o)) return e;
+  if (o.form == VIDEOMLA_FORM_MATERIALIZED)
+    return fail(VIDEOMLA_EUNSUPPORTED, "the whole layer runs the latent form only");
+  return VIDEOMLA_OK;
+}
 }  // namespace
 
-size_t videomla_attend_layer_workspace_bytes(const videomla_dims* d, int32_t d_q, int32_t batch) {
+size_t videomla_attend_layer_workspace_bytes(const videomla_dims* d, int32_t d_q, int32_t batch,
+                                             const videomla_attend_opts* opts) {
   if (check_dims(d) || check_layer_shape(d, d_q) || batch <= 0) return 0;
+  Opts o;
+  if (resolve_layer_opts(d, opts, o)) return 0;
   if (!latent_attend_supported(d->d_c, d->d_rope)) return 0;
-  return layer_workspace(d, d_q, batch).total;
+  return layer_workspace(d, d_q, batch, o).total;
 }
 
 int videomla_attend_layer(const videomla_dims* d, const videomla_window* w, int32_t batch,
                           int32_t d_q, const uint16_t* x, const void* weights,
                           size_t weights_bytes, const uint16_t* c_kv, const uint16_t* k_r,
-                          uint16_t* y, void* workspace, size_t workspace_bytes, void* stream) {
-  if (int e = check_dims(d)) return e;
-  if (int e = check_window(w)) return e;
-  if (batch <= 0) return fail(VIDEOMLA_EINVAL, "batch must be positive, got %d", batch);
+                          uint16_t* y, void* workspace, size_t workspace_bytes,
+                          const videomla_attend_opts* opts, void* stream) {
+  if (int e = check_attend_args(d, w, batch)) return e;
   if (int e = check_layer_shape(d, d_q)) return e;
+  Opts o;
+  if (int e = resolve_layer_opts(d, opts, o)) return e;
   if (!x || !weights || !c_kv || !k_r || !y) return fail(VIDEOMLA_EINVAL, "NULL tensor pointer");
   if (int e = check_attend_shape(d)) return e;
   if (!aligned16(x) || !aligned16(weights) || !aligned16(c_kv) || !aligned16(k_r) || !aligned16(y))
@@ -845,24 +968,22 @@ int videomla_attend_layer(const videomla_dims* d, const videomla_window* w, int3
   if (weights_bytes < W.total)
     return fail(VIDEOMLA_EWORKSPACE, "layer weights of %zu bytes expected, %zu given", W.total,
                 weights_bytes);
-  const LayerWorkspace L = layer_workspace(d, d_q, batch);
-  if (!workspace || workspace_bytes < L.total)
-    return fail(VIDEOMLA_EWORKSPACE, "workspace of %zu bytes needed, %zu given", L.total,
-                workspace ? workspace_bytes : (size_t)0);
-  if (!aligned16(workspace)) return fail(VIDEOMLA_EALIGN, "workspace must be 16-byte aligned");
+  const LayerWorkspace L = layer_workspace(d, d_q, batch, o);
+  if (int e = check_workspace(workspace, workspace_bytes, L.total)) return e;
 
   char* ws = static_cast<char*>(workspace);
   const char* wb = static_cast<const char*>(weights);
-  AttendArgs a = attend_args(d, w, batch, L.att, ws, c_kv, k_r);
+  AttendArgs a = attend_args(d, w, batch, o, L.att, ws, c_kv, k_r);
   uint16_t* u = reinterpret_cast<uint16_t*>(ws + L.u_off);
   uint16_t* o_lat = reinterpret_cast<uint16_t*>(ws + L.olat_off);
-  const int M = batch * a.geo.chunk_tokens;
+  const int M = batch * o.q_count;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  videomla_timer* t = o.timer;
 
   GemmArgs g1{};  // u = W_down^Q x
   g1.a = reinterpret_cast<const uint16_t*>(wb + W.wdq_off); g1.b = x; g1.out = u;
   g1.M = M; g1.N = W.d_q_pad; g1.K = d->d_model; g1.ldo = W.d_q_pad; g1.epi = kEpiStore;
-  hipError_t e = timed(K_Q_DOWN, s, [&] { return launch_gemm_nt(g1, s); });
+  hipError_t e = timed(t, K_Q_DOWN, s, [&] { return launch_gemm_nt(g1, s); });
   if (e != hipSuccess) return hip_fail(e, "q_down");
 
   GemmArgs g2{};  // q_cat from c^Q = g_Q u / rms(u) (the gain is in the packed weights)
@@ -871,49 +992,98 @@ int videomla_attend_layer(const videomla_dims* d, const videomla_window* w, int3
   g2.epi = kEpiQcat;
   g2.q_heads = d->n_heads; g2.q_dc = d->d_c; g2.q_dr = d->d_rope; g2.q_norm_dim = d_q;
   g2.qscale = a.qscale; g2.eps = d->kv_norm_eps; g2.geo = a.geo; g2.rope = a.rope;
-  e = timed(K_Q_UP, s, [&] { return launch_gemm_nt(g2, s); });
+  e = timed(t, K_Q_UP, s, [&] { return launch_gemm_nt(g2, s); });
   if (e != hipSuccess) return hip_fail(e, "q_up");
 
-  if (int r = run_attention(a, s)) return r;
-  e = timed(K_LATENT_MERGE, s, [&] { return launch_latent_merge(a, o_lat, W.k_out_pad, s); });
+  if (int r = run_attention(a, t, s)) return r;
+  e = timed(t, K_LATENT_MERGE, s, [&] { return launch_latent_merge(a, o_lat, W.k_out_pad, s); });
   if (e != hipSuccess) return hip_fail(e, "latent_merge");
 
   GemmArgs g3{};  // y = [B_1 .. B_H] o_lat
   g3.a = reinterpret_cast<const uint16_t*>(wb + W.bo_off); g3.b = o_lat; g3.out = y;
   g3.M = M; g3.N = d->d_model; g3.K = W.k_out_pad; g3.ldo = d->d_model; g3.epi = kEpiStore;
-  e = timed(K_OUT_MIX, s, [&] { return launch_gemm_nt(g3, s); });
+  e = timed(t, K_OUT_MIX, s, [&] { return launch_gemm_nt(g3, s); });
   if (e != hipSuccess) return hip_fail(e, "out_mix");
   return ok();
 }
 
-int videomla_timing_enable(int32_t enable) {
-  g_timing = enable != 0;
+// ---- timers -------------------------------------------------------------------------------------
+
+int videomla_timer_create(videomla_timer** timer) {
+  if (!timer) return fail(VIDEOMLA_EINVAL, "NULL timer pointer");
+  *timer = new (std::nothrow) videomla_timer();
+  if (!*timer) return fail(VIDEOMLA_EINVAL, "out of host memory");
   return ok();
 }
 
-int videomla_timing_only(const char* kernel) {
-  if (!kernel) {
-    g_timing_only = -1;
-    return ok();
+int videomla_timer_destroy(videomla_timer* timer) {
+  if (!timer) return ok();
+  for (const auto& r : timer->pending) {
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
   }
-  for (int k = 0; k < K_COUNT; ++k)
-    if (std::strcmp(kernel, kKernelNames[k]) == 0) {
-      g_timing_only = k;
-      return ok();
-    }
-  return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
+  for (hipEvent_t e : timer->pool) (void)hipEventDestroy(e);
+  if (timer->open.start) (void)hipEventDestroy(timer->open.start);
+  delete timer;
+  return ok();
 }
 
-int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms) {
-  if (!kernel || !count || !total_ms) return fail(VIDEOMLA_EINVAL, "NULL argument");
-  int id = -1;
-  for (int k = 0; k < K_COUNT; ++k)
-    if (std::strcmp(kernel, kKernelNames[k]) == 0) id = k;
+int videomla_timer_only(videomla_timer* timer, const char* kernel) {
+  if (!timer) return fail(VIDEOMLA_EINVAL, "NULL timer");
+  if (!kernel) {
+    timer->only = -1;
+    return ok();
+  }
+  const int id = kernel_id(kernel);
+  if (id < 0) return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
+  timer->only = id;
+  return ok();
+}
+
+int videomla_timer_begin(videomla_timer* timer, const char* kernel, void* stream) {
+  if (!timer || !kernel) return fail(VIDEOMLA_EINVAL, "NULL argument");
+  const int id = kernel_id(kernel);
+  if (id < 0) return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
+  if (timer->open.start) timer->pool.push_back(timer->open.start);  // an unmatched begin
+  timer->open = {-1, nullptr, nullptr};
+  hipEvent_t e = take_event(timer);
+  if (!e) return fail(VIDEOMLA_EHIP, "hipEventCreate failed");
+  const hipError_t r = hipEventRecord(e, reinterpret_cast<hipStream_t>(stream));
+  if (r != hipSuccess) {
+    timer->pool.push_back(e);
+    return hip_fail(r, "hipEventRecord");
+  }
+  timer->open = {id, e, nullptr};
+  return ok();
+}
+
+int videomla_timer_end(videomla_timer* timer, const char* kernel, void* stream) {
+  if (!timer || !kernel) return fail(VIDEOMLA_EINVAL, "NULL argument");
+  const int id = kernel_id(kernel);
+  if (id < 0) return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
+  if (!timer->open.start || timer->open.kernel != id)
+    return fail(VIDEOMLA_EINVAL, "videomla_timer_end('%s') without its videomla_timer_begin", kernel);
+  hipEvent_t e = take_event(timer);
+  if (!e) return fail(VIDEOMLA_EHIP, "hipEventCreate failed");
+  const hipError_t r = hipEventRecord(e, reinterpret_cast<hipStream_t>(stream));
+  if (r != hipSuccess) {
+    timer->pool.push_back(e);
+    return hip_fail(r, "hipEventRecord");
+  }
+  timer->pending.push_back({id, timer->open.start, e});
+  timer->open = {-1, nullptr, nullptr};
+  return ok();
+}
+
+int videomla_timer_read(videomla_timer* timer, const char* kernel, int64_t* count,
+                        double* total_ms) {
+  if (!timer || !kernel || !count || !total_ms) return fail(VIDEOMLA_EINVAL, "NULL argument");
+  const int id = kernel_id(kernel);
   if (id < 0) return fail(VIDEOMLA_EINVAL, "unknown kernel name '%s'", kernel);
   *count = 0;
   *total_ms = 0.0;
-  std::vector<TimingRec> keep;
-  for (const TimingRec& r : g_pending) {
+  std::vector<videomla_timer::Rec> keep;
+  for (const auto& r : timer->pending) {
     if (r.kernel != id) {
       keep.push_back(r);
       continue;
@@ -925,10 +1095,10 @@ int videomla_timing_read(const char* kernel, int64_t* count, double* total_ms) {
     }
     *count += 1;
     *total_ms += ms;
-    g_event_pool.push_back(r.start);
-    g_event_pool.push_back(r.stop);
+    timer->pool.push_back(r.start);
+    timer->pool.push_back(r.stop);
   }
-  g_pending.swap(keep);
+  timer->pending.swap(keep);
   return ok();
 }
 

@@ -120,6 +120,10 @@ __device__ __forceinline__ TokenPos token_pos(const Geometry& g, int n) {
   p.x = r % g.grid_w;
   return p;
 }
+// Absolute position of query token n of an attention call (chunk token q_begin + n).
+__device__ __forceinline__ TokenPos query_pos(const Geometry& g, int n) {
+  return token_pos(g, g.q_begin + n);
+}
 // Frame slot of absolute frame f: f mod W without a sink; with S sink frames, f for f < S and
 // S + (f - S) mod (W - S) otherwise.
 __device__ __forceinline__ int64_t frame_slot(const Geometry& g, int64_t f) {
@@ -153,14 +157,13 @@ __device__ __forceinline__ void rope_rotate(const RopeTable& t, int pair, const 
 }
 
 // Partial results of row block rbg: the workgroups owning its first and last units, under the
-// even split or (bal_on) the adaptive one whose weights the attention call stored.
+// even split or (bal_on) the weighted one whose weights the partition state holds (unchanged
+// since the attention kernel read them: only bal_prep_kernel writes them, before it).
 __device__ inline int attend_split_count(const AttendArgs& a, int64_t rbg) {
   const int64_t lo = rbg * a.tiles_per_row, hi = lo + a.tiles_per_row - 1;
   if (!a.bal_on) return attend_owner(hi, a.units, a.n_wg) - attend_owner(lo, a.units, a.n_wg) + 1;
-  const uint32_t* st = a.bal_state + (a.bal_seq & 1) * kBalSlot;
   uint32_t w[8];
-#pragma unroll
-  for (int x = 0; x < 8; ++x) w[x] = st[x];
+  bal_weights(a.bal_state, a.n_wg, w);
   return bal_owner(w, a.n_wg, a.units, hi) - bal_owner(w, a.n_wg, a.units, lo) + 1;
 }
 

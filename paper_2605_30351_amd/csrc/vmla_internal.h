@@ -25,6 +25,10 @@ struct RopeTable {
 struct Geometry {
   int32_t grid_h, grid_w, window_frames;
   int32_t chunk_tokens;   // chunk_frames * HW
+  // Queries of an attention call: chunk tokens q_begin .. q_begin + q_count - 1 (the whole
+  // chunk unless the call asks for a block of its query rows); q_count tokens per batch element
+  // in the query, output and workspace tensors.
+  int32_t q_begin, q_count;
   int64_t frame_end;      // absolute first frame of the chunk
   int64_t ring_tokens;    // window_frames * HW (ring rows per batch element)
   // Attention sink: frames 0 .. sink_frames-1 keep frame slots 0 .. sink_frames-1, later frames
@@ -76,11 +80,13 @@ struct AttendArgs {
   int64_t units;           // U = batch * row_blocks * T
   int32_t max_seg;         // partial-result slots the workspace holds
   float qscale;            // softmax scale * log2(e), folded into the absorbed query
-  // Adaptive partition (latent path, optional): two state slots of kBalSlot words in the
-  // workspace; the call with sequence number bal_seq reads slot (bal_seq - 1) & 1 and writes
-  // slot bal_seq & 1 (see bal_* below). bal_on = 0: the even split above.
+  // Weighted partition (optional): the state area of kBalSlot words in the workspace (see bal_*
+  // below). bal_on: split by the weights the state holds (equal weights, i.e. the even split, if
+  // it holds no valid record for this G); bal_rec: the call is adaptive, bal_prep_kernel has
+  // set the weights from the previous adaptive call's times and the attention kernel records
+  // its own. bal_on = 0: the even split above, the state is not read.
   uint32_t* bal_state;
-  int32_t bal_on, bal_seq;
+  int32_t bal_on, bal_rec;
   Geometry geo;
   RopeTable rope;
   // dense per-head comparator only (rows are (head, token) pairs, each head padded to nq_pad)
@@ -116,7 +122,7 @@ struct GemmArgs {
   // per-head epilogue: output column o goes to head o / head_w, column col_off + o % head_w
   int32_t head_w, head_ld, col_off;
   float qscale, eps;
-  Geometry geo;            // token t of the flat [B][Nq] order sits at chunk index t % Nq
+  Geometry geo;            // token t of the flat [B][q_count] order is query t % q_count
   RopeTable rope;
 };
 
@@ -132,15 +138,26 @@ __host__ __device__ inline int attend_owner(int64_t unit, int64_t units, int n_w
   return (int)(((unit + 1) * (int64_t)n_wg - 1) / units);
 }
 
-// Adaptive partition of the attention units. Workgroup k runs on XCD k mod 8 and gets a share of
+// Weighted partition of the attention units. Workgroup k runs on XCD k mod 8 and gets a share of
 // the units proportional to its XCD's integer weight w[k mod 8] in [kBalMin, kBalMax]:
 // workgroup k takes [start(k), start(k+1)) with start(k) = floor(U cum(k) / cum(G)), cum(k) the
-// summed weights of workgroups 0 .. k-1. Equal weights give the even split. A state slot holds
-// the weights a call used (words 0..7), its G (8), a marker (9) and each workgroup's duration in
-// 100 MHz ticks (kBalHead + k); the next call sets each XCD's weight proportional to the work per
-// time that XCD achieved. Any slot content that fails the checks means equal weights.
+// summed weights of workgroups 0 .. k-1. Equal weights give the even split. The state area holds
+// the weights (words 0..7), the G they were set for (8), a marker (9) and each workgroup's
+// duration in 100 MHz ticks (kBalHead + k) as the last adaptive call recorded it. An adaptive
+// call first runs bal_prep_kernel (one workgroup, stream-ordered between the previous call's
+// last reader of the weights and this call's attention kernel): it sets each XCD's weight
+// proportional to the work per time that XCD achieved, writes G and the marker, and clears the
+// durations. Any state that fails the checks means equal weights.
 constexpr uint32_t kBalMin = 820, kBalMax = 1280, kBalOne = 1024, kBalMark = 0x564d4c42u;
 constexpr int kBalHead = 16, kBalMaxWg = 4096, kBalSlot = kBalHead + kBalMaxWg;
+
+// The weights a partition state holds for G workgroups: its words 0..7 if the marker, G and
+// every weight check out, else equal weights.
+__host__ __device__ inline void bal_weights(const uint32_t* st, int G, uint32_t (&w)[8]) {
+  bool ok = st[9] == kBalMark && st[8] == (uint32_t)G;
+  for (int x = 0; x < 8; ++x) ok = ok && st[x] >= kBalMin && st[x] <= kBalMax;
+  for (int x = 0; x < 8; ++x) w[x] = ok ? st[x] : kBalOne;
+}
 
 __host__ __device__ inline int64_t bal_cum(const uint32_t* w, int k) {
   int64_t s = 0;
@@ -181,6 +198,7 @@ hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s);
 size_t write_weights_packed_elems(int d_model, int d_c, int d_rope);
 hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
 hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s);
+hipError_t launch_bal_prep(const AttendArgs& a, hipStream_t s);
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);

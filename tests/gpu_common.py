@@ -72,33 +72,62 @@ class Layer:
             self.vm.cache_write(d, fe, self.inp.batch, xs, self.w_dkv, self.w_kr, self.gamma,
                                 self.c_kv, self.k_r, self.slots)
 
-    def attend(self, fe, materialized=False):
-        """videomla_attend, or videomla_attend_materialized (per-head K/V reconstructed)."""
+    def attend(self, fe, opts=None, ws=None):
+        """videomla_attend (opts None) or videomla_attend_ex with these options, into a fresh
+        workspace unless `ws` is given; with a query range the queries and outputs are the
+        range's tokens."""
         d = self.inp.dims
-        size = (self.vm.attend_materialized_workspace_bytes if materialized
-                else self.vm.attend_workspace_bytes)(d, self.inp.batch)
-        ws = torch.empty(size, dtype=torch.uint8, device="cuda")
-        self.vm.attend(d, fe, self.inp.batch, self.q_nope, self.q_r, self.w_uk, self.w_uv,
-                       self.c_kv, self.k_r, self.out, ws, materialized=materialized)
+        B = self.inp.batch
+        if ws is None:
+            ws = torch.empty(self.vm.attend_workspace_bytes(d, B, opts), dtype=torch.uint8,
+                             device="cuda")
+        q_nope, q_r, out = self.q_nope, self.q_r, self.out
+        if opts is not None and (opts.query_begin or opts.query_count):
+            lo, n = opts.query_begin, opts.n_queries(d)
+            q_nope = q_nope[:, lo:lo + n].contiguous()
+            q_r = q_r[:, lo:lo + n].contiguous()
+            out = torch.zeros((B, n, d.n_heads, d.d_v), dtype=torch.bfloat16, device="cuda")
+        self.vm.attend(d, fe, B, q_nope, q_r, self.w_uk, self.w_uv, self.c_kv, self.k_r, out, ws,
+                       opts=opts)
         torch.cuda.synchronize()
-        return bf16_to_f64(host_bits(self.out))
+        return bf16_to_f64(host_bits(out))
 
 
 U_BF16 = 2.0 ** -9
 
 
-def assert_attention_close(got, want, label=""):
+def scaled_bars(want):
+    """Bars scaled by the output magnitude, for outputs of order one (the peaked-softmax
+    variants): six bf16 roundings on the path (u = 2^-9) and the score perturbation u|s| they
+    cause give max|err| <= 8u max|out| and mean|err| <= 4u mean|out|, never below the fixed
+    bars."""
+    return (max(ATOL_MAX, 8 * U_BF16 * np.abs(want).max()),
+            max(ATOL_MEAN, 4 * U_BF16 * np.abs(want).mean()))
+
+
+def assert_attention_close(got, want, label="", scaled=False, bars=None):
+    """max-abs <= 2e-2, mean-abs <= 2e-3 and relative L2 <= 1e-2 (the stated tolerance). With
+    scaled=True the max and mean bars are scaled_bars(want) instead; `bars` = (max, mean,
+    rel-L2) given by the caller (a bound derived for that case) overrides all three. Both the
+    fixed and the scaled bars are printed."""
     err = np.abs(got - want)
     rel = np.linalg.norm(got - want) / np.linalg.norm(want)
-    max_bar = max(ATOL_MAX, 8 * U_BF16 * np.abs(want).max())
-    mean_bar = max(ATOL_MEAN, 4 * U_BF16 * np.abs(want).mean())
-    msg = (f"{label}: max {err.max():.3e} (bar {max_bar:.2e}) mean {err.mean():.3e} "
-           f"(bar {mean_bar:.2e}) relL2 {rel:.3e} |out| max {np.abs(want).max():.3e} "
-           f"mean {np.abs(want).mean():.3e}")
+    s_max, s_mean = scaled_bars(want)
+    rel_bar = REL_L2
+    if bars is not None:
+        max_bar, mean_bar, rel_bar, kind = bars[0], bars[1], bars[2], "derived"
+    elif scaled:
+        max_bar, mean_bar, kind = s_max, s_mean, "scaled"
+    else:
+        max_bar, mean_bar, kind = ATOL_MAX, ATOL_MEAN, "fixed"
+    msg = (f"{label}: max {err.max():.3e} mean {err.mean():.3e} relL2 {rel:.3e} | {kind} bars "
+           f"{max_bar:.2e} / {mean_bar:.2e} / relL2 {rel_bar:.2e} (fixed {ATOL_MAX:.0e} / {ATOL_MEAN:.0e}, scaled "
+           f"{s_max:.2e} / {s_mean:.2e}) |out| max {np.abs(want).max():.3e} "
+           f"mean {np.abs(want).mean():.3e} n={got.size}")
     print(msg, flush=True)
     assert err.max() <= max_bar, msg
     assert err.mean() <= mean_bar, msg
-    assert rel <= REL_L2, msg
+    assert rel <= rel_bar, msg
 
 
 def check_written_chunk(layer, fe, before_c, before_k):

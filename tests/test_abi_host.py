@@ -135,12 +135,115 @@ def test_packed_write_weights_size_and_validation():
     assert _write(_dims_struct(WAN, d_model=4096)) == L.EUNSUPPORTED
 
 
-def test_timing_selection():
-    """videomla_timing_only takes the kernel names that videomla_timing_read knows, or NULL."""
-    vm.timing_only("latent_attend")
-    vm.timing_only(None)
-    assert L.raw().videomla_timing_only(b"no_such_kernel") == L.EINVAL
-    assert L.raw().videomla_timing_only(None) == L.OK
+def test_timer_lifecycle_and_names():
+    """A timer is a caller-owned object: videomla_timer_only takes the kernel names that
+    videomla_timer_read knows, or NULL; reads of a fresh timer are empty."""
+    t = vm.Timer()
+    t.only("latent_attend")
+    t.only(None)
+    assert t.read("latent_attend") == (0, 0.0)
+    with pytest.raises(vm.VideomlaError):
+        t.only("no_such_kernel")
+    with pytest.raises(vm.VideomlaError):
+        t.read("nope")
+    lib = L.raw()
+    # an end without its begin, an unknown name (host-side checks: no event is recorded)
+    assert lib.videomla_timer_end(t.handle, b"cache_write", None) == L.EINVAL
+    assert lib.videomla_timer_begin(t.handle, b"no_such_kernel", None) == L.EINVAL
+    t.close()
+    lib = L.raw()
+    assert lib.videomla_timer_only(None, b"latent_attend") == L.EINVAL
+    assert lib.videomla_timer_begin(None, b"cache_write", None) == L.EINVAL
+    assert lib.videomla_timer_create(None) == L.EINVAL
+    assert lib.videomla_timer_destroy(None) == L.OK
+
+
+def _opts(**kw):
+    o = L.VideomlaAttendOpts()
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def _attend_ex(d, opts, fe=0, batch=1, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+    w = L.VideomlaWindow(fe)
+    return L.raw().videomla_attend_ex(ctypes.byref(d), ctypes.byref(w), batch, q, FAKE, FAKE,
+                                      FAKE, FAKE, FAKE, FAKE, ws, ws_bytes,
+                                      ctypes.byref(opts) if opts is not None else None, None)
+
+
+def test_attend_options_are_validated():
+    d = L.make_dims(WAN)
+    for bad in (dict(partition=3), dict(partition=-1), dict(form=7), dict(n_workgroups=-1),
+                dict(n_workgroups=(1 << 20) + 1), dict(query_begin=-1),
+                dict(query_begin=4680), dict(query_begin=4000, query_count=681),
+                dict(query_count=-2)):
+        assert _attend_ex(d, _opts(**bad)) == L.EINVAL, bad
+        assert L.raw().videomla_attend_workspace_bytes_ex(
+            ctypes.byref(d), 1, ctypes.byref(_opts(**bad))) == 0, bad
+    # the last query range that fits, and NULL options (= videomla_attend)
+    assert vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(query_begin=4000, query_count=680)) > 0
+    assert (L.raw().videomla_attend_workspace_bytes_ex(ctypes.byref(d), 1, None)
+            == vm.attend_workspace_bytes(WAN, 1))
+    need = vm.attend_workspace_bytes(WAN, 1)
+    assert _attend_ex(d, None, ws_bytes=need - 1) == L.EWORKSPACE
+    assert _attend_ex(d, _opts(partition=2), ws_bytes=need - 1) == L.EWORKSPACE
+
+
+def test_query_range_sizes_the_workspace():
+    """A block of the chunk's query rows needs the workspace of that many rows."""
+    full = vm.attend_workspace_bytes(WAN, 1)
+    part = vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(query_begin=1560, query_count=1560))
+    assert part < full
+    assert part >= 1560 * 12 * 224 * 2 + 1560 * 12 * 192 * 4
+    few = vm.attend_workspace_bytes(WAN, 8, vm.AttendOpts(query_count=16))
+    assert 0 < few < full
+    assert (vm.dense_attend_workspace_bytes(WAN, 8, vm.AttendOpts(query_count=16))
+            < vm.dense_attend_workspace_bytes(WAN, 8))
+
+
+def test_auto_form_follows_the_cost_model():
+    """The cost model picks the materialized form where its cheaper score outweighs the
+    reconstruction (a 3-frame Wan chunk), the latent form for few queries, and never the
+    materialized form on shapes it is not built for."""
+    mat = vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(form="materialized"))
+    lat = vm.attend_workspace_bytes(WAN, 1)
+    assert mat > lat
+    assert vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(form="auto")) == mat
+    few = vm.AttendOpts(form="auto", query_count=52)
+    assert vm.attend_workspace_bytes(WAN, 1, few) == vm.attend_workspace_bytes(
+        WAN, 1, vm.AttendOpts(query_count=52))
+    # no materialized kernel is built for d_v = 96: AUTO falls back to the latent form
+    d96 = WAN.replace(d_v=96)
+    assert (vm.attend_workspace_bytes(d96, 1, vm.AttendOpts(form="auto"))
+            == vm.attend_workspace_bytes(d96, 1))
+    assert vm.attend_workspace_bytes(d96, 1, vm.AttendOpts(form="materialized")) == 0
+
+
+def test_two_threads_with_different_options():
+    """The library keeps no configuration between calls: two threads asking at the same time
+    for the workspace of different options each get their own answer, and each thread reads its
+    own last error."""
+    import threading
+    one = vm.AttendOpts(n_workgroups=1)
+    want = {0: vm.attend_workspace_bytes(WAN, 1), 1: vm.attend_workspace_bytes(WAN, 1, one)}
+    assert want[0] != want[1]
+    bad = {0: _dims_struct(WAN, d_c=100), 1: _dims_struct(WAN, d_nope=100)}
+    seen = {0: set(), 1: set()}
+    errors = {0: set(), 1: set()}
+
+    def run(k):
+        for _ in range(200):
+            seen[k].add(vm.attend_workspace_bytes(WAN, 1, one if k else None))
+            _attend(bad[k])
+            errors[k].add(L.raw().videomla_last_error().decode())
+    threads = [threading.Thread(target=run, args=(k,)) for k in (0, 1)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert seen == {0: {want[0]}, 1: {want[1]}}
+    assert len(errors[0]) == 1 and len(errors[1]) == 1 and errors[0] != errors[1], errors
 
 
 def test_dc_sweep_shapes():
@@ -159,26 +262,28 @@ def test_dc_sweep_shapes():
 def test_materialized_attend_validation():
     """The materialized form is built for d_v = 128 with keys of d_nope + d_rope = 128 (the
     paper's 96 + 32) or 160 (128 + 32), no sink."""
-    assert vm.attend_materialized_workspace_bytes(WAN_PAPER, 1) > 0
-    assert vm.attend_materialized_workspace_bytes(WAN, 1) > 0
-    assert vm.attend_materialized_workspace_bytes(WAN.replace(d_nope=112), 1) == 0
-    mat = L.raw().videomla_attend_materialized
+    mat = vm.AttendOpts(form="materialized")
+    assert vm.attend_workspace_bytes(WAN_PAPER, 1, mat) > 0
+    assert vm.attend_workspace_bytes(WAN, 1, mat) > 0
+    assert vm.attend_workspace_bytes(WAN.replace(d_nope=112), 1, mat) == 0
+    o = _opts(form=1)
 
     def call(d, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
-        w = L.VideomlaWindow(0)
-        return mat(ctypes.byref(d), ctypes.byref(w), 1, q, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                   ws, ws_bytes, None)
+        return _attend_ex(d, o, ws=ws, ws_bytes=ws_bytes, q=q)
     d = L.make_dims(WAN_PAPER)
     assert call(_dims_struct(WAN, d_nope=112)) == L.EUNSUPPORTED
     assert call(_dims_struct(WAN_PAPER, sink_frames=1, window_frames=7)) == L.EUNSUPPORTED
     assert call(d, q=None) == L.EINVAL
     assert call(d, q=MISALIGNED) == L.EALIGN
-    need = vm.attend_materialized_workspace_bytes(WAN_PAPER, 1)
+    need = vm.attend_workspace_bytes(WAN_PAPER, 1, mat)
     assert call(d, ws=None) == L.EWORKSPACE
     assert call(d, ws_bytes=need - 1) == L.EWORKSPACE
     # the reconstructed rows dominate: ring x heads x (K_h | V_h) in bf16
     assert need >= 32760 * 12 * 256 * 2
-    assert vm.attend_materialized_workspace_bytes(WAN, 1) >= 32760 * 12 * 288 * 2
+    assert vm.attend_workspace_bytes(WAN, 1, mat) >= 32760 * 12 * 288 * 2
+    # the partition state sits after the partial results, not over the query rows
+    adaptive = vm.AttendOpts(form="materialized", partition="adaptive")
+    assert vm.attend_workspace_bytes(WAN, 1, adaptive) == vm.attend_workspace_bytes(WAN, 1, mat)
 
 
 def test_attend_rejects_bad_args():
@@ -197,26 +302,14 @@ def test_attend_rejects_bad_args():
 def test_workspace_tracks_the_work_partition():
     rows = WAN.chunk_tokens * WAN.n_heads
     one_row_block_each = rows * 224 * 2 + rows * 192 * 4 + rows * 8
-    try:
-        vm.set_attend_workgroups(1)       # one workgroup walks every row block whole
-        assert vm.attend_workspace_bytes(WAN, 1) >= one_row_block_each
-        single = vm.attend_workspace_bytes(WAN, 1)
-        vm.set_attend_workgroups(256)     # 220 row blocks over 256 workgroups: up to 3 parts each
-        assert vm.attend_workspace_bytes(WAN, 1) > single
-        vm.set_attend_workgroups(5000)    # more workgroups than some windows have tiles
-        assert vm.attend_workspace_bytes(WAN, 1) > vm.attend_workspace_bytes(WAN, 1) - 1
-        assert vm.attend_workspace_bytes(WAN, 2) > 0
-    finally:
-        vm.set_attend_workgroups(0)
-    with pytest.raises(vm.VideomlaError):
-        vm.set_attend_workgroups(-1)
-
-
-def test_timing_read_validates_names():
-    n, t = vm.timing_read("latent_attend")
-    assert (n, t) == (0, 0.0)
-    with pytest.raises(vm.VideomlaError):
-        vm.timing_read("nope")
+    # one workgroup walks every row block whole
+    single = vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(n_workgroups=1))
+    assert single >= one_row_block_each
+    # 220 row blocks over 256 workgroups: up to 3 parts each
+    assert vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(n_workgroups=256)) > single
+    # more workgroups than some windows have tiles
+    assert vm.attend_workspace_bytes(WAN, 1, vm.AttendOpts(n_workgroups=5000)) > single
+    assert vm.attend_workspace_bytes(WAN, 2) > 0
 
 
 def test_dense_cache_bytes_per_token():
@@ -233,10 +326,11 @@ def _dense_write(d, fe=0, batch=1, x=FAKE):
                                               FAKE, FAKE, None, None)
 
 
-def _dense_attend(d, fe=0, batch=1, ws=FAKE, ws_bytes=1 << 40, q=FAKE):
+def _dense_attend(d, fe=0, batch=1, ws=FAKE, ws_bytes=1 << 40, q=FAKE, opts=None):
     w = L.VideomlaWindow(fe)
     return L.raw().videomla_dense_attend(ctypes.byref(d), ctypes.byref(w), batch, q, FAKE, FAKE,
-                                         ws, ws_bytes, None)
+                                         ws, ws_bytes,
+                                         ctypes.byref(opts) if opts is not None else None, None)
 
 
 def test_dense_calls_reject_bad_args():
@@ -254,7 +348,8 @@ def test_dense_calls_reject_bad_args():
     assert _dense_attend(d, ws=None) == L.EWORKSPACE
     assert _dense_attend(d, ws_bytes=need - 1) == L.EWORKSPACE
     assert _dense_attend(_dims_struct(WAN, d_v=64)) == L.EUNSUPPORTED
-    assert vm.dense_attend_workspace_bytes(_dims_struct(WAN, d_v=64), 1) == 0
+    assert vm.dense_attend_workspace_bytes(WAN.replace(d_v=64), 1) == 0
+    assert _dense_attend(d, opts=_opts(partition=5)) == L.EINVAL
 
 
 def test_dense_workspace_covers_padded_rows():
@@ -299,7 +394,8 @@ def test_layer_calls_validate_and_size():
 
     def layer(d=d, d_q=768, x=FAKE, weights=FAKE, weights_bytes=wb, ws_ptr=FAKE, ws_bytes=1 << 40):
         return L.raw().videomla_attend_layer(ctypes.byref(d), ctypes.byref(w), 1, d_q, x, weights,
-                                             weights_bytes, FAKE, FAKE, FAKE, ws_ptr, ws_bytes, None)
+                                             weights_bytes, FAKE, FAKE, FAKE, ws_ptr, ws_bytes,
+                                             None, None)
     assert layer(x=None) == L.EINVAL
     assert layer(d_q=0) == L.EINVAL
     assert layer(x=MISALIGNED) == L.EALIGN
@@ -308,6 +404,10 @@ def test_layer_calls_validate_and_size():
     assert layer(ws_bytes=ws - 1) == L.EWORKSPACE
     assert layer(d=_dims_struct(WAN, d_c=112)) == L.EUNSUPPORTED
     assert layer(d=_dims_struct(WAN, d_model=1000)) == L.EUNSUPPORTED
+    # the whole layer runs the latent form only
+    assert vm.attend_layer_workspace_bytes(WAN, 768, 1, vm.AttendOpts(form="materialized")) == 0
+    assert (vm.attend_layer_workspace_bytes(WAN, 768, 1, vm.AttendOpts(form="auto"))
+            == vm.attend_layer_workspace_bytes(WAN, 768, 1))
     prep = L.raw().videomla_prepare_layer_weights
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, wb, None) == L.EINVAL
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, wb - 1, None) == L.EWORKSPACE

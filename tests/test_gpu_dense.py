@@ -27,9 +27,7 @@ def vm():
         pytest.skip("no GPU")
     ensure_built()
     import paper_2605_30351_amd as m
-    m.set_attend_workgroups(0)
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -61,13 +59,22 @@ class DenseLayer:
         self.vm.dense_cache_write(d, fe, self.inp.batch, xs, self.w_k, self.w_v, self.kv,
                                   self.slots)
 
-    def attend(self, fe):
+    def attend(self, fe, opts=None, ws=None):
+        """videomla_dense_attend with these options (None: the defaults), into a fresh workspace
+        unless `ws` is given; with a query range the queries and outputs are the range's."""
         d = self.inp.dims
-        ws = torch.empty(self.vm.dense_attend_workspace_bytes(d, self.inp.batch),
-                         dtype=torch.uint8, device="cuda")
-        self.vm.dense_attend(d, fe, self.inp.batch, self.q, self.kv, self.out, ws)
+        B = self.inp.batch
+        if ws is None:
+            ws = torch.empty(self.vm.dense_attend_workspace_bytes(d, B, opts), dtype=torch.uint8,
+                             device="cuda")
+        q, out = self.q, self.out
+        if opts is not None and (opts.query_begin or opts.query_count):
+            lo, n = opts.query_begin, opts.n_queries(d)
+            q = q[:, lo:lo + n].contiguous()
+            out = torch.zeros((B, n, d.n_heads, d.d_v), dtype=torch.bfloat16, device="cuda")
+        self.vm.dense_attend(d, fe, B, q, self.kv, out, ws, opts=opts)
         torch.cuda.synchronize()
-        return bf16_to_f64(host_bits(self.out))
+        return bf16_to_f64(host_bits(out))
 
 
 def check_dense_chunk(layer, fe, before):
@@ -139,13 +146,7 @@ def test_dense_split_keys_match_single_pass(vm):
     layer = DenseLayer(vm, inp)
     for fe in (0, 2, 4):
         layer.write(fe)
-    outs = []
-    try:
-        for n_wg in (1, 2, 7, 64):
-            vm.set_attend_workgroups(n_wg)
-            outs.append(layer.attend(4))
-    finally:
-        vm.set_attend_workgroups(0)
+    outs = [layer.attend(4, vm.AttendOpts(n_workgroups=n_wg)) for n_wg in (1, 2, 7, 64)]
     want = O.dense_chunk_attention(inp, 1, 4)
     for o in outs:
         assert_attention_close(o[1], want, "dense split")

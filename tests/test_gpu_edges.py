@@ -7,7 +7,6 @@
 * a window exactly one chunk long (every chunk replaces the whole ring and attends to itself);
 * a batch of 8 small rollouts at once.
 """
-import numpy as np
 import pytest
 import torch
 
@@ -23,12 +22,12 @@ def vm():
     ensure_built()
     import paper_2605_30351_amd as m
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
 from tests.gpu_common import (assert_attention_close, check_written_chunk,  # noqa: E402
                               host_bits, layer_for)
+from tests.bf16_storage import storage_bars  # noqa: E402
 from workloads import TINY, WAN, Dims, make_layer_inputs  # noqa: E402
 
 
@@ -58,35 +57,28 @@ def test_packed_write_at_most_outputs(vm):
 
 
 def _rollout_every_output(vm, dims, n_frames, batch, seed, modes, workgroups=(1, 0),
-                          pool=False):
-    """Every write and every output of a rollout. pool: the error bars apply to all outputs of
-    the rollout together rather than to each call's, for shapes whose call yields a single
-    query row (32 values: the mean error of one row is too noisy a statistic for the mean bar;
-    a CPU emulation of the path's bf16 storage points reproduces the per-row errors)."""
+                          storage_bound=False):
+    """Every write and every output of a rollout, each call checked on its own. storage_bound:
+    each call's bars are the fixed ones or 1.5 times the error that bf16 storage alone gives on
+    that call (tests/bf16_storage.py), whichever is larger, for shapes whose call yields a
+    single query row (tests/test_bf16_storage.py shows that storage alone exceeds the fixed
+    mean and relative-L2 bars on one call of the one-token grid)."""
     inp = make_layer_inputs(dims, seed=seed, n_frames=n_frames, batch=batch)
     for mode in modes:
         layer = layer_for(vm, inp, mode)
         exact = total = 0
-        pooled_got, pooled_want = [], []
         for fe in range(0, n_frames, dims.chunk_frames):
             before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
             layer.write(fe)
             for e, n in check_written_chunk(layer, fe, before_c, before_k):
                 exact, total = exact + e, total + n
             for wg in workgroups:
-                vm.set_attend_workgroups(wg)
-                got = layer.attend(fe)
+                got = layer.attend(fe, vm.AttendOpts(n_workgroups=wg))
                 for b in range(batch):
                     want = O.chunk_attention(inp, b, fe)
-                    if pool:
-                        pooled_got.append(got[b].ravel())
-                        pooled_want.append(want.ravel())
-                    else:
-                        assert_attention_close(got[b], want, f"{mode} fe={fe} b={b} wg={wg}")
-            vm.set_attend_workgroups(0)
-        if pool:
-            assert_attention_close(np.concatenate(pooled_got), np.concatenate(pooled_want),
-                                   f"{mode} whole rollout")
+                    bars = storage_bars(inp, b, fe, want) if storage_bound else None
+                    assert_attention_close(got[b], want, f"{mode} fe={fe} b={b} wg={wg}",
+                                           bars=bars)
         assert exact / total >= 0.99, f"{exact}/{total} exactly rounded"
 
 
@@ -96,7 +88,7 @@ def test_one_token_grid(vm):
     dims = Dims(d_model=64, n_heads=1, d_nope=32, d_rope=8, d_c=16, d_v=32, grid_h=1, grid_w=1,
                 window_frames=3, chunk_frames=1, rope_pairs=(2, 1, 1))
     _rollout_every_output(vm, dims, n_frames=7, batch=2, seed=52,
-                          modes=("plain_weights", "packed_weights"), pool=True)
+                          modes=("plain_weights", "packed_weights"), storage_bound=True)
 
 
 def test_window_of_one_chunk(vm):

@@ -25,9 +25,7 @@ def vm():
         pytest.skip("no GPU")
     ensure_built()
     import paper_2605_30351_amd as m
-    m.set_attend_workgroups(0)
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -54,16 +52,26 @@ class FullLayer:
         d = self.inp.dims
         return self.x[:, fe * d.hw:(fe + d.chunk_frames) * d.hw].contiguous()
 
-    def step(self, fe):
+    def step(self, fe, opts=None, ws=None, write=True):
+        """Cache write of the chunk (unless write=False), then videomla_attend_layer with these
+        options; with a query range x and y are the range's tokens."""
         d, B = self.inp.dims, self.inp.batch
         xs = self.chunk(fe)
-        self.vm.cache_write(d, fe, B, xs, self.w_dkv, self.w_kr, self.gamma, self.c_kv, self.k_r)
-        ws = torch.empty(self.vm.attend_layer_workspace_bytes(d, self.inp.d_q, B),
-                         dtype=torch.uint8, device="cuda")
+        if write:
+            self.vm.cache_write(d, fe, B, xs, self.w_dkv, self.w_kr, self.gamma, self.c_kv,
+                                self.k_r)
+        if ws is None:
+            ws = torch.empty(self.vm.attend_layer_workspace_bytes(d, self.inp.d_q, B, opts),
+                             dtype=torch.uint8, device="cuda")
+        y = self.y
+        if opts is not None and (opts.query_begin or opts.query_count):
+            lo, n = opts.query_begin, opts.n_queries(d)
+            xs = xs[:, lo:lo + n].contiguous()
+            y = torch.zeros((B, n, d.d_model), dtype=torch.bfloat16, device="cuda")
         self.vm.attend_layer(d, fe, B, self.inp.d_q, xs, self.weights, self.c_kv, self.k_r,
-                             self.y, ws)
+                             y, ws, opts=opts)
         torch.cuda.synchronize()
-        return bf16_to_f64(host_bits(self.y))
+        return bf16_to_f64(host_bits(y))
 
 
 @pytest.mark.parametrize("dims", [TINY, TINY_SINK], ids=["plain", "sink"])

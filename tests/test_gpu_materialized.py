@@ -1,5 +1,5 @@
-"""GPU parity of the materialized-K/V attention (videomla_attend_materialized: per-head keys
-and values reconstructed from the latent ring, then standard attention) against the fp64
+"""GPU parity of the materialized-K/V attention (videomla_attend_ex with the materialized form:
+per-head keys and values reconstructed from the latent ring, then standard attention) against the fp64
 oracle, whose reference is that same training form. Bars as in tests/test_gpu_parity.py.
 Both head splits it is built for: the paper's d_nope 96 + d_rope 32 (keys as wide as the
 128-wide values) and d_nope 128 + d_rope 32 (160-wide keys)."""
@@ -19,7 +19,6 @@ def vm():
     ensure_built()
     import paper_2605_30351_amd as m
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -38,13 +37,11 @@ def test_small_every_output(vm, dims):
         layer.write(fe)
         lat = layer.attend(fe)
         for wg in ((1, 3, 7, 0) if fe in (0, 6, 12) else (0,)):
-            vm.set_attend_workgroups(wg)
-            got = layer.attend(fe, materialized=True)
+            got = layer.attend(fe, vm.AttendOpts(n_workgroups=wg, form="materialized"))
             for b in range(2):
                 want = O.chunk_attention(inp, b, fe)
                 assert_attention_close(got[b], want, f"materialized fe={fe} b={b} wg={wg}")
                 assert_attention_close(got[b], lat[b], f"materialized vs latent fe={fe} b={b}")
-        vm.set_attend_workgroups(0)
 
 
 @pytest.mark.parametrize("dims", [WAN_PAPER, WAN], ids=["nope96", "nope128"])
@@ -55,9 +52,10 @@ def test_wan_geometry(vm, dims):
     layer = Layer(vm, inp, packed=True)
     rows = sample_rows(dims.chunk_tokens, k=24, seed=5)
     layer.write(0)
-    got = layer.attend(0, materialized=True)
+    mat = vm.AttendOpts(form="materialized")
+    got = layer.attend(0, mat)
     assert_attention_close(got[0][rows], O.chunk_attention(inp, 0, 0, rows=rows), "wan fe=0")
     for fe in range(3, 22, 3):
         layer.write(fe)
-    got = layer.attend(21, materialized=True)
+    got = layer.attend(21, mat)
     assert_attention_close(got[0][rows], O.chunk_attention(inp, 0, 21, rows=rows), "wan fe=21")

@@ -6,16 +6,15 @@ elements, and every element is within one bf16 ulp of it or within 2^-16 of the 
 it (the fp32 sum over d_model terms carries an absolute error near 1e-7 at unit scale, which
 exceeds one ulp only for values within about 2^-16 of zero); slots are bit-exact and every slot
 outside the written frames is bitwise unchanged; attention outputs satisfy max-abs <= 2e-2,
-mean-abs <= 2e-3 and relative L2 <= 1e-2.
+mean-abs <= 2e-3 and relative L2 <= 1e-2, the stated tolerance, on every case here except
+the peaked-softmax variants.
 
-Where outputs are of order one (the tiny shapes, the peaked-softmax variants with queries x4)
-an absolute 2e-2 is about one bf16 ulp of the output itself, so the bars are the larger of the
-absolute ones and bars scaled by the output magnitude. The path rounds six times to bf16
-(query, latent, RoPE key, probabilities, merged latent, output; unit roundoff u = 2^-9), and
-rounding the query and the cached key moves each score by about u|s|, which the softmax turns
-into relative weight errors of the same size: max|err| <= max(2e-2, 8u max|out|) and
-mean|err| <= max(2e-3, 4u mean|out|), always with the relative-L2 bar. At the Wan shape the
-outputs stay below 0.4, so the absolute bars are the binding ones there.
+The peaked variants (queries x4) have outputs of order one, where an absolute 2e-2 is about one
+bf16 ulp of the output itself; their bars are scaled by the output magnitude. The path rounds
+six times to bf16 (query, latent, RoPE key, probabilities, merged latent, output; unit roundoff
+u = 2^-9), and rounding the query and the cached key moves each score by about u|s|, which the
+softmax turns into relative weight errors of the same size: max|err| <= max(2e-2, 8u max|out|)
+and mean|err| <= max(2e-3, 4u mean|out|), always with the relative-L2 bar.
 """
 import numpy as np
 import pytest
@@ -33,7 +32,6 @@ def vm():
     ensure_built()
     import paper_2605_30351_amd as m
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -58,12 +56,10 @@ def test_tiny_rollout_write_and_attend(vm, norm, packed):
         for e, n in check_written_chunk(layer, fe, before_c, before_k):
             exact, total = exact + e, total + n
         for wg in (1, 2, 3, 0):
-            vm.set_attend_workgroups(wg)
-            got = layer.attend(fe)
+            got = layer.attend(fe, vm.AttendOpts(n_workgroups=wg))
             for b in range(2):
                 want = O.chunk_attention(inp, b, fe)
                 assert_attention_close(got[b], want, f"tiny fe={fe} b={b} workgroups={wg}")
-        vm.set_attend_workgroups(0)
     assert exact / total >= 0.999, f"{exact}/{total} exactly rounded"
 
 
@@ -73,7 +69,7 @@ def test_tiny_peaked_softmax(vm):
     for fe in range(6):
         layer.write(fe)
     got = layer.attend(5)
-    assert_attention_close(got[0], O.chunk_attention(inp, 0, 5), "tiny peaked")
+    assert_attention_close(got[0], O.chunk_attention(inp, 0, 5), "tiny peaked", scaled=True)
 
 
 # -------------------------------------------------------------------------------------------
@@ -138,14 +134,17 @@ def test_wan_batch4_packed_write_matches_oracle(vm):
 
 @pytest.mark.parametrize("variant", ["wan", "peaked", "paper_dims"])
 def test_wan_attend_full_window(vm, variant):
+    """The wrapped 21-frame window. The measured configuration compares every one of the
+    4,680 x 12 output rows with the oracle; the variants compare sampled rows."""
     dims = WAN_PAPER if variant == "paper_dims" else WAN
     inp = make_layer_inputs(dims, seed=1, n_frames=24, q_gain=4.0 if variant == "peaked" else 1.0)
     layer = Layer(vm, inp)
     _roll(layer, 21)
     got = layer.attend(21)
-    rows = sample_rows(dims.chunk_tokens)
+    rows = np.arange(dims.chunk_tokens) if variant == "wan" else sample_rows(dims.chunk_tokens)
     want = O.chunk_attention(inp, 0, 21, rows=rows)
-    assert_attention_close(got[0][rows], want, f"wan attend {variant}")
+    assert_attention_close(got[0][rows], want, f"wan attend {variant} ({len(rows)} tokens)",
+                           scaled=variant == "peaked")
 
 
 def test_wan_attend_partial_windows_and_work_partitions(vm):
@@ -159,16 +158,27 @@ def test_wan_attend_partial_windows_and_work_partitions(vm):
         layer.write(fe)
     want = O.chunk_attention(inp, 0, 18, rows=rows)  # exactly 21 frames, no wrap yet
     for wg in (0, 1, 37, 300):
-        vm.set_attend_workgroups(wg)
-        got = layer.attend(18)
+        got = layer.attend(18, vm.AttendOpts(n_workgroups=wg))
         assert_attention_close(got[0][rows], want, f"wan fe=18 workgroups={wg}")
-    vm.set_attend_workgroups(0)
 
 
 def test_wan_attend_is_deterministic(vm):
+    """Two calls give bitwise identical outputs in the default (even) partition and in the
+    frozen partition the benchmark measures (weights calibrated by adaptive calls on the same
+    workspace, then frozen); the frozen outputs match the oracle."""
     inp = make_layer_inputs(WAN, seed=7, n_frames=24)
     layer = Layer(vm, inp)
     _roll(layer, 21)
     a = layer.attend(21).copy()
     b = layer.attend(21)
     assert np.array_equal(a, b)
+    ws = torch.empty(vm.attend_workspace_bytes(WAN, 1), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        layer.attend(21, vm.AttendOpts(partition="adaptive"), ws=ws)
+    frozen = vm.AttendOpts(partition="frozen")
+    fa = layer.attend(21, frozen, ws=ws).copy()
+    fb = layer.attend(21, frozen, ws=ws)
+    assert np.array_equal(fa, fb)
+    rows = sample_rows(WAN.chunk_tokens, k=12, seed=7)
+    assert_attention_close(fa[0][rows], O.chunk_attention(inp, 0, 21, rows=rows), "wan frozen")
+    assert_attention_close(fa[0], a[0], "frozen vs even split")

@@ -29,9 +29,7 @@ def vm():
         pytest.skip("no GPU")
     ensure_built()
     import paper_2605_30351_amd as m
-    m.set_attend_workgroups(0)
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402

@@ -30,9 +30,7 @@ def vm():
         pytest.skip("no GPU")
     ensure_built()
     import paper_2605_30351_amd as m
-    m.set_attend_workgroups(0)
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -53,12 +51,10 @@ def test_tiny_sink_rollout(vm):
         exact = sum(e for e, _ in stats) / sum(n for _, n in stats)
         assert exact >= 0.99, exact
         for n_wg in ((0, 1, 3, 64) if fe in (4, 11) else (0,)):
-            vm.set_attend_workgroups(n_wg)
-            got = layer.attend(fe)
+            got = layer.attend(fe, vm.AttendOpts(n_workgroups=n_wg))
             for b in range(inp.batch):
                 want = O.chunk_attention(inp, b, fe)
                 assert_attention_close(got[b], want, f"tiny sink fe={fe} b={b} n_wg={n_wg}")
-        vm.set_attend_workgroups(0)
         fe = vm.window_advance(d, fe)
 
 

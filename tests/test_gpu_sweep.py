@@ -18,7 +18,6 @@ def vm():
     ensure_built()
     import paper_2605_30351_amd as m
     yield m
-    m.set_attend_workgroups(0)
 
 
 from oracle import videomla_oracle as O  # noqa: E402
@@ -44,12 +43,10 @@ def test_small_every_output(vm, d_c):
             for e, n in check_written_chunk(layer, fe, before_c, before_k):
                 exact, total = exact + e, total + n
             for wg in ((1, 3, 0) if fe in (0, 6, 12) else (0,)):
-                vm.set_attend_workgroups(wg)
-                got = layer.attend(fe)
+                got = layer.attend(fe, vm.AttendOpts(n_workgroups=wg))
                 for b in range(2):
                     assert_attention_close(got[b], O.chunk_attention(inp, b, fe),
                                            f"d_c={d_c} packed={packed} fe={fe} b={b} wg={wg}")
-            vm.set_attend_workgroups(0)
         assert exact / total >= 0.999, f"{exact}/{total} exactly rounded"
 
 
