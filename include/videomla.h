@@ -241,6 +241,25 @@ int videomla_attend(const videomla_dims* dims, const videomla_window* win, int32
                     uint16_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * videomla_attend_noalloc -- for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): videomla_attend with the
+ * same arguments minus the workspace, which is a static device array of the library instead,
+ * VIDEOMLA_NOALLOC_SCRATCH_BYTES (64 MiB) on every device it runs on, held until the process
+ * ends. Results are videomla_attend's, bit for bit. The call allocates nothing: on its first
+ * call on a device it looks up that device's copy of the array. Shapes whose workspace
+ * (videomla_attend_workspace_bytes) exceeds the array are rejected with VIDEOMLA_EWORKSPACE
+ * before anything is enqueued (the Wan chunk of 4,680 queries needs about 156 MB: use
+ * videomla_attend there). Every call on a device shares that device's array: calls that
+ * overlap on one device (other streams, other threads) race, so the caller must order them.
+ * Nothing in the array needs to start at zero (each call writes what it reads).
+ */
+#define VIDEOMLA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int videomla_attend_noalloc(const videomla_dims* dims, const videomla_window* win, int32_t batch,
+                            const uint16_t* q_nope, const uint16_t* q_r, const uint16_t* w_uk,
+                            const uint16_t* w_uv, const uint16_t* c_kv, const uint16_t* k_r,
+                            uint16_t* out, void* stream);
+
+/*
  * videomla_attend_ex -- videomla_attend with options (videomla_attend_opts; NULL = the
  * defaults, which make it videomla_attend). With query_begin / query_count, q_nope, q_r and out
  * hold [batch][query_count][n_heads][...] and the queries sit at chunk tokens query_begin ..;

@@ -12,6 +12,7 @@ from ._lib import (  # noqa: F401
     attend,
     attend_layer,
     attend_layer_workspace_bytes,
+    attend_noalloc,
     attend_workspace_bytes,
     cache_bytes_per_token,
     cache_write,
@@ -29,4 +30,4 @@ from ._lib import (  # noqa: F401
     window_advance,
     write_weights_bytes,
 )
-from ._lib import LIB_PATH  # noqa: F401
+from ._lib import LIB_PATH, NOALLOC_SCRATCH_BYTES  # noqa: F401

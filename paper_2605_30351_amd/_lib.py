@@ -25,7 +25,7 @@ OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = 0, 1, 2, 3, 4, 5
 EXPORTED = (
     "videomla_cache_write", "videomla_write_weights_bytes", "videomla_prepare_write_weights",
     "videomla_cache_write_prepared", "videomla_attend_workspace_bytes", "videomla_attend",
-    "videomla_attend_workspace_bytes_ex", "videomla_attend_ex",
+    "videomla_attend_workspace_bytes_ex", "videomla_attend_ex", "videomla_attend_noalloc",
     "videomla_window_advance", "videomla_cache_bytes_per_token", "videomla_valid_tokens",
     "videomla_slot_of", "videomla_last_error",
     "videomla_timer_create", "videomla_timer_destroy", "videomla_timer_only",
@@ -37,6 +37,7 @@ EXPORTED = (
 )
 
 PARTITION = {"even": 0, "adaptive": 1, "frozen": 2}
+NOALLOC_SCRATCH_BYTES = 64 << 20  # VIDEOMLA_NOALLOC_SCRATCH_BYTES
 FORM = {"latent": 0, "materialized": 1, "auto": 2}
 
 
@@ -85,6 +86,8 @@ _lib.videomla_attend_workspace_bytes_ex.restype = ctypes.c_size_t
 _lib.videomla_attend_ex.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P,
                                     ctypes.c_size_t, _OP, _P]
 _lib.videomla_attend_ex.restype = ctypes.c_int
+_lib.videomla_attend_noalloc.argtypes = [_DP, _WP, ctypes.c_int32, _P, _P, _P, _P, _P, _P, _P, _P]
+_lib.videomla_attend_noalloc.restype = ctypes.c_int
 _lib.videomla_window_advance.argtypes = [_DP, _WP]
 _lib.videomla_window_advance.restype = ctypes.c_int
 _lib.videomla_cache_bytes_per_token.argtypes = [_DP]
@@ -355,6 +358,27 @@ def attend(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r,
     else:
         o = opts.struct()
         _check(_lib.videomla_attend_ex(*args, ctypes.byref(o), _stream(stream)))
+
+
+def attend_noalloc(dims, frame_end: int, batch: int, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out,
+                   stream=None):
+    """videomla_attend_noalloc on torch tensors: videomla_attend with the library's static
+    scratch array as its workspace (shapes needing more than NOALLOC_SCRATCH_BYTES raise)."""
+    d = make_dims(dims)
+    hw = d.grid_h * d.grid_w
+    nq = d.chunk_frames * hw
+    _need(q_nope, "q_nope", batch * nq * d.n_heads * d.d_nope)
+    _need(q_r, "q_r", batch * nq * d.n_heads * d.d_rope)
+    _need(w_uk, "w_uk", d.n_heads * d.d_nope * d.d_c)
+    _need(w_uv, "w_uv", d.n_heads * d.d_v * d.d_c)
+    _need(c_kv, "c_kv", batch * d.window_frames * hw * d.d_c)
+    _need(k_r, "k_r", batch * d.window_frames * hw * d.d_rope)
+    _need(out, "out", batch * nq * d.n_heads * d.d_v)
+    w = VideomlaWindow(int(frame_end))
+    _check(_lib.videomla_attend_noalloc(
+        ctypes.byref(d), ctypes.byref(w), int(batch), _ptr(q_nope, "q_nope"), _ptr(q_r, "q_r"),
+        _ptr(w_uk, "w_uk"), _ptr(w_uv, "w_uv"), _ptr(c_kv, "c_kv"), _ptr(k_r, "k_r"),
+        _ptr(out, "out"), _stream(stream)))
 
 
 def dense_cache_bytes_per_token(dims) -> int:

@@ -20,13 +20,17 @@ namespace {
 
 thread_local std::string g_err;
 
-int fail(int code, const char* fmt, ...) {
+void set_error(const char* fmt, va_list ap) {
   char buf[512];
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  g_err = buf;
+}
+
+int fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  set_error(fmt, ap);
   va_end(ap);
-  g_err = buf;
   return code;
 }
 
@@ -34,6 +38,18 @@ int ok() {
   g_err.clear();
   return VIDEOMLA_OK;
 }
+
+}  // namespace
+
+int vmla::report_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  set_error(fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 

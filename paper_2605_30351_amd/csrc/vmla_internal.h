@@ -191,6 +191,10 @@ __host__ __device__ inline int bal_max_seg(int G, int64_t U, int T) {
   return (int)(n < G ? n : G);
 }
 
+// Sets the calling thread's last-error message (videomla_last_error) and returns `code`; for
+// the C-ABI sources other than videomla_api.cpp.
+int report_error(int code, const char* fmt, ...);
+
 // Launchers (one per kernel). Return the launch status.
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s);
 int cache_write_tokens_per_wg(int64_t tokens, int n_cu);

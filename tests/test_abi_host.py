@@ -412,3 +412,20 @@ def test_layer_calls_validate_and_size():
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, wb, None) == L.EINVAL
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, wb - 1, None) == L.EWORKSPACE
     assert prep(ctypes.byref(d), 768, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, MISALIGNED, wb, None) == L.EALIGN
+
+def test_noalloc_rejects_before_launch():
+    """videomla_attend_noalloc: invalid dims are reported as videomla_attend reports them, and a
+    shape whose workspace exceeds the static scratch array (the Wan chunk: about 156 MB) is
+    rejected with EWORKSPACE; both before any device work."""
+    lib = L.raw()
+
+    def call(d, batch=1):
+        w = L.VideomlaWindow(21)
+        return lib.videomla_attend_noalloc(ctypes.byref(d), ctypes.byref(w), batch, FAKE, FAKE,
+                                           FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert vm.attend_workspace_bytes(WAN, 1) > vm.NOALLOC_SCRATCH_BYTES
+    assert call(L.make_dims(WAN)) == L.EWORKSPACE
+    assert "static scratch" in lib.videomla_last_error().decode()
+    assert call(_dims_struct(WAN, d_rope=7)) == L.EINVAL
+    assert call(_dims_struct(WAN, d_c=100)) == L.EUNSUPPORTED
+    assert call(L.make_dims(TINY), batch=0) == L.EINVAL
