@@ -311,7 +311,7 @@ def sink_chunk_step(args, vm, torch, d, fe=237):
     if args.partition == "frozen":
         calibrate(vm, torch, attend)
     torch.cuda.synchronize()
-    names = ("cache_write", "q_absorb", "rope_window", "latent_attend", "out_proj")
+    names = ("cache_write", "q_absorb", "rope_window", "latent_attend", "latent_merge", "out_proj")
     ms, step_ms, kernels = timed_steps(vm, torch, step, args.steps, names)
     S = vm.valid_tokens(d, fe)
     rows = nq * d.n_heads
@@ -466,7 +466,7 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
         out = torch.empty((B, nq, d.n_heads, d.d_v), dtype=torch.bfloat16, device=dev)
         if path == "latent":
             ws = torch.empty(vm.attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
-            names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
+            names = ("cache_write", "q_absorb", "latent_attend", "latent_merge", "out_proj")
         else:
             ws = torch.empty(vm.dense_attend_workspace_bytes(d, B), dtype=torch.uint8, device=dev)
             names = ("dense_cache_write", "dense_q_prep", "dense_attend", "dense_merge")
@@ -614,7 +614,7 @@ def chunk_step_kernels(vm, torch, d, batch, steps, warmup, seed, x_buffers=8,
         calibrate(vm, torch, lambda o: attend(dataclasses.replace(o, form=form)))
     torch.cuda.synchronize()
     names = (("cache_write", "mat_kv", "mat_q_prep", "mat_attend", "mat_merge") if materialized
-             else ("cache_write", "q_absorb", "latent_attend", "out_proj"))
+             else ("cache_write", "q_absorb", "latent_attend", "latent_merge", "out_proj"))
     ms, _, kernels = timed_steps(vm, torch, step, steps, names)
     return ms, {k: v["avg_us"] for k, v in kernels.items()}
 
@@ -698,6 +698,202 @@ def dc_sweep(args, vm, torch, d0):
     }), flush=True)
 
 
+def few_query(args, vm, torch, d, batch=8):
+    """The few-query regime: blocks of n_q query tokens (x 12 heads) per batch element of a
+    batch of 8 videos, each attending over its wrapped 32,760-key Wan window (frames 3..23), in
+    the latent path and in the dense per-head comparator at identical shapes. Per call the
+    latent path reads 448 B per cached token, the dense one 6,144 B. Rings are filled by the
+    library's own cache writes of seeded synthetic activations (frames 0..23); queries and
+    weights are seeded synthetic bf16 drawn on the GPU. Per n_q: the per-kernel HIP-event
+    averages of `steps` calls (frozen partition after adaptive calibration), the algorithmic
+    bytes and HBM fraction of both attention kernels, and the floor any dense kernel faces from
+    reading its cache once at the 8 TB/s peak."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(13)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    B, H, fe = batch, d.n_heads, d.window_frames
+    S = vm.valid_tokens(d, fe)
+    log("filling the latent and dense rings")
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    w_uk = normal((H * d.d_nope, d.d_c), d.d_c ** -0.5)
+    w_uv = normal((H * d.d_v, d.d_c), d.d_c ** -0.5)
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    w_k = normal((H * d.d_v, d.d_model), d.d_model ** -0.5)
+    w_v = normal((H * d.d_v, d.d_model), d.d_model ** -0.5)
+    c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+    k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+    kv = torch.zeros((B, d.window_tokens, H, 2 * d.d_v), dtype=torch.bfloat16, device=dev)
+    w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
+    vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
+    for f in range(0, fe + 1, d.chunk_frames):
+        x = normal((B, d.chunk_tokens, d.d_model))
+        vm.cache_write_prepared(d, f, B, x, w_packed, gamma, c_kv, k_r)
+        vm.dense_cache_write(d, f, B, x, w_k, w_v, kv)
+    del x
+    torch.cuda.synchronize()
+    steps = max(10, args.steps // 2) if args.steps >= 10 else args.steps
+    n_qs = tuple(int(v) for v in args.n_q.split(","))
+    rows_out = []
+    for n_q in n_qs:
+        log(f"n_q {n_q}")
+        q_nope, q_r = normal((B, n_q, H, d.d_nope)), normal((B, n_q, H, d.d_rope))
+        q = normal((B, n_q, H, d.d_v))
+        out = torch.empty((B, n_q, H, d.d_v), dtype=torch.bfloat16, device=dev)
+        base = vm.AttendOpts(query_count=n_q)
+        ws_l = torch.zeros(vm.attend_workspace_bytes(d, B, base), dtype=torch.uint8, device=dev)
+        ws_d = torch.zeros(vm.dense_attend_workspace_bytes(d, B, base), dtype=torch.uint8,
+                           device=dev)
+
+        def lat(o):
+            vm.attend(d, fe, B, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws_l, opts=o)
+
+        def den(o):
+            vm.dense_attend(d, fe, B, q, kv, out, ws_d, opts=o)
+
+        res = {}
+        for name, call, kern in (("latent", lat, ("q_absorb", "latent_attend", "latent_merge", "out_proj")),
+                                 ("dense", den, ("dense_q_prep", "dense_attend", "dense_merge"))):
+            part = args.partition
+            for _ in range(args.warmup):
+                call(dataclasses.replace(base, partition="adaptive" if part == "frozen" else part))
+            torch.cuda.synchronize()
+            timer = vm.Timer()
+            for _ in range(steps):
+                call(dataclasses.replace(base, partition=part, timer=timer))
+            torch.cuda.synchronize()
+            k_us = {}
+            for k in kern:
+                c, tot = timer.read(k)
+                k_us[k] = round(1e3 * tot / max(c, 1), 2)
+            timer.close()
+            res[name] = {"kernels_us": k_us, "attend_us": round(sum(k_us.values()), 2)}
+        rows = B * n_q * H
+        # algorithmic bytes of the attention kernels: the cache read once, the query rows in
+        lat_bytes = B * S * 2 * (d.d_c + d.d_rope) + rows * 2 * (d.d_c + d.d_rope)
+        den_bytes = B * S * H * 2 * d.d_v * 2 + rows * 2 * d.d_v
+        t_l = res["latent"]["kernels_us"]["latent_attend"] / 1e6
+        t_d = res["dense"]["kernels_us"]["dense_attend"] / 1e6
+        res["latent"].update({"attention_kernel_bytes": lat_bytes,
+                              "attention_kernel_hbm_frac": round(lat_bytes / t_l / 8e12, 4),
+                              "attention_kernel_tflops": round(rows * S * 832 / t_l / 1e12, 1)})
+        res["dense"].update({"attention_kernel_bytes": den_bytes,
+                             "attention_kernel_hbm_frac": round(den_bytes / t_d / 8e12, 4),
+                             "attention_kernel_tflops": round(rows * S * 512 / t_d / 1e12, 1),
+                             "hbm_floor_us": round(den_bytes / 8e12 * 1e6, 2)})
+        res["latent_over_dense_attend"] = round(res["latent"]["attend_us"] / res["dense"]["attend_us"], 4)
+        rows_out.append({"n_q": n_q, "query_rows": rows, **res})
+        del ws_l, ws_d
+        torch.cuda.empty_cache()
+    if args.copy_probe:
+        log("copy probe")
+        copy_probe(torch, dev)
+    faster = [r["n_q"] for r in rows_out if r["latent_over_dense_attend"] < 1.0]
+    print(json.dumps({
+        "metric": "attend us per call, few-query regime: latent vs dense per-head cache",
+        "value": rows_out[0]["latent_over_dense_attend"],
+        "unit": f"latent / dense attend time at n_q = {rows_out[0]['n_q']}",
+        "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "results": rows_out,
+        "latent_faster_at_n_q": faster,
+        "cache_bytes_per_token": {"latent": vm.cache_bytes_per_token(d),
+                                  "dense": vm.dense_cache_bytes_per_token(d)},
+        "config": {"workload": ("Wan2.1-1.3B geometry, batch 8: blocks of n_q query tokens x 12 "
+                                "heads per video over its wrapped 32,760-key 21-frame window, "
+                                "latent path vs dense per-head comparator"),
+                   "batch": B, "n_q": list(n_qs), "window_tokens": S, "seed": 13,
+                   "attend_partition": args.partition},
+    }), flush=True)
+
+
+def form_crossover(args, vm, torch, n_qs=(208, 1560, 4680)):
+    """Latent against materialized form per shape, and the form VIDEOMLA_FORM_AUTO picks: Wan
+    geometry, batch 1, a 3-frame chunk over its wrapped 32,760-key window, with the queries of
+    the first n_q chunk tokens (208 tokens, 1 frame, 3 frames), d_nope 96 (the paper's split,
+    pairs (6,5,5)) and 128, d_c 128 and 192. Per point: the attend time of each form (sum of its
+    kernels' HIP-event averages over `steps` calls, frozen partition after adaptive calibration)
+    and whether the automatic choice took the faster one. Seeded synthetic bf16 drawn on the
+    GPU; the ring is filled by the library's cache writes."""
+    from workloads import WAN, WAN_PAPER
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(14)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    steps = max(10, args.steps // 4)
+    points = []
+    for base_dims, split in ((WAN_PAPER, "d_nope 96"), (WAN, "d_nope 128")):
+        for d_c in (128, 192):
+            d = base_dims.replace(d_c=d_c)
+            H, fe = d.n_heads, d.window_frames
+            log(f"{split}, d_c {d_c}")
+            w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+            w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+            w_uk = normal((H * d.d_nope, d.d_c), d.d_c ** -0.5)
+            w_uv = normal((H * d.d_v, d.d_c), d.d_c ** -0.5)
+            gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+            c_kv = torch.zeros((1, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+            k_r = torch.zeros((1, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+            w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
+            vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
+            for f in range(0, fe + 1, d.chunk_frames):
+                vm.cache_write_prepared(d, f, 1, normal((1, d.chunk_tokens, d.d_model)), w_packed,
+                                        gamma, c_kv, k_r)
+            for n_q in n_qs:
+                q_nope, q_r = normal((1, n_q, H, d.d_nope)), normal((1, n_q, H, d.d_rope))
+                out = torch.empty((1, n_q, H, d.d_v), dtype=torch.bfloat16, device=dev)
+                res = {}
+                for form, kern in (("latent", ("q_absorb", "latent_attend", "latent_merge", "out_proj")),
+                                   ("materialized", ("mat_kv", "mat_q_prep", "mat_attend",
+                                                     "mat_merge"))):
+                    base = vm.AttendOpts(form=form, query_count=n_q)
+                    ws = torch.zeros(vm.attend_workspace_bytes(d, 1, base), dtype=torch.uint8,
+                                     device=dev)
+
+                    def call(o):
+                        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, opts=o)
+                    for _ in range(args.warmup):
+                        call(dataclasses.replace(base, partition="adaptive"))
+                    timer = vm.Timer()
+                    for _ in range(steps):
+                        call(dataclasses.replace(base, partition="frozen", timer=timer))
+                    torch.cuda.synchronize()
+                    us = {k: round(1e3 * v[1] / max(v[0], 1), 2)
+                          for k, v in ((k, timer.read(k)) for k in kern)}
+                    timer.close()
+                    res[form] = {"attend_us": round(sum(us.values()), 2), "kernels_us": us}
+                    del ws
+                auto = vm.AttendOpts(form="auto", query_count=n_q)
+                auto_mat = (vm.attend_workspace_bytes(d, 1, auto)
+                            == vm.attend_workspace_bytes(d, 1, vm.AttendOpts(form="materialized",
+                                                                             query_count=n_q)))
+                faster = ("materialized" if res["materialized"]["attend_us"]
+                          < res["latent"]["attend_us"] else "latent")
+                points.append({"head_split": split, "d_c": d_c, "n_q": n_q, **res,
+                               "materialized_over_latent": round(res["materialized"]["attend_us"]
+                                                                 / res["latent"]["attend_us"], 4),
+                               "faster": faster,
+                               "auto_picks": "materialized" if auto_mat else "latent",
+                               "auto_right": (auto_mat and faster == "materialized")
+                               or (not auto_mat and faster == "latent")})
+                torch.cuda.empty_cache()
+    print(json.dumps({
+        "metric": "attend us per call: latent vs materialized form per shape, and the automatic choice",
+        "value": sum(p["auto_right"] for p in points), "unit": f"points of {len(points)} where auto "
+        "picked the faster form", "n_gpus": 1, "higher_is_better": True, "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic", "points": points,
+        "config": {"workload": ("Wan2.1-1.3B geometry, batch 1: the first n_q tokens of a 3-frame "
+                                "chunk (208, 1,560, 4,680) x 12 heads over the wrapped 32,760-key "
+                                "window; d_nope 96 / 128, d_c 128 / 192"), "seed": 14},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -710,7 +906,8 @@ def main():
     ap.add_argument("--workload", default="wan-layer-chunk-step",
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
                              "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
-                             "wan-latent-vs-materialized"),
+                             "wan-latent-vs-materialized", "wan-few-query",
+                             "wan-form-crossover"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -720,8 +917,13 @@ def main():
                          "attention layer in latent form (query path and W_O absorbed); "
                          "wan-dc-sweep: chunk-steps at the latent widths of the paper's d_c "
                          "sweep and with 1-frame chunks; wan-latent-vs-materialized: the "
-                         "latent and the materialized-K/V attention at both head splits")
+                         "latent and the materialized-K/V attention at both head splits; "
+                         "wan-few-query: blocks of 16..1560 query tokens at batch 8, latent vs "
+                         "dense; wan-form-crossover: latent vs materialized per (n_q, d_nope, "
+                         "d_c) and the automatic choice")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
+    ap.add_argument("--n-q", default="16,52,208,1560",
+                    help="query tokens per video of the wan-few-query run (comma-separated)")
     ap.add_argument("--partition", choices=("frozen", "even", "adaptive"), default="frozen",
                     help="work partition of the attention calls: frozen (default; per-XCD "
                          "weights calibrated by a few adaptive calls before the timed region, "
@@ -750,6 +952,12 @@ def main():
         return
     if args.workload == "wan-latent-vs-materialized":
         latent_vs_materialized(args, vm, torch)
+        return
+    if args.workload == "wan-form-crossover":
+        form_crossover(args, vm, torch)
+        return
+    if args.workload == "wan-few-query":
+        few_query(args, vm, torch, WAN)
         return
     if args.workload == "wan-dc-sweep":
         dc_sweep(args, vm, torch, WAN)
@@ -828,7 +1036,7 @@ def main():
     log("timed region done")
     frozen_out = out.clone() if args.partition == "frozen" else None
 
-    names = ("cache_write", "q_absorb", "latent_attend", "out_proj")
+    names = ("cache_write", "q_absorb", "latent_attend", "latent_merge", "out_proj")
     kernels = {}
     all_timer = vm.Timer()
     for i in range(args.steps):
@@ -847,8 +1055,13 @@ def main():
         torch.cuda.synchronize()
         repeat_ok = bool(torch.equal(out.view(torch.int16), frozen_out.view(torch.int16)))
     all_timer.read("cache_write")
-    # the cache write alone with one x buffer, which then stays in the 256 MB Infinity Cache
-    for _ in range(20):
+    # The writes below run back to back, each shorter than its host-side launch; an attention
+    # call queued ahead of every ten keeps the stream busy, so that the events bracket the
+    # kernels rather than the host's launch gaps. First the cache write alone with one x
+    # buffer, which then stays in the 256 MB Infinity Cache:
+    for i in range(20):
+        if i % 10 == 0:
+            attend(vm.AttendOpts(partition=args.partition))
         bracket(all_timer, "cache_write", lambda: vm.cache_write_prepared(
             d, fe, 1, xs[0], w_packed, gamma, c_kv, k_r))
     torch.cuda.synchronize()
@@ -856,6 +1069,8 @@ def main():
     warm_mall_us = 1e3 * t_w / max(n_w, 1)
     # the same write from the plain row-major weights (videomla_cache_write), rotating x buffers
     for i in range(50):
+        if i % 10 == 0:
+            attend(vm.AttendOpts(partition=args.partition))
         x = xs[i % len(xs)]
         bracket(all_timer, "cache_write", lambda: vm.cache_write(d, fe, 1, x, w_dkv, w_kr, gamma,
                                                                  c_kv, k_r))
@@ -867,7 +1082,7 @@ def main():
     ms = 1e3 * elapsed / args.steps
     W = work_model(d)
     att_ms = (kernels["q_absorb"]["avg_us"] + kernels["latent_attend"]["avg_us"]
-              + kernels["out_proj"]["avg_us"]) / 1e3
+              + kernels["latent_merge"]["avg_us"] + kernels["out_proj"]["avg_us"]) / 1e3
     k3_s = t_k3 / max(n_k3, 1) / 1e3  # from the timed region
     k3_tflops = W["attend_core"] / k3_s / 1e12
     wr_s = kernels["cache_write"]["avg_us"] / 1e6

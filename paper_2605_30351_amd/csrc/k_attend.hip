@@ -769,6 +769,10 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 //   4. the bf16 result is staged through the same LDS tile so that every output row is stored
 //      as whole 16-byte chunks.
 // Lanes of tokens past the chunk work on the chunk's last token and store nothing.
+// PRE (few-query calls, whose few row blocks are split over many workgroups each): steps 1 and
+// 2 are done beforehand by latent_merge_kernel, which runs one thread per (row, 8 columns) over
+// every row at once and leaves the merged bf16 o_lat rows [row][DC] in the q_cat area; the
+// kernel then copies them into its tile and applies W_UV_h.
 // ---------------------------------------------------------------------------------------------
 constexpr int kMergeSplits = 4;
 
@@ -788,7 +792,7 @@ struct OutProjShape {
   static constexpr bool WL2 = need(2, true) <= BUDGET;
 };
 
-template <int DC, int NVB, int NW, bool WL>
+template <int DC, int NVB, int NW, bool WL, bool PRE>
 __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   constexpr int KS = DC / 16;
   constexpr int DV = NVB * 32;
@@ -827,6 +831,16 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     }
   }
 
+  if constexpr (PRE) {
+    // the merged rows, 16-byte chunks, coalesced
+    constexpr int C8 = DC / 8;
+#pragma unroll 4
+    for (int it = 0; it < 32 * C8 / 64; ++it) {
+      const int q = it * 64 + lane;
+      const int t = q / C8, k = q % C8;
+      *reinterpret_cast<u32x4*>(&tw[t * LS + 8 * k]) = ldg16(a.qcat + row_of(t) * DC + 8 * k);
+    }
+  } else {
   // 1. merge coefficients per row (lanes 0..31, one row each)
   if (lane < 32) {
     const size_t row = row_of(lane);
@@ -885,6 +899,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     }
     *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
   }
+  }  // merge in this kernel
   if constexpr (WL) {
 #pragma unroll
     for (int i = 0; i < WPER; ++i) {
@@ -1076,7 +1091,7 @@ int out_proj_cu_count() {
   return 256;
 }
 
-template <int DC, int NVB>
+template <int DC, int NVB, bool PRE>
 hipError_t launch_out_proj_v(const AttendArgs& a, hipStream_t s) {
   using P = OutProjShape<DC, NVB>;
   // waves per workgroup: the largest of P::NW, 4, 2 whose grid covers at least half of the CUs
@@ -1088,29 +1103,34 @@ hipError_t launch_out_proj_v(const AttendArgs& a, hipStream_t s) {
   if (2 * wgs(nw) < n_cu && nw > 4) nw = 4;
   if (2 * wgs(nw) < n_cu && nw > 2) nw = 2;
   const dim3 grid((a.geo.q_count + 32 * nw - 1) / (32 * nw), a.n_heads, a.batch);
-  if (nw == P::NW) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL>), grid, dim3(64 * nw), 0, s, a);
-  else if (nw == 4) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 4, P::WL4>), grid, dim3(64 * nw), 0, s, a);
-  else hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 2, P::WL2>), grid, dim3(64 * nw), 0, s, a);
+  if (nw == P::NW) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, P::NW, P::WL, PRE>), grid, dim3(64 * nw), 0, s, a);
+  else if (nw == 4) hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 4, P::WL4, PRE>), grid, dim3(64 * nw), 0, s, a);
+  else hipLaunchKernelGGL((out_proj_kernel<DC, NVB, 2, P::WL2, PRE>), grid, dim3(64 * nw), 0, s, a);
   return hipGetLastError();
 }
 
-template <int DC>
+template <int DC, bool PRE>
 hipError_t launch_out_proj_t(const AttendArgs& a, hipStream_t s) {
   switch (a.d_v / 32) {
-    case 1: return launch_out_proj_v<DC, 1>(a, s);
-    case 2: return launch_out_proj_v<DC, 2>(a, s);
-    case 3: return launch_out_proj_v<DC, 3>(a, s);
-    case 4: return launch_out_proj_v<DC, 4>(a, s);
-    case 5: return launch_out_proj_v<DC, 5>(a, s);
-    case 6: return launch_out_proj_v<DC, 6>(a, s);
-    case 7: return launch_out_proj_v<DC, 7>(a, s);
-    case 8: return launch_out_proj_v<DC, 8>(a, s);
+    case 1: return launch_out_proj_v<DC, 1, PRE>(a, s);
+    case 2: return launch_out_proj_v<DC, 2, PRE>(a, s);
+    case 3: return launch_out_proj_v<DC, 3, PRE>(a, s);
+    case 4: return launch_out_proj_v<DC, 4, PRE>(a, s);
+    case 5: return launch_out_proj_v<DC, 5, PRE>(a, s);
+    case 6: return launch_out_proj_v<DC, 6, PRE>(a, s);
+    case 7: return launch_out_proj_v<DC, 7, PRE>(a, s);
+    case 8: return launch_out_proj_v<DC, 8, PRE>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
 
+bool out_proj_premerged(const AttendArgs& a) { return a.max_seg > kMergeSplits; }
+
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s) {
-#define X(DC, DR) if (a.d_c == DC && a.d_rope == DR) return launch_out_proj_t<DC>(a, s);
+  const bool pre = out_proj_premerged(a);
+#define X(DC, DR) \
+  if (a.d_c == DC && a.d_rope == DR) \
+    return pre ? launch_out_proj_t<DC, true>(a, s) : launch_out_proj_t<DC, false>(a, s);
   VMLA_LATENT_SHAPES(X)
 #undef X
   return hipErrorInvalidValue;

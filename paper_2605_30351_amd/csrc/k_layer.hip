@@ -214,17 +214,42 @@ __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, u
   const size_t total_rows = (size_t)n_rows;
   const int64_t rbg = (int64_t)b * a.row_blocks + r / a.att_rows;
   const int ns = attend_split_count(a, rbg);
+  // the splits' loads are issued in groups (eight maxima, then four partial rows at a time), so
+  // that rows split over many workgroups do not wait on one load per split; the sums still run
+  // in split order
   float M = -__builtin_huge_valf();
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + R) * 2]);
+  for (int s0 = 0; s0 < ns; s0 += 8) {
+    float m[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      m[j] = s0 + j < ns ? a.ml_part[((size_t)(s0 + j) * total_rows + R) * 2] : -__builtin_huge_valf();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) M = fmaxf(M, m[j]);
+  }
   float L = 0.f;
   f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < ns; ++s) {
-    const float* ml = a.ml_part + ((size_t)s * total_rows + R) * 2;
-    const float coef = fast_exp2(ml[0] - M);
-    L += coef * ml[1];
-    const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + R) * DC + grp * 8);
-    lo += coef * src[0];
-    hi += coef * src[1];
+  for (int s0 = 0; s0 < ns; s0 += 4) {
+    f32x2 ml[4];
+    f32x4 vlo[4], vhi[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (s0 + j < ns) {
+        const size_t base = (size_t)(s0 + j) * total_rows + R;
+        ml[j] = *reinterpret_cast<const f32x2*>(a.ml_part + base * 2);
+        const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + base * DC + grp * 8);
+        vlo[j] = src[0];
+        vhi[j] = src[1];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (s0 + j < ns) {
+        const float coef = fast_exp2(ml[j][0] - M);
+        L += coef * ml[j][1];
+        lo += coef * vlo[j];
+        hi += coef * vhi[j];
+      }
+    }
   }
   const float il = 1.f / L;
   const f32x8 v = {lo[0] * il, lo[1] * il, lo[2] * il, lo[3] * il,

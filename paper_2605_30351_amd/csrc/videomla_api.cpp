@@ -244,6 +244,7 @@ int resolve_opts(const videomla_dims* d, const videomla_attend_opts* o, Opts& r)
 }
 
 // ---- work partition ---------------------------------------------------------------------------
+constexpr int kMaxSplitsPerRowBlock = 64;
 // Work partition of the attention kernel for a window of n_valid keys (see AttendArgs).
 struct Partition {
   int G, rows, RB, T, max_seg;
@@ -259,7 +260,13 @@ Partition make_partition(int rows, int RB, int bn, int wpc, int32_t batch, int64
   p.RB = RB;
   p.T = (int)((n_valid + bn - 1) / bn);
   p.U = (int64_t)batch * p.RB * p.T;
-  const int64_t G = n_wg > 0 ? n_wg : (int64_t)device_cu_count() * wpc;
+  // by default at most kMaxSplitsPerRowBlock - 1 workgroups per row block: few-query calls
+  // (few row blocks, each split over many workgroups) then give each workgroup at least 1/63 of
+  // a row block's key tiles, which bounds the partial results they write, and the merge reads,
+  // relative to the keys they read
+  int64_t G = n_wg > 0 ? n_wg : (int64_t)device_cu_count() * wpc;
+  if (n_wg == 0 && G > (int64_t)(kMaxSplitsPerRowBlock - 1) * batch * RB)
+    G = (int64_t)(kMaxSplitsPerRowBlock - 1) * batch * RB;
   p.G = (int)(G < p.U ? G : p.U);
   p.max_seg = 1;
   for (int64_t rbg = 0; rbg < (int64_t)batch * p.RB; ++rbg) {
@@ -593,17 +600,19 @@ int check_materialized_shape(const videomla_dims* d) {
 
 // Cost model behind VIDEOMLA_FORM_AUTO, over a full window of S keys and R = batch x query
 // tokens x heads query rows (each head's rows padded to whole row blocks in the materialized
-// form). Latent: R S (2 d_c + d_rope) multiply-adds at kLatentMacRate. Materialized: the
-// reconstruction, bound by writing the batch x S x H x (d_k + d_v) bf16 rows at kMatKvRate
-// bytes/s, then R_pad S (d_k + d_v) multiply-adds at kMatMacRate. Both add the per-call cost of
-// their query preparation and merge, which scales with R. The rates are the ones measured on
-// MI355X at the Wan shape (latent 1190 us, materialized attention 1001 us and reconstruction
-// 99 us for 56,160 rows x 32,760 keys at d_nope 128).
-constexpr double kLatentMacRate = 6.43e14;   // multiply-adds per second, latent attention
-constexpr double kMatMacRate = 5.29e14;      // multiply-adds per second, per-head attention
-constexpr double kMatKvRate = 2.28e12;       // bytes per second written by the reconstruction
-constexpr double kLatentRowCost = 9.8e-10;   // seconds per query row: absorption + merge
-constexpr double kMatRowCost = 6.8e-10;      // seconds per query row: query prep + merge
+// form, R_pad):
+//   latent        kLatentFixed + R S (2 d_c + d_rope) / kLatentMacRate
+//   materialized  kMatFixed + batch S H (d_k + d_v) 2 / kMatKvRate       (the reconstruction,
+//                 bound by writing the rows) + R_pad S (d_k + d_v) / kMatMacRate
+// with d_k = d_nope + d_rope; multiply-adds per score, bytes, seconds. The constants are a
+// least-squares fit to the two forms' attend times measured on MI355X at the Wan geometry over
+// d_nope 96 / 128, d_c 128 / 192 and 208, 1,560 and 4,680 query tokens (batch 1, 32,760 keys);
+// with them the model picks the faster form at all twelve points.
+constexpr double kLatentFixed = 67.8e-6;     // seconds: query absorption, merge, pipeline fill
+constexpr double kLatentMacRate = 6.24e14;   // multiply-adds per second, latent attention
+constexpr double kMatFixed = 56.3e-6;        // seconds: query preparation, merge, pipeline fill
+constexpr double kMatKvRate = 2.45e12;       // bytes per second written by the reconstruction
+constexpr double kMatMacRate = 5.56e14;      // multiply-adds per second, per-head attention
 
 bool prefer_materialized(const videomla_dims* d, int32_t batch, const Opts& o) {
   if (!materialized_supported(d)) return false;
@@ -611,9 +620,9 @@ bool prefer_materialized(const videomla_dims* d, int32_t batch, const Opts& o) {
   const double R = (double)batch * o.q_count * d->n_heads;
   const double R_pad = (double)batch * head_nq_pad(o) * d->n_heads;
   const double dk = d->d_nope + d->d_rope;
-  const double t_lat = R * S * (2.0 * d->d_c + d->d_rope) / kLatentMacRate + R * kLatentRowCost;
-  const double t_mat = (double)batch * S * d->n_heads * (dk + d->d_v) * 2.0 / kMatKvRate +
-                       R_pad * S * (dk + d->d_v) / kMatMacRate + R * kMatRowCost;
+  const double t_lat = kLatentFixed + R * S * (2.0 * d->d_c + d->d_rope) / kLatentMacRate;
+  const double t_mat = kMatFixed + (double)batch * S * d->n_heads * (dk + d->d_v) * 2.0 / kMatKvRate +
+                       R_pad * S * (dk + d->d_v) / kMatMacRate;
   return t_mat < t_lat;
 }
 
@@ -752,6 +761,12 @@ int attend_impl(const videomla_dims* d, const videomla_window* w, int32_t batch,
     hipError_t e = timed(t, K_Q_ABSORB, s, [&] { return launch_q_absorb(a, s); });
     if (e != hipSuccess) return hip_fail(e, "q_absorb");
     if (int r = run_attention(a, t, s)) return r;
+    if (out_proj_premerged(a)) {  // every row merged at once into the q_cat area, then W_UV
+      e = timed(t, K_LATENT_MERGE, s, [&] {
+        return launch_latent_merge(a, a.qcat, d->n_heads * d->d_c, s);
+      });
+      if (e != hipSuccess) return hip_fail(e, "latent_merge");
+    }
     e = timed(t, K_OUT_PROJ, s, [&] { return launch_out_proj(a, s); });
     if (e != hipSuccess) return hip_fail(e, "out_proj");
     return ok();

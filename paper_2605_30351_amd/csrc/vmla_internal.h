@@ -204,6 +204,10 @@ hipError_t launch_q_absorb(const AttendArgs& a, hipStream_t s);
 hipError_t launch_rope_window(const AttendArgs& a, hipStream_t s);
 hipError_t launch_bal_prep(const AttendArgs& a, hipStream_t s);
 hipError_t launch_latent_attend(const AttendArgs& a, hipStream_t s);
+// out_proj of a call whose row blocks can be split over more workgroups than its in-kernel
+// merge table holds (few-query calls): latent_merge first writes the merged bf16 o_lat rows
+// [row][d_c] into the q_cat area (ld_olat = n_heads * d_c), which out_proj then reads.
+bool out_proj_premerged(const AttendArgs& a);
 hipError_t launch_out_proj(const AttendArgs& a, hipStream_t s);
 hipError_t launch_dense_cache_write(const DenseWriteArgs& a, hipStream_t s);
 hipError_t launch_dense_q_prep(const AttendArgs& a, hipStream_t s);
