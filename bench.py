@@ -548,6 +548,19 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
     la, da = lat["kernels_last_chunk"], den["kernels_last_chunk"]
     lat_call = sum(v["avg_us"] for v in la.values())
     den_call = sum(v["avg_us"] for v in da.values())
+    # the attention kernels at the full window: their MFMA fractions, and the latent/dense time
+    # ratio they would have at equal MFMA efficiency (the ratio of their algorithmic FLOPs)
+    S_full = d.window_tokens
+    rows_full = B * nq * d.n_heads
+    lat_att_flop = rows_full * S_full * (2 * (d.d_c + d.d_rope) + 2 * d.d_c)
+    den_att_flop = rows_full * S_full * 4 * d.d_v
+    eff = {"latent_attend_mfma_frac": round(lat_att_flop / (la["latent_attend"]["avg_us"] / 1e6)
+                                            / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+           "dense_attend_mfma_frac": round(den_att_flop / (da["dense_attend"]["avg_us"] / 1e6)
+                                           / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+           "attention_time_ratio_at_equal_mfma_efficiency": round(lat_att_flop / den_att_flop, 4),
+           "attention_time_ratio_measured": round(la["latent_attend"]["avg_us"]
+                                                  / da["dense_attend"]["avg_us"], 4)}
     print(json.dumps({
         "metric": "ms per chunk: 30 layers x 4 denoising steps, latent vs dense per-head cache",
         "value": lat["ms_per_chunk"], "unit": "ms", "n_gpus": 1, "steps": n_chunks, "warmup": 1,
@@ -555,6 +568,7 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
         "latent": lat, "dense": den,
         "latent_over_dense_time": round(lat["seconds"] / den["seconds"], 3),
         "latent_over_dense_time_per_call_full_window": round(lat_call / den_call, 3),
+        "attention_kernels_full_window": eff,
         "cache_bytes": {"latent": lat_bytes, "dense": den_bytes,
                         "dense_over_latent": round(den_bytes / lat_bytes, 3)},
         "config": {"workload": (f"Wan2.1-1.3B rollout, batch 4: {n_chunks} chunks of 3 frames "
@@ -894,6 +908,63 @@ def form_crossover(args, vm, torch, n_qs=(208, 1560, 4680)):
     }), flush=True)
 
 
+def xcd_balance(args, vm, torch, d, n_calls=12):
+    """The per-XCD imbalance the weighted partition corrects, read from the library's own
+    record: the partition state at the end of the attention workspace holds the weights a call
+    used and each workgroup's duration (100 MHz ticks). The first adaptive call on a fresh
+    workspace splits evenly (no record yet), so its durations are the even split's; each later
+    adaptive call re-weights the XCDs from the previous one's. Wan chunk-step shape, batch 1,
+    wrapped window; latent_attend timed by HIP events."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(15)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq, H = d.chunk_tokens, d.n_heads
+    c_kv, k_r = normal((1, d.window_tokens, d.d_c)), normal((1, d.window_tokens, d.d_rope))
+    q_nope, q_r = normal((1, nq, H, d.d_nope)), normal((1, nq, H, d.d_rope))
+    w_uk = normal((H * d.d_nope, d.d_c), d.d_c ** -0.5)
+    w_uv = normal((H * d.d_v, d.d_c), d.d_c ** -0.5)
+    out = torch.empty((1, nq, H, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.zeros(vm.attend_workspace_bytes(d, 1), dtype=torch.uint8, device=dev)
+    state_words, state_bytes = 16 + 4096, ((16 + 4096) * 4 + 255) // 256 * 256
+    fe = d.window_frames
+    for _ in range(args.warmup):  # clock ramp, on another workspace
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out,
+                  torch.empty_like(ws))
+    torch.cuda.synchronize()
+    timer = vm.Timer()
+    rows = []
+    for call in range(n_calls):
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws,
+                  opts=vm.AttendOpts(partition="adaptive", timer=timer))
+        torch.cuda.synchronize()
+        _, t_ms = timer.read("latent_attend")
+        st = ws[-state_bytes:][:state_words * 4].cpu().numpy().view(np.uint32)
+        G = int(st[8])
+        dur = st[16:16 + G].astype(np.float64) / 100.0  # us
+        per_xcd = [float(dur[x::8].max()) for x in range(8)]
+        spread = [float(dur[x::8].max() - dur[x::8].min()) for x in range(8)]
+        rows.append({"call": call, "weights": [int(v) for v in st[:8]],
+                     "xcd_slowest_workgroup_us": [round(v, 1) for v in per_xcd],
+                     "slowest_over_fastest_xcd": round(max(per_xcd) / min(per_xcd), 4),
+                     "within_xcd_spread_us_max": round(max(spread), 1),
+                     "latent_attend_us": round(1e3 * t_ms, 1)})
+    timer.close()
+    print(json.dumps({
+        "metric": "per-XCD workgroup times of latent_attend under the even and the weighted split",
+        "value": rows[0]["slowest_over_fastest_xcd"], "unit": "slowest / fastest XCD, even split",
+        "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "calls": rows,
+        "config": {"workload": ("Wan2.1-1.3B layer attend (4,680 x 12 query rows over 32,760 keys), "
+                                "batch 1; call 0 splits evenly (no record), later calls re-weight"),
+                   "seed": 15},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -907,7 +978,7 @@ def main():
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
                              "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
                              "wan-latent-vs-materialized", "wan-few-query",
-                             "wan-form-crossover"),
+                             "wan-form-crossover", "wan-xcd-balance"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -920,7 +991,8 @@ def main():
                          "latent and the materialized-K/V attention at both head splits; "
                          "wan-few-query: blocks of 16..1560 query tokens at batch 8, latent vs "
                          "dense; wan-form-crossover: latent vs materialized per (n_q, d_nope, "
-                         "d_c) and the automatic choice")
+                         "d_c) and the automatic choice; wan-xcd-balance: per-XCD workgroup "
+                         "times from the partition's own record")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     ap.add_argument("--n-q", default="16,52,208,1560",
                     help="query tokens per video of the wan-few-query run (comma-separated)")
@@ -952,6 +1024,9 @@ def main():
         return
     if args.workload == "wan-latent-vs-materialized":
         latent_vs_materialized(args, vm, torch)
+        return
+    if args.workload == "wan-xcd-balance":
+        xcd_balance(args, vm, torch, WAN)
         return
     if args.workload == "wan-form-crossover":
         form_crossover(args, vm, torch)

@@ -258,6 +258,219 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   }
 }
 
+// cache_write_wide_kernel (packed weights, more than 32 tokens per compute unit: batched calls).
+// One workgroup per compute unit takes up to 16 TB tokens and all outputs, so that the weight
+// panel, which every token needs whole, is streamed once per compute unit rather than once per
+// 32 tokens. x no longer fits in LDS whole: it passes through a ring of three buffers of one
+// phase each (KPRE / 2 k-steps of columns, in contraction order), filled by a loader wave (the
+// last wave) that issues only these loads, so that it counts them exactly (a phase is a
+// compile-time number of loads) while the compute waves' weight loads stay in flight. Two
+// phases are in flight while a third is contracted, and one barrier per phase hands a buffer
+// from the compute waves to the loader and back. The compute waves are those of
+// cache_write_packed_kernel (one per 32 outputs, the same packed panel, the same MFMA), each with
+// TB token blocks of accumulators. The loader also computes the tokens' ring rows and RoPE
+// angles, and every wave takes part in the stores. LDS (dynamic, cache_write_wide_lds_bytes):
+// three x buffers [KPRE / 4 column blocks][16 TB rows][64], swizzled like the packed kernel's x
+// tile (the output tile reuses them), then the per-wave sums of squares [waves - 1][16 TB], the
+// ring rows [16 TB] and (cos, sin) [16 TB][d_rope / 2].
+constexpr int kWideBufs = 3;
+
+template <int KPRE, int TB>
+__global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a) {
+  constexpr int OB = 2, OPW = 16 * OB;
+  constexpr int ROWS = 16 * TB;            // token rows of the x buffers (>= the block's tokens)
+  constexpr int PK = KPRE / 2;             // k-steps per phase
+  constexpr int PB = PK / 2;               // column blocks of 64 per phase
+  constexpr int XB = PB * ROWS * 64;       // elements per x buffer
+  constexpr int LPP = PB * ROWS / 8;       // loads per phase (1 KB each, all from the loader)
+  static_assert(PK % 2 == 0 && 2 * LPP < 64, "two phases of loads within the vmcnt range");
+  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+  const int nwave = blockDim.x >> 6, ncw = nwave - 1;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool loader = wave == ncw;
+  const int r = lane & 15, q = lane >> 4;
+  const int dm = a.d_model, DC = a.d_c, DR = a.d_rope, NO = DC + DR;
+  const int n_tok = a.geo.chunk_tokens;
+  const int64_t M = (int64_t)a.batch * n_tok;
+  const int64_t g0 = (int64_t)blockIdx.x * a.tok_per_wg;
+  const int ntok = (int)(M - g0 < a.tok_per_wg ? M - g0 : a.tok_per_wg);  // 1 .. ROWS
+  const int nks = dm / 32, nblk = dm / 64;
+  const int nph = nks / PK;                // phases (KPRE divides nks)
+  const int npair = DR / 2;
+  uint16_t* xbuf = smem;
+  float* ssq_part = reinterpret_cast<float*>(smem + kWideBufs * XB);
+  int64_t* tok_slot = reinterpret_cast<int64_t*>(ssq_part + ncw * ROWS);
+  f32x2* rope_cs = reinterpret_cast<f32x2*>(tok_slot + ROWS);
+
+  // contraction order: k-step i is column k-step (i + rot) mod nks, rot a whole column block
+  const int rotb = (int)((blockIdx.x >> 3) % (unsigned)nblk);
+  const int rot = 2 * rotb;
+  auto kstep = [&](int i) { const int k = i + rot; return k < nks ? k : k - nks; };
+
+  if (loader) {
+    // phase p's columns into buffer p mod 3; rows past the block's tokens repeat its last token
+    auto issue_x = [&](int p) {
+      uint16_t* buf = xbuf + (p % kWideBufs) * XB;
+#pragma unroll
+      for (int j = 0; j < PB; ++j) {
+        int b = rotb + p * PB + j;
+        if (b >= nblk) b -= nblk;
+#pragma unroll
+        for (int rg = 0; rg < ROWS / 8; ++rg) {
+          const int t = rg * 8 + (lane >> 3), cs = lane & 7;
+          const int cc = cs ^ ((t >> 1) & 7);
+          const int tt = t < ntok ? t : ntok - 1;
+          lds_dma16(a.x + (size_t)(g0 + tt) * dm + b * 64 + cc * 8,
+                    __builtin_amdgcn_readfirstlane(lds_addr(buf + (j * ROWS + rg * 8) * 64)));
+        }
+      }
+    };
+    issue_x(0);
+    if (nph > 1) issue_x(1);
+    for (int p = 0; p < nph; ++p) {
+      // phase p has landed once at most the next phase's loads are outstanding (vector memory
+      // operations, the ring-row stores below included, complete in issue order)
+      if (p + 1 < nph) wait_vmcnt<LPP>();
+      else wait_vmcnt<0>();
+      if (p == 0) {
+        // each token's ring row (and slot), and its RoPE (cos, sin), while phase 1 lands
+        for (int t = lane; t < ntok; t += 64) {
+          const int g = (int)g0 + t;  // batch * chunk_tokens < 2^31 (validated on the host)
+          const int b = g / n_tok, n = g - b * n_tok;
+          const TokenPos pos = token_pos(a.geo, n);
+          const int64_t slot = ring_slot(a.geo, pos);
+          tok_slot[t] = (int64_t)b * a.geo.ring_tokens + slot;
+          if (b == 0 && a.slots) a.slots[n] = (int32_t)slot;
+          for (int pr = 0; pr < npair; ++pr) {
+            float u = 1.f, w = 0.f;  // rotating (1, 0) gives (cos, sin); identity with a sink
+            if (a.geo.sink_frames == 0) rope_rotate(a.rope, pr, pos, u, w);
+            rope_cs[t * npair + pr] = f32x2{u, w};
+          }
+        }
+      }
+      __syncthreads();  // phase p visible; the compute waves are done with phase p - 1
+      if (p + 2 < nph) issue_x(p + 2);  // into the buffer phase p - 1 left
+    }
+    __syncthreads();  // the compute waves' sums of squares are in LDS
+    __syncthreads();  // the output tile is complete
+  } else {
+    // RMSNorm gain of this lane's outputs OPW wave + 16 ob + 4q .. +3
+    u32x2 gam[OB];
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob) {
+      const int o = OPW * wave + 16 * ob + 4 * q;
+      gam[ob] = u32x2{0u, 0u};
+      if (a.gamma && o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
+    }
+    // this wave's packed panel slice (as in cache_write_packed_kernel), KPRE k-steps ahead
+    const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * OB) * 512 + lane * 8;
+    u32x4 wb[KPRE][OB];
+#pragma unroll
+    for (int j = 0; j < KPRE; ++j) {
+      const int k = kstep(j);
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob) wb[j][ob] = ldg16(wpan + (OB * k + ob) * 512);
+    }
+    f32x4 acc[OB][TB];
+#pragma unroll
+    for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) acc[ob][tb] = f32x4{};
+    // k-step jj of the phase in buffer `buf`: column block jj / 2, chunks 4 (jj & 1) + q
+    auto mma_step = [&](const uint16_t* buf, int jj, const u32x4 (&w)[OB]) {
+      const int j = jj >> 1, cc = 4 * (jj & 1) + q;
+      bf16x8 xb[TB];
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        const int t = 16 * tb + r;
+        xb[tb] = as_bf16x8(*reinterpret_cast<const u32x4*>(&buf[xpos(j, t, cc, ROWS) * 8]));
+      }
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) acc[ob][tb] = mfma16(as_bf16x8(w[ob]), xb[tb], acc[ob][tb]);
+    };
+    for (int i0 = 0; i0 < nks; i0 += KPRE) {  // two phases per pass over the weight ring
+      const bool refill = i0 + KPRE < nks;
+#pragma unroll
+      for (int j = 0; j < KPRE; ++j) {
+        const int ph = (i0 + j) / PK;
+        if (j % PK == 0) __syncthreads();  // phase ph is in its buffer
+        mma_step(xbuf + (ph % kWideBufs) * XB, j % PK, wb[j]);
+        if (refill) {
+          const int kn = kstep(i0 + j + KPRE);
+#pragma unroll
+          for (int ob = 0; ob < OB; ++ob) wb[j][ob] = ldg16(wpan + (OB * kn + ob) * 512);
+        }
+      }
+    }
+    // sums of squares of the latent outputs per token
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      float ss = 0.f;
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int o = OPW * wave + 16 * ob + 4 * q + e;
+          if (o < DC) ss += acc[ob][tb][e] * acc[ob][tb][e];
+        }
+      ss += __shfl_xor(ss, 16);
+      ss += __shfl_xor(ss, 32);
+      if (q == 0) ssq_part[wave * ROWS + 16 * tb + r] = ss;
+    }
+    __syncthreads();  // every wave is past its last x read: the output tile reuses the buffers
+    // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
+    const int ots = NO + 8;
+    uint16_t* ot = xbuf;
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      const int t = 16 * tb + r;
+      const int tc = t < ntok ? t : ntok - 1;
+      float tot = 0.f;
+      for (int w = 0; w < ncw; ++w) tot += ssq_part[w * ROWS + t];
+      const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
+#pragma unroll
+      for (int ob = 0; ob < OB; ++ob) {
+        const int o = OPW * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
+        f32x4 v = acc[ob][tb];
+        if (o + 4 <= DC) {
+          v = v * rstd;
+          if (a.gamma) {
+            v[0] *= __uint_as_float(gam[ob][0] << 16);
+            v[1] *= __uint_as_float(gam[ob][0] & 0xffff0000u);
+            v[2] *= __uint_as_float(gam[ob][1] << 16);
+            v[3] *= __uint_as_float(gam[ob][1] & 0xffff0000u);
+          }
+        } else if (o < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
+          const f32x2 c0 = rope_cs[tc * npair + (o - DC) / 2];
+          const f32x2 c1 = rope_cs[tc * npair + (o - DC) / 2 + 1];
+          v = f32x4{v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
+                    v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
+        } else {
+          continue;  // padding outputs past d_c + d_rope
+        }
+        *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(v);
+      }
+    }
+    __syncthreads();  // the output tile is complete
+  }
+
+  // stores: token t's row of NO/8 chunks (c_kv, then k_r) to its ring slot, coalesced
+  const int ots = NO + 8;
+  const uint16_t* ot = xbuf;
+  const int cpt = NO / 8;
+  for (int i = threadIdx.x; i < ntok * cpt; i += nwave * 64) {
+    const int t = i / cpt, ch = i - t * cpt;
+    const int64_t row = tok_slot[t];
+    const u32x4 val = *reinterpret_cast<const u32x4*>(&ot[t * ots + ch * 8]);
+    const int o = ch * 8;
+    if (o < DC) stg16(a.c_kv + (size_t)row * DC + o, val);
+    else stg16(a.k_r + (size_t)row * DR + (o - DC), val);
+  }
+}
+
 // Packed weight panel for cache_write_packed_kernel: W' = [W_DKV; W_KR; zero rows up to a whole
 // number of wave slices of 16 OB rows]. Entry ((w * nks + k) * OB + ob) * 512 + 8 l + j holds
 // W'[16 OB w + 16 ob + l % 16][32 k + 8 (l / 16) + j]: the MFMA 16x16x32 A operand of lane l for
@@ -456,6 +669,51 @@ int cache_write_tokens_per_wg(int64_t tokens, int n_cu) {
   return (int)(per < 1 ? 1 : (per > kTokTile ? kTokTile : per));
 }
 
+namespace {
+constexpr int kWideMaxTokens = 80;  // 5 token blocks of 16 per workgroup
+
+// The wide kernel's KPRE for these dims, or 0 when it does not apply: packed weights with 32
+// outputs per wave and at most 7 compute waves (d_c + d_rope <= 224), d_model a multiple of
+// 384 or 256, and more than 32 tokens per compute unit.
+int wide_kpre(const WriteArgs& a, int n_cu) {
+  const int no = a.d_c + a.d_rope, nks = a.d_model / 32;
+  if (!a.w_packed || write_blocks_per_wave(no) != 2 || (no + 31) / 32 > 7) return 0;
+  if ((int64_t)a.batch * a.geo.chunk_tokens <= (int64_t)kTokTile * n_cu) return 0;
+  return nks % 12 == 0 ? 12 : nks % 8 == 0 ? 8 : 0;
+}
+
+size_t cache_write_wide_lds_bytes(int kpre, int tb, int ncw, int npair) {
+  const size_t rows = 16 * (size_t)tb;
+  return kWideBufs * (size_t)(kpre / 4) * rows * 64 * 2 + ncw * rows * 4 + rows * 8 +
+         rows * npair * 8;
+}
+
+template <int KPRE>
+hipError_t launch_wide(const WriteArgs& a, int n_cu, hipStream_t s) {
+  WriteArgs b = a;
+  const int64_t M = (int64_t)a.batch * a.geo.chunk_tokens;
+  const int64_t per = (M + n_cu - 1) / n_cu;
+  b.tok_per_wg = (int)(per > kWideMaxTokens ? kWideMaxTokens : per);
+  const int tb = (b.tok_per_wg + 15) / 16;
+  const int ncw = (a.d_c + a.d_rope + 31) / 32;
+  const size_t lds = cache_write_wide_lds_bytes(KPRE, tb, ncw, a.d_rope / 2);
+  const dim3 grid((unsigned)((M + b.tok_per_wg - 1) / b.tok_per_wg)), block((ncw + 1) * 64);
+  auto go = [&](auto kernel) {
+    // dynamic LDS beyond the default limit (up to 136 KB at the Wan shape)
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, b);
+    return hipGetLastError();
+  };
+  switch (tb) {
+    case 3: return go(cache_write_wide_kernel<KPRE, 3>);
+    case 4: return go(cache_write_wide_kernel<KPRE, 4>);
+    default: return go(cache_write_wide_kernel<KPRE, 5>);
+  }
+}
+}  // namespace
+
 size_t write_weights_packed_elems(int d_model, int d_c, int d_rope) {
   const int ob = write_blocks_per_wave(d_c + d_rope), opw = 16 * ob;
   return (size_t)((d_c + d_rope + opw - 1) / opw) * (d_model / 32) * ob * 512;
@@ -470,6 +728,9 @@ hipError_t launch_pack_write_weights(const WriteArgs& a, hipStream_t s) {
 
 hipError_t launch_cache_write(const WriteArgs& a, hipStream_t s) {
   if (!a.w_packed) return launch_cache_write_staged(a, s);
+  if (const int kpre = wide_kpre(a, a.n_cu)) {  // batched calls: the panel once per compute unit
+    return kpre == 12 ? launch_wide<12>(a, a.n_cu, s) : launch_wide<8>(a, a.n_cu, s);
+  }
   // validated by the caller: d_model % 64 == 0, d_model <= kMaxWriteDModel, d_c % 16 == 0,
   // d_rope % 8 == 0, d_c + d_rope <= 576, 1 <= tok_per_wg <= 32
   const int ob = write_blocks_per_wave(a.d_c + a.d_rope);

@@ -514,7 +514,8 @@ int cache_write_common(const videomla_dims* d, const videomla_window* w, int32_t
   a.eps = d->kv_norm_eps;
   a.geo = make_geo(d, w);
   a.rope = make_rope(d);
-  a.tok_per_wg = cache_write_tokens_per_wg((int64_t)batch * a.geo.chunk_tokens, device_cu_count());
+  a.n_cu = device_cu_count();
+  a.tok_per_wg = cache_write_tokens_per_wg((int64_t)batch * a.geo.chunk_tokens, a.n_cu);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const hipError_t e = launch_cache_write(a, s);
   if (e != hipSuccess) return hip_fail(e, "cache_write");

@@ -51,6 +51,7 @@ struct WriteArgs {
   uint16_t* w_packed_out;    // pack_write_weights_kernel output
   int32_t batch, d_model, d_c, d_rope;
   int32_t tok_per_wg;     // tokens of the flat [B][chunk] order per workgroup (1 .. 32)
+  int32_t n_cu;           // compute units of the device (the batched write's grid)
   float eps;
   Geometry geo;
   RopeTable rope;

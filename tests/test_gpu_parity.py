@@ -121,8 +121,25 @@ def test_packed_weight_panel_layout(vm):
         assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("batch", [2, 3])
+def test_wan_batched_packed_write_matches_oracle(vm, batch):
+    """Batches whose tokens exceed 32 per compute unit take the wide cache write (one workgroup
+    per compute unit, up to 80 tokens: 37 tokens = 3 blocks of 16 at batch 2, 55 = 4 blocks at
+    batch 3; blocks span batch elements); the write after a full ring, evicting frames 0..2."""
+    inp = make_layer_inputs(WAN, seed=9, n_frames=24, batch=batch)
+    layer = Layer(vm, inp, packed=True)
+    for fe in range(0, 21, 3):
+        layer.write(fe)
+    before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
+    layer.write(21)
+    stats = check_written_chunk(layer, 21, before_c, before_k)
+    exact = sum(e for e, _ in stats) / sum(n for _, n in stats)
+    assert exact >= 0.999
+
+
 def test_wan_batch4_packed_write_matches_oracle(vm):
-    """Batch 4 (18,720 tokens: full 32-token workgroups, blocks spanning batch elements)."""
+    """Batch 4 (18,720 tokens: the wide cache write, 74 tokens = 5 blocks of 16 per workgroup,
+    blocks spanning batch elements)."""
     inp = make_layer_inputs(WAN, seed=8, n_frames=3, batch=4)
     layer = Layer(vm, inp, packed=True)
     before_c, before_k = host_bits(layer.c_kv), host_bits(layer.k_r)
