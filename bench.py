@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "59c3d7765eb75c2a5da2dda30a98fae6d87d67188d758e2af198677a38427a54",
-                  "bytes": 305102101}
+                  "sha256": "acbc9bfeec5a341009d67556c48222d20bf58f32e84b3e91a37e0d75639ffc19",
+                  "bytes": 303320211}
 
 
 def log(msg):
@@ -525,6 +525,9 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
 
     lat = run("latent")
     den = run("dense")
+    if args.copy_probe:
+        log("copy probe")
+        copy_probe(torch, dev)
     # algorithmic work of the whole rollout (valid window per chunk)
     lat_flop = den_flop = 0
     fe = 0

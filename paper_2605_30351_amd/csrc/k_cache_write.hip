@@ -30,6 +30,8 @@
 // LDS stages of kKC columns each, filled by direct global-to-LDS loads in an XOR-swizzled
 // layout; the four waves share every staged chunk and split the 32-row output blocks between
 // them. Same epilogue steps, with 8-byte stores straight from the accumulators.
+#include <type_traits>
+
 #include "vmla_device.h"
 
 namespace vmla {
@@ -42,6 +44,89 @@ constexpr int kMaxWaves = 9;   // d_c + d_rope <= 288 with 32 outputs per wave, 
 // accumulator element i of lane l is D[4(l/16) + i][l%16].
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// (cos, sin) of the angle pos_axis * theta of RoPE pair `pair` at position p, for the keys the
+// cache write rotates: the angle in turns is reduced to [-1/2, 1/2] in double precision, as in
+// rope_rotate, and the hardware cosine and sine, which take their argument in turns, finish it.
+// Over that range they are within 1.3e-7 (2^-22.9) of the exact values, measured against double
+// precision on 2^22 points; the library sincosf of the angle in radians, whose fp32 product
+// 2 pi r rounds first, is within 2.1e-7. Either is far below the bf16 rounding of the cached keys.
+__device__ __forceinline__ f32x2 rope_cos_sin(const RopeTable& t, int pair, const TokenPos& p) {
+  const int ax = t.axis[pair];
+  const double pos = ax == 0 ? (double)p.f : (ax == 1 ? (double)p.y : (double)p.x);
+  const double turns = pos * t.theta[pair] * 0.15915494309189533577;  // 1 / (2 pi)
+  const float r = (float)(turns - rint(turns));
+  return f32x2{__builtin_amdgcn_cosf(r), __builtin_amdgcn_sinf(r)};
+}
+
+// RMSNorm sum of squares of token rows 16 tb + r (tb < TB): the sum over the waves w < n of
+// part[w * stride + row], added in the order w = 0, 1, ... Every load is issued before the
+// first add (rows of waves past n are read at wave n - 1 and replaced by zero, which leaves the
+// sum unchanged); a loop bounded by the run-time n would wait for each load in turn.
+template <int MAXW, int TB>
+__device__ __forceinline__ void sum_wave_parts(const float* part, int stride, int n, int r,
+                                               float (&tot)[TB]) {
+  float v[MAXW][TB];
+#pragma unroll
+  for (int w = 0; w < MAXW; ++w) {
+    const int wr = w < n ? w : n - 1;
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) v[w][tb] = part[wr * stride + 16 * tb + r];
+  }
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) {
+    tot[tb] = 0.f;
+#pragma unroll
+    for (int w = 0; w < MAXW; ++w) tot[tb] += w < n ? v[w][tb] : 0.f;
+  }
+}
+
+constexpr uint32_t kOneBf16x2 = 0x3F803F80u;  // two bf16 ones: the gain when there is none
+
+// The epilogue's output tile: normalized latents times the gain, and rotated RoPE keys, rounded
+// to bf16 into ot[t][0 .. NO) (row stride ots). Lane (r, q) holds outputs o0 + 16 ob + 4q + e
+// (o0 = the wave's first output) of token 16 tb + r in acc[ob][tb][e]; gam[ob] holds the gains of
+// its four latent outputs as bf16 pairs (ones without a gain), rstd[tb] the token's reciprocal
+// RMS (one without a gain), rope_cs[t * cs_stride + i] the (cos, sin) of token t's pair i.
+// With d_c % 16 == 0 every 16-output block is all latent or all RoPE key (and padding), so that
+// the branch is uniform per block and the token blocks inside it are straight-line code, which
+// the compiler interleaves; a per-lane branch inside the token loop would serialize them.
+template <int OB, int TB>
+__device__ __forceinline__ void write_out_tile(const f32x4 (&acc)[OB][TB], const u32x2 (&gam)[OB],
+                                               const float (&rstd)[TB], const f32x2* rope_cs,
+                                               int cs_stride, int o_wave, int DC, int NO, int r,
+                                               int q, int ntok, uint16_t* ot, int ots) {
+#pragma unroll
+  for (int ob = 0; ob < OB; ++ob) {
+    const int o0 = o_wave + 16 * ob;  // first output of the block
+    const int o = o0 + 4 * q;         // first of this lane's four consecutive outputs
+    if (o0 + 16 <= DC) {
+      const float g0 = __uint_as_float(gam[ob][0] << 16);
+      const float g1 = __uint_as_float(gam[ob][0] & 0xffff0000u);
+      const float g2 = __uint_as_float(gam[ob][1] << 16);
+      const float g3 = __uint_as_float(gam[ob][1] & 0xffff0000u);
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        f32x4 v = acc[ob][tb] * rstd[tb];
+        v = f32x4{v[0] * g0, v[1] * g1, v[2] * g2, v[3] * g3};
+        *reinterpret_cast<bf16x4*>(&ot[(16 * tb + r) * ots + o]) = to_bf16x4(v);
+      }
+    } else if (o0 < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
+      const bool live = o < NO;  // else padding past d_c + d_rope
+      const int pr = live ? (o - DC) / 2 : 0;
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
+        const int t = 16 * tb + r;
+        const int tc = t < ntok ? t : ntok - 1;
+        const f32x2 c0 = rope_cs[tc * cs_stride + pr], c1 = rope_cs[tc * cs_stride + pr + 1];
+        const f32x4 v = acc[ob][tb];
+        const f32x4 w = {v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
+                         v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
+        if (live) *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(w);
+      }
+    }
+  }
 }
 
 // x tile layout: column blocks of 64 columns (8 chunks of 16 bytes); block b holds rows
@@ -77,13 +162,11 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   // RMSNorm gain of this lane's outputs 32 wave + 16 ob + 4q .. +3, fetched first
   constexpr int OPW = 16 * OB;  // outputs per wave
   u32x2 gam[OB];
-  if (a.gamma) {
 #pragma unroll
-    for (int ob = 0; ob < OB; ++ob) {
-      const int o = OPW * wave + 16 * ob + 4 * q;
-      gam[ob] = u32x2{0u, 0u};
-      if (o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
-    }
+  for (int ob = 0; ob < OB; ++ob) {
+    const int o = OPW * wave + 16 * ob + 4 * q;
+    gam[ob] = u32x2{kOneBf16x2, kOneBf16x2};
+    if (a.gamma && o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
   }
 
   // ---- contraction order: k-step i of this workgroup is column k-step (i + rot) mod nks, rot
@@ -136,11 +219,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
       tok_slot[lane] = (int64_t)b * a.geo.ring_tokens + slot;
       if (b == 0 && a.slots) a.slots[n] = (int32_t)slot;
     }
-    for (int pr = wave; pr < npair; pr += nwave) {
-      float u = 1.f, w = 0.f;  // rotating (1, 0) gives (cos, sin); identity with a sink
-      if (a.geo.sink_frames == 0) rope_rotate(a.rope, pr, pos, u, w);
-      rope_cs[lane][pr] = f32x2{u, w};
-    }
+    for (int pr = wave; pr < npair; pr += nwave)  // identity with a sink
+      rope_cs[lane][pr] = a.geo.sink_frames == 0 ? rope_cos_sin(a.rope, pr, pos) : f32x2{1.f, 0.f};
   }
   // loads complete in issue order: once at most the OB KPRE weight loads issued after them are
   // outstanding, this wave's first-phase x loads (and the gain) have landed
@@ -215,35 +295,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
   const int ots = NO + 8;  // row stride (elements): 16 bytes of padding per row
   uint16_t* ot = xs;
+  float tot[2], rstd[2];
+  sum_wave_parts<kMaxWaves>(&ssq_part[0][0], kTokTile, nwave, r, tot);
 #pragma unroll
-  for (int tb = 0; tb < 2; ++tb) {
-    const int t = 16 * tb + r;
-    const int tc = t < ntok ? t : ntok - 1;
-    float tot = 0.f;
-    for (int w = 0; w < nwave; ++w) tot += ssq_part[w][t];
-    const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
-#pragma unroll
-    for (int ob = 0; ob < OB; ++ob) {
-      const int o = OPW * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
-      f32x4 v = acc[ob][tb];
-      if (o + 4 <= DC) {
-        v = v * rstd;
-        if (a.gamma) {
-          v[0] *= __uint_as_float(gam[ob][0] << 16);
-          v[1] *= __uint_as_float(gam[ob][0] & 0xffff0000u);
-          v[2] *= __uint_as_float(gam[ob][1] << 16);
-          v[3] *= __uint_as_float(gam[ob][1] & 0xffff0000u);
-        }
-      } else if (o < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
-        const f32x2 c0 = rope_cs[tc][(o - DC) / 2], c1 = rope_cs[tc][(o - DC) / 2 + 1];
-        v = f32x4{v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
-                  v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
-      } else {
-        continue;  // padding outputs past d_c + d_rope
-      }
-      *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(v);
-    }
-  }
+  for (int tb = 0; tb < 2; ++tb) rstd[tb] = a.gamma ? rsqrtf(tot[tb] / (float)DC + a.eps) : 1.f;
+  write_out_tile(acc, gam, rstd, &rope_cs[0][0], kMaxRopePairs, OPW * wave, DC, NO, r, q, ntok,
+                 ot, ots);
   __syncthreads();
 
   // ---- stores: token t's row of NO/8 chunks (c_kv, then k_r) to its ring slot, coalesced ---
@@ -268,11 +325,11 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
 // phases are in flight while a third is contracted, and one barrier per phase hands a buffer
 // from the compute waves to the loader and back. The compute waves are those of
 // cache_write_packed_kernel (one per 32 outputs, the same packed panel, the same MFMA), each with
-// TB token blocks of accumulators. The loader also computes the tokens' ring rows and RoPE
-// angles, and every wave takes part in the stores. LDS (dynamic, cache_write_wide_lds_bytes):
-// three x buffers [KPRE / 4 column blocks][16 TB rows][64], swizzled like the packed kernel's x
-// tile (the output tile reuses them), then the per-wave sums of squares [waves - 1][16 TB], the
-// ring rows [16 TB] and (cos, sin) [16 TB][d_rope / 2].
+// TB token blocks of accumulators. All waves share the tokens' ring rows and RoPE angles while
+// the first phase lands, and every wave takes part in the stores. LDS (dynamic,
+// cache_write_wide_lds_bytes): three x buffers [KPRE / 4 column blocks][16 TB rows][64],
+// swizzled like the packed kernel's x tile (the output tile reuses them), then the per-wave sums
+// of squares [waves - 1][16 TB], the ring rows [16 TB] and (cos, sin) [16 TB][d_rope / 2].
 constexpr int kWideBufs = 3;
 
 template <int KPRE, int TB>
@@ -308,6 +365,39 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
   const int rot = 2 * rotb;
   auto kstep = [&](int i) { const int k = i + rot; return k < nks ? k : k - nks; };
 
+  // each token's ring row (and slot) and the (cos, sin) of its RoPE pair angles, computed by all
+  // waves while the first phase of x lands: wave w takes the pairs w, w + nwave, .. (a pair index
+  // uniform across the wave, so that the angle table is read by scalar loads) and wave 0, a
+  // compute wave, the ring rows
+  auto tables = [&]() {
+    constexpr int NT = (ROWS + 63) / 64;  // tokens per lane
+    TokenPos pos[NT];
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+      const int t = lane + 64 * k;
+      const int g = (int)g0 + (t < ntok ? t : ntok - 1);  // < 2^31 (validated on the host)
+      const int b = g / n_tok, n = g - b * n_tok;
+      pos[k] = token_pos(a.geo, n);
+      if (wave == 0 && t < ntok) {
+        const int64_t slot = ring_slot(a.geo, pos[k]);
+        tok_slot[t] = (int64_t)b * a.geo.ring_tokens + slot;
+        if (b == 0 && a.slots) a.slots[n] = (int32_t)slot;
+      }
+    }
+    for (int p = wave; p < npair; p += nwave) {
+      // the pair index made visibly uniform, so that its table entries are read once, by scalar
+      // loads (as a per-lane index they become vector loads that each wait for every load)
+      const int pr = __builtin_amdgcn_readfirstlane(p);
+#pragma unroll
+      for (int k = 0; k < NT; ++k) {
+        const int t = lane + 64 * k;
+        const f32x2 cs =  // identity with a sink
+            a.geo.sink_frames == 0 ? rope_cos_sin(a.rope, pr, pos[k]) : f32x2{1.f, 0.f};
+        if (t < ntok) rope_cs[t * npair + pr] = cs;
+      }
+    }
+  };
+
   if (loader) {
     // phase p's columns into buffer p mod 3; rows past the block's tokens repeat its last token
     auto issue_x = [&](int p) {
@@ -328,27 +418,12 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     };
     issue_x(0);
     if (nph > 1) issue_x(1);
+    tables();  // after the phase loads: a memory operation in it only makes the waits stricter
     for (int p = 0; p < nph; ++p) {
       // phase p has landed once at most the next phase's loads are outstanding (vector memory
-      // operations, the ring-row stores below included, complete in issue order)
+      // operations complete in issue order)
       if (p + 1 < nph) wait_vmcnt<LPP>();
       else wait_vmcnt<0>();
-      if (p == 0) {
-        // each token's ring row (and slot), and its RoPE (cos, sin), while phase 1 lands
-        for (int t = lane; t < ntok; t += 64) {
-          const int g = (int)g0 + t;  // batch * chunk_tokens < 2^31 (validated on the host)
-          const int b = g / n_tok, n = g - b * n_tok;
-          const TokenPos pos = token_pos(a.geo, n);
-          const int64_t slot = ring_slot(a.geo, pos);
-          tok_slot[t] = (int64_t)b * a.geo.ring_tokens + slot;
-          if (b == 0 && a.slots) a.slots[n] = (int32_t)slot;
-          for (int pr = 0; pr < npair; ++pr) {
-            float u = 1.f, w = 0.f;  // rotating (1, 0) gives (cos, sin); identity with a sink
-            if (a.geo.sink_frames == 0) rope_rotate(a.rope, pr, pos, u, w);
-            rope_cs[t * npair + pr] = f32x2{u, w};
-          }
-        }
-      }
       __syncthreads();  // phase p visible; the compute waves are done with phase p - 1
       if (p + 2 < nph) issue_x(p + 2);  // into the buffer phase p - 1 left
     }
@@ -360,9 +435,12 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
 #pragma unroll
     for (int ob = 0; ob < OB; ++ob) {
       const int o = OPW * wave + 16 * ob + 4 * q;
-      gam[ob] = u32x2{0u, 0u};
+      gam[ob] = u32x2{kOneBf16x2, kOneBf16x2};
       if (a.gamma && o + 4 <= DC) gam[ob] = *reinterpret_cast<const u32x2*>(a.gamma + o);
     }
+    // the tables first: issuing a weight ring's loads can stall this wave until the compute
+    // unit's memory pipeline, which the loader's x loads fill first, has room for them
+    tables();
     // this wave's packed panel slice (as in cache_write_packed_kernel), KPRE k-steps ahead
     const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * OB) * 512 + lane * 8;
     u32x4 wb[KPRE][OB];
@@ -391,20 +469,26 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) acc[ob][tb] = mfma16(as_bf16x8(w[ob]), xb[tb], acc[ob][tb]);
     };
-    for (int i0 = 0; i0 < nks; i0 += KPRE) {  // two phases per pass over the weight ring
-      const bool refill = i0 + KPRE < nks;
+    // one pass = two phases = the KPRE k-steps of the weight ring. The refill is a compile-time
+    // choice, so that the steady-state passes issue their loads on every path and the compiler
+    // counts the outstanding loads exactly; a run-time condition would make it wait for all of
+    // them (the whole ring) at every pass.
+    auto pass = [&](int i0, auto refill) {
 #pragma unroll
       for (int j = 0; j < KPRE; ++j) {
         const int ph = (i0 + j) / PK;
         if (j % PK == 0) __syncthreads();  // phase ph is in its buffer
         mma_step(xbuf + (ph % kWideBufs) * XB, j % PK, wb[j]);
-        if (refill) {
+        if constexpr (decltype(refill)::value) {
           const int kn = kstep(i0 + j + KPRE);
 #pragma unroll
           for (int ob = 0; ob < OB; ++ob) wb[j][ob] = ldg16(wpan + (OB * kn + ob) * 512);
         }
       }
-    }
+    };
+    int i0 = 0;
+    for (; i0 < nks - KPRE; i0 += KPRE) pass(i0, std::true_type{});
+    pass(i0, std::false_type{});
     // sums of squares of the latent outputs per token
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -424,36 +508,12 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
     const int ots = NO + 8;
     uint16_t* ot = xbuf;
+    float tot[TB];
+    sum_wave_parts<7>(ssq_part, ROWS, ncw, r, tot);  // at most 8 waves, one of them the loader
+    float rstd[TB];
 #pragma unroll
-    for (int tb = 0; tb < TB; ++tb) {
-      const int t = 16 * tb + r;
-      const int tc = t < ntok ? t : ntok - 1;
-      float tot = 0.f;
-      for (int w = 0; w < ncw; ++w) tot += ssq_part[w * ROWS + t];
-      const float rstd = a.gamma ? rsqrtf(tot / (float)DC + a.eps) : 1.f;
-#pragma unroll
-      for (int ob = 0; ob < OB; ++ob) {
-        const int o = OPW * wave + 16 * ob + 4 * q;  // first of 4 consecutive outputs
-        f32x4 v = acc[ob][tb];
-        if (o + 4 <= DC) {
-          v = v * rstd;
-          if (a.gamma) {
-            v[0] *= __uint_as_float(gam[ob][0] << 16);
-            v[1] *= __uint_as_float(gam[ob][0] & 0xffff0000u);
-            v[2] *= __uint_as_float(gam[ob][1] << 16);
-            v[3] *= __uint_as_float(gam[ob][1] & 0xffff0000u);
-          }
-        } else if (o < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
-          const f32x2 c0 = rope_cs[tc * npair + (o - DC) / 2];
-          const f32x2 c1 = rope_cs[tc * npair + (o - DC) / 2 + 1];
-          v = f32x4{v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
-                    v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
-        } else {
-          continue;  // padding outputs past d_c + d_rope
-        }
-        *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(v);
-      }
-    }
+    for (int tb = 0; tb < TB; ++tb) rstd[tb] = a.gamma ? rsqrtf(tot[tb] / (float)DC + a.eps) : 1.f;
+    write_out_tile(acc, gam, rstd, rope_cs, npair, OPW * wave, DC, NO, r, q, ntok, ot, ots);
     __syncthreads();  // the output tile is complete
   }
 
@@ -629,8 +689,11 @@ __global__ __launch_bounds__(kWaves * 64) void cache_write_staged_kernel(const W
       } else if (o >= DC && o + 4 <= DC + DR) {
         const int ch = o - DC;  // channels ch .. ch+3 = RoPE pairs ch/2 and ch/2 + 1
         if (a.geo.sink_frames == 0) {  // with a sink the ring keeps the unrotated key
-          rope_rotate(a.rope, ch / 2, pos, v[0], v[1]);
-          rope_rotate(a.rope, ch / 2 + 1, pos, v[2], v[3]);
+          const f32x2 c0 = rope_cos_sin(a.rope, ch / 2, pos);
+          const f32x2 c1 = rope_cos_sin(a.rope, ch / 2 + 1, pos);
+          const float r0 = v[0] * c0[0] - v[1] * c0[1], r1 = v[0] * c0[1] + v[1] * c0[0];
+          const float r2 = v[2] * c1[0] - v[3] * c1[1], r3 = v[2] * c1[1] + v[3] * c1[0];
+          v[0] = r0, v[1] = r1, v[2] = r2, v[3] = r3;
         }
         const f32x4 fv = {v[0], v[1], v[2], v[3]};
         *reinterpret_cast<bf16x4*>(kdst + ch) = to_bf16x4(fv);
