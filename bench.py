@@ -968,6 +968,90 @@ def xcd_balance(args, vm, torch, d, n_calls=12):
     }), flush=True)
 
 
+def library_references(args, vm, torch, d):
+    """Reference rates of the vendor GEMM library (hipBLASLt, through torch.matmul) on this machine:
+    large square bf16 products (a practical dense MFMA ceiling, against the published 2.5 PF)
+    and the cache write's bare projection x [B*Nq, d_model] @ [W_DKV; W_KR]^T at the Wan shape,
+    next to the library's fused cache write of the same tokens (projection + RMSNorm + RoPE +
+    ring scatter). Every call is bracketed by HIP events on the current stream, with a long
+    product queued ahead of every ten calls so that the events time kernels, not host launch
+    gaps. Seeded synthetic bf16 drawn on the GPU; x cycles through 8 buffers."""
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    filler_a, filler_b = normal((8192, 8192)), normal((8192, 8192))
+
+    def timed(fn, n=60, warm=10):
+        for _ in range(warm):
+            fn(0)
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n)]
+        for i in range(n):
+            if i % 10 == 0:
+                torch.matmul(filler_a, filler_b)
+            ev[i][0].record()
+            fn(i)
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+        return sum(t) / len(t), t[len(t) // 2]
+
+    gemms = []
+    for (m, n, k) in ((8192, 8192, 8192), (16384, 16384, 4096)):
+        a, b = normal((m, k)), normal((k, n))
+        avg, med = timed(lambda i: torch.matmul(a, b), n=20, warm=5)
+        gemms.append({"m": m, "n": n, "k": k, "avg_us": round(avg, 2),
+                      "tflops": round(2 * m * n * k / (avg * 1e-6) / 1e12, 1),
+                      "frac_of_2.5pf": round(2 * m * n * k / (avg * 1e-6) / 1e12
+                                             / MFMA_BF16_PEAK_TFLOPS, 4)})
+        del a, b
+    log(f"square GEMMs: {gemms}")
+
+    no = d.d_c + d.d_rope
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    w_t = torch.cat([w_dkv, w_kr], 0).t().contiguous()          # [d_model, d_c + d_rope]
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
+    vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
+    proj = []
+    for B in (1, 2, 4, 8):
+        M = B * d.chunk_tokens
+        xs = [normal((B, d.chunk_tokens, d.d_model)) for _ in range(8)]
+        y = torch.empty((M, no), dtype=torch.bfloat16, device=dev)
+        c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+        k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+        lib, _ = timed(lambda i: torch.matmul(xs[i % 8].view(M, d.d_model), w_t, out=y))
+        fused, _ = timed(lambda i: vm.cache_write_prepared(d, 21, B, xs[i % 8], w_packed, gamma,
+                                                           c_kv, k_r))
+        byts = M * (2 * d.d_model + 2 * no) + 2 * d.d_model * no
+        proj.append({"batch": B, "tokens": M, "library_gemm_us": round(lib, 2),
+                     "fused_cache_write_us": round(fused, 2),
+                     "fused_over_library": round(fused / lib, 3),
+                     "algorithmic_bytes": byts,
+                     "fused_hbm_frac": round(byts / (fused * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "library_hbm_frac": round(byts / (lib * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)})
+        log(f"projection batch {B}: {proj[-1]}")
+        del xs, y, c_kv, k_r
+        torch.cuda.empty_cache()
+    print(json.dumps({
+        "metric": "vendor GEMM library references: square bf16 products and the cache write's "
+                  "bare projection vs the fused cache write",
+        "value": proj[0]["fused_over_library"], "unit": "fused cache write / library GEMM time, batch 1",
+        "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "square_gemms": gemms, "cache_write_projection": proj,
+        "config": {"workload": ("torch.matmul (hipBLASLt) bf16: square products, and "
+                                "x[B*4680, 1536] @ [W_DKV; W_KR]^T (1536 x 224) at batch 1-8 "
+                                "against videomla_cache_write_prepared on the same tokens"),
+                   "seed": 7},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -981,7 +1065,7 @@ def main():
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
                              "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
                              "wan-latent-vs-materialized", "wan-few-query",
-                             "wan-form-crossover", "wan-xcd-balance"),
+                             "wan-form-crossover", "wan-xcd-balance", "library-references"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -995,7 +1079,9 @@ def main():
                          "wan-few-query: blocks of 16..1560 query tokens at batch 8, latent vs "
                          "dense; wan-form-crossover: latent vs materialized per (n_q, d_nope, "
                          "d_c) and the automatic choice; wan-xcd-balance: per-XCD workgroup "
-                         "times from the partition's own record")
+                         "times from the partition's own record; library-references: the "
+                         "vendor GEMM library's rate on square products and on the cache "
+                         "write's bare projection, next to the fused cache write")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     ap.add_argument("--n-q", default="16,52,208,1560",
                     help="query tokens per video of the wan-few-query run (comma-separated)")
@@ -1030,6 +1116,9 @@ def main():
         return
     if args.workload == "wan-xcd-balance":
         xcd_balance(args, vm, torch, WAN)
+        return
+    if args.workload == "library-references":
+        library_references(args, vm, torch, WAN)
         return
     if args.workload == "wan-form-crossover":
         form_crossover(args, vm, torch)

@@ -115,15 +115,23 @@ __device__ __forceinline__ void write_out_tile(const f32x4 (&acc)[OB][TB], const
     } else if (o0 < NO) {  // channels o-DC .. +3 = RoPE pairs (o-DC)/2 and (o-DC)/2 + 1
       const bool live = o < NO;  // else padding past d_c + d_rope
       const int pr = live ? (o - DC) / 2 : 0;
+      // every (cos, sin) read before the first tile write: the compiler cannot tell the two LDS
+      // areas apart, and would otherwise wait for each write before the next read
+      f32x2 c0[TB], c1[TB];
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) {
         const int t = 16 * tb + r;
         const int tc = t < ntok ? t : ntok - 1;
-        const f32x2 c0 = rope_cs[tc * cs_stride + pr], c1 = rope_cs[tc * cs_stride + pr + 1];
+        c0[tb] = rope_cs[tc * cs_stride + pr];
+        c1[tb] = rope_cs[tc * cs_stride + pr + 1];
+      }
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) {
         const f32x4 v = acc[ob][tb];
-        const f32x4 w = {v[0] * c0[0] - v[1] * c0[1], v[0] * c0[1] + v[1] * c0[0],
-                         v[2] * c1[0] - v[3] * c1[1], v[2] * c1[1] + v[3] * c1[0]};
-        if (live) *reinterpret_cast<bf16x4*>(&ot[t * ots + o]) = to_bf16x4(w);
+        const f32x2 a0 = c0[tb], a1 = c1[tb];
+        const f32x4 w = {v[0] * a0[0] - v[1] * a0[1], v[0] * a0[1] + v[1] * a0[0],
+                         v[2] * a1[0] - v[3] * a1[1], v[2] * a1[1] + v[3] * a1[0]};
+        if (live) *reinterpret_cast<bf16x4*>(&ot[(16 * tb + r) * ots + o]) = to_bf16x4(w);
       }
     }
   }
