@@ -125,17 +125,28 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 
   // RoPE part and zero padding: 32 tokens x (DR/2) pairs per wave.
   const int tok0 = blockIdx.x * 128 + wave * 32;
-  for (int it = lane; it < 32 * (DR / 2); it += 64) {
-    const int t = tok0 + it / (DR / 2), p = it % (DR / 2);
-    if (t >= Nq) continue;
+  auto rope_one = [&](int t, int p, const RopePair& rp) {
     const size_t r = ((size_t)b * Nq + t) * H + h;
     const uint32_t raw = *reinterpret_cast<const uint32_t*>(a.q_r + r * DR + 2 * p);
     float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff)), v = bf16_bits_to_f32((uint16_t)(raw >> 16));
-    rope_rotate(a.rope, p, rope_pos(a.geo, query_pos(a.geo, t)), u, v);
+    rotate_by(rope_cos_sin(rp, rope_pos(a.geo, query_pos(a.geo, t))), u, v);
     const uint32_t packed =
         (uint32_t)to_bf16_bits(u * a.qscale) | ((uint32_t)to_bf16_bits(v * a.qscale) << 16);
     *reinterpret_cast<uint32_t*>(STAGE ? ot + (t - tok0) * OS + DC + 2 * p
                                        : a.qcat + r * DQKP + DC + 2 * p) = packed;
+  };
+  constexpr int NP = DR / 2;
+  if constexpr (64 % NP == 0) {
+    // lane l keeps pair l mod NP for all its tokens, so that it reads that pair's table entries
+    // once (a per-iteration read would be a vector load waiting for every load in flight)
+    const int p = lane % NP;
+    const RopePair rp = rope_pair(a.rope, p);
+    for (int t = tok0 + lane / NP; t < tok0 + 32 && t < Nq; t += 64 / NP) rope_one(t, p, rp);
+  } else {
+    for (int it = lane; it < 32 * NP; it += 64) {
+      const int t = tok0 + it / NP, p = it % NP;
+      if (t < Nq) rope_one(t, p, rope_pair(a.rope, p));
+    }
   }
   if (DQKP > DC + DR) {
     for (int t = tok0 + lane; t < tok0 + 32 && t < Nq; t += 64) {

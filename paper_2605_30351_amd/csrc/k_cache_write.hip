@@ -46,20 +46,6 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// (cos, sin) of the angle pos_axis * theta of RoPE pair `pair` at position p, for the keys the
-// cache write rotates: the angle in turns is reduced to [-1/2, 1/2] in double precision, as in
-// rope_rotate, and the hardware cosine and sine, which take their argument in turns, finish it.
-// Over that range they are within 1.3e-7 (2^-22.9) of the exact values, measured against double
-// precision on 2^22 points; the library sincosf of the angle in radians, whose fp32 product
-// 2 pi r rounds first, is within 2.1e-7. Either is far below the bf16 rounding of the cached keys.
-__device__ __forceinline__ f32x2 rope_cos_sin(const RopeTable& t, int pair, const TokenPos& p) {
-  const int ax = t.axis[pair];
-  const double pos = ax == 0 ? (double)p.f : (ax == 1 ? (double)p.y : (double)p.x);
-  const double turns = pos * t.theta[pair] * 0.15915494309189533577;  // 1 / (2 pi)
-  const float r = (float)(turns - rint(turns));
-  return f32x2{__builtin_amdgcn_cosf(r), __builtin_amdgcn_sinf(r)};
-}
-
 // RMSNorm sum of squares of token rows 16 tb + r (tb < TB): the sum over the waves w < n of
 // part[w * stride + row], added in the order w = 0, 1, ... Every load is issued before the
 // first add (rows of waves past n are read at wave n - 1 and replaced by zero, which leaves the

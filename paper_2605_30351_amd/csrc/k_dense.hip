@@ -29,6 +29,7 @@ constexpr float kNegInfD = -__builtin_huge_valf();
 constexpr int kDwTok = 128, kDwOut = 128, kDwKC = 64, kDwStages = 3;
 constexpr int kDwRows = kDwTok + kDwOut;          // staged rows per stage
 constexpr int kDwLoads = kDwRows * 8 / 64;        // 1 KB loads per stage (32)
+constexpr int kDwMaxPairs = 64;  // RoPE pairs whose angle table fits the stage memory
 
 __device__ __forceinline__ int dw_swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
 
@@ -95,6 +96,28 @@ __global__ __launch_bounds__(256, 1) void dense_cache_write_kernel(const DenseWr
     }
   }
 
+  // (cos, sin) of every (token, RoPE pair) of a tile holding K outputs, computed once into the
+  // free stage memory: wave w takes the pairs w, w + 4, .. (a pair index uniform across the wave,
+  // so that its table entries are read by scalar loads), lanes the tile's tokens. Rows are padded
+  // by one entry so that the epilogue's reads (32 tokens at one pair) hit distinct banks. Heads
+  // wider than 2 kDwMaxPairs take the angles per lane instead.
+  const int npair = DH / 2, cs_ld = npair + 1;
+  const bool cs_table = o0 < hd && npair <= kDwMaxPairs;  // uniform
+  const f32x2* cs_tab = reinterpret_cast<const f32x2*>(&stage[0][0]);
+  if (cs_table) {
+    f32x2* tab = reinterpret_cast<f32x2*>(&stage[0][0]);
+    __syncthreads();  // every wave is past its last stage read
+    TokenPos tp[kDwTok / 64];
+#pragma unroll
+    for (int k = 0; k < kDwTok / 64; ++k) tp[k] = token_pos(a.geo, min(n0 + lane + 64 * k, n_tok - 1));
+    for (int p = wave; p < npair; p += 4) {
+      const RopePair rp = rope_pair(a.rope, __builtin_amdgcn_readfirstlane(p));
+#pragma unroll
+      for (int k = 0; k < kDwTok / 64; ++k) tab[(lane + 64 * k) * cs_ld + p] = rope_cos_sin(rp, tp[k]);
+    }
+    __syncthreads();
+  }
+
   // epilogue: lane holds token n, outputs o0 + 32 m + 8 i + 4 g + j (4 consecutive channels of
   // one head: two RoPE pairs when they belong to K)
   const int n = n0 + wave * 32 + l32;
@@ -111,7 +134,11 @@ __global__ __launch_bounds__(256, 1) void dense_cache_write_kernel(const DenseWr
       const bool is_k = o < hd;
       const int oo = is_k ? o : o - hd;
       const int h = oo / DH, ch = oo % DH;
-      if (is_k) {
+      if (is_k && cs_table) {
+        const f32x2* row = cs_tab + (wave * 32 + l32) * cs_ld + ch / 2;
+        rotate_by(row[0], v[0], v[1]);
+        rotate_by(row[1], v[2], v[3]);
+      } else if (is_k) {
         rope_rotate(a.rope, ch / 2, pos, v[0], v[1]);
         rope_rotate(a.rope, ch / 2 + 1, pos, v[2], v[3]);
       }
