@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "acbc9bfeec5a341009d67556c48222d20bf58f32e84b3e91a37e0d75639ffc19",
-                  "bytes": 303320211}
+                  "sha256": "3a9fac5b492ffaf3324c3e8c2f0f2b12a035a56171b1804b0f11db5ac3024719",
+                  "bytes": 306883247}
 
 
 def log(msg):
@@ -525,6 +525,20 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
 
     lat = run("latent")
     den = run("dense")
+    # the vendor GEMM library (torch.matmul) on each path's bare cache projection at this batch,
+    # x [B Nq, d_model] @ [W_DKV; W_KR]^T or [W_K; W_V]^T: the dense comparator's cache write at
+    # the library's rate, for the comparison below
+    filler_a, filler_b = normal((8192, 8192)), normal((8192, 8192))
+    x2 = [xs[i].view(B * nq, d.d_model) for i in range(len(xs))]
+    lib_proj = {}
+    for name, n_out in (("latent", d.d_c + d.d_rope), ("dense", 2 * d.n_heads * d.d_v)):
+        w_t = normal((d.d_model, n_out), d.d_model ** -0.5)
+        y = torch.empty((B * nq, n_out), dtype=torch.bfloat16, device=dev)
+        avg, _ = event_timed(torch, lambda i: torch.matmul(x2[i % len(x2)], w_t, out=y),
+                             lambda: torch.matmul(filler_a, filler_b))
+        lib_proj[name] = round(avg, 2)
+        del w_t, y
+    del filler_a, filler_b
     if args.copy_probe:
         log("copy probe")
         copy_probe(torch, dev)
@@ -572,6 +586,9 @@ def rollout_comparison(args, vm, torch, d, batch=4, n_layers=30, n_steps=4):
         "latent_over_dense_time": round(lat["seconds"] / den["seconds"], 3),
         "latent_over_dense_time_per_call_full_window": round(lat_call / den_call, 3),
         "attention_kernels_full_window": eff,
+        "library_projection_us": lib_proj,
+        "latent_over_dense_per_call_full_window_dense_write_at_library_rate": round(
+            lat_call / (den_call - da["dense_cache_write"]["avg_us"] + lib_proj["dense"]), 3),
         "cache_bytes": {"latent": lat_bytes, "dense": den_bytes,
                         "dense_over_latent": round(den_bytes / lat_bytes, 3)},
         "config": {"workload": (f"Wan2.1-1.3B rollout, batch 4: {n_chunks} chunks of 3 frames "
@@ -968,6 +985,26 @@ def xcd_balance(args, vm, torch, d, n_calls=12):
     }), flush=True)
 
 
+def event_timed(torch, fn, filler, n=60, warm=10):
+    """Mean and median microseconds of fn(i), each call bracketed by HIP events on the current
+    stream, with filler() (a long kernel) queued ahead of every ten calls so that the events time
+    the kernels rather than host launch gaps."""
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for i in range(n):
+        if i % 10 == 0:
+            filler()
+        ev[i][0].record()
+        fn(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+    return sum(t) / len(t), t[len(t) // 2]
+
+
 def library_references(args, vm, torch, d):
     """Reference rates of the vendor GEMM library (hipBLASLt, through torch.matmul) on this machine:
     large square bf16 products (a practical dense MFMA ceiling, against the published 2.5 PF)
@@ -986,20 +1023,7 @@ def library_references(args, vm, torch, d):
     filler_a, filler_b = normal((8192, 8192)), normal((8192, 8192))
 
     def timed(fn, n=60, warm=10):
-        for _ in range(warm):
-            fn(0)
-        torch.cuda.synchronize()
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(n)]
-        for i in range(n):
-            if i % 10 == 0:
-                torch.matmul(filler_a, filler_b)
-            ev[i][0].record()
-            fn(i)
-            ev[i][1].record()
-        torch.cuda.synchronize()
-        t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
-        return sum(t) / len(t), t[len(t) // 2]
+        return event_timed(torch, fn, lambda: torch.matmul(filler_a, filler_b), n, warm)
 
     gemms = []
     for (m, n, k) in ((8192, 8192, 8192), (16384, 16384, 4096)):
