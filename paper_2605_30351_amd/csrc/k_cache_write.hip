@@ -139,7 +139,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   __shared__ __attribute__((aligned(16))) uint16_t xs[kTokTile * kMaxWriteDModel];
   __shared__ float ssq_part[kMaxWaves][kTokTile];
   __shared__ int64_t tok_slot[kTokTile];
-  __shared__ f32x2 rope_cs[kTokTile][kMaxRopePairs];  // (cos, sin) of each token's pair angles
+  // (cos, sin) of each token's pair angles; rows padded by one entry, so that the lanes of one
+  // pair (one token each) hit different banks
+  __shared__ f32x2 rope_cs[kTokTile][kMaxRopePairs + 1];
 
   const int nwave = blockDim.x >> 6;
   const int lane = threadIdx.x & 63;
@@ -293,7 +295,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   sum_wave_parts<kMaxWaves>(&ssq_part[0][0], kTokTile, nwave, r, tot);
 #pragma unroll
   for (int tb = 0; tb < 2; ++tb) rstd[tb] = a.gamma ? rsqrtf(tot[tb] / (float)DC + a.eps) : 1.f;
-  write_out_tile(acc, gam, rstd, &rope_cs[0][0], kMaxRopePairs, OPW * wave, DC, NO, r, q, ntok,
+  write_out_tile(acc, gam, rstd, &rope_cs[0][0], kMaxRopePairs + 1, OPW * wave, DC, NO, r, q, ntok,
                  ot, ots);
   __syncthreads();
 
@@ -323,7 +325,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
 // the first phase lands, and every wave takes part in the stores. LDS (dynamic,
 // cache_write_wide_lds_bytes): three x buffers [KPRE / 4 column blocks][16 TB rows][64],
 // swizzled like the packed kernel's x tile (the output tile reuses them), then the per-wave sums
-// of squares [waves - 1][16 TB], the ring rows [16 TB] and (cos, sin) [16 TB][d_rope / 2].
+// of squares [waves - 1][16 TB], the ring rows [16 TB] and (cos, sin) [16 TB][d_rope / 2 + 1].
 constexpr int kWideBufs = 3;
 
 template <int KPRE, int TB>
@@ -349,6 +351,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
   const int nks = dm / 32, nblk = dm / 64;
   const int nph = nks / PK;                // phases (KPRE divides nks)
   const int npair = DR / 2;
+  const int cs_ld = npair + 1;  // (cos, sin) row stride, padded as in the packed kernel
   uint16_t* xbuf = smem;
   float* ssq_part = reinterpret_cast<float*>(smem + kWideBufs * XB);
   int64_t* tok_slot = reinterpret_cast<int64_t*>(ssq_part + ncw * ROWS);
@@ -387,7 +390,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
         const int t = lane + 64 * k;
         const f32x2 cs =  // identity with a sink
             a.geo.sink_frames == 0 ? rope_cos_sin(a.rope, pr, pos[k]) : f32x2{1.f, 0.f};
-        if (t < ntok) rope_cs[t * npair + pr] = cs;
+        if (t < ntok) rope_cs[t * cs_ld + pr] = cs;
       }
     }
   };
@@ -507,7 +510,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     float rstd[TB];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) rstd[tb] = a.gamma ? rsqrtf(tot[tb] / (float)DC + a.eps) : 1.f;
-    write_out_tile(acc, gam, rstd, rope_cs, npair, OPW * wave, DC, NO, r, q, ntok, ot, ots);
+    write_out_tile(acc, gam, rstd, rope_cs, cs_ld, OPW * wave, DC, NO, r, q, ntok, ot, ots);
     __syncthreads();  // the output tile is complete
   }
 
@@ -742,7 +745,7 @@ int wide_kpre(const WriteArgs& a, int n_cu) {
 size_t cache_write_wide_lds_bytes(int kpre, int tb, int ncw, int npair) {
   const size_t rows = 16 * (size_t)tb;
   return kWideBufs * (size_t)(kpre / 4) * rows * 64 * 2 + ncw * rows * 4 + rows * 8 +
-         rows * npair * 8;
+         rows * (npair + 1) * 8;
 }
 
 template <int KPRE>
