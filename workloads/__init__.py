@@ -136,11 +136,13 @@ class LayerInputs:
 
 
 def make_layer_inputs(dims: Dims, seed: int, n_frames: int, batch: int = 1, norm: bool = True,
-                      q_gain: float = 1.0) -> LayerInputs:
+                      q_gain: float = 1.0, random_gain: bool = False) -> LayerInputs:
     """Draw one layer's inputs in a fixed order: x frames, W_DKV, W_KR, W_UK, W_UV, q_nope, q_R.
 
     `q_gain` multiplies the float32 query draws before rounding (4.0 gives the peaked-softmax
-    variant whose scaled scores have std of about 4).
+    variant whose scaled scores have std of about 4). With `norm`, the RMSNorm gain is all ones,
+    or with `random_gain` drawn uniform in [0.5, 1.5) from a stream of its own (seed, 7), so that
+    the other draws are the same either way.
     """
     rng = np.random.Generator(np.random.PCG64(seed))
     d = dims
@@ -150,6 +152,9 @@ def make_layer_inputs(dims: Dims, seed: int, n_frames: int, batch: int = 1, norm
     w_uk = _normal_bf16(rng, (d.n_heads * d.d_nope, d.d_c), 1.0 / np.sqrt(d.d_c))
     w_uv = _normal_bf16(rng, (d.n_heads * d.d_v, d.d_c), 1.0 / np.sqrt(d.d_c))
     gamma = f32_to_bf16_bits(np.ones(d.d_c, np.float32)) if norm else None
+    if norm and random_gain:
+        g_rng = np.random.Generator(np.random.PCG64([seed, 7]))
+        gamma = f32_to_bf16_bits(g_rng.uniform(0.5, 1.5, size=d.d_c).astype(np.float32))
     qn = rng.standard_normal(size=(batch, d.chunk_tokens, d.n_heads, d.d_nope), dtype=np.float32)
     qr = rng.standard_normal(size=(batch, d.chunk_tokens, d.n_heads, d.d_rope), dtype=np.float32)
     if q_gain != 1.0:
