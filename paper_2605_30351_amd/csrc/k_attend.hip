@@ -13,6 +13,7 @@
 // token reads the same ring tile: the heads are folded into the query rows (the cache is
 // head-shared), so each [c_kv | k_r] tile is staged in LDS once per workgroup and serves all
 // its rows.
+#include <type_traits>
 #include "vmla_device.h"
 
 namespace vmla {
@@ -769,16 +770,22 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
 // out_proj: grid (ceil(Nq / (32 NW)), H, B), NW waves x 32 tokens, one head per workgroup.
 // Each wave handles the rows (token n, head h) of its 32 tokens:
 //   1. merge coefficients of every row over its key splits s: M = max_s m_s,
-//      L = sum_s 2^(m_s - M) l_s, coef_s = 2^(m_s - M) / L (kept in LDS for up to kMergeSplits
-//      splits, so that the partial rows' loads below do not wait on per-row scalars)
+//      L = sum_s 2^(m_s - M) l_s, coef_s = 2^(m_s - M) / L, kept in LDS; the first group's
+//      split-0 partial rows are already in flight meanwhile
 //   2. o_lat = sum_s coef_s O_s, streamed as 16-byte chunks that cover the rows' partial results
-//      contiguously, rounded to bf16 into an LDS tile [32][DC]
+//      contiguously, rounded to bf16 into an LDS tile [32][DC]. A lane's chunks go in groups,
+//      and the loads of every split of a group (about 24 per lane) are issued before the first
+//      is used: the partial results come from HBM, and few loads in flight per wave would
+//      leave the kernel bound by their latency
 //   3. out^T[v][token] = W_UV_h[v][:] . o_lat[token][:] with MFMA (A = W_UV rows, B = o_lat
 //      rows from LDS). Where it fits (WL), W_UV_h is staged in LDS once per workgroup with
-//      whole-line loads, issued at the start and stored after the merge (their latency passes
-//      under it); otherwise every wave reads its A operands from global memory.
+//      whole-line loads, issued at the start and stored once the coefficients' loads are back
+//      (their latency passes under those); otherwise every wave reads its A operands from
+//      global memory.
 //   4. the bf16 result is staged through the same LDS tile so that every output row is stored
 //      as whole 16-byte chunks.
+// The one workgroup barrier follows step 1. Steps 2-4 of a wave touch only its own tile, so a
+// wave whose rows have fewer splits runs its MFMAs and stores while the others still load.
 // Lanes of tokens past the chunk work on the chunk's last token and store nothing.
 // PRE (few-query calls, whose few row blocks are split over many workgroups each): steps 1 and
 // 2 are done beforehand by latent_merge_kernel, which runs one thread per (row, 8 columns) over
@@ -791,7 +798,7 @@ template <int DC, int NVB>
 struct OutProjShape {
   static constexpr int DV = NVB * 32;
   static constexpr int LS = (DC > DV ? DC : DV) + 8;  // LDS row stride (elements); +16 B per row
-  static constexpr int ROWB = 32 * (4 + 4 + 4 + 4 * kMergeSplits);  // per-wave row scalars
+  static constexpr int ROWB = 32 * (4 + 4 * kMergeSplits);  // per-wave row scalars
   static constexpr int BUDGET = 160 * 1024 - 512;
   static constexpr int need(int nw, bool wl) { return nw * (32 * LS * 2 + ROWB) + (wl ? DV * LS * 2 : 0); }
   // the most waves per workgroup (8, else 4) that fit with W_UV_h in LDS, else 4 reading it
@@ -813,7 +820,6 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   static_assert((32 * CH) % 64 == 0 && (32 * DV / 8) % 64 == 0, "whole 64-lane passes");
   __shared__ __attribute__((aligned(16))) uint16_t tileo[NW][32 * LS];
   __shared__ __attribute__((aligned(16))) uint16_t wlds[WL ? DV * LS : 8];
-  __shared__ float row_m[NW][32], row_il[NW][32];
   __shared__ float row_coef[NW][32][kMergeSplits];
   __shared__ int row_ns[NW][32];
 
@@ -842,6 +848,20 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     }
   }
 
+  // merge helpers (calls that are not merged beforehand): every row has at most kMergeSplits
+  // splits, since calls with more are merged beforehand
+  constexpr int NI = 32 * CH / 64;            // 16-byte chunks of the wave's 32 rows per lane
+  // chunks per group for a wave whose rows have up to ns splits: the loads of every split of a
+  // group are in flight together, about 24 per lane
+  constexpr auto group = [](int ns) { int g = 24 / ns < NI ? 24 / ns : NI; while (NI % g) --g; return g; };
+  constexpr int NP = group(kMergeSplits);     // split-0 chunks loaded before the coefficients
+  auto part = [&](int s, int i) {             // split s's partial of this lane's chunk i
+    const int q = i * 64 + lane, t = q / CH, k = q % CH;
+    return reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row_of(t)) * DC + 4 * k);
+  };
+  f32x4 v0[NP];
+  int nsw = 1;                                // the wave's largest split count (uniform)
+
   if constexpr (PRE) {
     // the merged rows, 16-byte chunks, coalesced
     constexpr int C8 = DC / 8;
@@ -852,12 +872,16 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       *reinterpret_cast<u32x4*>(&tw[t * LS + 8 * k]) = ldg16(a.qcat + row_of(t) * DC + 8 * k);
     }
   } else {
-  // 1. merge coefficients per row (lanes 0..31, one row each)
+  // 1. every row has a split 0: the first group's loads go out before the coefficients are known
+#pragma unroll
+  for (int i = 0; i < NP; ++i) v0[i] = *part(0, i);
+  // merge coefficients per row (lanes 0..31, one row each): M = max_s m_s, L = sum_s 2^(m_s - M) l_s
+  const size_t row = row_of(lane & 31);
+  const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
+  const int ns = attend_split_count(a, rbg);
+#pragma unroll
+  for (int s = 1; s < kMergeSplits; ++s) nsw += __ballot(ns > s) != 0;
   if (lane < 32) {
-    const size_t row = row_of(lane);
-    const int64_t rbg = (int64_t)b * a.row_blocks + (int)((row - (size_t)b * Nq * H) / a.att_rows);
-    const int ns = attend_split_count(a, rbg);
-    // the (max, sum) pairs of the first kMergeSplits splits, all loads issued together
     f32x2 ml[kMergeSplits];
 #pragma unroll
     for (int s = 0; s < kMergeSplits; ++s)
@@ -866,51 +890,17 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     float M = kNegInf;
 #pragma unroll
     for (int s = 0; s < kMergeSplits; ++s) M = fmaxf(M, ml[s][0]);
-    for (int s = kMergeSplits; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + row) * 2]);
     float L = 0.f;
 #pragma unroll
     for (int s = 0; s < kMergeSplits; ++s)
       if (s < ns) L += fast_exp2(ml[s][0] - M) * ml[s][1];
-    for (int s = kMergeSplits; s < ns; ++s) {
-      const float* p = a.ml_part + ((size_t)s * total_rows + row) * 2;
-      L += fast_exp2(p[0] - M) * p[1];
-    }
     const float il = 1.f / L;
 #pragma unroll
     for (int s = 0; s < kMergeSplits; ++s)
       row_coef[wave][lane][s] = s < ns ? fast_exp2(ml[s][0] - M) * il : 0.f;
-    row_m[wave][lane] = M;
-    row_il[wave][lane] = il;
     row_ns[wave][lane] = ns;
   }
-  __syncthreads();
-
-  // 2. merged, normalized o_lat rows -> bf16 LDS tile
-#pragma unroll 4
-  for (int it = 0; it < 32 * CH / 64; ++it) {
-    const int q = it * 64 + lane;
-    const int t = q / CH, k = q % CH;
-    const size_t row = row_of(t);
-    const int ns = row_ns[wave][t];
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < kMergeSplits; ++s) {
-      if (s < ns) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
-        acc += row_coef[wave][t][s] * v;
-      }
-    }
-    if (ns > kMergeSplits) {  // rare: more splits than the coefficient table holds
-      const float M = row_m[wave][t], il = row_il[wave][t];
-      for (int s = kMergeSplits; s < ns; ++s) {
-        const float coef = fast_exp2(a.ml_part[((size_t)s * total_rows + row) * 2] - M) * il;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + row) * DC + 4 * k);
-        acc += coef * v;
-      }
-    }
-    *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
-  }
-  }  // merge in this kernel
+  }  // coefficients in this kernel
   if constexpr (WL) {
 #pragma unroll
     for (int i = 0; i < WPER; ++i) {
@@ -918,7 +908,53 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       if (c < DV * WCPR) *reinterpret_cast<u32x4*>(&wlds[(c / WCPR) * LS + (c % WCPR) * 8]) = wv[i];
     }
   }
-  __syncthreads();  // the o_lat tiles and (WL) the W_UV_h tile are complete
+  __syncthreads();  // the W_UV_h tile (WL), the coefficient tables or (PRE) the copied rows
+  // From here on each wave works on its own LDS tile only. The LDS operations of one wave take
+  // effect in program order, so the steps below need no workgroup barrier; wave_order() keeps
+  // the compiler from moving LDS accesses across a step boundary.
+  auto wave_order = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  if constexpr (!PRE) {
+  // 2. o_lat = sum_s coef_s O_s per group of chunks, rounded to bf16 into the LDS tile. NS is the
+  // wave's largest split count; a row with fewer splits reads its last one again (the same lines, from
+  // cache) and weighs it by a zero coefficient, so the loads need no per-lane branches.
+  auto merge = [&](auto nsc) {
+    constexpr int NS = decltype(nsc)::value, NG = group(NS);
+#pragma unroll
+    for (int g = 0; g < NI / NG; ++g) {
+      f32x4 u[NS][NG];
+#pragma unroll
+      for (int i = 0; i < NG; ++i) u[0][i] = g * NG + i < NP ? v0[g * NG + i] : *part(0, g * NG + i);
+#pragma unroll
+      for (int s = 1; s < NS; ++s)
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+          const int t = ((g * NG + i) * 64 + lane) / CH;
+          u[s][i] = *part(min(s, row_ns[wave][t] - 1), g * NG + i);
+        }
+#pragma unroll
+      for (int i = 0; i < NG; ++i) {
+        const int q = (g * NG + i) * 64 + lane, t = q / CH, k = q % CH;
+        f32x4 acc = row_coef[wave][t][0] * u[0][i];
+#pragma unroll
+        for (int s = 1; s < NS; ++s) acc += row_coef[wave][t][s] * u[s][i];
+        *reinterpret_cast<bf16x4*>(&tw[t * LS + 4 * k]) = to_bf16x4(acc);
+      }
+    }
+  };
+  static_assert(kMergeSplits == 4, "one case per split count");
+  switch (nsw) {
+    case 1: merge(std::integral_constant<int, 1>{}); break;
+    case 2: merge(std::integral_constant<int, 2>{}); break;
+    case 3: merge(std::integral_constant<int, 3>{}); break;
+    default: merge(std::integral_constant<int, 4>{}); break;
+  }
+  }  // merge in this kernel
+  wave_order();  // the wave's o_lat tile is complete
 
   // 3. out^T = W_UV_h o_lat^T
   f32x16 acc[NVB];
@@ -934,7 +970,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       acc[vb] = mfma32(aw, bo, acc[vb]);
     }
   }
-  __syncthreads();  // every lane is done reading the o_lat tile
+  wave_order();  // every lane of the wave is done reading its o_lat tile
 
   // 4. stage the bf16 output rows and store them whole
 #pragma unroll
@@ -944,7 +980,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       const f32x4 v = {acc[vb][4 * i], acc[vb][4 * i + 1], acc[vb][4 * i + 2], acc[vb][4 * i + 3]};
       *reinterpret_cast<bf16x4*>(&tw[l32 * LS + vb * 32 + 8 * i + 4 * g]) = to_bf16x4(v);
     }
-  __syncthreads();
+  wave_order();
 #pragma unroll
   for (int it = 0; it < 32 * DV / 8 / 64; ++it) {
     const int q = it * 64 + lane;
