@@ -61,11 +61,39 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   const uint16_t* qn = a.q_nope + row * dn;
   uint16_t* dst = a.qcat + row * DQKP;
 
-  // this lane's query row, B-operand layout (dims ks*16 + 8g .. +8), issued before the W wait
-  const u32x4 zero = {0, 0, 0, 0};
+  // this lane's query row, B-operand layout (dims ks*16 + 8g .. +8), issued before the W wait.
+  // The loads are unconditional: a lane past the chunk reads token 0's row and stores nothing,
+  // and the steps ks >= nks, which read the last step again, feed no MFMA.
   bf16x8 bq[KN];
 #pragma unroll
-  for (int ks = 0; ks < KN; ++ks) bq[ks] = as_bf16x8(ok && ks < nks ? ldg16(qn + ks * 16 + 8 * g) : zero);
+  for (int ks = 0; ks < KN; ++ks) bq[ks] = as_bf16x8(ldg16(qn + min(ks, nks - 1) * 16 + 8 * g));
+  // the RoPE part's (u, v) pairs of this lane (pair p = lane mod NP of tokens tok0 + lane / NP +
+  // TPI j), loaded now so that their latency passes under the contraction; tokens past the
+  // chunk read the last token and are not written
+  constexpr int NP = DR / 2;
+  constexpr bool PAIR_PER_LANE = 64 % NP == 0;
+  constexpr int TPI = PAIR_PER_LANE ? 64 / NP : 1, NIT = (32 + TPI - 1) / TPI;
+  const int tok0 = blockIdx.x * 128 + wave * 32;
+  uint32_t qraw[PAIR_PER_LANE ? NIT : 1];
+  RopePair rp{};
+  if constexpr (PAIR_PER_LANE) {
+    rp = rope_pair(a.rope, lane % NP);  // a per-lane read of the kernel arguments: issued early too
+#pragma unroll
+    for (int j = 0; j < NIT; ++j) {
+      const int t = min(tok0 + lane / NP + TPI * j, Nq - 1);
+      qraw[j] = *reinterpret_cast<const uint32_t*>(a.q_r + (((size_t)b * Nq + t) * H + h) * DR + 2 * (lane % NP));
+    }
+  }
+  // the rotation positions (frame, row, column) of the wave's 32 tokens, computed once per token
+  // by lanes 0..31 while the loads are in flight (the divisions that split a token index into
+  // its position would otherwise be repeated by every lane that rotates one of its pairs)
+  __shared__ double qpos[4][3][32];
+  if (lane < 32) {
+    const TokenPos tp = rope_pos(a.geo, query_pos(a.geo, min(tok0 + lane, Nq - 1)));
+    qpos[wave][0][lane] = (double)tp.f;
+    qpos[wave][1][lane] = (double)tp.y;
+    qpos[wave][2][lane] = (double)tp.x;
+  }
 
   const uint16_t* wsrc = a.w_uk + (size_t)h * dn * DC;
   constexpr bool STAGE = AbsorbChunk<DC>::STAGE;
@@ -125,28 +153,30 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
   }
 
   // RoPE part and zero padding: 32 tokens x (DR/2) pairs per wave.
-  const int tok0 = blockIdx.x * 128 + wave * 32;
-  auto rope_one = [&](int t, int p, const RopePair& rp) {
+  auto rope_one = [&](int t, int p, const RopePair& rp, uint32_t raw) {
     const size_t r = ((size_t)b * Nq + t) * H + h;
-    const uint32_t raw = *reinterpret_cast<const uint32_t*>(a.q_r + r * DR + 2 * p);
     float u = bf16_bits_to_f32((uint16_t)(raw & 0xffff)), v = bf16_bits_to_f32((uint16_t)(raw >> 16));
-    rotate_by(rope_cos_sin(rp, rope_pos(a.geo, query_pos(a.geo, t))), u, v);
+    rotate_by(rope_cos_sin_at(qpos[wave][rp.axis][t - tok0], rp.theta), u, v);
     const uint32_t packed =
         (uint32_t)to_bf16_bits(u * a.qscale) | ((uint32_t)to_bf16_bits(v * a.qscale) << 16);
     *reinterpret_cast<uint32_t*>(STAGE ? ot + (t - tok0) * OS + DC + 2 * p
                                        : a.qcat + r * DQKP + DC + 2 * p) = packed;
   };
-  constexpr int NP = DR / 2;
-  if constexpr (64 % NP == 0) {
+  if constexpr (PAIR_PER_LANE) {
     // lane l keeps pair l mod NP for all its tokens, so that it reads that pair's table entries
     // once (a per-iteration read would be a vector load waiting for every load in flight)
     const int p = lane % NP;
-    const RopePair rp = rope_pair(a.rope, p);
-    for (int t = tok0 + lane / NP; t < tok0 + 32 && t < Nq; t += 64 / NP) rope_one(t, p, rp);
+#pragma unroll
+    for (int j = 0; j < NIT; ++j) {
+      const int t = tok0 + lane / NP + TPI * j;
+      if (t < tok0 + 32 && t < Nq) rope_one(t, p, rp, qraw[j]);
+    }
   } else {
     for (int it = lane; it < 32 * NP; it += 64) {
       const int t = tok0 + it / NP, p = it % NP;
-      if (t < Nq) rope_one(t, p, rope_pair(a.rope, p));
+      if (t < Nq)
+        rope_one(t, p, rope_pair(a.rope, p),
+                 *reinterpret_cast<const uint32_t*>(a.q_r + (((size_t)b * Nq + t) * H + h) * DR + 2 * p));
     }
   }
   if (DQKP > DC + DR) {

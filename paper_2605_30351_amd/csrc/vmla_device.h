@@ -156,11 +156,17 @@ __device__ __forceinline__ RopePair rope_pair(const RopeTable& t, int pair) {
 // are within 1.3e-7 (2^-22.9) of the exact values, measured against double precision on 2^22
 // points; the library sincosf of the angle in radians, whose fp32 product 2 pi r rounds first,
 // is within 2.1e-7. Either is far below the bf16 rounding of the rotated vectors.
-__device__ __forceinline__ f32x2 rope_cos_sin(const RopePair& rp, const TokenPos& p) {
-  const double pos = rp.axis == 0 ? (double)p.f : (rp.axis == 1 ? (double)p.y : (double)p.x);
-  const double turns = pos * rp.theta * 0.15915494309189533577;  // 1 / (2 pi)
+__device__ __forceinline__ f32x2 rope_cos_sin_at(double pos, double theta) {
+  const double turns = pos * theta * 0.15915494309189533577;  // 1 / (2 pi)
   const float r = (float)(turns - rint(turns));
   return f32x2{__builtin_amdgcn_cosf(r), __builtin_amdgcn_sinf(r)};
+}
+// The position along the pair's axis (0: frame, 1: row, 2: column).
+__device__ __forceinline__ double rope_axis_pos(int axis, const TokenPos& p) {
+  return axis == 0 ? (double)p.f : (axis == 1 ? (double)p.y : (double)p.x);
+}
+__device__ __forceinline__ f32x2 rope_cos_sin(const RopePair& rp, const TokenPos& p) {
+  return rope_cos_sin_at(rope_axis_pos(rp.axis, p), rp.theta);
 }
 __device__ __forceinline__ f32x2 rope_cos_sin(const RopeTable& t, int pair, const TokenPos& p) {
   return rope_cos_sin(rope_pair(t, pair), p);
