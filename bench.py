@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "3a9fac5b492ffaf3324c3e8c2f0f2b12a035a56171b1804b0f11db5ac3024719",
-                  "bytes": 306883247}
+                  "sha256": "fd8a84b486ecce745485ec9c9229eb125c08740f1cc11d42ce1f6fa279934b42",
+                  "bytes": 307201141}
 
 
 def log(msg):
