@@ -223,7 +223,9 @@ __global__ __launch_bounds__(256) void mat_rope_fill_kernel(const AttendArgs a, 
 }
 
 // ---------------------------------------------------------------------------------------------
-// dense_merge: one thread per (output row, 8 columns); output rows in [B][Nq][H] order.
+// dense_merge: one thread per (output row, 8 columns), in the partial results' head-major row
+// order [B][H][Nq], so that a wave reads consecutive partial rows; output rows are stored in
+// [B][Nq][H] order.
 // out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the key splits s of the row.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
@@ -231,12 +233,13 @@ __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int H = a.n_heads, Nq = a.geo.q_count;
   const int64_t n_out = (int64_t)a.batch * Nq * H;
-  const int64_t R = e / gpr;
+  const int64_t Rp = e / gpr;  // row in [B][H][Nq] order
   const int grp = (int)(e % gpr);
-  if (R >= n_out) return;
-  const int h = (int)(R % H);
-  const int64_t bn = R / H;
-  const int n = (int)(bn % Nq), b = (int)(bn / Nq);
+  if (Rp >= n_out) return;
+  const int n = (int)(Rp % Nq);
+  const int64_t bh = Rp / Nq;
+  const int h = (int)(bh % H), b = (int)(bh / H);
+  const int64_t R = ((int64_t)b * Nq + n) * H + h;  // output row
   const int rows_b = H * a.nq_pad;
   const int r = h * a.nq_pad + n;                    // row within the batch element
   const size_t total_rows = (size_t)a.batch * rows_b;
@@ -244,16 +247,45 @@ __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
   const int64_t rbg = (int64_t)b * a.row_blocks + r / a.att_rows;
   const int ns = attend_split_count(a, rbg);
   float M = kNegInfD;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + orow) * 2]);
   float L = 0.f;
   f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < ns; ++s) {
-    const float* ml = a.ml_part + ((size_t)s * total_rows + orow) * 2;
-    const float coef = fast_exp2(ml[0] - M);
-    L += coef * ml[1];
-    const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + orow) * DH + grp * 8);
-    lo += coef * src[0];
-    hi += coef * src[1];
+  if (ns <= 4) {
+    // every load of the row's splits issued together (one memory round trip), summed in split
+    // order as below
+    f32x2 ml[4];
+    f32x4 vlo[4], vhi[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < ns) {
+        const size_t base = (size_t)s * total_rows + orow;
+        ml[s] = *reinterpret_cast<const f32x2*>(a.ml_part + base * 2);
+        const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + base * DH + grp * 8);
+        vlo[s] = src[0];
+        vhi[s] = src[1];
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      if (s < ns) M = fmaxf(M, ml[s][0]);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < ns) {
+        const float coef = fast_exp2(ml[s][0] - M);
+        L += coef * ml[s][1];
+        lo += coef * vlo[s];
+        hi += coef * vhi[s];
+      }
+    }
+  } else {
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, a.ml_part[((size_t)s * total_rows + orow) * 2]);
+    for (int s = 0; s < ns; ++s) {
+      const float* ml = a.ml_part + ((size_t)s * total_rows + orow) * 2;
+      const float coef = fast_exp2(ml[0] - M);
+      L += coef * ml[1];
+      const f32x4* src = reinterpret_cast<const f32x4*>(a.o_part + ((size_t)s * total_rows + orow) * DH + grp * 8);
+      lo += coef * src[0];
+      hi += coef * src[1];
+    }
   }
   const float il = 1.f / L;
   const f32x8 v = {lo[0] * il, lo[1] * il, lo[2] * il, lo[3] * il,
