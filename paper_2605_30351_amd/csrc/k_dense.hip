@@ -229,15 +229,17 @@ __global__ __launch_bounds__(256) void mat_rope_fill_kernel(const AttendArgs a, 
 // out = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s over the key splits s of the row.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void dense_merge_kernel(const AttendArgs a) {
-  const int DH = a.d_v, gpr = DH / 8;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int H = a.n_heads, Nq = a.geo.q_count;
-  const int64_t n_out = (int64_t)a.batch * Nq * H;
-  const int64_t Rp = e / gpr;  // row in [B][H][Nq] order
+  // 32-bit index arithmetic: the launcher keeps the thread count below 2^32
+  const int DH = a.d_v;
+  const uint32_t gpr = (uint32_t)DH / 8;
+  const uint32_t e = blockIdx.x * 256u + threadIdx.x;
+  const uint32_t H = (uint32_t)a.n_heads, Nq = (uint32_t)a.geo.q_count;
+  const uint32_t n_out = (uint32_t)a.batch * Nq * H;
+  const uint32_t Rp = e / gpr;  // row in [B][H][Nq] order
   const int grp = (int)(e % gpr);
   if (Rp >= n_out) return;
   const int n = (int)(Rp % Nq);
-  const int64_t bh = Rp / Nq;
+  const uint32_t bh = Rp / Nq;
   const int h = (int)(bh % H), b = (int)(bh / H);
   const int64_t R = ((int64_t)b * Nq + n) * H + h;  // output row
   const int rows_b = H * a.nq_pad;
@@ -324,6 +326,7 @@ hipError_t launch_mat_rope_fill(const AttendArgs& a, uint16_t* kv, hipStream_t s
 
 hipError_t launch_dense_merge(const AttendArgs& a, hipStream_t s) {
   const int64_t threads = (int64_t)a.batch * a.geo.q_count * a.n_heads * (a.d_v / 8);
+  if (threads >= (int64_t(1) << 32) - 256) return hipErrorInvalidValue;  // 32-bit indices
   hipLaunchKernelGGL(dense_merge_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                      a);
   return hipGetLastError();

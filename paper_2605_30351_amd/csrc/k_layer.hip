@@ -194,21 +194,23 @@ __global__ __launch_bounds__(P::kThreads, P::kMinBlocks) void gemm_nt_kernel(con
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, uint16_t* o_lat,
                                                            int ld_olat) {
-  const int DC = a.d_c, gpr = DC / 8, H = a.n_heads;
+  // 32-bit index arithmetic: the launcher keeps the thread count below 2^32
+  const int DC = a.d_c, H = a.n_heads;
+  const uint32_t gpr = (uint32_t)DC / 8;
   const int Nq = a.geo.q_count;
-  const int rows_b = Nq * H;
-  const int64_t n_rows = (int64_t)a.batch * rows_b;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const uint32_t rows_b = (uint32_t)(Nq * H);
+  const uint32_t n_rows = (uint32_t)a.batch * rows_b;
+  const uint32_t e = blockIdx.x * 256u + threadIdx.x;
   if (e >= n_rows * gpr) {
-    const int pad_groups = (ld_olat - H * DC) / 8;
-    const int64_t z = e - n_rows * gpr;
-    if (pad_groups == 0 || z >= (int64_t)a.batch * Nq * pad_groups) return;
+    const uint32_t pad_groups = (uint32_t)(ld_olat - H * DC) / 8;
+    const uint32_t z = e - n_rows * gpr;
+    if (pad_groups == 0 || z >= (uint32_t)a.batch * Nq * pad_groups) return;
     const int64_t tok = z / pad_groups;
     const int grp = (int)(z % pad_groups);
     *reinterpret_cast<u32x4*>(o_lat + tok * ld_olat + H * DC + grp * 8) = u32x4{0, 0, 0, 0};
     return;
   }
-  const int64_t R = e / gpr;  // global query row = token * H + h
+  const uint32_t R = e / gpr;  // global query row = token * H + h
   const int grp = (int)(e % gpr);
   const int b = (int)(R / rows_b), r = (int)(R % rows_b);
   const size_t total_rows = (size_t)n_rows;
@@ -254,8 +256,8 @@ __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, u
   const float il = 1.f / L;
   const f32x8 v = {lo[0] * il, lo[1] * il, lo[2] * il, lo[3] * il,
                    hi[0] * il, hi[1] * il, hi[2] * il, hi[3] * il};
-  const int64_t tok = R / H;
-  const int h = (int)(R % H);
+  const int64_t tok = R / (uint32_t)H;
+  const int h = (int)(R % (uint32_t)H);
   *reinterpret_cast<bf16x8*>(o_lat + tok * ld_olat + h * DC + grp * 8) = to_bf16x8(v);
 }
 
@@ -343,6 +345,7 @@ hipError_t launch_latent_merge(const AttendArgs& a, uint16_t* o_lat, int ld_olat
   const int64_t rows = (int64_t)a.batch * a.geo.q_count * a.n_heads;
   const int64_t pad = (int64_t)a.batch * a.geo.q_count * ((ld_olat - a.n_heads * a.d_c) / 8);
   const int64_t threads = rows * (a.d_c / 8) + pad;
+  if (threads >= (int64_t(1) << 32) - 256) return hipErrorInvalidValue;  // 32-bit indices
   hipLaunchKernelGGL(latent_merge_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
                      a, o_lat, ld_olat);
   return hipGetLastError();

@@ -191,10 +191,10 @@ __device__ __forceinline__ void rope_rotate(const RopeTable& t, int pair, const 
 // since the attention kernel read them: only bal_prep_kernel writes them, before it).
 __device__ inline int attend_split_count(const AttendArgs& a, int64_t rbg) {
   const int64_t lo = rbg * a.tiles_per_row, hi = lo + a.tiles_per_row - 1;
-  if (!a.bal_on) return attend_owner(hi, a.units, a.n_wg) - attend_owner(lo, a.units, a.n_wg) + 1;
+  if (!a.bal_on) return attend_owner_fd(hi, a.units, a.n_wg) - attend_owner_fd(lo, a.units, a.n_wg) + 1;
   uint32_t w[8];
   bal_weights(a.bal_state, a.n_wg, w);
-  return bal_owner(w, a.n_wg, a.units, hi) - bal_owner(w, a.n_wg, a.units, lo) + 1;
+  return bal_owner_fd(w, a.n_wg, a.units, hi) - bal_owner_fd(w, a.n_wg, a.units, lo) + 1;
 }
 
 }  // namespace vmla

@@ -183,6 +183,38 @@ __host__ __device__ inline int bal_owner(const uint32_t* w, int G, int64_t U, in
   }
   return (int)(k < G - 1 ? k : G - 1);
 }
+// floor(n / d) for n >= 0, d >= 1, exactly. Below 2^53 both operands are exact doubles, and
+// the truncated, correctly rounded quotient is already floor(n / d): a quotient q + r/d with
+// r >= 1 sits at least 1/d above q and 1/d below q + 1, more than half an ulp of it (at most
+// n 2^-53 / d). The two correction steps only guard against a division that is not correctly
+// rounded.
+__host__ __device__ inline int64_t floor_div(int64_t n, int64_t d) {
+  if (n >= (int64_t(1) << 53)) return n / d;
+  int64_t q = (int64_t)((double)n / (double)d);
+  if (q * d > n) --q;
+  else if ((q + 1) * d <= n) ++q;
+  return q;
+}
+// attend_owner and bal_owner with their divisions done by floor_div: the same results. The
+// merge kernels compute a row block's split count per thread, where the 64-bit integer
+// division sequence would dominate; the attention kernel keeps the integer forms, whose code
+// its register allocation was tuned with.
+__host__ __device__ inline int attend_owner_fd(int64_t unit, int64_t units, int n_wg) {
+  return (int)floor_div((unit + 1) * (int64_t)n_wg - 1, units);
+}
+__host__ __device__ inline int bal_owner_fd(const uint32_t* w, int G, int64_t U, int64_t unit) {
+  // C <= cum(G) <= kBalMax G < 2^32 for the at most 2^20 workgroups of a call; S < 2^14
+  const uint32_t C = (uint32_t)floor_div((unit + 1) * bal_cum(w, G) - 1, U);
+  uint32_t S = 0;
+  for (int x = 0; x < 8; ++x) S += w[x];
+  int64_t r = C % S, k = (int64_t)(C / S) * 8;
+  for (int x = 0; x < 7 && r >= (int64_t)w[x]; ++x) {
+    r -= w[x];
+    ++k;
+  }
+  return (int)(k < G - 1 ? k : G - 1);
+}
+
 // Partial-result slots a row block of T units can need under any weights: every range holds at
 // least floor(U kBalMin / (kBalMin + (G - 1) kBalMax)) - 1 units.
 __host__ __device__ inline int bal_max_seg(int G, int64_t U, int T) {
