@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "fd8a84b486ecce745485ec9c9229eb125c08740f1cc11d42ce1f6fa279934b42",
-                  "bytes": 307201141}
+                  "sha256": "892df25134ff7cce77e207d7440775a0f4a420e885c118bf3ccad3ae560a2150",
+                  "bytes": 314389371}
 
 
 def log(msg):
