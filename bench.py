@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "892df25134ff7cce77e207d7440775a0f4a420e885c118bf3ccad3ae560a2150",
-                  "bytes": 314389371}
+                  "sha256": "7931cfaf9ed8aa0c3b5043df171b25d0527a04e244d5fcef4a8a49bb34cac1f4",
+                  "bytes": 309992314}
 
 
 def log(msg):

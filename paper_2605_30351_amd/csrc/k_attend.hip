@@ -867,7 +867,8 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   uint16_t* tw = tileo[wave];
   const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
 
-  // 0. W_UV_h [DV][DC] for LDS: every load of this thread issued now, stored after the merge
+  // 0. W_UV_h [DV][DC] for LDS: every load of this thread issued now, stored once the
+  //    coefficients' loads are back
   constexpr int WCPR = DC / 8, WPER = WL ? (DV * WCPR + NT - 1) / NT : 1;
   u32x4 wv[WPER];
   if constexpr (WL) {
@@ -949,9 +950,10 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   };
 
   if constexpr (!PRE) {
-  // 2. o_lat = sum_s coef_s O_s per group of chunks, rounded to bf16 into the LDS tile. NS is the
-  // wave's largest split count; a row with fewer splits reads its last one again (the same lines, from
-  // cache) and weighs it by a zero coefficient, so the loads need no per-lane branches.
+  // 2. o_lat = sum_s coef_s O_s per group of chunks, rounded to bf16 into the LDS tile. NS is
+  // the wave's largest split count; a row with fewer splits reads its last one again (the same
+  // lines, from cache) and weighs it by a zero coefficient, so the loads need no per-lane
+  // branches.
   auto merge = [&](auto nsc) {
     constexpr int NS = decltype(nsc)::value, NG = group(NS);
 #pragma unroll
