@@ -216,26 +216,25 @@ __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, u
   const size_t total_rows = (size_t)n_rows;
   const int64_t rbg = (int64_t)b * a.row_blocks + r / a.att_rows;
   const int ns = attend_split_count(a, rbg);
-  // the splits' loads are issued in groups (sixteen maxima, then eight partial rows at a time),
-  // so that rows split over many workgroups (few-query calls: about 32 splits) wait on few
-  // round trips; the sums still run in split order
-  constexpr int GM = 16, GP = 8;
+  // the splits' loads are issued in groups (eight maxima, then four partial rows at a time), so
+  // that rows split over many workgroups do not wait on one load per split; the sums still run
+  // in split order
   float M = -__builtin_huge_valf();
-  for (int s0 = 0; s0 < ns; s0 += GM) {
-    float m[GM];
+  for (int s0 = 0; s0 < ns; s0 += 8) {
+    float m[8];
 #pragma unroll
-    for (int j = 0; j < GM; ++j)
+    for (int j = 0; j < 8; ++j)
       m[j] = s0 + j < ns ? a.ml_part[((size_t)(s0 + j) * total_rows + R) * 2] : -__builtin_huge_valf();
 #pragma unroll
-    for (int j = 0; j < GM; ++j) M = fmaxf(M, m[j]);
+    for (int j = 0; j < 8; ++j) M = fmaxf(M, m[j]);
   }
   float L = 0.f;
   f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
-  for (int s0 = 0; s0 < ns; s0 += GP) {
-    f32x2 ml[GP];
-    f32x4 vlo[GP], vhi[GP];
+  for (int s0 = 0; s0 < ns; s0 += 4) {
+    f32x2 ml[4];
+    f32x4 vlo[4], vhi[4];
 #pragma unroll
-    for (int j = 0; j < GP; ++j) {
+    for (int j = 0; j < 4; ++j) {
       if (s0 + j < ns) {
         const size_t base = (size_t)(s0 + j) * total_rows + R;
         ml[j] = *reinterpret_cast<const f32x2*>(a.ml_part + base * 2);
@@ -245,7 +244,7 @@ __global__ __launch_bounds__(256) void latent_merge_kernel(const AttendArgs a, u
       }
     }
 #pragma unroll
-    for (int j = 0; j < GP; ++j) {
+    for (int j = 0; j < 4; ++j) {
       if (s0 + j < ns) {
         const float coef = fast_exp2(ml[j][0] - M);
         L += coef * ml[j][1];
