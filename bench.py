@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "7931cfaf9ed8aa0c3b5043df171b25d0527a04e244d5fcef4a8a49bb34cac1f4",
-                  "bytes": 309992314}
+                  "sha256": "0b4573913d079660c27b49889c5d5268be03b6c8c03a61332ea5a3fb2417cf5e",
+                  "bytes": 309744937}
 
 
 def log(msg):
@@ -985,6 +985,188 @@ def xcd_balance(args, vm, torch, d, n_calls=12):
     }), flush=True)
 
 
+STAMP_POINTS = {
+    "cache_write_packed": {0: "start", 1: "x first half landed", 2: "x second half landed",
+                           3: "last MFMA issued", 4: "sums of squares exchanged",
+                           5: "output tile complete", 6: "stores complete"},
+    "cache_write_wide": {0: "start", 1: "tables done",
+                         **{2 + p: f"phase {p} landed" for p in range(10)},
+                         12: "last MFMA issued", 13: "sums of squares exchanged",
+                         14: "output tile complete", 15: "stores complete"},
+    "q_absorb": {0: "start", 1: "W_UK_h staged", 2: "last MFMA issued", 3: "latent part written",
+                 4: "RoPE part written", 5: "rows staged", 6: "stores complete"},
+    "latent_attend": {0: "start", 1: "first two tiles landed", 10: "last step done",
+                      11: "partial results stored"},
+    "out_proj": {0: "start", 1: "coefficients and W_UV_h in LDS", 2: "o_lat merged",
+                 3: "last MFMA issued", 4: "output rows staged", 5: "stores complete"},
+}
+
+
+def stamp_summary(rec, points):
+    """Per point: the median over workgroups of the time (us) at which the last wave of the
+    workgroup reached it, after the workgroup's start (its first wave's point 0); plus the
+    workgroups' own durations and the span from the first start to the last point."""
+    import numpy as np
+    live = rec[:, :, 0].max(axis=1) > 0
+    r = rec[live].astype(np.float64)             # [wg][wave][point], 100 MHz ticks
+    r[r == 0] = np.nan
+    start = np.nanmin(r[:, :, 0], axis=1)        # [wg]
+    last = np.nanmax(r, axis=(1, 2))
+    out = {"workgroups": int(live.sum()),
+           "span_us": round(float(np.nanmax(last) - np.nanmin(start)) / 100, 2),
+           "workgroup_us_median": round(float(np.median(last - start)) / 100, 2),
+           "workgroup_us_max": round(float(np.max(last - start)) / 100, 2),
+           "start_spread_us": round(float(np.nanmax(start) - np.nanmin(start)) / 100, 2),
+           "points_us": {}}
+    for p, name in points.items():
+        if p == 0:
+            continue
+        col = np.nanmax(r[:, :, p], axis=1) - start
+        col = col[~np.isnan(col)]
+        if len(col):
+            out["points_us"][name] = round(float(np.median(col)) / 100, 2)
+    return out
+
+
+def attend_step_waves(rec):
+    """latent_attend, steps 200..203 of every workgroup: the step time (barrier release to
+    barrier release); per SIMD (waves w and w + 4) how long each wave waits at the barrier after
+    its instruction stream ends, the older wave (w) and the younger (w + 4) apart; the time from
+    the last wave's stream end to the release; and how far apart the four SIMDs end."""
+    import numpy as np
+    live = rec[:, :, 0].max(axis=1) > 0
+    r = rec[live].astype(np.float64)
+    steps, older, younger, alone, last_gap, simd_spread = [], [], [], [], [], []
+    for i in range(4):
+        end, rel = r[:, :, 2 + 2 * i], r[:, :, 3 + 2 * i]    # [wg][wave]
+        ok = (end > 0).all(axis=1) & (rel > 0).all(axis=1)
+        release = rel[ok].min(axis=1)
+        older.append((release[:, None] - end[ok][:, 0:4]).ravel())
+        younger.append((release[:, None] - end[ok][:, 4:8]).ravel())
+        alone.append(np.abs(end[ok][:, 4:8] - end[ok][:, 0:4]).ravel())
+        # the barrier's own delay: from the last wave's stream end to the release (this includes
+        # the wait for the next tile's loads), and how far apart the SIMDs end
+        last_gap.append(release - end[ok].max(axis=1))
+        simd_end = np.maximum(end[ok][:, 0:4], end[ok][:, 4:8])
+        simd_spread.append(simd_end.max(axis=1) - simd_end.min(axis=1))
+        if i > 0:
+            prev = r[:, :, 1 + 2 * i]
+            ok2 = ok & (prev > 0).all(axis=1)
+            steps.append(rel[ok2].min(axis=1) - prev[ok2].min(axis=1))
+    cat = lambda xs: np.concatenate(xs) / 100.0  # noqa: E731
+    s, o, y, a = cat(steps), cat(older), cat(younger), cat(alone)
+    return {"step_us_median": round(float(np.median(s)), 3),
+            "older_wave_barrier_wait_us_median": round(float(np.median(o)), 3),
+            "younger_wave_barrier_wait_us_median": round(float(np.median(y)), 3),
+            "older_wave_ends_first_fraction": round(float(np.mean(o >= y)), 3),
+            "one_wave_alone_us_median": round(float(np.median(a)), 3),
+            "last_stream_end_to_release_us_median": round(float(np.median(cat(last_gap))), 3),
+            "simd_end_spread_us_median": round(float(np.median(cat(simd_spread))), 3),
+            "samples": int(len(o))}
+
+
+def phase_timelines(args, vm, torch, d, reps=5):
+    """Phase timelines of the stamped kernels (the diagnostic build, loaded because this
+    workload sets VIDEOMLA_LIBRARY=stamps): the Wan chunk-step at batch 1 (packed cache write,
+    q_absorb, latent_attend on the frozen partition, out_proj) and the batch-4 cache write
+    (wide kernel), each recorded `reps` times after warm-up. Every figure is the median of the
+    per-record figures of stamp_summary / attend_step_waves. The stamped kernels' own HIP-event
+    times are reported beside them: the stamps' stores and waits make them a little slower
+    than the product build's."""
+    import numpy as np
+    if not vm.STAMPS:
+        raise RuntimeError("wan-phase-timelines needs the diagnostic build (VIDEOMLA_LIBRARY=stamps)")
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(21)
+
+    def normal(shape, std=1.0):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    nq, H = d.chunk_tokens, d.n_heads
+    w_dkv = normal((d.d_c, d.d_model), d.d_model ** -0.5)
+    w_kr = normal((d.d_rope, d.d_model), d.d_model ** -0.5)
+    w_uk = normal((H * d.d_nope, d.d_c), d.d_c ** -0.5)
+    w_uv = normal((H * d.d_v, d.d_c), d.d_c ** -0.5)
+    gamma = torch.ones(d.d_c, dtype=torch.bfloat16, device=dev)
+    w_packed = torch.empty(vm.write_weights_bytes(d), dtype=torch.uint8, device=dev)
+    vm.prepare_write_weights(d, w_dkv, w_kr, w_packed)
+    rings = {}
+    for B in (1, 4):
+        c_kv = torch.zeros((B, d.window_tokens, d.d_c), dtype=torch.bfloat16, device=dev)
+        k_r = torch.zeros((B, d.window_tokens, d.d_rope), dtype=torch.bfloat16, device=dev)
+        for f in range(0, d.window_frames, d.chunk_frames):
+            vm.cache_write_prepared(d, f, B, normal((B, nq, d.d_model)), w_packed, gamma, c_kv, k_r)
+        rings[B] = (c_kv, k_r, normal((B, nq, d.d_model)))
+    q_nope, q_r = normal((1, nq, H, d.d_nope)), normal((1, nq, H, d.d_rope))
+    out = torch.empty((1, nq, H, d.d_v), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(vm.attend_workspace_bytes(d, 1), dtype=torch.uint8, device=dev)
+    fe = d.window_frames
+
+    def write(B):
+        c_kv, k_r, x = rings[B]
+        vm.cache_write_prepared(d, fe, B, x, w_packed, gamma, c_kv, k_r)
+
+    def attend(o):
+        c_kv, k_r, _ = rings[1]
+        vm.attend(d, fe, 1, q_nope, q_r, w_uk, w_uv, c_kv, k_r, out, ws, opts=o)
+
+    def step(i, timer=None):
+        bracket(timer, "cache_write", lambda: write(1))
+        attend(vm.AttendOpts(partition="frozen", timer=timer))
+
+    for i in range(args.warmup):
+        step(i)
+        write(4)
+    calibrate(vm, torch, attend)
+    # the stamped kernels' own times, before any stamp buffer is attached
+    _, _, kernels = timed_steps(vm, torch, step, 10, ("cache_write", "q_absorb", "latent_attend",
+                                                      "out_proj"))
+    buf = torch.zeros(vm.stamps_buffer_bytes() // 8, dtype=torch.int64, device=dev)
+    vm.stamps_attach(buf)
+    L = vm._lib
+    shape = (L.STAMP_KERNELS, L.STAMP_WORKGROUPS, L.STAMP_WAVES, L.STAMP_POINTS)
+    per = {k: [] for k in STAMP_POINTS}
+    steps = []
+    try:
+        for _ in range(reps):
+            buf.zero_()
+            step(0)
+            write(4)
+            torch.cuda.synchronize()
+            rec = buf.cpu().numpy().view(np.uint64).reshape(shape)
+            for k, pts in STAMP_POINTS.items():
+                per[k].append(stamp_summary(rec[L.STAMP_KERNEL[k]], pts))
+            steps.append(attend_step_waves(rec[L.STAMP_KERNEL["latent_attend"]]))
+    finally:
+        vm.stamps_attach(None)
+        torch.cuda.synchronize()
+
+    def med(rows):
+        keys = rows[0].keys()
+        res = {}
+        for key in keys:
+            if isinstance(rows[0][key], dict):
+                res[key] = med([r[key] for r in rows])
+            else:
+                res[key] = round(float(np.median([r[key] for r in rows])), 3)
+        return res
+
+    print(json.dumps({
+        "metric": "phase timelines of the stamped kernels (median over workgroups, then over records)",
+        "value": med(per["latent_attend"])["span_us"], "unit": "us (latent_attend span)",
+        "n_gpus": 1, "higher_is_better": False, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "records": reps,
+        "stamped_build_event_us": {k: v["avg_us"] for k, v in kernels.items()},
+        "kernels": {k: med(v) for k, v in per.items()},
+        "latent_attend_steps_200_203": med(steps),
+        "config": {"workload": ("Wan2.1-1.3B chunk-step at batch 1 (cache write of 4,680 tokens, "
+                                "attend of 4,680 x 12 query rows over 32,760 keys, frozen "
+                                "partition) and the batch-4 cache write, diagnostic build"),
+                   "seed": 21},
+    }), flush=True)
+
+
 def event_timed(torch, fn, filler, n=60, warm=10):
     """Mean and median microseconds of fn(i), each call bracketed by HIP events on the current
     stream, with filler() (a long kernel) queued ahead of every ten calls so that the events time
@@ -1089,7 +1271,8 @@ def main():
                     choices=("wan-layer-chunk-step", "wan-30-layer-chunk", "wan-rollout-b4",
                              "wan-sink-chunk-step", "wan-full-layer-chunk-step", "wan-dc-sweep",
                              "wan-latent-vs-materialized", "wan-few-query",
-                             "wan-form-crossover", "wan-xcd-balance", "library-references"),
+                             "wan-form-crossover", "wan-xcd-balance", "library-references",
+                             "wan-phase-timelines"),
                     help="wan-layer-chunk-step: the headline (one layer's write + attend); "
                          "wan-30-layer-chunk: one chunk through 30 layers x 4 denoising steps "
                          "plus the window advance; wan-rollout-b4: batch-4 rollout of --chunks "
@@ -1105,7 +1288,9 @@ def main():
                          "d_c) and the automatic choice; wan-xcd-balance: per-XCD workgroup "
                          "times from the partition's own record; library-references: the "
                          "vendor GEMM library's rate on square products and on the cache "
-                         "write's bare projection, next to the fused cache write")
+                         "write's bare projection, next to the fused cache write; "
+                         "wan-phase-timelines: per-phase times of the kernels from the "
+                         "diagnostic build's stamps (libvideomla_stamps.so)")
     ap.add_argument("--chunks", type=int, default=80, help="chunks of the wan-rollout-b4 run")
     ap.add_argument("--n-q", default="16,52,208,1560",
                     help="query tokens per video of the wan-few-query run (comma-separated)")
@@ -1123,8 +1308,14 @@ def main():
     import numpy as np
     import torch
 
+    if args.workload == "wan-phase-timelines":
+        os.environ["VIDEOMLA_LIBRARY"] = "stamps"  # read by the binding at import
     import paper_2605_30351_amd as vm
     from workloads import WAN, make_layer_inputs
+
+    if args.workload == "wan-phase-timelines":
+        phase_timelines(args, vm, torch, WAN)
+        return
 
     if args.workload == "wan-30-layer-chunk":
         thirty_layer_chunk(args, vm, torch, WAN)

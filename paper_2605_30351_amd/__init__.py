@@ -30,4 +30,4 @@ from ._lib import (  # noqa: F401
     window_advance,
     write_weights_bytes,
 )
-from ._lib import LIB_PATH, NOALLOC_SCRATCH_BYTES  # noqa: F401
+from ._lib import LIB_PATH, NOALLOC_SCRATCH_BYTES, STAMPS, stamps_attach, stamps_buffer_bytes  # noqa: F401

@@ -3,6 +3,9 @@
 Every computation runs in the library's HIP kernels; this module converts torch tensors to
 device pointers, the current HIP stream to a handle, and return codes to exceptions. It raises
 at import time if the shared library has not been built, and never falls back to anything else.
+
+With VIDEOMLA_LIBRARY=stamps in the environment at import, it loads the diagnostic build
+libvideomla_stamps.so instead (the same calls, plus phase stamps: include/videomla_stamps.h).
 """
 from __future__ import annotations
 
@@ -13,10 +16,15 @@ import os
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libvideomla.so")
+_VARIANT = os.environ.get("VIDEOMLA_LIBRARY", "")
+if _VARIANT not in ("", "stamps"):
+    raise ImportError(f"VIDEOMLA_LIBRARY={_VARIANT!r}: only 'stamps' (the diagnostic build) is known")
+STAMPS = _VARIANT == "stamps"
+LIB_PATH = os.path.join(_PKG, "libvideomla_stamps.so" if STAMPS else "libvideomla.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2605_30351_amd/build.py`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with "
+                      f"`python paper_2605_30351_amd/build.py{' --stamps' if STAMPS else ''}`")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -35,6 +43,12 @@ EXPORTED = (
     "videomla_layer_weights_bytes", "videomla_prepare_layer_weights",
     "videomla_attend_layer_workspace_bytes", "videomla_attend_layer",
 )
+
+# the diagnostic build's one extra call (include/videomla_stamps.h)
+EXPORTED_STAMPS = ("videomla_stamps_attach",)
+STAMP_KERNELS, STAMP_WORKGROUPS, STAMP_WAVES, STAMP_POINTS = 5, 2048, 8, 16
+STAMP_KERNEL = {"cache_write_packed": 0, "cache_write_wide": 1, "q_absorb": 2,
+                "latent_attend": 3, "out_proj": 4}
 
 PARTITION = {"even": 0, "adaptive": 1, "frozen": 2}
 NOALLOC_SCRATCH_BYTES = 64 << 20  # VIDEOMLA_NOALLOC_SCRATCH_BYTES
@@ -130,6 +144,9 @@ _lib.videomla_attend_layer_workspace_bytes.restype = ctypes.c_size_t
 _lib.videomla_attend_layer.argtypes = [_DP, _WP, ctypes.c_int32, ctypes.c_int32, _P, _P,
                                        ctypes.c_size_t, _P, _P, _P, _P, ctypes.c_size_t, _OP, _P]
 _lib.videomla_attend_layer.restype = ctypes.c_int
+if STAMPS:
+    _lib.videomla_stamps_attach.argtypes = [_P, ctypes.c_int64]
+    _lib.videomla_stamps_attach.restype = ctypes.c_int
 
 
 class VideomlaError(RuntimeError):
@@ -505,3 +522,23 @@ def slot_of(dims, f: int, y: int, x: int) -> int:
 def raw():
     """The loaded ctypes library (for tests that call the C ABI directly)."""
     return _lib
+
+
+def stamps_buffer_bytes() -> int:
+    """Size of the phase-stamp buffer (VIDEOMLA_STAMP_BUFFER_BYTES)."""
+    return STAMP_KERNELS * STAMP_WORKGROUPS * STAMP_WAVES * STAMP_POINTS * 8
+
+
+def stamps_attach(buf: torch.Tensor | None):
+    """Diagnostic build only: record the phase stamps of later calls into `buf`, a device tensor
+    of stamps_buffer_bytes() bytes (None detaches). The records are uint64
+    [kernel][workgroup][wave][point] (include/videomla_stamps.h)."""
+    if not STAMPS:
+        raise VideomlaError(EUNSUPPORTED, "phase stamps need VIDEOMLA_LIBRARY=stamps at import")
+    if buf is None:
+        _check(_lib.videomla_stamps_attach(None, 0))
+        return
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise VideomlaError(EINVAL, "the stamp buffer must be a contiguous device tensor")
+    _check(_lib.videomla_stamps_attach(ctypes.c_void_p(buf.data_ptr()),
+                                       buf.numel() * buf.element_size()))

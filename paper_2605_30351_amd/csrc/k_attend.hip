@@ -57,6 +57,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
 
   const int n = blockIdx.x * 128 + wave * 32 + l32;
   const bool ok = n < Nq;
+  VMLA_STAMP(a, kStampQAbsorb, 0);
   const size_t row = ((size_t)b * Nq + (ok ? n : 0)) * H + h;
   const uint16_t* qn = a.q_nope + row * dn;
   uint16_t* dst = a.qcat + row * DQKP;
@@ -120,6 +121,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
       }
     }
     __syncthreads();
+    if (c0 == 0) VMLA_STAMP(a, kStampQAbsorb, 1);
 
     f32x16 acc[NCB];
 #pragma unroll
@@ -136,6 +138,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
         }
       }
     }
+    if (c0 == 0) VMLA_STAMP(a, kStampQAbsorb, 2);
     if (STAGE) __syncthreads();  // every wave is done reading W_UK_h: its area holds the rows
     if (ok || STAGE) {
 #pragma unroll
@@ -151,6 +154,8 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
         }
     }
   }
+
+  VMLA_STAMP(a, kStampQAbsorb, 3);
 
   // RoPE part and zero padding: 32 tokens x (DR/2) pairs per wave.
   auto rope_one = [&](int t, int p, const RopePair& rp, uint32_t raw) {
@@ -188,8 +193,10 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
       }
     }
   }
+  VMLA_STAMP(a, kStampQAbsorb, 4);
   if constexpr (STAGE) {
     __syncthreads();  // the wave's rows are complete in its tile
+    VMLA_STAMP(a, kStampQAbsorb, 5);
     constexpr int CPR = DQKP / 8;  // 16-byte chunks per row
     for (int i = lane; i < 32 * CPR; i += 64) {
       const int t = i / CPR, k = i - t * CPR;
@@ -198,6 +205,7 @@ __global__ __launch_bounds__(256) void q_absorb_kernel(const AttendArgs a) {
             *reinterpret_cast<const u32x4*>(&ot[t * OS + k * 8]);
     }
   }
+  VMLA_STAMP_DRAINED(a, kStampQAbsorb, 6);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -383,6 +391,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   // query rows per batch element: (token, head) pairs, head-minor (latent); (head, token)
   // pairs with every head padded to whole row blocks (dense: a row block is one head's)
   const int rows_b = DENSE ? a.n_heads * a.nq_pad : a.geo.q_count * a.n_heads;
+  if (!DENSE) VMLA_STAMP(a, kStampAttend, 0);
+  int stamp_step = 0;  // steps taken by this workgroup (used by the phase stamps only)
 
   // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
   // tiles of one row block is a segment with its own partial result.
@@ -726,8 +736,17 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       l_run[qb] = lsum[qb];
     }
     xch_put((t + 1) & 1, s_nxt);
+    // phase stamps: the stream's end is read here and stored after the barrier, so that the
+    // wait below has no stamp store to drain
+    const bool stamped = !DENSE && stamp_step >= 200 && stamp_step < 204;
+    const uint64_t stream_end = stamped ? VMLA_STAMP_NOW() : 0;
     wait_vmcnt<0>();  // this wave's part of tile t+2 is in LDS
     __syncthreads();
+    if (stamped) {
+      VMLA_STAMP(a, kStampAttend, 3 + 2 * (stamp_step - 200));
+      VMLA_STAMP_AT(a, kStampAttend, 2 + 2 * (stamp_step - 200), stream_end);
+    }
+    ++stamp_step;
     xch_add((t + 1) & 1, s_nxt);
     if (kbase + 2 * BN > key_end) mask_tail(kbase + BN, s_nxt);  // only near the split's end
     own_max_of(s_nxt);
@@ -740,6 +759,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   }
   wait_vmcnt<0>();
   __syncthreads();
+  if (!DENSE && stamp_step == 0) VMLA_STAMP(a, kStampAttend, 1);
 
   f32x16 s_a[QB][C::KB], s_b[QB][C::KB];
   if (n_tiles > 0) scores(tile[0], s_a);
@@ -765,6 +785,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     pn = tmp;
   }
   if (t < n_tiles) step(t, s_a, s_b, pc, pn, ps);
+  if (!DENSE) VMLA_STAMP(a, kStampAttend, 10);  // the segment processed last keeps its stamp
 
   // ---- write unnormalized O_lat and (max, sum) of this split -------------------------------
   const size_t total_rows = (size_t)a.batch * rows_b;
@@ -792,6 +813,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
     }
   }
   }  // segments
+  if (!DENSE) VMLA_STAMP_DRAINED(a, kStampAttend, 11);
   if (a.bal_rec && tid == 0)
     a.bal_state[kBalHead + blockIdx.x] = (uint32_t)(__builtin_amdgcn_s_memrealtime() - bal_t0);
 }
@@ -866,6 +888,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   };
   uint16_t* tw = tileo[wave];
   const uint16_t* w = a.w_uv + (size_t)h * DV * DC;
+  VMLA_STAMP(a, kStampOutProj, 0);
 
   // 0. W_UV_h [DV][DC] for LDS: every load of this thread issued now, stored once the
   //    coefficients' loads are back
@@ -940,6 +963,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     }
   }
   __syncthreads();  // the W_UV_h tile (WL), the coefficient tables or (PRE) the copied rows
+  VMLA_STAMP(a, kStampOutProj, 1);
   // From here on each wave works on its own LDS tile only. The LDS operations of one wave take
   // effect in program order, so the steps below need no workgroup barrier; wave_order() keeps
   // the compiler from moving LDS accesses across a step boundary.
@@ -987,6 +1011,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
   }
   }  // merge in this kernel
   wave_order();  // the wave's o_lat tile is complete
+  VMLA_STAMP(a, kStampOutProj, 2);
 
   // 3. out^T = W_UV_h o_lat^T
   f32x16 acc[NVB];
@@ -1003,6 +1028,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
     }
   }
   wave_order();  // every lane of the wave is done reading its o_lat tile
+  VMLA_STAMP(a, kStampOutProj, 3);
 
   // 4. stage the bf16 output rows and store them whole
 #pragma unroll
@@ -1013,6 +1039,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       *reinterpret_cast<bf16x4*>(&tw[l32 * LS + vb * 32 + 8 * i + 4 * g]) = to_bf16x4(v);
     }
   wave_order();
+  VMLA_STAMP(a, kStampOutProj, 4);
 #pragma unroll
   for (int it = 0; it < 32 * DV / 8 / 64; ++it) {
     const int q = it * 64 + lane;
@@ -1021,6 +1048,7 @@ __global__ __launch_bounds__(NW * 64) void out_proj_kernel(const AttendArgs a) {
       *reinterpret_cast<u32x4*>(a.out + row_of(t) * DV + 8 * k) =
           *reinterpret_cast<const u32x4*>(&tw[t * LS + 8 * k]);
   }
+  VMLA_STAMP_DRAINED(a, kStampOutProj, 5);
 }
 
 // Tile shapes per supported (d_c, d_rope).

@@ -154,6 +154,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   const int ntok = (int)(M - g0 < a.tok_per_wg ? M - g0 : a.tok_per_wg);  // >= 1 by the grid
   const int rows_pad = (ntok + 7) & ~7;
   const int ngrp = rows_pad / 8;                 // direct loads per column block
+  VMLA_STAMP(a, kStampWritePacked, 0);
 
   // RMSNorm gain of this lane's outputs 32 wave + 16 ob + 4q .. +3, fetched first
   constexpr int OPW = 16 * OB;  // outputs per wave
@@ -222,6 +223,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   // outstanding, this wave's first-phase x loads (and the gain) have landed
   wait_vmcnt<OB * KPRE>();
   __syncthreads();
+  VMLA_STAMP(a, kStampWritePacked, 1);
 
   f32x4 acc[OB][2];  // [output block][token block]
 #pragma unroll
@@ -263,10 +265,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
     for (; i0 < i_ph1; i0 += KPRE) steady(i0);
     wait_vmcnt<OB * KPRE>();
     __syncthreads();
+    VMLA_STAMP(a, kStampWritePacked, 2);
   }
   for (; i0 < nks - KPRE; i0 += KPRE) steady(i0);
 #pragma unroll
   for (int j = 0; j < KPRE; ++j) mma_step(i0 + j, wb[j]);
+  VMLA_STAMP(a, kStampWritePacked, 3);
 
   // ---- epilogue. Lane (r, q) holds, for token 16 tb + r of the block, outputs
   // OPW wave + 16 ob + 4q + e (e = 0..3) in acc[ob][tb][e] ---------------------------------
@@ -287,6 +291,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
     if (q == 0) ssq_part[wave][16 * tb + r] = ss[tb];
   }
   __syncthreads();  // every wave is past its last x read: the tile area is reused below
+  VMLA_STAMP(a, kStampWritePacked, 4);
 
   // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
   const int ots = NO + 8;  // row stride (elements): 16 bytes of padding per row
@@ -298,6 +303,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
   write_out_tile(acc, gam, rstd, &rope_cs[0][0], kMaxRopePairs + 1, OPW * wave, DC, NO, r, q, ntok,
                  ot, ots);
   __syncthreads();
+  VMLA_STAMP(a, kStampWritePacked, 5);
 
   // ---- stores: token t's row of NO/8 chunks (c_kv, then k_r) to its ring slot, coalesced ---
   const int cpt = NO / 8;
@@ -309,6 +315,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void cache_write_packed_kernel(cons
     if (o < DC) stg16(a.c_kv + (size_t)row * DC + o, val);
     else stg16(a.k_r + (size_t)row * DR + (o - DC), val);
   }
+  VMLA_STAMP_DRAINED(a, kStampWritePacked, 6);
 }
 
 // cache_write_wide_kernel (packed weights, more than 32 tokens per compute unit: batched calls).
@@ -361,6 +368,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
   const int rotb = (int)((blockIdx.x >> 3) % (unsigned)nblk);
   const int rot = 2 * rotb;
   auto kstep = [&](int i) { const int k = i + rot; return k < nks ? k : k - nks; };
+  VMLA_STAMP(a, kStampWriteWide, 0);
 
   // each token's ring row (and slot) and the (cos, sin) of its RoPE pair angles, computed by all
   // waves while the first phase of x lands: wave w takes the pairs w, w + nwave, .. (a pair index
@@ -438,6 +446,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     // the tables first: issuing a weight ring's loads can stall this wave until the compute
     // unit's memory pipeline, which the loader's x loads fill first, has room for them
     tables();
+    VMLA_STAMP(a, kStampWriteWide, 1);
     // this wave's packed panel slice (as in cache_write_packed_kernel), KPRE k-steps ahead
     const uint16_t* wpan = a.w_packed + ((size_t)wave * nks * OB) * 512 + lane * 8;
     u32x4 wb[KPRE][OB];
@@ -475,6 +484,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
       for (int j = 0; j < KPRE; ++j) {
         const int ph = (i0 + j) / PK;
         if (j % PK == 0) __syncthreads();  // phase ph is in its buffer
+        if (j % PK == 0 && ph < 10) VMLA_STAMP(a, kStampWriteWide, 2 + ph);
         mma_step(xbuf + (ph % kWideBufs) * XB, j % PK, wb[j]);
         if constexpr (decltype(refill)::value) {
           const int kn = kstep(i0 + j + KPRE);
@@ -486,6 +496,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     int i0 = 0;
     for (; i0 < nks - KPRE; i0 += KPRE) pass(i0, std::true_type{});
     pass(i0, std::false_type{});
+    VMLA_STAMP(a, kStampWriteWide, 12);
     // sums of squares of the latent outputs per token
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
@@ -502,6 +513,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
       if (q == 0) ssq_part[wave * ROWS + 16 * tb + r] = ss;
     }
     __syncthreads();  // every wave is past its last x read: the output tile reuses the buffers
+    VMLA_STAMP(a, kStampWriteWide, 13);
     // normalized latents and rotated keys, rounded to bf16, into the tile ot[t][0 .. NO)
     const int ots = NO + 8;
     uint16_t* ot = xbuf;
@@ -512,6 +524,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     for (int tb = 0; tb < TB; ++tb) rstd[tb] = a.gamma ? rsqrtf(tot[tb] / (float)DC + a.eps) : 1.f;
     write_out_tile(acc, gam, rstd, rope_cs, cs_ld, OPW * wave, DC, NO, r, q, ntok, ot, ots);
     __syncthreads();  // the output tile is complete
+    VMLA_STAMP(a, kStampWriteWide, 14);
   }
 
   // stores: token t's row of NO/8 chunks (c_kv, then k_r) to its ring slot, coalesced
@@ -526,6 +539,7 @@ __global__ __launch_bounds__(512) void cache_write_wide_kernel(const WriteArgs a
     if (o < DC) stg16(a.c_kv + (size_t)row * DC + o, val);
     else stg16(a.k_r + (size_t)row * DR + (o - DC), val);
   }
+  VMLA_STAMP_DRAINED(a, kStampWriteWide, 15);
 }
 
 // Packed weight panel for cache_write_packed_kernel: W' = [W_DKV; W_KR; zero rows up to a whole

@@ -12,6 +12,9 @@
 #include <vector>
 
 #include "videomla.h"
+#ifdef VMLA_PHASE_STAMPS
+#include "videomla_stamps.h"
+#endif
 #include "vmla_internal.h"
 
 using namespace vmla;
@@ -1135,3 +1138,27 @@ int videomla_timer_read(videomla_timer* timer, const char* kernel, int64_t* coun
 }
 
 }  // extern "C"
+
+#ifdef VMLA_PHASE_STAMPS
+// The diagnostic build's one process-wide setting: the buffer the next launches record into.
+namespace {
+uint64_t* g_stamps = nullptr;
+static_assert(kStampBufferBytes == VIDEOMLA_STAMP_BUFFER_BYTES, "stamp buffer layout");
+}  // namespace
+
+uint64_t* vmla::stamp_buffer() { return g_stamps; }
+
+extern "C" int videomla_stamps_attach(void* device_buffer, int64_t bytes) {
+  if (device_buffer == nullptr) {
+    g_stamps = nullptr;
+    return ok();
+  }
+  if (bytes < kStampBufferBytes)
+    return fail(VIDEOMLA_EINVAL, "stamp buffer of %lld bytes, %lld needed", (long long)bytes,
+                (long long)kStampBufferBytes);
+  if ((reinterpret_cast<uintptr_t>(device_buffer) & 7u) != 0)
+    return fail(VIDEOMLA_EALIGN, "stamp buffer is not 8-byte aligned");
+  g_stamps = static_cast<uint64_t*>(device_buffer);
+  return ok();
+}
+#endif

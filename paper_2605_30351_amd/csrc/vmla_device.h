@@ -76,6 +76,42 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Phase stamps (diagnostic build only; see vmla_internal.h). VMLA_STAMP(args, kernel, point)
+// records the real-time counter for this (workgroup, wave) with a plain vector store from lane 0;
+// VMLA_STAMP_DRAINED first waits for the wave's outstanding memory operations, so that the
+// point marks their completion. VMLA_STAMP_NOW() reads the counter only, and
+// VMLA_STAMP_AT(args, kernel, point, t) stores such a reading later, where the store cannot
+// delay a wait that follows the point. All are fenced for the scheduler, so that the point
+// stays where it is written. In the product build they are empty (VMLA_STAMP_NOW() is 0).
+#ifdef VMLA_PHASE_STAMPS
+__device__ __forceinline__ uint64_t stamp_now() {
+  __builtin_amdgcn_sched_barrier(0);
+  const uint64_t now = __builtin_amdgcn_s_memrealtime();
+  __builtin_amdgcn_sched_barrier(0);
+  return now;
+}
+__device__ __forceinline__ void phase_stamp_at(uint64_t* buf, int kernel, int point, uint64_t t) {
+  const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int wave = threadIdx.x >> 6;  // every stamped kernel has one-dimensional workgroups
+  if (buf != nullptr && (threadIdx.x & 63) == 0 && wg < kStampWorkgroups && wave < kStampWaves)
+    buf[(((int64_t)kernel * kStampWorkgroups + wg) * kStampWaves + wave) * kStampPoints + point] = t;
+  __builtin_amdgcn_sched_barrier(0);
+}
+#define VMLA_STAMP_NOW() ::vmla::stamp_now()
+#define VMLA_STAMP_AT(args, kernel, point, t) ::vmla::phase_stamp_at((args).stamps, (kernel), (point), (t))
+#define VMLA_STAMP(args, kernel, point) VMLA_STAMP_AT(args, kernel, point, ::vmla::stamp_now())
+#define VMLA_STAMP_DRAINED(args, kernel, point) \
+  do {                                          \
+    ::vmla::wait_vmcnt<0>();                    \
+    VMLA_STAMP(args, kernel, point);            \
+  } while (0)
+#else
+#define VMLA_STAMP_NOW() ((uint64_t)0)
+#define VMLA_STAMP_AT(args, kernel, point, t) ((void)0)
+#define VMLA_STAMP(args, kernel, point) ((void)0)
+#define VMLA_STAMP_DRAINED(args, kernel, point) ((void)0)
+#endif
+
 // LDS transpose read (ds_read_b64_tr_b16). Within each group of 16 lanes, source lane s points
 // at 4 consecutive 16-bit elements M[s][0..3]; result lane i receives M[4e + i/4][i%4],
 // e = 0..3. If source lane s addresses row (R0 + s/4), columns C0 + 4(s%4) .. +4 of a row-major

@@ -39,7 +39,30 @@ struct Geometry {
   int64_t local_lo;       // first recent frame of the chunk's context (sink_frames > 0 only)
 };
 
+#ifdef VMLA_PHASE_STAMPS
+// Phase stamps, in the diagnostic build only (the same sources compiled with
+// VMLA_PHASE_STAMPS into libvideomla_stamps.so). Lane 0 of every wave of the stamped kernels
+// writes the 100 MHz real-time counter at named points of the kernel into a caller-owned
+// device buffer of uint64 [kernel][workgroup][wave][point]; the launch arguments carry the
+// buffer that videomla_stamps_attach last set. The product build has neither the field nor
+// the stores.
+constexpr int kStampKernels = 5, kStampWorkgroups = 2048, kStampWaves = 8, kStampPoints = 16;
+constexpr int64_t kStampBufferBytes =
+    (int64_t)kStampKernels * kStampWorkgroups * kStampWaves * kStampPoints * 8;
+enum StampKernel {
+  kStampWritePacked = 0,  // cache_write_packed_kernel
+  kStampWriteWide = 1,    // cache_write_wide_kernel
+  kStampQAbsorb = 2,      // q_absorb_kernel
+  kStampAttend = 3,       // latent_attend_kernel (latent form)
+  kStampOutProj = 4,      // out_proj_kernel
+};
+uint64_t* stamp_buffer();  // the attached buffer, or nullptr (videomla_api.cpp)
+#endif
+
 struct WriteArgs {
+#ifdef VMLA_PHASE_STAMPS
+  uint64_t* stamps = stamp_buffer();
+#endif
   const uint16_t* x;      // [B][chunk_tokens][d_model]
   const uint16_t* w_dkv;  // [d_c][d_model]
   const uint16_t* w_kr;   // [d_rope][d_model]
@@ -58,6 +81,9 @@ struct WriteArgs {
 };
 
 struct AttendArgs {
+#ifdef VMLA_PHASE_STAMPS
+  uint64_t* stamps = stamp_buffer();
+#endif
   const uint16_t* q_nope;  // [B][Nq][H][d_nope]
   const uint16_t* q_r;     // [B][Nq][H][d_rope]
   const uint16_t* w_uk;    // [H*d_nope][d_c]

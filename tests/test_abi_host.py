@@ -35,6 +35,51 @@ def test_every_declared_symbol_is_exported():
     assert set(names) == set(L.EXPORTED)
 
 
+STAMPS_HEADER = os.path.join(os.path.dirname(HEADER), "videomla_stamps.h")
+
+
+def test_stamps_build_exports_the_same_calls_plus_attach():
+    """The diagnostic build exports every call of both headers; the product library does not
+    export the stamps call."""
+    from tests._build_once import ensure_stamps_built
+    text = re.sub(r"/\*.*?\*/", "", open(STAMPS_HEADER).read(), flags=re.S)
+    extra = sorted(set(re.findall(r"\b(videomla_[a-z_]+)\s*\(", text)))
+    assert extra == sorted(L.EXPORTED_STAMPS)
+    st = ctypes.CDLL(ensure_stamps_built())
+    for n in _declared() + extra:
+        assert hasattr(st, n), n
+    assert not hasattr(ctypes.CDLL(L.LIB_PATH), "videomla_stamps_attach")
+    size = re.search(r"#define VIDEOMLA_STAMP_KERNELS (\d+).*?#define VIDEOMLA_STAMP_WORKGROUPS (\d+)"
+                     r".*?#define VIDEOMLA_STAMP_WAVES (\d+).*?#define VIDEOMLA_STAMP_POINTS (\d+)",
+                     text, flags=re.S)
+    dims = tuple(int(x) for x in size.groups())
+    assert dims == (L.STAMP_KERNELS, L.STAMP_WORKGROUPS, L.STAMP_WAVES, L.STAMP_POINTS)
+    assert L.stamps_buffer_bytes() == 8 * np.prod(dims)
+
+
+def test_stamps_attach_validates_without_touching_memory():
+    """Attach only stores the pointer: a too small or misaligned buffer is refused, NULL
+    detaches. No kernel runs, so the (never dereferenced) addresses need no GPU."""
+    from tests._build_once import ensure_stamps_built
+    st = ctypes.CDLL(ensure_stamps_built())
+    st.videomla_stamps_attach.argtypes = [ctypes.c_void_p, ctypes.c_int64]
+    st.videomla_stamps_attach.restype = ctypes.c_int
+    st.videomla_last_error.restype = ctypes.c_char_p
+    need = L.stamps_buffer_bytes()
+    assert st.videomla_stamps_attach(ctypes.c_void_p(0x1000), need - 8) == L.EINVAL
+    assert b"bytes" in st.videomla_last_error()
+    assert st.videomla_stamps_attach(ctypes.c_void_p(0x1004), need) == L.EALIGN
+    assert st.videomla_stamps_attach(None, 0) == L.OK
+    assert st.videomla_last_error() == b""
+
+
+def test_stamps_calls_need_the_stamps_build():
+    if L.STAMPS:
+        pytest.skip("this process loaded the diagnostic build")
+    with pytest.raises(vm.VideomlaError):
+        vm.stamps_attach(None)
+
+
 def test_struct_layout_matches_header():
     # 10 int32 + 2*3 int32 + 3 float + 1 int32 = 20 * 4 bytes, no padding
     assert ctypes.sizeof(L.VideomlaDims) == 80
