@@ -1124,8 +1124,7 @@ def phase_timelines(args, vm, torch, d, reps=5):
                                                       "out_proj"))
     buf = torch.zeros(vm.stamps_buffer_bytes() // 8, dtype=torch.int64, device=dev)
     vm.stamps_attach(buf)
-    L = vm._lib
-    shape = (L.STAMP_KERNELS, L.STAMP_WORKGROUPS, L.STAMP_WAVES, L.STAMP_POINTS)
+    shape = (vm.STAMP_KERNELS, vm.STAMP_WORKGROUPS, vm.STAMP_WAVES, vm.STAMP_POINTS)
     per = {k: [] for k in STAMP_POINTS}
     steps = []
     try:
@@ -1136,8 +1135,8 @@ def phase_timelines(args, vm, torch, d, reps=5):
             torch.cuda.synchronize()
             rec = buf.cpu().numpy().view(np.uint64).reshape(shape)
             for k, pts in STAMP_POINTS.items():
-                per[k].append(stamp_summary(rec[L.STAMP_KERNEL[k]], pts))
-            steps.append(attend_step_waves(rec[L.STAMP_KERNEL["latent_attend"]]))
+                per[k].append(stamp_summary(rec[vm.STAMP_KERNEL[k]], pts))
+            steps.append(attend_step_waves(rec[vm.STAMP_KERNEL["latent_attend"]]))
     finally:
         vm.stamps_attach(None)
         torch.cuda.synchronize()

@@ -30,4 +30,14 @@ from ._lib import (  # noqa: F401
     window_advance,
     write_weights_bytes,
 )
-from ._lib import LIB_PATH, NOALLOC_SCRATCH_BYTES, STAMPS, stamps_attach, stamps_buffer_bytes  # noqa: F401
+from ._lib import LIB_PATH, NOALLOC_SCRATCH_BYTES  # noqa: F401
+from ._lib import (  # noqa: F401  (the diagnostic build: include/videomla_stamps.h)
+    STAMP_KERNEL,
+    STAMP_KERNELS,
+    STAMP_POINTS,
+    STAMP_WAVES,
+    STAMP_WORKGROUPS,
+    STAMPS,
+    stamps_attach,
+    stamps_buffer_bytes,
+)

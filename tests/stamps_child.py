@@ -11,7 +11,6 @@ import numpy as np  # noqa: E402
 import torch  # noqa: E402
 
 import paper_2605_30351_amd as vm  # noqa: E402
-from paper_2605_30351_amd import _lib as L  # noqa: E402
 from tests.stamps_run import run  # noqa: E402
 
 # Expected grids at the Wan shape on a 256-CU device (each launcher's own arithmetic):
@@ -30,7 +29,7 @@ EXPECT = {  # kernel: (workgroups, waves, points in the order they are reached)
 
 def check(rec, name):
     n_wg, waves, pts = EXPECT[name]
-    k = rec[L.STAMP_KERNEL[name]].astype(np.int64)  # [workgroup][wave][point]
+    k = rec[vm.STAMP_KERNEL[name]].astype(np.int64)  # [workgroup][wave][point]
     live = np.nonzero(k[:, :, 0].max(axis=1))[0]
     assert list(live) == list(range(n_wg)), (name, len(live), n_wg)
     seq = k[:n_wg, :waves][:, :, pts]
@@ -50,7 +49,7 @@ def main():
     buf = torch.zeros(vm.stamps_buffer_bytes() // 8, dtype=torch.int64, device="cuda:0")
     outs = run(vm, buf)
     rec = buf.cpu().numpy().view(np.uint64).reshape(
-        L.STAMP_KERNELS, L.STAMP_WORKGROUPS, L.STAMP_WAVES, L.STAMP_POINTS)
+        vm.STAMP_KERNELS, vm.STAMP_WORKGROUPS, vm.STAMP_WAVES, vm.STAMP_POINTS)
     for name in EXPECT:
         check(rec, name)
     for name, t in outs.items():
