@@ -1019,7 +1019,7 @@ def stamp_summary(rec, points):
            "start_spread_us": round(float(np.nanmax(start) - np.nanmin(start)) / 100, 2),
            "points_us": {}}
     for p, name in points.items():
-        if p == 0:
+        if p == 0 or np.isnan(r[:, :, p]).all():  # the start, or a point no wave reached
             continue
         col = np.nanmax(r[:, :, p], axis=1) - start
         col = col[~np.isnan(col)]
