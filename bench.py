@@ -32,8 +32,8 @@ HBM_PEAK_GBPS = 8000.0           # MI355X published HBM3E bandwidth
 ATTEND_TRAFFIC = {"sources": ("paper_2605_30351_amd/csrc/k_attend.hip",
                               "paper_2605_30351_amd/csrc/vmla_device.h",
                               "paper_2605_30351_amd/csrc/vmla_internal.h"),
-                  "sha256": "0b4573913d079660c27b49889c5d5268be03b6c8c03a61332ea5a3fb2417cf5e",
-                  "bytes": 309744937}
+                  "sha256": "a47ad6e1a56563d990164ba0c5ef2ddd24ccda38ab5361571a63f588d2140e4c",
+                  "bytes": 307742817}
 
 
 def log(msg):
@@ -1065,6 +1065,32 @@ def attend_step_waves(rec):
             "samples": int(len(o))}
 
 
+def attend_segments(rec):
+    """latent_attend: the switch between a workgroup's two segments (first segment's last step
+    to the second's first two tiles landed, split at the partial results' issue), the tail from
+    the last step to the partial results stored, and the workgroup durations of one- and
+    two-segment workgroups."""
+    import numpy as np
+    live = rec[:, :, 0].max(axis=1) > 0
+    r = rec[live].astype(np.float64)
+    r[r == 0] = np.nan
+    start = np.nanmin(r[:, :, 0], axis=1)
+    end = np.nanmax(r[:, :, 11], axis=1)
+    def row_max(p):  # the last wave's stamp per workgroup; NaN where no wave recorded it
+        m = np.where(np.isnan(r[:, :, p]), -np.inf, r[:, :, p]).max(axis=1)
+        return np.where(np.isinf(m), np.nan, m)
+    last, p12, p13, p14 = (row_max(p) for p in (10, 12, 13, 14))
+    two = ~np.isnan(p14)
+    us = lambda x: round(float(np.median(x)) / 100, 2) if len(x) else None  # noqa: E731
+    return {"two_segment_workgroups": int(two.sum()),
+            "switch_us_median": us(p14[two] - p12[two]),
+            "switch_stores_issued_us_median": us(p13[two] - p12[two]),
+            "switch_to_tiles_landed_us_median": us(p14[two] - p13[two]),
+            "end_tail_us_median": us(end - last),
+            "one_segment_workgroup_us_median": us((end - start)[~two]),
+            "two_segment_workgroup_us_median": us((end - start)[two])}
+
+
 def phase_timelines(args, vm, torch, d, reps=5):
     """Phase timelines of the stamped kernels (the diagnostic build, loaded because this
     workload sets VIDEOMLA_LIBRARY=stamps): the Wan chunk-step at batch 1 (packed cache write,
@@ -1126,7 +1152,7 @@ def phase_timelines(args, vm, torch, d, reps=5):
     vm.stamps_attach(buf)
     shape = (vm.STAMP_KERNELS, vm.STAMP_WORKGROUPS, vm.STAMP_WAVES, vm.STAMP_POINTS)
     per = {k: [] for k in STAMP_POINTS}
-    steps = []
+    steps, segs = [], []
     try:
         for _ in range(reps):
             buf.zero_()
@@ -1137,6 +1163,7 @@ def phase_timelines(args, vm, torch, d, reps=5):
             for k, pts in STAMP_POINTS.items():
                 per[k].append(stamp_summary(rec[vm.STAMP_KERNEL[k]], pts))
             steps.append(attend_step_waves(rec[vm.STAMP_KERNEL["latent_attend"]]))
+            segs.append(attend_segments(rec[vm.STAMP_KERNEL["latent_attend"]]))
     finally:
         vm.stamps_attach(None)
         torch.cuda.synchronize()
@@ -1147,6 +1174,8 @@ def phase_timelines(args, vm, torch, d, reps=5):
         for key in keys:
             if isinstance(rows[0][key], dict):
                 res[key] = med([r[key] for r in rows])
+            elif any(r[key] is None for r in rows):
+                res[key] = None
             else:
                 res[key] = round(float(np.median([r[key] for r in rows])), 3)
         return res
@@ -1159,6 +1188,7 @@ def phase_timelines(args, vm, torch, d, reps=5):
         "stamped_build_event_us": {k: v["avg_us"] for k, v in kernels.items()},
         "kernels": {k: med(v) for k, v in per.items()},
         "latent_attend_steps_200_203": med(steps),
+        "latent_attend_segments": med(segs),
         "config": {"workload": ("Wan2.1-1.3B chunk-step at batch 1 (cache write of 4,680 tokens, "
                                 "attend of 4,680 x 12 query rows over 32,760 keys, frozen "
                                 "partition) and the batch-4 cache write, diagnostic build"),

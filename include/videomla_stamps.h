@@ -51,7 +51,10 @@ extern "C" {
  *   2 + 2i / 3 + 2i the instruction stream of the workgroup's step 200 + i ended / its
  *   barrier passed (i < 4). The stream's end is read before the step's wait for its tile
  *   loads, and stored only after the barrier, so the wait has no stamp store to drain;
- *   10 last step done; 11 partial results stored.
+ *   10 last step done; 11 partial results stored;
+ *   12 the first segment's last step done and 13 its partial results issued (every
+ *   workgroup); 14 the second segment's first two tiles landed (workgroups with a second
+ *   segment only).
  * - 4, the merge of key splits with W_UV_h:
  *   0 start; 1 coefficients and W_UV_h in LDS; 2 merged o_lat tile complete;
  *   3 last MFMA issued; 4 output rows staged; 5 stores complete.

@@ -393,6 +393,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   const int rows_b = DENSE ? a.n_heads * a.nq_pad : a.geo.q_count * a.n_heads;
   if (!DENSE) VMLA_STAMP(a, kStampAttend, 0);
   int stamp_step = 0;  // steps taken by this workgroup (used by the phase stamps only)
+  int stamp_seg = 0;   // segments finished by this workgroup (the same)
 
   // This workgroup's share of the (batch, row block, key tile) units; each maximal run of
   // tiles of one row block is a segment with its own partial result.
@@ -760,6 +761,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   wait_vmcnt<0>();
   __syncthreads();
   if (!DENSE && stamp_step == 0) VMLA_STAMP(a, kStampAttend, 1);
+  if (!DENSE && stamp_seg == 1) VMLA_STAMP(a, kStampAttend, 14);
 
   f32x16 s_a[QB][C::KB], s_b[QB][C::KB];
   if (n_tiles > 0) scores(tile[0], s_a);
@@ -786,6 +788,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
   }
   if (t < n_tiles) step(t, s_a, s_b, pc, pn, ps);
   if (!DENSE) VMLA_STAMP(a, kStampAttend, 10);  // the segment processed last keeps its stamp
+  if (!DENSE && stamp_seg == 0) VMLA_STAMP(a, kStampAttend, 12);
 
   // ---- write unnormalized O_lat and (max, sum) of this split -------------------------------
   const size_t total_rows = (size_t)a.batch * rows_b;
@@ -812,6 +815,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void latent_attend_kernel(const Atten
       ml[1] = l_tot;
     }
   }
+  if (!DENSE && stamp_seg == 0) VMLA_STAMP(a, kStampAttend, 13);
+  ++stamp_seg;
   }  // segments
   if (!DENSE) VMLA_STAMP_DRAINED(a, kStampAttend, 11);
   if (a.bal_rec && tid == 0)

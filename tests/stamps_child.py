@@ -40,6 +40,13 @@ def check(rec, name):
         loader = k[:n_wg, waves]
         assert (loader[:, 0] > 0).all() and (loader[:, 15] >= loader[:, 0]).all(), name
         assert (loader[:, 1:15] == 0).all(), name
+    if name == "latent_attend":  # workgroups with two segments: the switch, in order
+        two = k[:n_wg, :, 14].max(axis=1) > 0
+        sw = k[:n_wg][two][:, :waves][:, :, [1, 12, 13, 14, 10, 11]]
+        assert two.sum() > 0 and (sw > 0).all() and (np.diff(sw, axis=2) >= 0).all(), name
+        one = k[:n_wg][~two][:, :waves]  # one segment: points 12 and 13 follow its last step
+        assert (one[:, :, 12] >= one[:, :, 10]).all() and (one[:, :, 13] >= one[:, :, 12]).all(), name
+        print(f"latent_attend: {int(two.sum())} workgroups with two segments, switch points in order")
     print(f"{name}: {n_wg} workgroups x {waves} waves, points {pts} recorded in order", flush=True)
 
 

@@ -52,3 +52,24 @@ def test_attend_step_waves_separates_older_and_younger_waves():
     assert out["last_stream_end_to_release_us_median"] == 0.05
     assert out["simd_end_spread_us_median"] == 0.03
     assert out["samples"] == 16
+
+
+def test_attend_segments_splits_the_switch_and_compares_segment_counts():
+    rec = _rec()
+    # workgroup 0: one segment, 1000 ticks; workgroups 1 and 2: two segments, 1200 and 1220
+    for w, (dur, two) in enumerate(((1000, False), (1200, True), (1220, True))):
+        rec[w, :, 0] = 10
+        rec[w, :, 10] = 10 + dur - 50     # last step done, 50 ticks before the stores are done
+        rec[w, :, 11] = 10 + dur
+        if two:
+            rec[w, :, 12] = 400           # first segment's last step
+            rec[w, :, 13] = 400 + 60 + 2 * w  # its partial results issued
+            rec[w, :, 14] = 400 + 110     # the second segment's first tiles landed
+    out = bench.attend_segments(rec)
+    assert out["two_segment_workgroups"] == 2
+    assert out["switch_us_median"] == 1.1
+    assert out["switch_stores_issued_us_median"] == 0.63
+    assert out["switch_to_tiles_landed_us_median"] == 0.47
+    assert out["end_tail_us_median"] == 0.5
+    assert out["one_segment_workgroup_us_median"] == 10.0
+    assert out["two_segment_workgroup_us_median"] == 12.1
